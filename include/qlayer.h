@@ -1,0 +1,180 @@
+/*
+ * qlayer.h -- C ABI of the MI355X (gfx950) quadratic-neuron layer library.
+ *
+ * The layer is the quadratic neuron of QuadraLib (arXiv 2204.01701, section
+ * 3.1, equation eq:2ndneuron3):
+ *
+ *     Y = (W_a * X + b_a) o (W_b * X + b_b) + (W_c * X + b_c)
+ *
+ * "o" is the elementwise (Hadamard) product (Table 1, note 3); each of the
+ * three terms T_t = W_t * X + b_t is an ordinary first-order layer (section
+ * 3.2, P4), which is why each keeps its own bias.  As a convolution "*" is the
+ * cross-correlation of a PyTorch nn.Conv2d (section 4.2: zero padding, floor
+ * output size, dilation 1, groups 1, kernel/stride/padding shared by the
+ * three terms).  As a fully-connected layer (section 3.2, P3) "*" is a
+ * matrix product.  The backward pass follows section 4.3 (eq:AD, eq:SD):
+ * with G = dl/dY, the per-term output gradients are
+ *
+ *     G_a = G o T_b,   G_b = G o T_a,   G_c = G
+ *
+ * and each term then back-propagates as an ordinary first-order layer.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  The library
+ *    keeps no pointer after a call returns and never allocates device memory.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t, passed as
+ *    void*; NULL = the null stream).  A return of QL_OK means "enqueued".
+ *  - Layouts (row-major, innermost last):
+ *      conv X, dX       : N x H x W x C          (NHWC)
+ *      conv W_t         : O x KH x KW x C        (OHWI), dW_t the same
+ *      conv Y, G, T_a, T_b : N x Ho x Wo x O     (NHWC),
+ *                          Ho = (H + 2*pad_h - KH) / stride_h + 1 (floor), Wo likewise
+ *      dense X, dX      : B x I;  W_t, dW_t : O x I;  Y, G, T_a, T_b : B x O
+ *      biases b_t, db_t : O
+ *  - dtype QL_F32: every tensor is float32.  dtype QL_BF16: X, W_t, Y, G,
+ *    T_a, T_b and dX are bfloat16 (stored as uint16), arithmetic is fp32
+ *    (MFMA with fp32 accumulation), bf16 outputs are rounded to nearest even.
+ *    Biases, dW_t and db_t are ALWAYS float32.
+ *  - Every tensor pointer must be 16-byte aligned.
+ *  - Errors: arguments are validated on the host before anything is
+ *    launched.  Invalid arguments (non-positive sizes, empty output, stride<1,
+ *    pad<0, unknown dtype, NULL required pointer, misaligned pointer) give
+ *    QL_EINVAL; a workspace smaller than the size query gives QL_EWORKSPACE;
+ *    a HIP launch error gives QL_EHIP.  Outputs are unspecified after a
+ *    non-QL_OK return.  No entry point aborts or throws.
+ *  - Workspaces: caller-allocated device memory of at least the size the
+ *    matching *_workspace_size() query returns for the same descriptor (the
+ *    query may return 0; the pointer may then be NULL).  Its contents on entry
+ *    are irrelevant.  Two calls that share a workspace must not overlap.
+ */
+#ifndef QLAYER_H
+#define QLAYER_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { QL_F32 = 0, QL_BF16 = 1 } ql_dtype;
+
+typedef enum {
+    QL_OK = 0,
+    QL_EINVAL = 1,       /* invalid argument */
+    QL_EUNSUPPORTED = 2, /* valid but not covered by the kernels */
+    QL_EWORKSPACE = 3,   /* workspace missing or too small */
+    QL_EHIP = 4          /* a HIP runtime / launch error */
+} ql_status;
+
+/* Geometry of a quadratic 2-D convolution layer. */
+typedef struct {
+    int n, c, h, w;         /* input X: N x H x W x C */
+    int o, kh, kw;          /* each W_t: O x KH x KW x C */
+    int stride_h, stride_w; /* >= 1 */
+    int pad_h, pad_w;       /* >= 0, symmetric zero padding */
+    ql_dtype dtype;
+} ql_conv_desc;
+
+/* Geometry of a quadratic fully-connected layer. */
+typedef struct {
+    int batch, in, out; /* X: batch x in, W_t: out x in, Y: batch x out */
+    ql_dtype dtype;
+} ql_linear_desc;
+
+/* Human-readable name of a status code (static storage). */
+const char *qlayer_status_string(ql_status s);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int qlayer_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Convolution forward -- section 3.1 eq:2ndneuron3 applied as a conv layer.
+ *   x          : X (N,H,W,C), required.
+ *   wa, wb, wc : W_a, W_b, W_c (O,KH,KW,C), required.
+ *   ba, bb, bc : b_a, b_b, b_c (O) float32; each may be NULL (= zero).
+ *   y          : Y (N,Ho,Wo,O); may be NULL only when ta and tb are given
+ *                (recompute mode of the hybrid back-propagation, section
+ *                4.3: only the term maps are regenerated).
+ *   ta, tb     : if non-NULL, T_a and T_b (N,Ho,Wo,O) are written as well
+ *                (the "saved" term maps the backward needs).  Recompute mode
+ *                and saved mode produce bitwise identical T_a, T_b.
+ *   workspace  : qlayer_conv2d_fwd_workspace_size(desc) bytes (split-K
+ *                partial sums for layers with few output pixels).
+ * T_c is never written.
+ * ------------------------------------------------------------------------- */
+size_t qlayer_conv2d_fwd_workspace_size(const ql_conv_desc *desc);
+ql_status qlayer_conv2d_fwd(const ql_conv_desc *desc, const void *x,
+                            const void *wa, const void *wb, const void *wc,
+                            const float *ba, const float *bb, const float *bc,
+                            void *y, void *ta, void *tb,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Convolution input gradient -- section 4.3 (eq:AD chain rule, eq:SD):
+ *   dX = sum_t  conv_transpose(G_t, W_t),  G_a = G o T_b, G_b = G o T_a, G_c = G.
+ *   gy     : G = dl/dY (N,Ho,Wo,O), required.
+ *   ta, tb : T_a, T_b (N,Ho,Wo,O) from a forward call, required.
+ *   wa, wb, wc : weights (O,KH,KW,C), required.
+ *   dx     : dX (N,H,W,C), written (not accumulated).
+ * The products G o T_b and G o T_a are formed on the fly and never stored.
+ * ------------------------------------------------------------------------- */
+size_t qlayer_conv2d_bwd_data_workspace_size(const ql_conv_desc *desc);
+ql_status qlayer_conv2d_bwd_data(const ql_conv_desc *desc, const void *gy,
+                                 const void *ta, const void *tb,
+                                 const void *wa, const void *wb, const void *wc,
+                                 void *dx, void *workspace, size_t workspace_bytes,
+                                 void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Convolution weight and bias gradients -- section 4.3 eq:SD:
+ *   dW_t[o,r,q,c] = sum_{n,i,j} G_t[n,i,j,o] X[n, i*s-p+r, j*s-p+q, c]
+ *   db_t[o]       = sum_{n,i,j} G_t[n,i,j,o]
+ *   x, gy, ta, tb  : required.
+ *   dwa, dwb, dwc  : float32 (O,KH,KW,C), required, written (not accumulated).
+ *   dba, dbb, dbc  : float32 (O); all three given or all three NULL (= skip).
+ *   workspace      : qlayer_conv2d_bwd_weight_workspace_size(desc) bytes
+ *                    (split-K partials, reduced in a fixed order, so results
+ *                    are deterministic run to run).
+ * ------------------------------------------------------------------------- */
+size_t qlayer_conv2d_bwd_weight_workspace_size(const ql_conv_desc *desc);
+ql_status qlayer_conv2d_bwd_weight(const ql_conv_desc *desc, const void *x, const void *gy,
+                                   const void *ta, const void *tb,
+                                   float *dwa, float *dwb, float *dwc,
+                                   float *dba, float *dbb, float *dbc,
+                                   void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Fully-connected forward -- section 3.2 P3: Y = (X W_a^T + b_a) o (X W_b^T + b_b)
+ * + X W_c^T + b_c.  Arguments as for qlayer_conv2d_fwd (biases may be NULL,
+ * y may be NULL when ta and tb are given).
+ * ------------------------------------------------------------------------- */
+size_t qlayer_linear_fwd_workspace_size(const ql_linear_desc *desc);
+ql_status qlayer_linear_fwd(const ql_linear_desc *desc, const void *x,
+                            const void *wa, const void *wb, const void *wc,
+                            const float *ba, const float *bb, const float *bc,
+                            void *y, void *ta, void *tb,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Fully-connected backward -- section 4.3 eq:SD for the dense layer:
+ *   dX = [G o T_b | G o T_a | G] [W_a; W_b; W_c],  dW_t = G_t^T X,  db_t = column sums of G_t.
+ *   x, gy, ta, tb, wa, wb, wc : required.
+ *   dx            : (B,I) or NULL to skip the input gradient.
+ *   dwa, dwb, dwc : float32 (O,I); all three or none (NULL = skip).
+ *   dba, dbb, dbc : float32 (O); all three or none; need dW.
+ *   At least one of dx / dW must be requested.
+ * ------------------------------------------------------------------------- */
+size_t qlayer_linear_bwd_workspace_size(const ql_linear_desc *desc);
+ql_status qlayer_linear_bwd(const ql_linear_desc *desc, const void *x, const void *gy,
+                            const void *ta, const void *tb,
+                            const void *wa, const void *wb, const void *wc,
+                            void *dx, float *dwa, float *dwb, float *dwc,
+                            float *dba, float *dbb, float *dbc,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QLAYER_H */

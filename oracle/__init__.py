@@ -1,0 +1,246 @@
+"""fp64 CPU oracle of the QuadraLib quadratic neuron -- TEST INFRASTRUCTURE ONLY.
+
+Only the test-suite, the CPU-baseline leg of ``bench.py`` and
+``__graft_entry__.smoke()`` may import this package.  The product library
+(``paper_2204_01701_amd``) never imports it, and this package imports
+nothing from the product.
+
+The arithmetic lives in ``qlayer_oracle.c`` (plain C, fp64, OpenMP over
+independent output elements); this module only compiles it and marshals
+numpy arrays through ctypes.  Every array is float64, C-contiguous, in the
+logical PyTorch layouts: activations N x C x H x W, conv weights
+O x C x KH x KW, FC inputs B x I, FC weights O x I.
+
+Definitions followed (arXiv 2204.01701):
+  * forward  -- section 3.1, equation eq:2ndneuron3, Y = (W_a X) o (W_b X) + W_c X,
+    each term an ordinary first-order neuron with its own bias (section 3.2 P4);
+  * backward -- section 4.3, equations eq:AD / eq:SD: G_a = G o T_b, G_b = G o T_a,
+    G_c = G, then the ordinary first-order gradients of each term.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "qlayer_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_D = ctypes.POINTER(ctypes.c_double)
+_L = ctypes.POINTER(ctypes.c_longlong)
+_I = ctypes.c_int
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (fp64, OpenMP, no FMA contraction)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build(force=True)
+    lib = ctypes.CDLL(_LIB_PATH)
+    conv_geom = [_I] * 11
+    w6 = [_D] * 6
+    lib.oracle_conv2d_fwd.argtypes = conv_geom + [_D] + w6 + [_D, _D, _D]
+    lib.oracle_conv2d_bwd.argtypes = conv_geom + [_D] + w6 + [_D] + [_D] * 7
+    lib.oracle_conv2d_fwd_at.argtypes = conv_geom + [_D] + w6 + [ctypes.c_longlong, _L, _D, _D, _D]
+    lib.oracle_conv2d_dx_at.argtypes = conv_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
+    lib.oracle_conv2d_dw_channel.argtypes = conv_geom + [_D] + w6 + [_D, _I] + [_D] * 6
+    lib.oracle_conv2d_out_size.argtypes = [_I] * 4
+    lib.oracle_conv2d_out_size.restype = _I
+    fc_geom = [_I] * 3
+    lib.oracle_linear_fwd.argtypes = fc_geom + [_D] + w6 + [_D, _D, _D]
+    lib.oracle_linear_bwd.argtypes = fc_geom + [_D] + w6 + [_D] + [_D] * 7
+    lib.oracle_linear_fwd_at.argtypes = fc_geom + [_D] + w6 + [ctypes.c_longlong, _L, _D, _D, _D]
+    lib.oracle_linear_dx_rows.argtypes = fc_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
+    lib.oracle_linear_dw_row.argtypes = fc_geom + [_D] + w6 + [_D, _I] + [_D] * 6
+    for f in ("oracle_conv2d_fwd", "oracle_conv2d_bwd", "oracle_conv2d_fwd_at", "oracle_conv2d_dx_at",
+              "oracle_conv2d_dw_channel", "oracle_linear_fwd", "oracle_linear_bwd",
+              "oracle_linear_fwd_at", "oracle_linear_dx_rows", "oracle_linear_dw_row"):
+        getattr(lib, f).restype = None
+    _lib = lib
+    return lib
+
+
+def _f64(a):
+    if a is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+    return a
+
+
+def _p(a):
+    if a is None:
+        return ctypes.cast(None, _D)
+    return a.ctypes.data_as(_D)
+
+
+def _pl(a):
+    return a.ctypes.data_as(_L)
+
+
+def _pair(v):
+    return (v, v) if isinstance(v, int) else tuple(v)
+
+
+def out_size(n: int, k: int, s: int, p: int) -> int:
+    """Output extent of a zero-padded cross-correlation with floor rounding."""
+    return _load().oracle_conv2d_out_size(n, k, s, p)
+
+
+def _conv_geom(x, w, stride, pad):
+    N, C, H, W = x.shape
+    O, C2, KH, KW = w.shape
+    assert C == C2, "weight input channels must match X"
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    return (N, C, H, W, O, KH, KW, sh, sw, ph, pw)
+
+
+def conv2d_fwd(x, wa, wb, wc, ba=None, bb=None, bc=None, stride=1, pad=0):
+    """Returns (Y, T_a, T_b), each N x O x Ho x Wo float64."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc = map(_f64, (x, wa, wb, wc, ba, bb, bc))
+    g = _conv_geom(x, wa, stride, pad)
+    N, O = g[0], g[4]
+    Ho, Wo = out_size(g[2], g[5], g[7], g[9]), out_size(g[3], g[6], g[8], g[10])
+    y = np.empty((N, O, Ho, Wo))
+    ta = np.empty_like(y)
+    tb = np.empty_like(y)
+    lib.oracle_conv2d_fwd(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(y), _p(ta), _p(tb))
+    return y, ta, tb
+
+
+def conv2d_bwd(x, wa, wb, wc, ba, bb, bc, gy, stride=1, pad=0):
+    """Returns dict dx, dwa, dwb, dwc, dba, dbb, dbc (float64)."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    g = _conv_geom(x, wa, stride, pad)
+    O = g[4]
+    out = {"dx": np.empty_like(x), "dwa": np.empty_like(wa), "dwb": np.empty_like(wa),
+           "dwc": np.empty_like(wa), "dba": np.empty(O), "dbb": np.empty(O), "dbc": np.empty(O)}
+    lib.oracle_conv2d_bwd(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
+                          *[_p(out[k]) for k in ("dx", "dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
+    return out
+
+
+def conv2d_fwd_at(x, wa, wb, wc, ba, bb, bc, idx, stride=1, pad=0):
+    """Y, T_a, T_b at positions idx (k x 4 array of (n, o, i, j))."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc = map(_f64, (x, wa, wb, wc, ba, bb, bc))
+    g = _conv_geom(x, wa, stride, pad)
+    idx = np.ascontiguousarray(np.asarray(idx, dtype=np.int64).reshape(-1, 4))
+    k = idx.shape[0]
+    y, ta, tb = np.empty(k), np.empty(k), np.empty(k)
+    lib.oracle_conv2d_fwd_at(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), k, _pl(idx),
+                             _p(y), _p(ta), _p(tb))
+    return y, ta, tb
+
+
+def conv2d_dx_at(x, wa, wb, wc, ba, bb, bc, gy, idx, stride=1, pad=0):
+    """dX at positions idx (k x 4 array of (n, c, h, w))."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    g = _conv_geom(x, wa, stride, pad)
+    idx = np.ascontiguousarray(np.asarray(idx, dtype=np.int64).reshape(-1, 4))
+    k = idx.shape[0]
+    dx = np.empty(k)
+    lib.oracle_conv2d_dx_at(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy), k,
+                            _pl(idx), _p(dx))
+    return dx
+
+
+def conv2d_dw_channel(x, wa, wb, wc, ba, bb, bc, gy, o, stride=1, pad=0):
+    """Weight gradients dW_t[o] (C x KH x KW each) and bias gradients db_t[o] of one channel."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    g = _conv_geom(x, wa, stride, pad)
+    shp = wa.shape[1:]
+    out = {"dwa": np.empty(shp), "dwb": np.empty(shp), "dwc": np.empty(shp),
+           "dba": np.empty(1), "dbb": np.empty(1), "dbc": np.empty(1)}
+    lib.oracle_conv2d_dw_channel(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
+                                 int(o), *[_p(out[k]) for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
+    return out
+
+
+def linear_fwd(x, wa, wb, wc, ba=None, bb=None, bc=None):
+    """Returns (Y, T_a, T_b), each B x O float64."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc = map(_f64, (x, wa, wb, wc, ba, bb, bc))
+    B, I = x.shape
+    O = wa.shape[0]
+    y, ta, tb = np.empty((B, O)), np.empty((B, O)), np.empty((B, O))
+    lib.oracle_linear_fwd(B, I, O, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc),
+                          _p(y), _p(ta), _p(tb))
+    return y, ta, tb
+
+
+def linear_bwd(x, wa, wb, wc, ba, bb, bc, gy):
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    B, I = x.shape
+    O = wa.shape[0]
+    out = {"dx": np.empty_like(x), "dwa": np.empty_like(wa), "dwb": np.empty_like(wa),
+           "dwc": np.empty_like(wa), "dba": np.empty(O), "dbb": np.empty(O), "dbc": np.empty(O)}
+    lib.oracle_linear_bwd(B, I, O, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
+                          *[_p(out[k]) for k in ("dx", "dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
+    return out
+
+
+def linear_fwd_at(x, wa, wb, wc, ba, bb, bc, idx):
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc = map(_f64, (x, wa, wb, wc, ba, bb, bc))
+    B, I = x.shape
+    O = wa.shape[0]
+    idx = np.ascontiguousarray(np.asarray(idx, dtype=np.int64).reshape(-1, 2))
+    k = idx.shape[0]
+    y, ta, tb = np.empty(k), np.empty(k), np.empty(k)
+    lib.oracle_linear_fwd_at(B, I, O, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), k,
+                             _pl(idx), _p(y), _p(ta), _p(tb))
+    return y, ta, tb
+
+
+def linear_dx_rows(x, wa, wb, wc, ba, bb, bc, gy, rows):
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    B, I = x.shape
+    O = wa.shape[0]
+    rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64).reshape(-1))
+    dx = np.empty((rows.shape[0], I))
+    lib.oracle_linear_dx_rows(B, I, O, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
+                              rows.shape[0], _pl(rows), _p(dx))
+    return dx
+
+
+def linear_dw_row(x, wa, wb, wc, ba, bb, bc, gy, o):
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    B, I = x.shape
+    O = wa.shape[0]
+    out = {"dwa": np.empty(I), "dwb": np.empty(I), "dwc": np.empty(I),
+           "dba": np.empty(1), "dbb": np.empty(1), "dbc": np.empty(1)}
+    lib.oracle_linear_dw_row(B, I, O, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
+                             int(o), *[_p(out[k]) for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
+    return out
+
+
+def num_threads() -> int:
+    """Threads OpenMP will use for oracle calls in this process."""
+    v = os.environ.get("OMP_NUM_THREADS")
+    if v and v.isdigit():
+        return int(v)
+    return len(os.sched_getaffinity(0))
