@@ -1,0 +1,295 @@
+#!/usr/bin/env python3
+"""Throughput of the quadratic-neuron layer (arXiv 2204.01701, eq:2ndneuron3) on one MI355X.
+
+One step = forward (saving T_a, T_b), input gradient and weight/bias gradients
+of each of the 13 quadratic 3x3 conv layers of a CIFAR VGG-16 at batch 128,
+bf16 inputs with fp32 accumulation, every layer on its own seeded synthetic
+input (X ~ N(0,1), He-scaled weights, biases ~ N(0, 0.01), G ~ N(0,1)).  All
+tensors are resident in HBM before the timed region.
+
+Algorithmic work per layer: 9U flops, U = 2*N*Ho*Wo*O*C*KH*KW (every tap
+counted, forward = input gradient = weight gradient = 3U; the elementwise
+product and the prologue products are not counted).  value = total 9U over
+the 13 layers / time per step, in TFLOP/s.
+
+Prints ONE JSON line.  --gpus N > 1 is refused: this build runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing leg")
+    ap.add_argument("--no-extra", action="store_true", help="skip the single-layer and dense workloads")
+    ap.add_argument("--cpu-target-s", type=float, default=15.0, help="approximate oracle sample time")
+    return ap.parse_args()
+
+
+class Layer:
+    """Device tensors and call wrappers of one quadratic conv layer."""
+
+    def __init__(self, ql, torch, L, cfg_id, layer_id, dev, bf16=True):
+        import numpy as np
+        import synth
+
+        self.L = L
+        self.ql = ql
+        dt = torch.bfloat16 if bf16 else torch.float32
+        inp = synth.conv_inputs(cfg_id, layer_id, L, bf16=bf16)
+
+        def nhwc(a):
+            return torch.from_numpy(np.ascontiguousarray(a)).permute(0, 2, 3, 1).contiguous().to(dev, dt)
+
+        self.desc = ql.conv_desc(L.n, L.c, L.h, L.w, L.o, L.k, L.k, L.stride, L.pad,
+                                 ql.QL_BF16 if bf16 else ql.QL_F32)
+        self.x = nhwc(inp["x"])
+        self.w = [nhwc(inp[k]) for k in ("wa", "wb", "wc")]
+        self.b = [torch.from_numpy(inp[k]).to(dev) for k in ("ba", "bb", "bc")]
+        self.gy = nhwc(inp["gy"])
+        self.y = torch.empty((L.n, L.ho, L.wo, L.o), device=dev, dtype=dt)
+        self.ta = torch.empty_like(self.y)
+        self.tb = torch.empty_like(self.y)
+        self.dx = torch.empty_like(self.x)
+        self.dw = [torch.empty((L.o, L.k, L.k, L.c), device=dev, dtype=torch.float32) for _ in range(3)]
+        self.db = [torch.empty(L.o, device=dev, dtype=torch.float32) for _ in range(3)]
+        need = max(ql.qlayer_conv2d_fwd_workspace_size(self.desc),
+                   ql.qlayer_conv2d_bwd_data_workspace_size(self.desc),
+                   ql.qlayer_conv2d_bwd_weight_workspace_size(self.desc))
+        self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        self.wsp = (self.ws.data_ptr(), self.ws.numel())
+        self.inp = inp
+
+    def fwd(self, st):
+        self.ql.qlayer_conv2d_fwd(self.desc, self.x, *self.w, *self.b, self.y, self.ta, self.tb,
+                                  workspace=self.wsp, stream=st)
+
+    def bwd_data(self, st):
+        self.ql.qlayer_conv2d_bwd_data(self.desc, self.gy, self.ta, self.tb, *self.w, self.dx,
+                                       workspace=self.wsp, stream=st)
+
+    def bwd_weight(self, st):
+        self.ql.qlayer_conv2d_bwd_weight(self.desc, self.x, self.gy, self.ta, self.tb, *self.dw, *self.db,
+                                         workspace=self.wsp, stream=st)
+
+
+def unit_flops(L):
+    return 2 * L.n * L.ho * L.wo * L.o * L.c * L.k * L.k
+
+
+def time_calls(torch, calls, steps, warmup, stream):
+    """Run `calls` (list of (family, fn)) warmup+steps times; return wall ms/step and
+    per-family event-measured milliseconds summed over the timed steps."""
+    for _ in range(warmup):
+        for _, fn in calls:
+            fn(stream)
+    torch.cuda.synchronize()
+    evs = []
+    t0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        for fam, fn in calls:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(stream)
+            e1.record(stream)
+            evs.append((fam, e0, e1))
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    ms_step = start.elapsed_time(stop) / steps
+    fam_ms = {}
+    fam_n = {}
+    for fam, e0, e1 in evs:
+        fam_ms[fam] = fam_ms.get(fam, 0.0) + e0.elapsed_time(e1)
+        fam_n[fam] = fam_n.get(fam, 0) + 1
+    return ms_step, wall, fam_ms, fam_n
+
+
+def cpu_baseline(layers_geom, target_s):
+    """Time the fp64 oracle on a bounded sample of the same workload: every layer's
+    forward + backward at a reduced batch, seeded exactly like the GPU inputs."""
+    import dataclasses
+
+    import oracle
+    import synth
+
+    def run(nimg):
+        t = 0.0
+        flops = 0
+        for li, L in enumerate(layers_geom):
+            Ls = dataclasses.replace(L, n=nimg)
+            inp = synth.conv_inputs(2, li, Ls, bf16=True)
+            t0 = time.perf_counter()
+            oracle.conv2d_fwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"],
+                              Ls.stride, Ls.pad)
+            oracle.conv2d_bwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"],
+                              inp["gy"], Ls.stride, Ls.pad)
+            t += time.perf_counter() - t0
+            flops += 9 * unit_flops(Ls)
+        return t, flops
+
+    t1, f1 = run(1)
+    n = 1
+    if t1 < target_s / 2:
+        n = int(min(layers_geom[0].n, max(1, math.floor(target_s / max(t1, 1e-3)))))
+        if n > 1:
+            t1, f1 = run(n)
+    return {"value": f1 / t1 / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"all 13 layers, forward + backward, batch {n} of 128 (fp64 direct summation; "
+                      f"{t1:.1f} s for {f1 / 1e9:.1f} GFLOP)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    import paper_2204_01701_amd as ql
+    import synth
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    ql.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+
+    geoms = synth.vgg16_layers(128)
+    layers = [Layer(ql, torch, L, 2, i, dev) for i, L in enumerate(geoms)]
+    calls = []
+    for i, ly in enumerate(layers):
+        calls.append((("fwd", i), ly.fwd))
+        calls.append((("bwd_data", i), ly.bwd_data))
+        calls.append((("bwd_weight", i), ly.bwd_weight))
+    ms_step, wall, fam_ms, fam_n = time_calls(torch, calls, args.steps, args.warmup, stream)
+
+    total_flops = sum(9 * unit_flops(L) for L in geoms)
+    value = total_flops / (ms_step * 1e-3) / 1e12
+
+    # per-layer table and per-family totals
+    per_layer = []
+    fam_tot = {"fwd": 0.0, "bwd_data": 0.0, "bwd_weight": 0.0}
+    for i, L in enumerate(geoms):
+        row = {"layer": i + 1, "shape": f"{L.c}->{L.o} {L.h}x{L.w}"}
+        for fam in ("fwd", "bwd_data", "bwd_weight"):
+            ms = fam_ms[(fam, i)] / fam_n[(fam, i)]
+            fam_tot[fam] += ms
+            row[f"{fam}_us"] = round(ms * 1e3, 1)
+            row[f"{fam}_tflops"] = round(3 * unit_flops(L) / (ms * 1e-3) / 1e12, 1)
+        per_layer.append(row)
+    dom = max(fam_tot, key=fam_tot.get)
+    dom_flops = sum(3 * unit_flops(L) for L in geoms)       # per step, 13 launches of the entry point
+    dom_avg_ms = fam_tot[dom] / len(geoms)                    # average duration per launch
+    achieved = dom_flops / len(geoms) / (dom_avg_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "kernel": f"qlayer_conv2d_{dom} (13 launches per step, avg {dom_avg_ms * 1e3:.1f} us)"}
+
+    extra = {}
+    if not args.no_extra:
+        extra = extra_workloads(ql, torch, dev, stream)
+
+    result = {
+        "metric": "quadratic-layer fwd+bwd TFLOP/s and % of bf16 MFMA peak on one MI355X",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "VGG-16 stack of 13 quadratic 3x3 conv layers, bf16, batch 128, 3x32x32, "
+                               "fwd + bwd_data + bwd_weight per layer",
+                   "global_batch": 128, "layers": 13, "gflop_per_step": round(total_flops / 1e9, 1)},
+        "pct_of_bf16_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
+        "wall_ms_per_step": round(wall, 4),
+        "roofline": roofline,
+        "per_family_us": {k: round(v * 1e3, 1) for k, v in fam_tot.items()},
+        "per_layer": per_layer,
+    }
+    if extra:
+        result["extra"] = extra
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(geoms, args.cpu_target_s)
+    print(json.dumps(result), flush=True)
+
+
+def extra_workloads(ql, torch, dev, stream, reps=10):
+    """The large single layer (N=64, 256->256, 56x56) and the dense layer (8192 x 4096 -> 4096),
+    each pass timed separately (reported beside the main metric)."""
+    import synth
+
+    out = {}
+    L = synth.LARGE_BF16
+    ly = Layer(ql, torch, L, 4, 0, dev)
+    calls = [("fwd", ly.fwd), ("bwd_data", ly.bwd_data), ("bwd_weight", ly.bwd_weight)]
+    ms, _, fam_ms, fam_n = time_calls(torch, calls, reps, 3, stream)
+    u = unit_flops(L)
+    out["large_conv_bf16"] = {
+        "shape": "N=64 C=256 56x56 -> 256, 3x3",
+        **{f"{f}_us": round(fam_ms[f] / fam_n[f] * 1e3, 1) for f in ("fwd", "bwd_data", "bwd_weight")},
+        **{f"{f}_tflops": round(3 * u / (fam_ms[f] / fam_n[f] * 1e-3) / 1e12, 1)
+           for f in ("fwd", "bwd_data", "bwd_weight")},
+        "fwd_bwd_tflops": round(9 * u / (ms * 1e-3) / 1e12, 1)}
+    del ly
+
+    D = synth.DENSE_BF16
+    inp = synth.dense_inputs(5, 0, D, bf16=True)
+    dt = torch.bfloat16
+    d = ql.linear_desc(D.batch, D.inp, D.out, ql.QL_BF16)
+    x = torch.from_numpy(inp["x"]).to(dev, dt)
+    w = [torch.from_numpy(inp[k]).to(dev, dt) for k in ("wa", "wb", "wc")]
+    b = [torch.from_numpy(inp[k]).to(dev) for k in ("ba", "bb", "bc")]
+    gy = torch.from_numpy(inp["gy"]).to(dev, dt)
+    y = torch.empty((D.batch, D.out), device=dev, dtype=dt)
+    ta, tb, dx = torch.empty_like(y), torch.empty_like(y), torch.empty_like(x)
+    dw = [torch.empty((D.out, D.inp), device=dev) for _ in range(3)]
+    db = [torch.empty(D.out, device=dev) for _ in range(3)]
+    need = max(ql.qlayer_linear_fwd_workspace_size(d), ql.qlayer_linear_bwd_workspace_size(d))
+    ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    wsp = (ws.data_ptr(), ws.numel())
+    calls = [("fwd", lambda st: ql.qlayer_linear_fwd(d, x, *w, *b, y, ta, tb, workspace=wsp, stream=st)),
+             ("bwd", lambda st: ql.qlayer_linear_bwd(d, x, gy, ta, tb, *w, dx, *dw, *db, workspace=wsp,
+                                                     stream=st))]
+    ms, _, fam_ms, fam_n = time_calls(torch, calls, reps, 3, stream)
+    u = D.unit_flops()
+    out["dense_bf16"] = {
+        "shape": "8192 x 4096 -> 4096",
+        "fwd_us": round(fam_ms["fwd"] / fam_n["fwd"] * 1e3, 1),
+        "bwd_us": round(fam_ms["bwd"] / fam_n["bwd"] * 1e3, 1),
+        "fwd_tflops": round(3 * u / (fam_ms["fwd"] / fam_n["fwd"] * 1e-3) / 1e12, 1),
+        "bwd_tflops": round(6 * u / (fam_ms["bwd"] / fam_n["bwd"] * 1e-3) / 1e12, 1),
+        "fwd_bwd_tflops": round(9 * u / (ms * 1e-3) / 1e12, 1)}
+    return out
+
+
+if __name__ == "__main__":
+    main()

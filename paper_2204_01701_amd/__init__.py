@@ -1,0 +1,228 @@
+"""MI355X (gfx950) quadratic-neuron layers -- Python binding of ``libqlayer.so``.
+
+The layer is the quadratic neuron of QuadraLib (arXiv 2204.01701, section 3.1,
+eq:2ndneuron3): Y = (W_a*X + b_a) o (W_b*X + b_b) + (W_c*X + b_c), applied as a
+2-D convolution and as a fully-connected layer, with the backward pass of
+section 4.3 (eq:SD).  All arithmetic runs in the HIP kernels of the C
+library; this module only marshals arguments through ctypes: torch tensors
+become device pointers, the current HIP stream becomes the stream argument,
+and workspaces are allocated with torch when the caller passes none.
+
+Function names, argument order and layouts match ``include/qlayer.h``:
+activations NHWC, conv weights OHWI, dense X B x I and W O x I, biases and
+weight/bias gradients float32.  Every function raises ``QLError`` on a
+non-zero status.  There is no fallback: if the library is not built, the
+import of the first function call fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "QL_F32", "QL_BF16", "QLError", "ConvDesc", "LinearDesc", "conv_desc", "linear_desc", "lib",
+    "qlayer_version", "qlayer_status_string",
+    "qlayer_conv2d_fwd_workspace_size", "qlayer_conv2d_fwd",
+    "qlayer_conv2d_bwd_data_workspace_size", "qlayer_conv2d_bwd_data",
+    "qlayer_conv2d_bwd_weight_workspace_size", "qlayer_conv2d_bwd_weight",
+    "qlayer_linear_fwd_workspace_size", "qlayer_linear_fwd",
+    "qlayer_linear_bwd_workspace_size", "qlayer_linear_bwd",
+]
+
+QL_F32 = 0
+QL_BF16 = 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqlayer.so")
+
+
+class QLError(RuntimeError):
+    def __init__(self, func, status):
+        self.status = status
+        super().__init__(f"{func} failed: status {status} ({qlayer_status_string(status)})")
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in
+                ("n", "c", "h", "w", "o", "kh", "kw", "stride_h", "stride_w", "pad_h", "pad_w", "dtype")]
+
+    @property
+    def ho(self):
+        return (self.h + 2 * self.pad_h - self.kh) // self.stride_h + 1
+
+    @property
+    def wo(self):
+        return (self.w + 2 * self.pad_w - self.kw) // self.stride_w + 1
+
+
+class LinearDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int), ("in_", ctypes.c_int), ("out", ctypes.c_int), ("dtype", ctypes.c_int)]
+
+
+def conv_desc(n, c, h, w, o, kh, kw, stride=1, pad=0, dtype=QL_BF16) -> ConvDesc:
+    sh, sw = (stride, stride) if isinstance(stride, int) else stride
+    ph, pw = (pad, pad) if isinstance(pad, int) else pad
+    return ConvDesc(n, c, h, w, o, kh, kw, sh, sw, ph, pw, dtype)
+
+
+def linear_desc(batch, inp, out, dtype=QL_BF16) -> LinearDesc:
+    return LinearDesc(batch, inp, out, dtype)
+
+
+_lib = None
+_vp = ctypes.c_void_p
+_sz = ctypes.c_size_t
+
+
+def lib():
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2204_01701_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    cd, ld = ctypes.POINTER(ConvDesc), ctypes.POINTER(LinearDesc)
+    L.qlayer_status_string.argtypes = [ctypes.c_int]
+    L.qlayer_status_string.restype = ctypes.c_char_p
+    L.qlayer_version.restype = ctypes.c_int
+    for name, d in (("conv2d_fwd", cd), ("conv2d_bwd_data", cd), ("conv2d_bwd_weight", cd),
+                    ("linear_fwd", ld), ("linear_bwd", ld)):
+        f = getattr(L, f"qlayer_{name}_workspace_size")
+        f.argtypes = [d]
+        f.restype = _sz
+    L.qlayer_conv2d_fwd.argtypes = [cd] + [_vp] * 10 + [_vp, _sz, _vp]
+    L.qlayer_conv2d_bwd_data.argtypes = [cd] + [_vp] * 7 + [_vp, _sz, _vp]
+    L.qlayer_conv2d_bwd_weight.argtypes = [cd] + [_vp] * 10 + [_vp, _sz, _vp]
+    L.qlayer_linear_fwd.argtypes = [ld] + [_vp] * 10 + [_vp, _sz, _vp]
+    L.qlayer_linear_bwd.argtypes = [ld] + [_vp] * 14 + [_vp, _sz, _vp]
+    for name in ("conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight", "linear_fwd", "linear_bwd"):
+        getattr(L, f"qlayer_{name}").restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def qlayer_version() -> int:
+    return lib().qlayer_version()
+
+
+def qlayer_status_string(status: int) -> str:
+    try:
+        return lib().qlayer_status_string(int(status)).decode()
+    except ImportError:
+        return "unknown"
+
+
+# --- marshalling -------------------------------------------------------------
+
+def _ptr(t):
+    """Device pointer of a tensor (None -> NULL).  Plain ints pass through (tests)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to qlayer must be contiguous")
+    return t.data_ptr()
+
+
+def _device(*tensors):
+    for t in tensors:
+        if t is not None and not isinstance(t, int):
+            return t.device
+    return None
+
+
+def _stream(stream, device):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    if device is None or device.type != "cuda":
+        return None
+    import torch
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _workspace(workspace, need, device):
+    """(pointer, bytes) of the workspace; allocates one with torch when none is given."""
+    if workspace is not None:
+        if isinstance(workspace, tuple):
+            return workspace
+        return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    if need == 0:
+        return None, 0
+    import torch
+    ws = torch.empty(need, dtype=torch.uint8, device=device)
+    _workspace.keep = ws  # keep alive until the next allocation; the stream orders reuse
+    return ws.data_ptr(), need
+
+
+def _check(func, status):
+    if status != 0:
+        raise QLError(func, status)
+
+
+# --- the C ABI, one Python function per entry point -------------------------
+
+def qlayer_conv2d_fwd_workspace_size(desc: ConvDesc) -> int:
+    return lib().qlayer_conv2d_fwd_workspace_size(ctypes.byref(desc))
+
+
+def qlayer_conv2d_fwd(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None, ta=None, tb=None,
+                      workspace=None, stream=None):
+    dev = _device(x, wa)
+    wp, wn = _workspace(workspace, qlayer_conv2d_fwd_workspace_size(desc), dev)
+    _check("qlayer_conv2d_fwd", lib().qlayer_conv2d_fwd(
+        ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
+        _ptr(y), _ptr(ta), _ptr(tb), wp, wn, _stream(stream, dev)))
+
+
+def qlayer_conv2d_bwd_data_workspace_size(desc: ConvDesc) -> int:
+    return lib().qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(desc))
+
+
+def qlayer_conv2d_bwd_data(desc, gy, ta, tb, wa, wb, wc, dx, workspace=None, stream=None):
+    dev = _device(gy, wa)
+    wp, wn = _workspace(workspace, qlayer_conv2d_bwd_data_workspace_size(desc), dev)
+    _check("qlayer_conv2d_bwd_data", lib().qlayer_conv2d_bwd_data(
+        ctypes.byref(desc), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(dx),
+        wp, wn, _stream(stream, dev)))
+
+
+def qlayer_conv2d_bwd_weight_workspace_size(desc: ConvDesc) -> int:
+    return lib().qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(desc))
+
+
+def qlayer_conv2d_bwd_weight(desc, x, gy, ta, tb, dwa, dwb, dwc, dba=None, dbb=None, dbc=None,
+                             workspace=None, stream=None):
+    dev = _device(x, gy)
+    wp, wn = _workspace(workspace, qlayer_conv2d_bwd_weight_workspace_size(desc), dev)
+    _check("qlayer_conv2d_bwd_weight", lib().qlayer_conv2d_bwd_weight(
+        ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(dwa), _ptr(dwb), _ptr(dwc),
+        _ptr(dba), _ptr(dbb), _ptr(dbc), wp, wn, _stream(stream, dev)))
+
+
+def qlayer_linear_fwd_workspace_size(desc: LinearDesc) -> int:
+    return lib().qlayer_linear_fwd_workspace_size(ctypes.byref(desc))
+
+
+def qlayer_linear_fwd(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None, ta=None, tb=None,
+                      workspace=None, stream=None):
+    dev = _device(x, wa)
+    wp, wn = _workspace(workspace, qlayer_linear_fwd_workspace_size(desc), dev)
+    _check("qlayer_linear_fwd", lib().qlayer_linear_fwd(
+        ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
+        _ptr(y), _ptr(ta), _ptr(tb), wp, wn, _stream(stream, dev)))
+
+
+def qlayer_linear_bwd_workspace_size(desc: LinearDesc) -> int:
+    return lib().qlayer_linear_bwd_workspace_size(ctypes.byref(desc))
+
+
+def qlayer_linear_bwd(desc, x, gy, ta, tb, wa, wb, wc, dx=None, dwa=None, dwb=None, dwc=None,
+                      dba=None, dbb=None, dbc=None, workspace=None, stream=None):
+    dev = _device(x, gy)
+    wp, wn = _workspace(workspace, qlayer_linear_bwd_workspace_size(desc), dev)
+    _check("qlayer_linear_bwd", lib().qlayer_linear_bwd(
+        ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc),
+        _ptr(dx), _ptr(dwa), _ptr(dwb), _ptr(dwc), _ptr(dba), _ptr(dbb), _ptr(dbc),
+        wp, wn, _stream(stream, dev)))

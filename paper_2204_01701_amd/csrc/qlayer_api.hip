@@ -1,0 +1,466 @@
+// qlayer_api.hip -- host side of the C ABI declared in include/qlayer.h:
+// argument validation, tile-configuration and split-K planning, workspace
+// carving and kernel launches on the caller's stream.  Nothing here touches
+// tensor data on the host and nothing allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdlib>
+
+#include "qlayer.h"
+#include "qconv_bwd_data.h"
+#include "qconv_bwd_weight.h"
+#include "qconv_fwd.h"
+
+using namespace ql;
+
+namespace {
+
+constexpr int kNumCUs = 256;         // MI355X compute units
+constexpr int kTargetBlocks = 2 * kNumCUs;
+constexpr size_t kAlign = 256;
+constexpr long long kMaxElems = (1LL << 31) - 1;  // 32-bit element offsets in the kernels
+constexpr size_t kMaxFwdSplitBytes = 48ull << 20;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+struct Geom {
+    int N, C, H, W, O, KH, KW, SH, SW, PH, PW, HO, WO;
+    ql_dtype dt;
+    size_t esize() const { return dt == QL_BF16 ? 2 : 4; }
+    int vec() const { return dt == QL_BF16 ? 8 : 4; }
+};
+
+ql_status make_geom(const ql_conv_desc *d, Geom &g) {
+    if (!d) return QL_EINVAL;
+    if (d->n <= 0 || d->c <= 0 || d->h <= 0 || d->w <= 0 || d->o <= 0 || d->kh <= 0 || d->kw <= 0)
+        return QL_EINVAL;
+    if (d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0) return QL_EINVAL;
+    if (d->dtype != QL_F32 && d->dtype != QL_BF16) return QL_EINVAL;
+    const long long eh = (long long)d->h + 2LL * d->pad_h - d->kh;
+    const long long ew = (long long)d->w + 2LL * d->pad_w - d->kw;
+    if (eh < 0 || ew < 0) return QL_EINVAL;  // empty output
+    g.N = d->n; g.C = d->c; g.H = d->h; g.W = d->w; g.O = d->o; g.KH = d->kh; g.KW = d->kw;
+    g.SH = d->stride_h; g.SW = d->stride_w; g.PH = d->pad_h; g.PW = d->pad_w;
+    g.HO = (int)(eh / d->stride_h + 1);
+    g.WO = (int)(ew / d->stride_w + 1);
+    g.dt = d->dtype;
+    const long long nx = (long long)g.N * g.H * g.W * g.C;
+    const long long ny = (long long)g.N * g.HO * g.WO * g.O;
+    const long long nw = (long long)g.O * g.KH * g.KW * g.C;
+    if (nx > kMaxElems || ny > kMaxElems || 3 * nw > kMaxElems || g.H + 2LL * g.PH > kMaxElems ||
+        g.W + 2LL * g.PW > kMaxElems)
+        return QL_EUNSUPPORTED;
+    return QL_OK;
+}
+
+ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
+    if (!d) return QL_EINVAL;
+    ql_conv_desc c{d->batch, d->in, 1, 1, d->out, 1, 1, 1, 1, 0, 0, d->dtype};
+    return make_geom(&c, g);
+}
+
+// Split-K planning: enough workgroups to fill the chip twice over.
+void plan_splits(int tiles, int stages_total, int min_stages, int &splits, int &sps) {
+    splits = 1;
+    if (tiles < kTargetBlocks && stages_total > min_stages) {
+        splits = std::min(cdiv(kTargetBlocks, tiles), std::max(1, stages_total / min_stages));
+    }
+    sps = cdiv(stages_total, splits);
+    splits = cdiv(stages_total, sps);
+}
+
+// ---------------------------------------------------------------------------
+// Forward planning.
+// ---------------------------------------------------------------------------
+struct FwdPlan {
+    int cfg;  // 0: BR=128 BCOL=128, 1: BR=64 BCOL=128
+    int BR, BCOL, KE;
+    int row_tiles, col_tiles, splits, sps, stages_total;
+    bool veck;
+    size_t ws_bytes;
+};
+
+FwdPlan plan_fwd(const Geom &g) {
+    FwdPlan p{};
+    const int M = g.N * g.HO * g.WO, K = g.KH * g.KW * g.C;
+    p.cfg = g.O <= 64 ? 1 : 0;
+    p.BR = p.cfg == 0 ? 128 : 64;
+    p.BCOL = 128;
+    p.KE = 64 / (int)g.esize();
+    p.veck = g.C % g.vec() == 0;
+    p.row_tiles = cdiv(g.O, p.BR);
+    p.col_tiles = cdiv(M, p.BCOL);
+    p.stages_total = cdiv(K, p.KE);
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, p.splits, p.sps);
+    // Keep the split partials modest: they cost HBM/L2 traffic.
+    while (p.splits > 1 && (size_t)p.splits * 3 * M * g.O * 4 > kMaxFwdSplitBytes) {
+        p.sps = cdiv(p.stages_total, p.splits - 1);
+        p.splits = cdiv(p.stages_total, p.sps);
+    }
+    p.ws_bytes = p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0;
+    return p;
+}
+
+// ---------------------------------------------------------------------------
+// Input-gradient planning.  Workspace: transposed weights, then split partials.
+// ---------------------------------------------------------------------------
+struct BwdDataPlan {
+    int cfg;  // 0: BR=128 BCOL=128, 1: BR=64 BCOL=128
+    int BR, BCOL, KE;
+    int row_tiles, col_tiles, splits, sps, stages_total;
+    bool veck, s1;
+    size_t wt_bytes, part_bytes, ws_bytes;
+};
+
+BwdDataPlan plan_bwd_data(const Geom &g) {
+    BwdDataPlan p{};
+    const int M = g.N * g.H * g.W, K = g.KH * g.KW * g.O;
+    p.cfg = g.C <= 64 ? 1 : 0;
+    p.BR = p.cfg == 0 ? 128 : 64;
+    p.BCOL = 128;
+    p.KE = 64 / (int)g.esize();
+    p.veck = g.O % g.vec() == 0;
+    p.s1 = g.SH == 1 && g.SW == 1;
+    p.row_tiles = cdiv(g.C, p.BR);
+    p.col_tiles = cdiv(M, p.BCOL);
+    p.stages_total = cdiv(K, p.KE);
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, p.splits, p.sps);
+    p.wt_bytes = align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
+    p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * M * g.C * sizeof(float)) : 0;
+    p.ws_bytes = p.wt_bytes + p.part_bytes;
+    return p;
+}
+
+// ---------------------------------------------------------------------------
+// Weight-gradient planning.  Workspace: dW partials, then db partials.
+// ---------------------------------------------------------------------------
+struct BwdWeightPlan {
+    int BKP, BO, KE;
+    int row_tiles, col_tiles, splits, sps, stages_total;
+    bool veck;
+    size_t dw_bytes, db_bytes, ws_bytes;
+};
+
+BwdWeightPlan plan_bwd_weight(const Geom &g) {
+    BwdWeightPlan p{};
+    const int M = g.N * g.HO * g.WO, KP = g.KH * g.KW * g.C;
+    p.BKP = 128;
+    p.BO = 64;
+    p.KE = 64 / (int)g.esize();
+    p.veck = g.C % g.vec() == 0 && g.O % g.vec() == 0;
+    p.row_tiles = cdiv(KP, p.BKP);
+    p.col_tiles = cdiv(g.O, p.BO);
+    p.stages_total = cdiv(M, p.KE);
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 8, p.splits, p.sps);
+    if (p.splits > 1) {
+        p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KP * sizeof(float));
+        p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));
+    }
+    p.ws_bytes = p.dw_bytes + p.db_bytes;
+    return p;
+}
+
+ql_status hip_status() {
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? QL_OK : QL_EHIP;
+}
+
+int grid_1d(long long total) {
+    long long b = (total + kThreads - 1) / kThreads;
+    return (int)std::max(1LL, std::min(b, 8LL * kNumCUs));
+}
+
+// ---------------------------------------------------------------------------
+// Launch helpers, one per kernel family, dispatching the template instances.
+// ---------------------------------------------------------------------------
+template <typename T>
+ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void *wa, const void *wb, const void *wc,
+                     const float *ba, const float *bb, const float *bc, void *y, void *ta, void *tb, void *ws,
+                     hipStream_t st) {
+    FwdArgs a{};
+    a.x = x;
+    a.w[0] = wa; a.w[1] = wb; a.w[2] = wc;
+    a.bias[0] = ba; a.bias[1] = bb; a.bias[2] = bc;
+    a.y = y; a.ta = ta; a.tb = tb;
+    a.ws = static_cast<float *>(ws);
+    a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
+    a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
+    a.M = g.N * g.HO * g.WO;
+    a.K = g.KH * g.KW * g.C;
+    a.row_tiles = p.row_tiles; a.col_tiles = p.col_tiles;
+    a.splits = p.splits; a.stages_per_split = p.sps; a.stages_total = p.stages_total;
+    a.fd_howo = make_fastdiv(g.HO * g.WO);
+    a.fd_wo = make_fastdiv(g.WO);
+    a.fd_c = make_fastdiv(g.C);
+    a.fd_kw = make_fastdiv(g.KW);
+    const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
+#define QL_FWD(BR, BCOL, WGR, WGC)                                                                      \
+    do {                                                                                                \
+        if (p.veck)                                                                                     \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BCOL, WGR, WGC, 64, true>), grid, block, 0, st, a);  \
+        else                                                                                            \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BCOL, WGR, WGC, 64, false>), grid, block, 0, st, a); \
+    } while (0)
+    if (p.cfg == 0)
+        QL_FWD(128, 128, 2, 2);
+    else
+        QL_FWD(64, 128, 2, 2);
+#undef QL_FWD
+    ql_status s = hip_status();
+    if (s != QL_OK || p.splits == 1) return s;
+    const long long MO = (long long)a.M * g.O;
+    hipLaunchKernelGGL((qconv_fwd_combine_kernel<T>), dim3(grid_1d(MO)), dim3(kThreads), 0, st,
+                       static_cast<const float *>(ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
+                       static_cast<T *>(ta), static_cast<T *>(tb));
+    return hip_status();
+}
+
+template <typename T>
+ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, const void *ta, const void *tb,
+                          const void *wa, const void *wb, const void *wc, void *dx, void *ws, hipStream_t st) {
+    T *wt = static_cast<T *>(ws);
+    const int khkw = g.KH * g.KW;
+    hipLaunchKernelGGL((qconv_weight_transpose_kernel<T>), dim3(cdiv(g.C, 32), cdiv(g.O, 32), 3 * khkw),
+                       dim3(kThreads), 0, st, static_cast<const T *>(wa), static_cast<const T *>(wb),
+                       static_cast<const T *>(wc), wt, g.O, khkw, g.C);
+    ql_status s = hip_status();
+    if (s != QL_OK) return s;
+    BwdDataArgs a{};
+    a.gy = gy; a.ta = ta; a.tb = tb;
+    const size_t wsz = (size_t)g.O * khkw * g.C;
+    a.wt[0] = wt; a.wt[1] = wt + wsz; a.wt[2] = wt + 2 * wsz;
+    a.dx = dx;
+    a.ws = reinterpret_cast<float *>(static_cast<char *>(ws) + p.wt_bytes);
+    a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
+    a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
+    a.M = g.N * g.H * g.W;
+    a.K = khkw * g.O;
+    a.row_tiles = p.row_tiles; a.col_tiles = p.col_tiles;
+    a.splits = p.splits; a.stages_per_split = p.sps; a.stages_total = p.stages_total;
+    a.fd_hw = make_fastdiv(g.H * g.W);
+    a.fd_w = make_fastdiv(g.W);
+    a.fd_o = make_fastdiv(g.O);
+    a.fd_kw = make_fastdiv(g.KW);
+    a.fd_sh = make_fastdiv(g.SH);
+    a.fd_sw = make_fastdiv(g.SW);
+    const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
+#define QL_BWD_DATA_S(BR, BCOL, VK, S1) \
+    hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, 64, VK, S1>), grid, block, 0, st, a)
+#define QL_BWD_DATA(BR, BCOL)                          \
+    do {                                               \
+        if (p.veck && p.s1) QL_BWD_DATA_S(BR, BCOL, true, true);        \
+        else if (p.veck) QL_BWD_DATA_S(BR, BCOL, true, false);          \
+        else if (p.s1) QL_BWD_DATA_S(BR, BCOL, false, true);            \
+        else QL_BWD_DATA_S(BR, BCOL, false, false);                     \
+    } while (0)
+    if (p.cfg == 0)
+        QL_BWD_DATA(128, 128);
+    else
+        QL_BWD_DATA(64, 128);
+#undef QL_BWD_DATA
+#undef QL_BWD_DATA_S
+    s = hip_status();
+    if (s != QL_OK || p.splits == 1) return s;
+    const long long total = (long long)a.M * g.C;
+    hipLaunchKernelGGL((qconv_bwd_data_reduce_kernel<T>), dim3(grid_1d(total)), dim3(kThreads), 0, st,
+                       static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx));
+    return hip_status();
+}
+
+template <typename T>
+ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x, const void *gy, const void *ta,
+                            const void *tb, float *dwa, float *dwb, float *dwc, float *dba, float *dbb, float *dbc,
+                            void *ws, hipStream_t st) {
+    BwdWeightArgs a{};
+    a.x = x; a.gy = gy; a.ta = ta; a.tb = tb;
+    a.dw[0] = dwa; a.dw[1] = dwb; a.dw[2] = dwc;
+    a.db[0] = dba; a.db[1] = dbb; a.db[2] = dbc;
+    a.ws_dw = static_cast<float *>(ws);
+    a.ws_db = reinterpret_cast<float *>(static_cast<char *>(ws) + p.dw_bytes);
+    a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
+    a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
+    a.M = g.N * g.HO * g.WO;
+    a.KP = g.KH * g.KW * g.C;
+    a.row_tiles = p.row_tiles; a.col_tiles = p.col_tiles;
+    a.splits = p.splits; a.stages_per_split = p.sps; a.stages_total = p.stages_total;
+    a.want_db = dba != nullptr;
+    a.fd_howo = make_fastdiv(g.HO * g.WO);
+    a.fd_wo = make_fastdiv(g.WO);
+    a.fd_c = make_fastdiv(g.C);
+    a.fd_kw = make_fastdiv(g.KW);
+    const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
+    if (p.veck)
+        hipLaunchKernelGGL((qconv_bwd_weight_kernel<T, 128, 64, 2, 2, 64, 4, true>), grid, block, 0, st, a);
+    else
+        hipLaunchKernelGGL((qconv_bwd_weight_kernel<T, 128, 64, 2, 2, 64, 4, false>), grid, block, 0, st, a);
+    ql_status s = hip_status();
+    if (s != QL_OK || p.splits == 1) return s;
+    const long long ndw = (long long)g.O * a.KP;
+    hipLaunchKernelGGL(qconv_bwd_weight_reduce_kernel, dim3(grid_1d(3 * ndw)), dim3(kThreads), 0, st,
+                       static_cast<const float *>(a.ws_dw), static_cast<const float *>(a.ws_db), p.splits, ndw,
+                       g.O, dwa, dwb, dwc, dba, dbb, dbc, a.want_db);
+    return hip_status();
+}
+
+ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *wb, const void *wc, const float *ba,
+                     const float *bb, const float *bc, void *y, void *ta, void *tb, void *ws, size_t ws_bytes,
+                     void *stream) {
+    if (!x || !wa || !wb || !wc) return QL_EINVAL;
+    if (!y && !(ta && tb)) return QL_EINVAL;
+    const void *ptrs[] = {x, wa, wb, wc, ba, bb, bc, y, ta, tb};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q)) return QL_EINVAL;
+    const FwdPlan p = plan_fwd(g);
+    if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
+    if (ws && !aligned16(ws)) return QL_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return g.dt == QL_BF16 ? launch_fwd<uint16_t>(g, p, x, wa, wb, wc, ba, bb, bc, y, ta, tb, ws, st)
+                           : launch_fwd<float>(g, p, x, wa, wb, wc, ba, bb, bc, y, ta, tb, ws, st);
+}
+
+ql_status bwd_data_common(const Geom &g, const void *gy, const void *ta, const void *tb, const void *wa,
+                          const void *wb, const void *wc, void *dx, void *ws, size_t ws_bytes, void *stream) {
+    if (!gy || !ta || !tb || !wa || !wb || !wc || !dx) return QL_EINVAL;
+    const void *ptrs[] = {gy, ta, tb, wa, wb, wc, dx};
+    for (const void *q : ptrs)
+        if (!aligned16(q)) return QL_EINVAL;
+    const BwdDataPlan p = plan_bwd_data(g);
+    if (ws_bytes < p.ws_bytes || !ws) return QL_EWORKSPACE;
+    if (!aligned16(ws)) return QL_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return g.dt == QL_BF16 ? launch_bwd_data<uint16_t>(g, p, gy, ta, tb, wa, wb, wc, dx, ws, st)
+                           : launch_bwd_data<float>(g, p, gy, ta, tb, wa, wb, wc, dx, ws, st);
+}
+
+ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const void *ta, const void *tb,
+                            float *dwa, float *dwb, float *dwc, float *dba, float *dbb, float *dbc, void *ws,
+                            size_t ws_bytes, void *stream) {
+    if (!x || !gy || !ta || !tb || !dwa || !dwb || !dwc) return QL_EINVAL;
+    const int nb = (dba != nullptr) + (dbb != nullptr) + (dbc != nullptr);
+    if (nb != 0 && nb != 3) return QL_EINVAL;
+    const void *ptrs[] = {x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q)) return QL_EINVAL;
+    const BwdWeightPlan p = plan_bwd_weight(g);
+    if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
+    if (ws && !aligned16(ws)) return QL_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return g.dt == QL_BF16
+               ? launch_bwd_weight<uint16_t>(g, p, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, ws, st)
+               : launch_bwd_weight<float>(g, p, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, ws, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *qlayer_status_string(ql_status s) {
+    switch (s) {
+        case QL_OK: return "ok";
+        case QL_EINVAL: return "invalid argument";
+        case QL_EUNSUPPORTED: return "unsupported configuration";
+        case QL_EWORKSPACE: return "workspace missing or too small";
+        case QL_EHIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+int qlayer_version(void) { return 100; }
+
+size_t qlayer_conv2d_fwd_workspace_size(const ql_conv_desc *desc) {
+    Geom g;
+    if (make_geom(desc, g) != QL_OK) return 0;
+    return plan_fwd(g).ws_bytes;
+}
+
+ql_status qlayer_conv2d_fwd(const ql_conv_desc *desc, const void *x, const void *wa, const void *wb, const void *wc,
+                            const float *ba, const float *bb, const float *bc, void *y, void *ta, void *tb,
+                            void *workspace, size_t workspace_bytes, void *stream) {
+    Geom g;
+    const ql_status s = make_geom(desc, g);
+    if (s != QL_OK) return s;
+    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, workspace, workspace_bytes, stream);
+}
+
+size_t qlayer_conv2d_bwd_data_workspace_size(const ql_conv_desc *desc) {
+    Geom g;
+    if (make_geom(desc, g) != QL_OK) return 0;
+    return plan_bwd_data(g).ws_bytes;
+}
+
+ql_status qlayer_conv2d_bwd_data(const ql_conv_desc *desc, const void *gy, const void *ta, const void *tb,
+                                 const void *wa, const void *wb, const void *wc, void *dx, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    Geom g;
+    const ql_status s = make_geom(desc, g);
+    if (s != QL_OK) return s;
+    return bwd_data_common(g, gy, ta, tb, wa, wb, wc, dx, workspace, workspace_bytes, stream);
+}
+
+size_t qlayer_conv2d_bwd_weight_workspace_size(const ql_conv_desc *desc) {
+    Geom g;
+    if (make_geom(desc, g) != QL_OK) return 0;
+    return plan_bwd_weight(g).ws_bytes;
+}
+
+ql_status qlayer_conv2d_bwd_weight(const ql_conv_desc *desc, const void *x, const void *gy, const void *ta,
+                                   const void *tb, float *dwa, float *dwb, float *dwc, float *dba, float *dbb,
+                                   float *dbc, void *workspace, size_t workspace_bytes, void *stream) {
+    Geom g;
+    const ql_status s = make_geom(desc, g);
+    if (s != QL_OK) return s;
+    return bwd_weight_common(g, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, workspace, workspace_bytes, stream);
+}
+
+size_t qlayer_linear_fwd_workspace_size(const ql_linear_desc *desc) {
+    Geom g;
+    if (linear_geom(desc, g) != QL_OK) return 0;
+    return plan_fwd(g).ws_bytes;
+}
+
+ql_status qlayer_linear_fwd(const ql_linear_desc *desc, const void *x, const void *wa, const void *wb,
+                            const void *wc, const float *ba, const float *bb, const float *bc, void *y, void *ta,
+                            void *tb, void *workspace, size_t workspace_bytes, void *stream) {
+    Geom g;
+    const ql_status s = linear_geom(desc, g);
+    if (s != QL_OK) return s;
+    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, workspace, workspace_bytes, stream);
+}
+
+size_t qlayer_linear_bwd_workspace_size(const ql_linear_desc *desc) {
+    Geom g;
+    if (linear_geom(desc, g) != QL_OK) return 0;
+    return std::max(plan_bwd_data(g).ws_bytes, plan_bwd_weight(g).ws_bytes);
+}
+
+ql_status qlayer_linear_bwd(const ql_linear_desc *desc, const void *x, const void *gy, const void *ta,
+                            const void *tb, const void *wa, const void *wb, const void *wc, void *dx, float *dwa,
+                            float *dwb, float *dwc, float *dba, float *dbb, float *dbc, void *workspace,
+                            size_t workspace_bytes, void *stream) {
+    Geom g;
+    ql_status s = linear_geom(desc, g);
+    if (s != QL_OK) return s;
+    const int nw = (dwa != nullptr) + (dwb != nullptr) + (dwc != nullptr);
+    const int nb = (dba != nullptr) + (dbb != nullptr) + (dbc != nullptr);
+    if ((nw != 0 && nw != 3) || (nb != 0 && nb != 3) || (nb == 3 && nw == 0)) return QL_EINVAL;
+    if (!dx && nw == 0) return QL_EINVAL;
+    if (!x || !gy || !ta || !tb || !wa || !wb || !wc) return QL_EINVAL;
+    // Validate everything before the first launch.
+    const void *ptrs[] = {x, gy, ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q)) return QL_EINVAL;
+    const size_t need = std::max(dx ? plan_bwd_data(g).ws_bytes : 0, nw ? plan_bwd_weight(g).ws_bytes : 0);
+    if (workspace_bytes < need || (need && !workspace)) return QL_EWORKSPACE;
+    if (dx) {
+        s = bwd_data_common(g, gy, ta, tb, wa, wb, wc, dx, workspace, workspace_bytes, stream);
+        if (s != QL_OK) return s;
+    }
+    if (nw) s = bwd_weight_common(g, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, workspace, workspace_bytes, stream);
+    return s;
+}
+
+}  // extern "C"

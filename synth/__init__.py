@@ -169,3 +169,48 @@ LARGE_BF16 = ConvLayer(n=64, c=256, h=56, w=56, o=256, k=3, stride=1, pad=1)
 
 # 5: dense bf16 layer, batch 8192, 4096 -> 4096, W ~ N(0, 1/4096), zero biases.
 DENSE_BF16 = DenseLayer(batch=8192, inp=4096, out=4096, w_var=1.0 / 4096, b_var=0.0)
+
+
+def random_conv_case(seed, N, C, H, W, O, KH, KW, stride=1, pad=0, bf16=False, w_var=None, b_var=0.01):
+    """Seeded inputs of an arbitrary conv geometry (ragged/odd shapes for parity tests).
+
+    X ~ N(0,1), W_t ~ N(0, w_var) (default 1/(C*KH*KW)), b_t ~ N(0, b_var), G ~ N(0,1).
+    """
+    wv = w_var if w_var is not None else 1.0 / (C * KH * KW)
+    Ho = (H + 2 * pad - KH) // stride + 1
+    Wo = (W + 2 * pad - KW) // stride + 1
+    s = list(seed) if isinstance(seed, (list, tuple)) else [seed]
+    out = {
+        "x": _normal(s + [X_ID], (N, C, H, W), 1.0),
+        "wa": _normal(s + [WA_ID], (O, C, KH, KW), np.sqrt(wv)),
+        "wb": _normal(s + [WB_ID], (O, C, KH, KW), np.sqrt(wv)),
+        "wc": _normal(s + [WC_ID], (O, C, KH, KW), np.sqrt(wv)),
+        "ba": _normal(s + [BA_ID], (O,), np.sqrt(b_var)),
+        "bb": _normal(s + [BB_ID], (O,), np.sqrt(b_var)),
+        "bc": _normal(s + [BC_ID], (O,), np.sqrt(b_var)),
+        "gy": _normal(s + [G_ID], (N, O, Ho, Wo), 1.0),
+    }
+    if bf16:
+        for k in ("x", "wa", "wb", "wc", "gy"):
+            out[k] = round_bf16(out[k])
+    return out
+
+
+def random_dense_case(seed, B, I, O, bf16=False, w_var=None, b_var=0.01):
+    """Seeded inputs of an arbitrary dense geometry: X ~ N(0,1), W_t ~ N(0, 1/I), b_t, G ~ N(0,1)."""
+    wv = w_var if w_var is not None else 1.0 / I
+    s = list(seed) if isinstance(seed, (list, tuple)) else [seed]
+    out = {
+        "x": _normal(s + [X_ID], (B, I), 1.0),
+        "wa": _normal(s + [WA_ID], (O, I), np.sqrt(wv)),
+        "wb": _normal(s + [WB_ID], (O, I), np.sqrt(wv)),
+        "wc": _normal(s + [WC_ID], (O, I), np.sqrt(wv)),
+        "ba": _normal(s + [BA_ID], (O,), np.sqrt(b_var)) if b_var > 0 else np.zeros(O, np.float32),
+        "bb": _normal(s + [BB_ID], (O,), np.sqrt(b_var)) if b_var > 0 else np.zeros(O, np.float32),
+        "bc": _normal(s + [BC_ID], (O,), np.sqrt(b_var)) if b_var > 0 else np.zeros(O, np.float32),
+        "gy": _normal(s + [G_ID], (B, O), 1.0),
+    }
+    if bf16:
+        for k in ("x", "wa", "wb", "wc", "gy"):
+            out[k] = round_bf16(out[k])
+    return out

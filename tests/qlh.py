@@ -1,0 +1,128 @@
+"""Test harness: moves seeded inputs to the GPU, runs the C ABI, brings results back.
+
+Layouts: the oracle works on the logical PyTorch layouts (NCHW / OIHW) in
+float64, the library on NHWC / OHWI.  These helpers only permute and convert;
+no arithmetic of the layer happens here.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import paper_2204_01701_amd as ql
+
+DEV = "cuda:0"
+
+
+def tdtype(bf16: bool):
+    return torch.bfloat16 if bf16 else torch.float32
+
+
+def qdtype(bf16: bool):
+    return ql.QL_BF16 if bf16 else ql.QL_F32
+
+
+def nchw_to_dev(a: np.ndarray, bf16: bool) -> torch.Tensor:
+    """(N,C,H,W) float32 numpy -> (N,H,W,C) device tensor; bf16 values must already be bf16-exact."""
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).permute(0, 2, 3, 1).contiguous()
+    return t.to(device=DEV, dtype=tdtype(bf16))
+
+
+def oihw_to_dev(a: np.ndarray, bf16: bool) -> torch.Tensor:
+    return nchw_to_dev(a, bf16)  # (O,C,KH,KW) -> (O,KH,KW,C): the same permutation
+
+
+def vec_to_dev(a, dtype=torch.float32):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV, dtype)
+
+
+def nhwc_to_np(t: torch.Tensor) -> np.ndarray:
+    """(N,H,W,C) device tensor -> (N,C,H,W) float64 numpy."""
+    return t.float().permute(0, 3, 1, 2).contiguous().cpu().numpy().astype(np.float64)
+
+
+def relerr(got, ref) -> float:
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    nr = np.linalg.norm(ref)
+    d = np.linalg.norm(got - ref)
+    return float(d / nr) if nr > 0 else float(d)
+
+
+def run_conv(inp: dict, stride: int, pad: int, bf16: bool, with_bias=True, recompute=False):
+    """Forward (saving T_a, T_b), input gradient and weight/bias gradients on the GPU.
+
+    inp: numpy float32 x (N,C,H,W), wa/wb/wc (O,C,KH,KW), ba/bb/bc (O), gy (N,O,Ho,Wo).
+    Returns the device tensors (NHWC / OHWI) in a dict.
+    """
+    N, C, H, W = inp["x"].shape
+    O, _, KH, KW = inp["wa"].shape
+    d = ql.conv_desc(N, C, H, W, O, KH, KW, stride, pad, qdtype(bf16))
+    dt = tdtype(bf16)
+    x = nchw_to_dev(inp["x"], bf16)
+    w = [oihw_to_dev(inp[k], bf16) for k in ("wa", "wb", "wc")]
+    b = [vec_to_dev(inp[k]) if with_bias else None for k in ("ba", "bb", "bc")]
+    y = torch.empty((N, d.ho, d.wo, O), device=DEV, dtype=dt)
+    ta = torch.empty_like(y)
+    tb = torch.empty_like(y)
+    ql.qlayer_conv2d_fwd(d, x, *w, *b, y, ta, tb)
+    out = {"y": y, "ta": ta, "tb": tb}
+    if recompute:
+        ta2 = torch.empty_like(y)
+        tb2 = torch.empty_like(y)
+        ql.qlayer_conv2d_fwd(d, x, *w, *b, None, ta2, tb2)
+        out["ta_re"], out["tb_re"] = ta2, tb2
+    if "gy" in inp:
+        gy = nchw_to_dev(inp["gy"], bf16)
+        dx = torch.empty_like(x)
+        ql.qlayer_conv2d_bwd_data(d, gy, ta, tb, *w, dx)
+        dw = [torch.empty((O, KH, KW, C), device=DEV, dtype=torch.float32) for _ in range(3)]
+        db = [torch.empty(O, device=DEV, dtype=torch.float32) for _ in range(3)]
+        ql.qlayer_conv2d_bwd_weight(d, x, gy, ta, tb, *dw, *db)
+        out.update({"dx": dx, "dwa": dw[0], "dwb": dw[1], "dwc": dw[2], "dba": db[0], "dbb": db[1],
+                    "dbc": db[2]})
+    torch.cuda.synchronize()
+    return out
+
+
+def conv_to_np(out: dict) -> dict:
+    """Device results -> float64 numpy in the oracle's layouts."""
+    res = {}
+    for k, v in out.items():
+        if v.dim() == 4:
+            res[k] = nhwc_to_np(v)
+        else:
+            res[k] = v.double().cpu().numpy()
+    return res
+
+
+def run_linear(inp: dict, bf16: bool):
+    B, I = inp["x"].shape
+    O = inp["wa"].shape[0]
+    d = ql.linear_desc(B, I, O, qdtype(bf16))
+    dt = tdtype(bf16)
+    x = torch.from_numpy(inp["x"]).to(DEV, dt)
+    w = [torch.from_numpy(inp[k]).to(DEV, dt) for k in ("wa", "wb", "wc")]
+    b = [vec_to_dev(inp[k]) for k in ("ba", "bb", "bc")]
+    y = torch.empty((B, O), device=DEV, dtype=dt)
+    ta, tb = torch.empty_like(y), torch.empty_like(y)
+    ql.qlayer_linear_fwd(d, x, *w, *b, y, ta, tb)
+    out = {"y": y, "ta": ta, "tb": tb}
+    if "gy" in inp:
+        gy = torch.from_numpy(inp["gy"]).to(DEV, dt)
+        dx = torch.empty_like(x)
+        dw = [torch.empty((O, I), device=DEV, dtype=torch.float32) for _ in range(3)]
+        db = [torch.empty(O, device=DEV, dtype=torch.float32) for _ in range(3)]
+        ql.qlayer_linear_bwd(d, x, gy, ta, tb, *w, dx, *dw, *db)
+        out.update({"dx": dx, "dwa": dw[0], "dwb": dw[1], "dwc": dw[2], "dba": db[0], "dbb": db[1],
+                    "dbc": db[2]})
+    torch.cuda.synchronize()
+    return out
+
+
+# Normwise relative error limits: fp32 forward 1e-5, gradients 1e-4; bf16 inputs with
+# fp32 accumulation 2e-2 for both.
+def tol(bf16: bool, grad: bool) -> float:
+    if bf16:
+        return 2e-2
+    return 1e-4 if grad else 1e-5

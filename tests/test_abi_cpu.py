@@ -1,0 +1,165 @@
+"""Host-side checks of the C ABI that need no GPU.
+
+* the library builds for gfx950 and exports every function include/qlayer.h declares;
+* invalid arguments are rejected on the host, before anything is launched;
+* workspace-size queries and status strings;
+* the division-by-invariant helper the kernels use for index arithmetic.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2204_01701_amd as ql
+from paper_2204_01701_amd import build as qbuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qlayer.h")
+
+QL_OK, QL_EINVAL, QL_EUNSUPPORTED, QL_EWORKSPACE, QL_EHIP = range(5)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if qbuild.is_stale():
+        qbuild.build()
+    return ql.lib()
+
+
+def _declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(qlayer_\w+)\s*\(", txt)))
+
+
+def test_header_declares_the_five_entry_points():
+    names = _declared_functions()
+    for f in ("qlayer_conv2d_fwd", "qlayer_conv2d_bwd_data", "qlayer_conv2d_bwd_weight",
+              "qlayer_linear_fwd", "qlayer_linear_bwd"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", ql.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (qlayer_\w+)", out))
+    missing = [f for f in _declared_functions() if f not in exported]
+    assert not missing, missing
+    for f in _declared_functions():
+        assert getattr(L, f) is not None
+
+
+def test_status_strings_and_version(L):
+    assert ql.qlayer_status_string(QL_OK) == "ok"
+    assert "invalid" in ql.qlayer_status_string(QL_EINVAL)
+    assert "workspace" in ql.qlayer_status_string(QL_EWORKSPACE)
+    assert ql.qlayer_version() >= 100
+
+
+FAKE = 1 << 20  # a 16-byte aligned fake device address; never dereferenced by these calls
+
+
+def _fwd(L, d, x=FAKE, wa=FAKE, wb=FAKE, wc=FAKE, y=FAKE, ta=None, tb=None, ws=None, wsb=0):
+    return L.qlayer_conv2d_fwd(ctypes.byref(d), x, wa, wb, wc, None, None, None, y, ta, tb, ws, wsb, None)
+
+
+def test_conv_descriptor_validation(L):
+    good = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32)
+    bad = [
+        ql.conv_desc(0, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32),       # n = 0
+        ql.conv_desc(2, 16, 8, 8, -1, 3, 3, 1, 1, ql.QL_F32),       # o < 0
+        ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 0, 1, ql.QL_F32),       # stride 0
+        ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, -1, ql.QL_F32),      # pad < 0
+        ql.conv_desc(2, 16, 2, 2, 16, 5, 5, 1, 0, ql.QL_F32),       # empty output
+        ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, 7),               # unknown dtype
+    ]
+    for d in bad:
+        assert _fwd(L, d) == QL_EINVAL
+        assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d)) == 0
+    assert L.qlayer_conv2d_fwd(None, FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, None, None, None, 0,
+                               None) == QL_EINVAL
+    # required pointers
+    assert _fwd(L, good, x=None) == QL_EINVAL
+    assert _fwd(L, good, wb=None) == QL_EINVAL
+    assert _fwd(L, good, y=None) == QL_EINVAL                      # no Y and no terms
+    assert _fwd(L, good, y=None, ta=FAKE) == QL_EINVAL             # recompute needs both terms
+    assert _fwd(L, good, x=FAKE + 4) == QL_EINVAL                  # misaligned
+    # oversize: more than 2^31 - 1 elements in one tensor
+    huge = ql.conv_desc(1 << 12, 1 << 10, 32, 32, 16, 3, 3, 1, 1, ql.QL_BF16)
+    assert _fwd(L, huge) == QL_EUNSUPPORTED
+
+
+def test_backward_validation(L):
+    d = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32)
+    ws = L.qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(d))
+    assert ws >= 3 * 16 * 9 * 16 * 4                                  # holds the transposed weights
+    args = [FAKE] * 7
+    assert L.qlayer_conv2d_bwd_data(ctypes.byref(d), *args, FAKE, ws - 1, None) == QL_EWORKSPACE
+    assert L.qlayer_conv2d_bwd_data(ctypes.byref(d), *args, None, ws, None) == QL_EWORKSPACE
+    args[1] = None                                                    # T_a missing
+    assert L.qlayer_conv2d_bwd_data(ctypes.byref(d), *args, FAKE, ws, None) == QL_EINVAL
+    # weight gradients: biases all or none
+    w = [FAKE] * 7
+    assert L.qlayer_conv2d_bwd_weight(ctypes.byref(d), *w, FAKE, None, None, FAKE, 1 << 30, None) == QL_EINVAL
+    assert L.qlayer_conv2d_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, None, None,
+                                      None, FAKE, 1 << 30, None) == QL_EINVAL
+    # dense backward: at least one output, dW all-or-none, db needs dW
+    dl = ql.linear_desc(64, 32, 48, ql.QL_BF16)
+    base = [FAKE] * 7
+    assert L.qlayer_linear_bwd(ctypes.byref(dl), *base, None, None, None, None, None, None, None,
+                               FAKE, 1 << 30, None) == QL_EINVAL
+    assert L.qlayer_linear_bwd(ctypes.byref(dl), *base, FAKE, FAKE, None, None, None, None, None,
+                               FAKE, 1 << 30, None) == QL_EINVAL
+    assert L.qlayer_linear_bwd(ctypes.byref(dl), *base, FAKE, None, None, None, FAKE, FAKE, FAKE,
+                               FAKE, 1 << 30, None) == QL_EINVAL
+
+
+def test_workspace_queries_are_consistent(L):
+    # split-K only where the output tiles cannot fill the GPU
+    big = ql.conv_desc(64, 256, 56, 56, 256, 3, 3, 1, 1, ql.QL_BF16)
+    small = ql.conv_desc(128, 512, 2, 2, 512, 3, 3, 1, 1, ql.QL_BF16)
+    assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(big)) == 0
+    assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(small)) > 0
+    assert L.qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(big)) > 0
+    dl = ql.linear_desc(8192, 4096, 4096, ql.QL_BF16)
+    need = L.qlayer_linear_bwd_workspace_size(ctypes.byref(dl))
+    assert need >= 3 * 4096 * 4096 * 2
+    for f in ("conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight"):
+        assert getattr(L, f"qlayer_{f}_workspace_size")(ctypes.byref(big)) % 256 == 0
+
+
+def test_fastdiv_host_formula(tmp_path):
+    """The multiply-shift division used for index arithmetic is exact (checked on the host)."""
+    src = tmp_path / "fd.cpp"
+    src.write_text(r'''
+#include "qfastdiv.h"
+#include <cstdio>
+#include <cstdint>
+int main() {
+    const uint32_t ds[] = {1, 2, 3, 5, 7, 9, 16, 27, 56, 64, 100, 576, 1000, 3136, 4096, 12544,
+                           200704, 262144, 1u << 20, 65537, 2147483647u};
+    uint64_t x = 88172645463325252ull;
+    for (uint32_t d : ds) {
+        ql::FastDiv f = ql::make_fastdiv(d);
+        for (int i = 0; i < 200000; ++i) {
+            x ^= x << 13; x ^= x >> 7; x ^= x << 17;
+            uint32_t n = (uint32_t)x;
+            if (i % 3 == 0) n &= 0x7fffffffu;
+            if (i < 4096) n = (uint32_t)i;
+            if (ql::fdiv_host(n, f) != n / d) { std::printf("FAIL d=%u n=%u\n", d, n); return 1; }
+        }
+        const uint32_t edge[] = {d - 1, d, d + 1, 2 * d - 1, 0xffffffffu, 0x7fffffffu};
+        for (uint32_t n : edge)
+            if (ql::fdiv_host(n, f) != n / d) { std::printf("FAIL d=%u n=%u\n", d, n); return 1; }
+    }
+    std::printf("ok\n");
+    return 0;
+}
+''')
+    exe = tmp_path / "fd"
+    subprocess.run(["g++", "-O2", "-std=c++17", "-I", os.path.join(ROOT, "paper_2204_01701_amd", "csrc"),
+                    str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert out.returncode == 0 and out.stdout.strip() == "ok", out.stdout
