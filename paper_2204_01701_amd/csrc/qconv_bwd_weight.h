@@ -1,60 +1,49 @@
 // qconv_bwd_weight.h -- weight and bias gradients of the quadratic convolution
-// layer (arXiv 2204.01701, section 4.3, eq:SD):
+// layer (arXiv 2204.01701, section 4.3, eq:SD), pipelined bf16 kernel:
 //
 //   dW_t[o,r,q,c] = sum_{n,i,j} G_t[n,i,j,o] X[n, i*s-p+r, j*s-p+q, c]
 //   db_t[o]       = sum_{n,i,j} G_t[n,i,j,o]
 //   G_a = G o T_b,  G_b = G o T_a,  G_c = G
 //
 // ONE implicit GEMM for the three terms, reducing over the output pixels:
-//
-//   rows    : k' = (r, q, c)           (operand: im2col of X)
-//   columns : (t, o), three blocks      (operand: G_t, formed in the prologue)
-//   K       : output pixels m = (n, i, j), split over workgroups
-//
-// Both operands arrive pixel-major (NHWC), so the staging threads load
-// PX pixels x VEC channels, form the G_t products in fp32 (accumulating the
-// bias sums on the way), transpose the block in registers and write
-// pixel-contiguous LDS rows.  Split-K partials go to a workspace and are
-// reduced in split order by a second kernel, so the result is deterministic.
+//   rows    : k' = (r, q, c)        (operand: im2col of X)
+//   columns : (t, o), three blocks   (operand: G_t)
+//   K       : output pixels m, split over workgroups
+// Both operands are pixel-major in memory (NHWC), so each K step copies
+// pixel rows unchanged into "natural" LDS tiles (qpipe.h) and the MFMA
+// fragments are read with ds_read_b64_tr_b16, which transposes on the way
+// out of LDS.  The G o T_b / G o T_a products are formed in fp32 on the
+// fragments; the bias sums are accumulated from the same fp32 values.  Split-K
+// partials go to a workspace reduced in split order (deterministic).
 #pragma once
 
-#include "qdevice.h"
+#include "qargs.h"
+#include "qpipe.h"
 
 namespace ql {
 
-struct BwdWeightArgs {
-    const void *x, *gy, *ta, *tb;
-    float *dw[3];
-    float *db[3];
-    float *ws_dw;  // [split][3][O][KP]
-    float *ws_db;  // [split][3][O]
-    int N, H, W, C, O, KH, KW, SH, SW, PH, PW, HO, WO;
-    int M, KP;  // M = N*HO*WO output pixels (reduction), KP = KH*KW*C
-    int row_tiles, col_tiles, splits, stages_per_split, stages_total;
-    int want_db;
-    FastDiv fd_howo, fd_wo, fd_c, fd_kw;
-};
-
-template <typename T, int BKP, int BO, int WGR, int WGC, int BKB, int PXG, bool VECK>
+template <int BKP, int BO, int WGR, int WGC, int NS>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWeightArgs a) {
-    constexpr int VEC = Elem<T>::VEC;
-    constexpr int ES = (int)sizeof(T);
-    constexpr int KE = BKB / ES;    // output pixels per K step
-    constexpr int PXX = 16 / ES;    // pixels per X staging job (one 16-byte LDS write per channel)
-    constexpr int PITCH = BKB + 16;
-    constexpr int ROWS = BKP + 3 * BO;
-    constexpr int NKV = BKP / VEC, NOV = BO / VEC;
-    constexpr int NJX = NKV * (KE / PXX);  // X jobs: PXX pixels x VEC channels
-    constexpr int NJG = NOV * (KE / PXG);  // G jobs: PXG pixels x VEC output channels, three terms
+    using T = uint16_t;                 // bf16 only: the transposed LDS read is 16-bit
+    constexpr int KE = 32;              // output pixels per K step (two MFMA k-chunks)
+    constexpr int SX = BKP / 8;         // 16-byte slots per X row
+    constexpr int SG = BO / 8;          // 16-byte slots per G / T_a / T_b row
+    constexpr int XB = KE * BKP * 2;    // bytes of the X tile
+    constexpr int GB = KE * BO * 2;     // bytes of each G-side tile
+    constexpr int STAGE = XB + 3 * GB;
+    constexpr int NIX = XB / 4096;      // DMA instructions per thread per K step
+    constexpr int NIG = GB / 4096;
+    constexpr int NI = NIX + 3 * NIG;
+    constexpr int RX = 64 / SX;         // rows one wave-instruction fills
+    constexpr int RG = 64 / SG;
     constexpr int MR = BKP / WGR / 32, MC = BO / WGC / 32;
     static_assert(WGR * WGC == kThreads / 64, "one wave per wave-tile");
-    static_assert(NJX + NJG <= kThreads, "one staging job per thread");
-    static_assert(PXG * ES == 8 || PXG * ES == 16, "G staging writes 8 or 16 bytes");
-    static_assert(MR >= 1 && MC >= 1 && BKB % 32 == 0 && KE % PXX == 0 && KE % PXG == 0, "tile shape");
+    static_assert(XB % 4096 == 0 && GB % 4096 == 0 && SX <= 64 && SG <= 64, "whole DMA rounds");
+    static_assert(MR >= 1 && MC >= 1, "tile shape");
 
-    __shared__ __attribute__((aligned(16))) char smem[2 * ROWS * PITCH];
+    __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
     const int wr = wave / WGC, wc = wave % WGC;
     int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int tiles = a.row_tiles * a.col_tiles;
@@ -62,164 +51,50 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
     bid -= split * tiles;
     const int rt = bid % a.row_tiles, ct = bid / a.row_tiles;
     const int s_begin = split * a.stages_per_split;
-    const int s_end = min(s_begin + a.stages_per_split, a.stages_total);
-    const bool do_db = a.want_db && rt == 0;
+    const int nst = min(a.stages_per_split, a.stages_total - s_begin);
 
     const T *__restrict__ x = static_cast<const T *>(a.x);
-    const T *__restrict__ gy = static_cast<const T *>(a.gy);
-    const T *__restrict__ gta = static_cast<const T *>(a.ta);
-    const T *__restrict__ gtb = static_cast<const T *>(a.tb);
+    const T *__restrict__ gsrc[3] = {static_cast<const T *>(a.gy), static_cast<const T *>(a.ta),
+                                     static_cast<const T *>(a.tb)};
 
-    const bool is_x = tid < NJX;
-    const bool is_g = !is_x && tid < NJX + NJG;
-    // X job: channels kv*VEC.. of row tile, pixels pg*PXX.. of each K step.
-    const int jx = tid, kv = jx % NKV, pgx = jx / NKV;
-    // G job: output channels ov*VEC.., pixels pg*PXG.. of each K step.
-    const int jg = tid - NJX, ov = jg % NOV, pgg = jg / NOV;
-
-    // X job geometry (fixed): the VEC rows k' = kbase + e.
-    const int kbase = rt * BKP + kv * VEC;
-    int xr[VEC], xq[VEC], xc[VEC];
-    bool xk[VEC];
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-        const int kk = VECK ? kbase : kbase + e;  // VECK: one tap for all VEC channels
-        const int tap = (int)fdiv((uint32_t)kk, a.fd_c);
-        xc[e] = kk - tap * a.C + (VECK ? e : 0);
-        xr[e] = (int)fdiv((uint32_t)tap, a.fd_kw);
-        xq[e] = tap - xr[e] * a.KW;
-        xk[e] = kbase + e < a.KP;
+    // X fill: instruction i of this wave writes rows RX * (4 i + wave) .. +RX;
+    // this lane fills row RX * (4 i + wave) + lane / SX at a fixed logical slot.
+    const int xslot = (lane % SX) ^ nat_swz<SX>(lane / SX);
+    const int kp = rt * BKP + 8 * xslot;  // first of the 8 k' this lane copies
+    const bool kp_ok = kp < a.KP;
+    int xr, xq, xc;
+    {
+        const int tap = (int)fdiv((uint32_t)kp, a.fd_c);
+        xc = kp - tap * a.C;
+        xr = (int)fdiv((uint32_t)tap, a.fd_kw);
+        xq = tap - xr * a.KW;
     }
-    const int obase = ct * BO + ov * VEC;
+    // G fill: same scheme with rows of SG slots.
+    const int gslot = (lane % SG) ^ nat_swz<SG>(lane / SG);
+    const int og = ct * BO + 8 * gslot;
+    const bool og_ok = og < a.O;
 
-    v4u rx[PXX];
-    v4u rg[3][PXG];
-    float dsum[3][VEC];
+    auto issue = [&](int s, int slot) {
+        char *base = smem + slot * STAGE + wave * 1024;
 #pragma unroll
-    for (int t = 0; t < 3; ++t)
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) dsum[t][e] = 0.0f;
-
-    auto load_stage = [&](int s) {
-        if (is_x) {
-            const int m0 = s * KE + pgx * PXX;
-            int n = (int)fdiv((uint32_t)m0, a.fd_howo);
-            const int rem = m0 - n * a.HO * a.WO;
-            int oh = (int)fdiv((uint32_t)rem, a.fd_wo);
-            int ow = rem - oh * a.WO;
-#pragma unroll
-            for (int p = 0; p < PXX; ++p) {
-                const bool mok = m0 + p < a.M;
-                const int ih0 = oh * a.SH - a.PH, iw0 = ow * a.SW - a.PW;
-                const size_t nb = (size_t)n * a.H;
-                if constexpr (VECK) {
-                    const int ih = ih0 + xr[0], iw = iw0 + xq[0];
-                    const bool ok = mok && xk[0] && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-                    rx[p] = ld16(x + ((nb + ih) * a.W + iw) * a.C + xc[0], ok);
-                } else {
-                    struct alignas(16) V { T e[VEC]; } v;
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        const int ih = ih0 + xr[e], iw = iw0 + xq[e];
-                        const bool ok =
-                            mok && xk[e] && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-                        v.e[e] = ok ? x[((nb + ih) * a.W + iw) * a.C + xc[e]] : T(0);
-                    }
-                    rx[p] = __builtin_bit_cast(v4u, v);
-                }
-                if (++ow == a.WO) {
-                    ow = 0;
-                    if (++oh == a.HO) {
-                        oh = 0;
-                        ++n;
-                    }
-                }
-            }
-        } else if (is_g) {
-            const int m0 = s * KE + pgg * PXG;
-#pragma unroll
-            for (int p = 0; p < PXG; ++p) {
-                const int m = m0 + p;
-                const size_t off = (size_t)m * a.O + obase;
-                if constexpr (VECK) {
-                    const bool ok = m < a.M && obase < a.O;
-                    rg[0][p] = ld16(gy + off, ok);
-                    rg[1][p] = ld16(gta + off, ok);
-                    rg[2][p] = ld16(gtb + off, ok);
-                } else {
-                    struct alignas(16) V { T e[VEC]; } v0, v1, v2;
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        const bool ok = m < a.M && obase + e < a.O;
-                        v0.e[e] = ok ? gy[off + e] : T(0);
-                        v1.e[e] = ok ? gta[off + e] : T(0);
-                        v2.e[e] = ok ? gtb[off + e] : T(0);
-                    }
-                    rg[0][p] = __builtin_bit_cast(v4u, v0);
-                    rg[1][p] = __builtin_bit_cast(v4u, v1);
-                    rg[2][p] = __builtin_bit_cast(v4u, v2);
-                }
-            }
+        for (int i = 0; i < NIX; ++i) {
+            const int m = s * KE + RX * (4 * i + wave) + lane / SX;
+            const int n = (int)fdiv((uint32_t)m, a.fd_howo);
+            const int rem = m - n * a.HO * a.WO;
+            const int oh = (int)fdiv((uint32_t)rem, a.fd_wo);
+            const int ow = rem - oh * a.WO;
+            const int ih = oh * a.SH - a.PH + xr, iw = ow * a.SW - a.PW + xq;
+            const bool ok = kp_ok && m < a.M && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+            dma16(dma_src(ok, x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + xc, a.zero), base + i * 4096);
         }
-    };
-
-    auto store_stage = [&](int b) {
-        char *base = smem + b * ROWS * PITCH;
-        if (is_x) {
-            // PXX pixels x VEC channels -> VEC rows of PXX pixel values (16 bytes each).
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                uint32_t d[4];
-                if constexpr (ES == 2) {
+        for (int i = 0; i < NIG; ++i) {
+            const int m = s * KE + RG * (4 * i + wave) + lane / SG;
+            const bool ok = og_ok && m < a.M;
+            const size_t off = (size_t)m * a.O + og;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) d[i] = vraw<T>(rx[2 * i], e) | (vraw<T>(rx[2 * i + 1], e) << 16);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) d[i] = vraw<T>(rx[i], e);
-                }
-                lds_write16(base + (kv * VEC + e) * PITCH + pgx * 16, v4u{d[0], d[1], d[2], d[3]});
-            }
-        } else if (is_g) {
-            // Prologue (eq:SD) in fp32, bias sums, then transpose to pixel-contiguous rows.
-            float gv[3][PXG][VEC];
-#pragma unroll
-            for (int p = 0; p < PXG; ++p)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    const float g = vget<T>(rg[0][p], e);
-                    gv[0][p][e] = g * vget<T>(rg[2][p], e);
-                    gv[1][p][e] = g * vget<T>(rg[1][p], e);
-                    gv[2][p][e] = g;
-                }
-#pragma unroll
-            for (int t = 0; t < 3; ++t)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    float sacc = 0.0f;
-#pragma unroll
-                    for (int p = 0; p < PXG; ++p) sacc += gv[t][p][e];
-                    dsum[t][e] += sacc;
-                    char *dst = base + (BKP + t * BO + ov * VEC + e) * PITCH + pgg * PXG * ES;
-                    if constexpr (ES == 2) {
-                        uint32_t d[PXG / 2];
-#pragma unroll
-                        for (int i = 0; i < PXG / 2; ++i)
-                            d[i] = (t == 2) ? (vraw<T>(rg[0][2 * i], e) | (vraw<T>(rg[0][2 * i + 1], e) << 16))
-                                            : pack_bf16x2(gv[t][2 * i][e], gv[t][2 * i + 1][e]);
-                        if constexpr (PXG == 4)
-                            *reinterpret_cast<v2u *>(dst) = v2u{d[0], d[1]};
-                        else
-                            lds_write16(dst, v4u{d[0], d[1], d[2], d[3]});
-                    } else {
-                        uint32_t d[PXG];
-#pragma unroll
-                        for (int i = 0; i < PXG; ++i) d[i] = __float_as_uint(gv[t][i][e]);
-                        if constexpr (PXG == 4)
-                            lds_write16(dst, v4u{d[0], d[1], d[2], d[3]});
-                        else
-                            *reinterpret_cast<v2u *>(dst) = v2u{d[0], d[1]};
-                    }
-                }
+            for (int u = 0; u < 3; ++u)
+                dma16(dma_src(ok, gsrc[u] + off, a.zero), base + XB + u * GB + i * 4096);
         }
     };
 
@@ -232,51 +107,63 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
             for (int mc = 0; mc < MC; ++mc)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[t][mr][mc][v] = 0.0f;
+    float dsum[3][MC];
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) dsum[t][mc] = 0.0f;
+    const bool sum_db = a.want_db && rt == 0 && wr == 0;
 
-    const int lrow = lane & 31, lhi = lane >> 5;
-    auto compute_stage = [&](int b) {
-        const char *base = smem + b * ROWS * PITCH;
+    v4u af[2][MR], gr[2][3][MC];  // two register sets: X and G, T_a, T_b fragments
+    auto read = [&](int slot, int ch, int set) {
+        const char *xt = smem + slot * STAGE;
+        const char *gt = xt + XB;
 #pragma unroll
-        for (int ch = 0; ch < BKB / 32; ++ch) {
-            const int coff = ch * 32 + lhi * 16;
-            v4u af[MR];
+        for (int mr = 0; mr < MR; ++mr) af[set][mr] = nat_frag_bf16<SX>(xt, 16 * ch, wr * (BKP / WGR) + mr * 32, lane);
 #pragma unroll
-            for (int mr = 0; mr < MR; ++mr)
-                af[mr] = lds_read16(base + (wr * (BKP / WGR) + mr * 32 + lrow) * PITCH + coff);
+        for (int mc = 0; mc < MC; ++mc)
+#pragma unroll
+            for (int u = 0; u < 3; ++u)
+                gr[set][u][mc] = nat_frag_bf16<SG>(gt + u * GB, 16 * ch, wc * (BO / WGC) + mc * 32, lane);
+    };
+    // Prologue products and bias sums in fp32, then the MFMAs.
+    auto mma = [&](int set) {
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) {
+            const v4u &g = gr[set][0][mc], &ta = gr[set][1][mc], &tb = gr[set][2][mc];
+            float fa[8], fb[8];
+            float sa = 0.0f, sb = 0.0f, sc = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float gv = vget<T>(g, e);
+                fa[e] = gv * vget<T>(tb, e);
+                fb[e] = gv * vget<T>(ta, e);
+                sa += fa[e];
+                sb += fb[e];
+                sc += gv;
+            }
+            if (sum_db) {
+                dsum[0][mc] += sa;
+                dsum[1][mc] += sb;
+                dsum[2][mc] += sc;
+            }
+            const v4u bt[3] = {vpack<T>(fa), vpack<T>(fb), g};
 #pragma unroll
             for (int t = 0; t < 3; ++t)
 #pragma unroll
-                for (int mc = 0; mc < MC; ++mc) {
-                    const v4u bf =
-                        lds_read16(base + (BKP + t * BO + wc * (BO / WGC) + mc * 32 + lrow) * PITCH + coff);
-#pragma unroll
-                    for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[mr], bf, acc[t][mr][mc]);
-                }
+                for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[set][mr], bt[t], acc[t][mr][mc]);
         }
     };
+    run_ring<NS, NI>(nst, s_begin, issue, read, mma);
 
-    if (s_begin < s_end) {
-        load_stage(s_begin);
-        store_stage(0);
-        __syncthreads();
-        for (int s = s_begin; s < s_end; ++s) {
-            const int b = (s - s_begin) & 1;
-            const bool more = s + 1 < s_end;
-            if (more) load_stage(s + 1);
-            compute_stage(b);
-            if (more) store_stage(b ^ 1);
-            __syncthreads();
-        }
-    }
-
-    // dW epilogue: rows k', columns o.  Lane holds 4 consecutive k' per group.
+    // dW epilogue: rows k', columns o; lane holds 4 consecutive k' per group.
     const int krow0 = rt * BKP + wr * (BKP / WGR);
     const int ocol0 = ct * BO + wc * (BO / WGC);
+    const int lrow = lane & 31, lhi = lane >> 5;
     const bool vec_out = (a.KP & 3) == 0;
 #pragma unroll
     for (int t = 0; t < 3; ++t) {
-        float *__restrict__ dst =
-            a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * a.KP;
+        float *__restrict__ dst = a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * a.KP;
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
@@ -300,58 +187,21 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
             }
     }
 
-    // Bias gradients: the G staging threads hold per-channel sums over their
-    // pixels; add them up across the pixel groups in a fixed order.
-    if (do_db) {
-        constexpr int NPG = KE / PXG;
-        float *red = reinterpret_cast<float *>(smem);  // [NPG][3][BO]; LDS is free after the last barrier
-        static_assert(NPG * 3 * BO * 4 <= 2 * ROWS * PITCH, "bias scratch fits");
-        if (is_g) {
+    // Bias gradients: lanes l and l + 32 hold the two pixel halves of channel l % 32.
+    if (sum_db) {
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+        for (int t = 0; t < 3; ++t)
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) red[(pgg * 3 + t) * BO + ov * VEC + e] = dsum[t][e];
-        }
-        __syncthreads();
-        for (int i = tid; i < 3 * BO; i += kThreads) {
-            const int t = i / BO, ol = i % BO;
-            const int o = ct * BO + ol;
-            if (o >= a.O) continue;
-            float s = 0.0f;
-            for (int pg = 0; pg < NPG; ++pg) s += red[(pg * 3 + t) * BO + ol];
-            if (a.splits == 1)
-                a.db[t][o] = s;
-            else
-                a.ws_db[((size_t)split * 3 + t) * a.O + o] = s;
-        }
-    }
-}
-
-// Split-K reduction of dW_t and db_t partials, in split order.
-__global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce_kernel(const float *__restrict__ ws_dw,
-                                                                           const float *__restrict__ ws_db,
-                                                                           int splits, long long ndw, int O,
-                                                                           float *dw0, float *dw1, float *dw2,
-                                                                           float *db0, float *db1, float *db2,
-                                                                           int want_db) {
-    const long long total = 3 * ndw + (want_db ? 3LL * O : 0LL);
-    for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-         idx += (long long)gridDim.x * blockDim.x) {
-        if (idx < 3 * ndw) {
-            const int t = (int)(idx / ndw);
-            const long long i = idx - t * ndw;
-            float s = 0.0f;
-            for (int sp = 0; sp < splits; ++sp) s += ws_dw[((size_t)sp * 3 + t) * ndw + i];
-            float *d = t == 0 ? dw0 : (t == 1 ? dw1 : dw2);
-            d[i] = s;
-        } else {
-            const long long j = idx - 3 * ndw;
-            const int t = (int)(j / O), o = (int)(j % O);
-            float s = 0.0f;
-            for (int sp = 0; sp < splits; ++sp) s += ws_db[((size_t)sp * 3 + t) * O + o];
-            float *d = t == 0 ? db0 : (t == 1 ? db1 : db2);
-            d[o] = s;
-        }
+            for (int mc = 0; mc < MC; ++mc) {
+                const float tot = dsum[t][mc] + __shfl_xor(dsum[t][mc], 32);
+                const int o = ocol0 + mc * 32 + lrow;
+                if (lhi == 0 && o < a.O) {
+                    if (a.splits == 1)
+                        a.db[t][o] = tot;
+                    else
+                        a.ws_db[((size_t)split * 3 + t) * a.O + o] = tot;
+                }
+            }
     }
 }
 

@@ -1,57 +1,41 @@
 // qconv_fwd.h -- forward of the quadratic convolution layer (arXiv 2204.01701,
-// section 3.1, eq:2ndneuron3), as ONE implicit GEMM with the three per-term
-// weights packed side by side:
+// section 3.1, eq:2ndneuron3), pipelined kernel for channel counts that are a
+// multiple of the 16-byte vector.
 //
+// ONE implicit GEMM with the three per-term weights packed side by side:
 //   rows    : output channels o, three row blocks per tile (W_a | W_b | W_c)
 //   columns : output pixels m = (n, oh, ow)
-//   K       : (r, q, c), contiguous in c for both NHWC X and OHWI W_t
-//
-// The im2col tile of X is staged in LDS once per K step and feeds all three
-// terms.  Each lane ends up holding T_a, T_b and T_c for the same (m, o), so
-// the product and sum Y = T_a o T_b + T_c (with the biases preloaded into the
-// accumulators) are applied in registers and only Y (plus, when requested,
-// T_a and T_b) is written to HBM.  T_c never leaves the registers.
-//
-// For layers with few output pixels the K range is split over workgroups;
-// the raw partial sums then go to a workspace and a second kernel applies the
-// biases and the product (the epilogue is not linear, so it must follow the
-// full sum).
+//   K       : (r, q, c), contiguous in c for NHWC X and OHWI W_t
+// Each K step moves 64 bytes of every tile row straight from global memory
+// into a ring of NS LDS stages (qpipe.h); the im2col tile of X is staged once
+// and feeds all three terms.  The biases are preloaded into the accumulators
+// and the epilogue forms Y = T_a o T_b + T_c in registers, so only Y (and,
+// when requested, T_a and T_b) is written to HBM.  T_c never leaves the
+// registers.  With split-K the raw partial sums go to a workspace instead and
+// qconv_fwd_combine_kernel applies the biases and the product.
 #pragma once
 
-#include "qdevice.h"
+#include "qargs.h"
+#include "qpipe.h"
 
 namespace ql {
 
-struct FwdArgs {
-    const void *x;
-    const void *w[3];
-    const float *bias[3];
-    void *y, *ta, *tb;
-    float *ws;  // split-K partials [split][3][M][O]
-    int N, H, W, C, O, KH, KW, SH, SW, PH, PW, HO, WO;
-    int M, K;  // GEMM extents: M = N*HO*WO pixels, K = KH*KW*C
-    int row_tiles, col_tiles, splits, stages_per_split, stages_total;
-    FastDiv fd_howo, fd_wo, fd_c, fd_kw;
-};
-
-template <typename T, int BR, int BCOL, int WGR, int WGC, int BKB, bool VECK>
+template <typename T, int BR, int BCOL, int WGR, int WGC, int NS>
 __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
     constexpr int VEC = Elem<T>::VEC;
-    constexpr int NB = BKB / 16;  // 16-byte vectors per row per K step
-    constexpr int KE = NB * VEC;  // reduction elements per K step
-    constexpr int PITCH = BKB + 16;
+    constexpr int KE = 64 / (int)sizeof(T);  // reduction elements per K step
     constexpr int ROWS = 3 * BR + BCOL;
-    constexpr int RSTEP = kThreads / NB;          // rows covered by one pass of the workgroup
-    constexpr int NVT = BR * NB / kThreads;       // weight vectors per thread per term
-    constexpr int NVP = BCOL * NB / kThreads;     // pixel vectors per thread
+    constexpr int STAGE = ROWS * 64;
+    constexpr int NIW = 3 * BR / 64;  // DMA instructions per thread per K step: weight rows
+    constexpr int NIX = BCOL / 64;    // ... pixel rows
+    constexpr int NI = NIW + NIX;
     constexpr int MR = BR / WGR / 32, MC = BCOL / WGC / 32;
     static_assert(WGR * WGC == kThreads / 64, "one wave per wave-tile");
-    static_assert((BR * NB) % kThreads == 0 && (BCOL * NB) % kThreads == 0, "even load split");
-    static_assert(MR >= 1 && MC >= 1 && BKB % 32 == 0, "tile shape");
+    static_assert(BR % 64 == 0 && BCOL % 64 == 0 && MR >= 1 && MC >= 1, "tile shape");
 
-    __shared__ __attribute__((aligned(16))) char smem[2 * ROWS * PITCH];
+    __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
     const int wr = wave / WGC, wc = wave % WGC;
     int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int tiles = a.row_tiles * a.col_tiles;
@@ -59,27 +43,31 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
     bid -= split * tiles;
     const int rt = bid % a.row_tiles, ct = bid / a.row_tiles;
     const int s_begin = split * a.stages_per_split;
-    const int s_end = min(s_begin + a.stages_per_split, a.stages_total);
+    const int nst = min(a.stages_per_split, a.stages_total - s_begin);
 
     const T *__restrict__ x = static_cast<const T *>(a.x);
-    const T *__restrict__ w0 = static_cast<const T *>(a.w[0]);
-    const T *__restrict__ w1 = static_cast<const T *>(a.w[1]);
-    const T *__restrict__ w2 = static_cast<const T *>(a.w[2]);
+    const T *wp[3] = {static_cast<const T *>(a.w[0]), static_cast<const T *>(a.w[1]),
+                      static_cast<const T *>(a.w[2])};
 
-    const int c16 = tid % NB;
-    const int rsub = tid / NB;
-
-    // Load descriptors, fixed for the whole K loop.
-    int woff[NVT];
+    // Fill geometry: DMA instruction i of this wave writes tile rows
+    // 16 * (4 i + wave) .. +16; this lane fills row 16 * (4 i + wave) + lane / 4,
+    // logical 16-byte column kcol (the same for every instruction).
+    const int kcol = km_fill_col(lane);
+    int woff[NIW];
+    int wterm[NIW];
 #pragma unroll
-    for (int j = 0; j < NVT; ++j) {
-        const int o = rt * BR + rsub + j * RSTEP;
-        woff[j] = (o < a.O) ? o * a.K : -1;
+    for (int i = 0; i < NIW; ++i) {
+        const int row = 16 * (4 * i + wave) + (lane >> 2);
+        const int t = row / BR;
+        const int o = rt * BR + (row - t * BR);
+        wterm[i] = t;
+        woff[i] = o < a.O ? o * a.K : -1;
     }
-    int xoff[NVP], ih0[NVP], iw0[NVP];
+    int xoff[NIX], ih0[NIX], iw0[NIX];
 #pragma unroll
-    for (int j = 0; j < NVP; ++j) {
-        const int m = ct * BCOL + rsub + j * RSTEP;
+    for (int j = 0; j < NIX; ++j) {
+        const int p = 16 * (4 * (NIW + j) + wave) + (lane >> 2) - 3 * BR;
+        const int m = ct * BCOL + p;
         if (m < a.M) {
             const int n = (int)fdiv((uint32_t)m, a.fd_howo);
             const int rem = m - n * a.HO * a.WO;
@@ -95,79 +83,28 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
         }
     }
 
-    v4u rw[3][NVT], rx[NVP];
-
-    auto load_stage = [&](int s) {
-        const int k = s * KE + c16 * VEC;
-        if constexpr (VECK) {
-            // C % VEC == 0: the VEC elements share one tap (r, q).
-            const bool kin = k < a.K;
-            const int tap = (int)fdiv((uint32_t)k, a.fd_c);
-            const int c = k - tap * a.C;
-            const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
-            const int q = tap - r * a.KW;
+    auto issue = [&](int s, int slot) {
+        char *base = smem + slot * STAGE + wave * 1024;
+        const int k = s * KE + kcol * VEC;
+        const bool kin = k < a.K;
+        const int tap = (int)fdiv((uint32_t)k, a.fd_c);
+        const int c = k - tap * a.C;
+        const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
+        const int q = tap - r * a.KW;
 #pragma unroll
-            for (int j = 0; j < NVT; ++j) {
-                const bool ok = kin && woff[j] >= 0;
-                rw[0][j] = ld16(w0 + woff[j] + k, ok);
-                rw[1][j] = ld16(w1 + woff[j] + k, ok);
-                rw[2][j] = ld16(w2 + woff[j] + k, ok);
-            }
+        for (int i = 0; i < NIW; ++i) {
+            const bool ok = kin && woff[i] >= 0;
+            dma16(dma_src(ok, wp[wterm[i]] + woff[i] + k, a.zero), base + i * 4096);
+        }
 #pragma unroll
-            for (int j = 0; j < NVP; ++j) {
-                const int ih = ih0[j] + r, iw = iw0[j] + q;
-                const bool ok = kin && xoff[j] >= 0 && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-                rx[j] = ld16(x + xoff[j] + (ih * a.W + iw) * a.C + c, ok);
-            }
-        } else {
-            // General C: every element decodes its own (r, q, c).
-            struct alignas(16) V { T e[VEC]; };
-            V vw[3][NVT], vx[NVP];
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                const int ke = k + e;
-                const bool kin = ke < a.K;
-                const int tap = (int)fdiv((uint32_t)ke, a.fd_c);
-                const int c = ke - tap * a.C;
-                const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
-                const int q = tap - r * a.KW;
-#pragma unroll
-                for (int j = 0; j < NVT; ++j) {
-                    const bool ok = kin && woff[j] >= 0;
-                    vw[0][j].e[e] = ok ? w0[woff[j] + ke] : T(0);
-                    vw[1][j].e[e] = ok ? w1[woff[j] + ke] : T(0);
-                    vw[2][j].e[e] = ok ? w2[woff[j] + ke] : T(0);
-                }
-#pragma unroll
-                for (int j = 0; j < NVP; ++j) {
-                    const int ih = ih0[j] + r, iw = iw0[j] + q;
-                    const bool ok =
-                        kin && xoff[j] >= 0 && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-                    vx[j].e[e] = ok ? x[xoff[j] + (ih * a.W + iw) * a.C + c] : T(0);
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < NVT; ++j)
-#pragma unroll
-                for (int t = 0; t < 3; ++t) rw[t][j] = __builtin_bit_cast(v4u, vw[t][j]);
-#pragma unroll
-            for (int j = 0; j < NVP; ++j) rx[j] = __builtin_bit_cast(v4u, vx[j]);
+        for (int j = 0; j < NIX; ++j) {
+            const int ih = ih0[j] + r, iw = iw0[j] + q;
+            const bool ok = kin && xoff[j] >= 0 && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+            dma16(dma_src(ok, x + xoff[j] + (ih * a.W + iw) * a.C + c, a.zero), base + (NIW + j) * 4096);
         }
     };
 
-    auto store_stage = [&](int b) {
-        char *base = smem + b * ROWS * PITCH;
-#pragma unroll
-        for (int t = 0; t < 3; ++t)
-#pragma unroll
-            for (int j = 0; j < NVT; ++j)
-                lds_write16(base + (t * BR + rsub + j * RSTEP) * PITCH + c16 * 16, rw[t][j]);
-#pragma unroll
-        for (int j = 0; j < NVP; ++j)
-            lds_write16(base + (3 * BR + rsub + j * RSTEP) * PITCH + c16 * 16, rx[j]);
-    };
-
-    // Accumulators; the biases are preloaded when the whole K range is ours.
+    // Accumulators, biases preloaded when this workgroup owns the whole K range.
     f32x16_t acc[3][MR][MC];
     const int lrow = lane & 31, lhi = lane >> 5;
     const int orow0 = rt * BR + wr * (BR / WGR);
@@ -187,39 +124,30 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
         }
     }
 
-    auto compute_stage = [&](int b) {
-        const char *base = smem + b * ROWS * PITCH;
+    // Fragment reads: row lrow of each 32-row block, logical column 2 * ch + lhi.
+    const int swz = (lrow >> 2) & 3;
+    const int colx0 = ((0 + lhi) ^ swz) << 4, colx1 = ((2 + lhi) ^ swz) << 4;
+    v4u bf[2][MC], af[2][3][MR];  // two register sets of fragments
+    auto read = [&](int slot, int ch, int set) {
+        const char *base = smem + slot * STAGE + lrow * 64 + (ch == 0 ? colx0 : colx1);
 #pragma unroll
-        for (int ch = 0; ch < BKB / 32; ++ch) {
-            const int coff = ch * 32 + lhi * 16;
-            v4u bf[MC];
+        for (int mc = 0; mc < MC; ++mc)
+            bf[set][mc] = lds_read16(base + (3 * BR + wc * (BCOL / WGC) + mc * 32) * 64);
 #pragma unroll
-            for (int mc = 0; mc < MC; ++mc)
-                bf[mc] = lds_read16(base + (3 * BR + wc * (BCOL / WGC) + mc * 32 + lrow) * PITCH + coff);
+        for (int t = 0; t < 3; ++t)
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
-#pragma unroll
-                for (int mr = 0; mr < MR; ++mr) {
-                    const v4u af = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32 + lrow) * PITCH + coff);
-#pragma unroll
-                    for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af, bf[mc], acc[t][mr][mc]);
-                }
-        }
+            for (int mr = 0; mr < MR; ++mr)
+                af[set][t][mr] = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32) * 64);
     };
-
-    if (s_begin < s_end) {
-        load_stage(s_begin);
-        store_stage(0);
-        __syncthreads();
-        for (int s = s_begin; s < s_end; ++s) {
-            const int b = (s - s_begin) & 1;
-            const bool more = s + 1 < s_end;
-            if (more) load_stage(s + 1);
-            compute_stage(b);
-            if (more) store_stage(b ^ 1);
-            __syncthreads();
-        }
-    }
+    auto mma = [&](int set) {
+#pragma unroll
+        for (int t = 0; t < 3; ++t)
+#pragma unroll
+            for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+                for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af[set][t][mr], bf[set][mc], acc[t][mr][mc]);
+    };
+    run_ring<NS, NI>(nst, s_begin, issue, read, mma);
 
     // Epilogue.
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
@@ -287,30 +215,6 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
                     }
                 }
         }
-    }
-}
-
-// Split-K epilogue: T_t = b_t + sum of the partials (in split order), then
-// Y = T_a o T_b + T_c.  One thread per output element.
-template <typename T>
-__global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float *__restrict__ ws, int splits,
-                                                                     long long MO, int O, const float *b0,
-                                                                     const float *b1, const float *b2, T *y, T *ta,
-                                                                     T *tb) {
-    for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < MO;
-         idx += (long long)gridDim.x * blockDim.x) {
-        const int o = (int)(idx % O);
-        float t3[3];
-        const float *bp[3] = {b0, b1, b2};
-#pragma unroll
-        for (int t = 0; t < 3; ++t) {
-            float s = 0.0f;
-            for (int sp = 0; sp < splits; ++sp) s += ws[((size_t)sp * 3 + t) * MO + idx];
-            t3[t] = (bp[t] ? bp[t][o] : 0.0f) + s;
-        }
-        if (y) y[idx] = from_f32<T>(t3[0] * t3[1] + t3[2]);
-        if (ta) ta[idx] = from_f32<T>(t3[0]);
-        if (tb) tb[idx] = from_f32<T>(t3[1]);
     }
 }
 

@@ -12,6 +12,27 @@
 #include "qconv_bwd_data.h"
 #include "qconv_bwd_weight.h"
 #include "qconv_fwd.h"
+#include "qconv_generic.h"
+
+namespace ql {
+// The 16 zero bytes masked-off lanes of the pipelined kernels load.
+__device__ __attribute__((aligned(16))) uint32_t g_zero16[4] = {0u, 0u, 0u, 0u};
+}  // namespace ql
+
+namespace {
+// Device address of g_zero16 on the current device (resolved once per device).
+const void *zero_page() {
+    static const void *addr[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    if (!addr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(ql::g_zero16)) != hipSuccess) return nullptr;
+        addr[dev] = p;
+    }
+    return addr[dev];
+}
+}  // namespace
 
 using namespace ql;
 
@@ -22,6 +43,13 @@ constexpr int kTargetBlocks = 2 * kNumCUs;
 constexpr size_t kAlign = 256;
 constexpr long long kMaxElems = (1LL << 31) - 1;  // 32-bit element offsets in the kernels
 constexpr size_t kMaxFwdSplitBytes = 48ull << 20;
+
+// Tuning override: QLAYER_<NAME>=<int> replaces a planner choice (for sweeps).
+int env_override(const char *name, int dflt) {
+    const char *v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    return std::atoi(v);
+}
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -76,8 +104,14 @@ void plan_splits(int tiles, int stages_total, int min_stages, int &splits, int &
 // ---------------------------------------------------------------------------
 // Forward planning.
 // ---------------------------------------------------------------------------
+// Pipelined forward tile configurations (rows = output channels per term,
+// columns = output pixels; per-wave tile in parentheses):
+//   0: 128 x 128 (32 x 128), 1: 64 x 256 (32 x 128), 2: 128 x 128 (64 x 64), 3: 64 x 128 (32 x 64).
+constexpr int kFwdBR[4] = {128, 64, 128, 64};
+constexpr int kFwdBCOL[4] = {128, 256, 128, 128};
+
 struct FwdPlan {
-    int cfg;  // 0: BR=128 BCOL=128, 1: BR=64 BCOL=128
+    int cfg;  // pipelined: index into kFwd*; generic: 0: 128 x 128, 1: 64 x 128
     int BR, BCOL, KE;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
@@ -87,11 +121,18 @@ struct FwdPlan {
 FwdPlan plan_fwd(const Geom &g) {
     FwdPlan p{};
     const int M = g.N * g.HO * g.WO, K = g.KH * g.KW * g.C;
-    p.cfg = g.O <= 64 ? 1 : 0;
-    p.BR = p.cfg == 0 ? 128 : 64;
-    p.BCOL = 128;
-    p.KE = 64 / (int)g.esize();
     p.veck = g.C % g.vec() == 0;
+    if (p.veck) {
+        p.cfg = env_override("QLAYER_FWD_CFG", g.O <= 64 ? 1 : 0);
+        if (p.cfg < 0 || p.cfg > 3) p.cfg = 0;
+        p.BR = kFwdBR[p.cfg];
+        p.BCOL = kFwdBCOL[p.cfg];
+    } else {
+        p.cfg = g.O <= 64 ? 1 : 0;
+        p.BR = p.cfg == 0 ? 128 : 64;
+        p.BCOL = 128;
+    }
+    p.KE = 64 / (int)g.esize();
     p.row_tiles = cdiv(g.O, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
@@ -108,8 +149,13 @@ FwdPlan plan_fwd(const Geom &g) {
 // ---------------------------------------------------------------------------
 // Input-gradient planning.  Workspace: transposed weights, then split partials.
 // ---------------------------------------------------------------------------
+// Pipelined input-gradient tile configurations (rows = input channels,
+// columns = input pixels):  0: 128 x 128, 1: 64 x 128, 2: 128 x 64.
+constexpr int kBdBR[3] = {128, 64, 128};
+constexpr int kBdBCOL[3] = {128, 128, 64};
+
 struct BwdDataPlan {
-    int cfg;  // 0: BR=128 BCOL=128, 1: BR=64 BCOL=128
+    int cfg;  // pipelined: index into kBd*; generic: 0: 128 x 128, 1: 64 x 128
     int BR, BCOL, KE;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck, s1;
@@ -119,11 +165,18 @@ struct BwdDataPlan {
 BwdDataPlan plan_bwd_data(const Geom &g) {
     BwdDataPlan p{};
     const int M = g.N * g.H * g.W, K = g.KH * g.KW * g.O;
-    p.cfg = g.C <= 64 ? 1 : 0;
-    p.BR = p.cfg == 0 ? 128 : 64;
-    p.BCOL = 128;
-    p.KE = 64 / (int)g.esize();
     p.veck = g.O % g.vec() == 0;
+    if (p.veck) {
+        p.cfg = env_override("QLAYER_BWD_DATA_CFG", g.C <= 64 ? 1 : 0);
+        if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
+        p.BR = kBdBR[p.cfg];
+        p.BCOL = kBdBCOL[p.cfg];
+    } else {
+        p.cfg = g.C <= 64 ? 1 : 0;
+        p.BR = p.cfg == 0 ? 128 : 64;
+        p.BCOL = 128;
+    }
+    p.KE = 64 / (int)g.esize();
     p.s1 = g.SH == 1 && g.SW == 1;
     p.row_tiles = cdiv(g.C, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
@@ -138,7 +191,14 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
 // ---------------------------------------------------------------------------
 // Weight-gradient planning.  Workspace: dW partials, then db partials.
 // ---------------------------------------------------------------------------
+// Pipelined (bf16) weight-gradient tile configurations (rows = k', columns =
+// output channels per term):  0: 128 x 64, 1: 128 x 128, 2: 64 x 64.
+constexpr int kBwBKP[3] = {128, 128, 64};
+constexpr int kBwBO[3] = {64, 128, 64};
+
 struct BwdWeightPlan {
+    int cfg;   // pipelined path only
+    bool pipe; // bf16 and vectorizable: pipelined kernel; otherwise the generic one
     int BKP, BO, KE;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
@@ -148,14 +208,23 @@ struct BwdWeightPlan {
 BwdWeightPlan plan_bwd_weight(const Geom &g) {
     BwdWeightPlan p{};
     const int M = g.N * g.HO * g.WO, KP = g.KH * g.KW * g.C;
-    p.BKP = 128;
-    p.BO = 64;
-    p.KE = 64 / (int)g.esize();
     p.veck = g.C % g.vec() == 0 && g.O % g.vec() == 0;
+    p.pipe = p.veck && g.dt == QL_BF16;
+    if (p.pipe) {
+        p.cfg = env_override("QLAYER_BWD_WEIGHT_CFG", g.O <= 64 ? 0 : 1);
+        if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
+        p.BKP = kBwBKP[p.cfg];
+        p.BO = kBwBO[p.cfg];
+    } else {
+        p.BKP = 128;
+        p.BO = 64;
+    }
+    p.KE = 64 / (int)g.esize();
     p.row_tiles = cdiv(KP, p.BKP);
     p.col_tiles = cdiv(g.O, p.BO);
     p.stages_total = cdiv(M, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 8, p.splits, p.sps);
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16),
+                p.splits, p.sps);
     if (p.splits > 1) {
         p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KP * sizeof(float));
         p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));
@@ -187,6 +256,8 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     a.bias[0] = ba; a.bias[1] = bb; a.bias[2] = bc;
     a.y = y; a.ta = ta; a.tb = tb;
     a.ws = static_cast<float *>(ws);
+    a.zero = zero_page();
+    if (!a.zero) return QL_EHIP;
     a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
     a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
     a.M = g.N * g.HO * g.WO;
@@ -198,18 +269,18 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     a.fd_c = make_fastdiv(g.C);
     a.fd_kw = make_fastdiv(g.KW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
-#define QL_FWD(BR, BCOL, WGR, WGC)                                                                      \
-    do {                                                                                                \
-        if (p.veck)                                                                                     \
-            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BCOL, WGR, WGC, 64, true>), grid, block, 0, st, a);  \
-        else                                                                                            \
-            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BCOL, WGR, WGC, 64, false>), grid, block, 0, st, a); \
-    } while (0)
-    if (p.cfg == 0)
-        QL_FWD(128, 128, 2, 2);
-    else
-        QL_FWD(64, 128, 2, 2);
-#undef QL_FWD
+    if (p.veck) {
+        switch (p.cfg) {
+            case 0: hipLaunchKernelGGL((qconv_fwd_kernel<T, 128, 128, 4, 1, 4>), grid, block, 0, st, a); break;
+            case 1: hipLaunchKernelGGL((qconv_fwd_kernel<T, 64, 256, 2, 2, 4>), grid, block, 0, st, a); break;
+            case 2: hipLaunchKernelGGL((qconv_fwd_kernel<T, 128, 128, 2, 2, 4>), grid, block, 0, st, a); break;
+            default: hipLaunchKernelGGL((qconv_fwd_kernel<T, 64, 128, 2, 2, 4>), grid, block, 0, st, a); break;
+        }
+    } else if (p.cfg == 0) {
+        hipLaunchKernelGGL((qconv_fwd_generic_kernel<T, 128, 128, 2, 2, 64, false>), grid, block, 0, st, a);
+    } else {
+        hipLaunchKernelGGL((qconv_fwd_generic_kernel<T, 64, 128, 2, 2, 64, false>), grid, block, 0, st, a);
+    }
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long MO = (long long)a.M * g.O;
@@ -235,6 +306,8 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.wt[0] = wt; a.wt[1] = wt + wsz; a.wt[2] = wt + 2 * wsz;
     a.dx = dx;
     a.ws = reinterpret_cast<float *>(static_cast<char *>(ws) + p.wt_bytes);
+    a.zero = zero_page();
+    if (!a.zero) return QL_EHIP;
     a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
     a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
     a.M = g.N * g.H * g.W;
@@ -248,21 +321,36 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.fd_sh = make_fastdiv(g.SH);
     a.fd_sw = make_fastdiv(g.SW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
-#define QL_BWD_DATA_S(BR, BCOL, VK, S1) \
-    hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, 64, VK, S1>), grid, block, 0, st, a)
-#define QL_BWD_DATA(BR, BCOL)                          \
-    do {                                               \
-        if (p.veck && p.s1) QL_BWD_DATA_S(BR, BCOL, true, true);        \
-        else if (p.veck) QL_BWD_DATA_S(BR, BCOL, true, false);          \
-        else if (p.s1) QL_BWD_DATA_S(BR, BCOL, false, true);            \
-        else QL_BWD_DATA_S(BR, BCOL, false, false);                     \
+#define QL_BD_PIPE(BR, BCOL, NS)                                                                            \
+    do {                                                                                                    \
+        if (p.s1)                                                                                           \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true>), grid, block, 0, st, a);  \
+        else                                                                                                \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, false>), grid, block, 0, st, a); \
     } while (0)
-    if (p.cfg == 0)
-        QL_BWD_DATA(128, 128);
-    else
-        QL_BWD_DATA(64, 128);
-#undef QL_BWD_DATA
-#undef QL_BWD_DATA_S
+#define QL_BD_GEN(BR, BCOL)                                                                                      \
+    do {                                                                                                         \
+        if (p.s1)                                                                                                \
+            hipLaunchKernelGGL((qconv_bwd_data_generic_kernel<T, BR, BCOL, 2, 2, 64, false, true>), grid, block, 0, \
+                               st, a);                                                                           \
+        else                                                                                                     \
+            hipLaunchKernelGGL((qconv_bwd_data_generic_kernel<T, BR, BCOL, 2, 2, 64, false, false>), grid, block, \
+                               0, st, a);                                                                        \
+    } while (0)
+    if (p.veck) {
+        if (p.cfg == 0)
+            QL_BD_PIPE(128, 128, 3);
+        else if (p.cfg == 1)
+            QL_BD_PIPE(64, 128, 4);
+        else
+            QL_BD_PIPE(128, 64, 4);
+    } else if (p.cfg == 0) {
+        QL_BD_GEN(128, 128);
+    } else {
+        QL_BD_GEN(64, 128);
+    }
+#undef QL_BD_PIPE
+#undef QL_BD_GEN
     s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long total = (long long)a.M * g.C;
@@ -281,6 +369,8 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     a.db[0] = dba; a.db[1] = dbb; a.db[2] = dbc;
     a.ws_dw = static_cast<float *>(ws);
     a.ws_db = reinterpret_cast<float *>(static_cast<char *>(ws) + p.dw_bytes);
+    a.zero = zero_page();
+    if (!a.zero) return QL_EHIP;
     a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
     a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
     a.M = g.N * g.HO * g.WO;
@@ -293,10 +383,22 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     a.fd_c = make_fastdiv(g.C);
     a.fd_kw = make_fastdiv(g.KW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
-    if (p.veck)
-        hipLaunchKernelGGL((qconv_bwd_weight_kernel<T, 128, 64, 2, 2, 64, 4, true>), grid, block, 0, st, a);
-    else
-        hipLaunchKernelGGL((qconv_bwd_weight_kernel<T, 128, 64, 2, 2, 64, 4, false>), grid, block, 0, st, a);
+    if constexpr (sizeof(T) == 2) {
+        if (p.pipe) {
+            switch (p.cfg) {
+                case 0: hipLaunchKernelGGL((qconv_bwd_weight_kernel<128, 64, 2, 2, 4>), grid, block, 0, st, a); break;
+                case 1: hipLaunchKernelGGL((qconv_bwd_weight_kernel<128, 128, 2, 2, 4>), grid, block, 0, st, a); break;
+                default: hipLaunchKernelGGL((qconv_bwd_weight_kernel<64, 64, 2, 2, 4>), grid, block, 0, st, a); break;
+            }
+        }
+    }
+    if (!p.pipe) {
+        if (p.veck)
+            hipLaunchKernelGGL((qconv_bwd_weight_generic_kernel<T, 128, 64, 2, 2, 64, 4, true>), grid, block, 0, st, a);
+        else
+            hipLaunchKernelGGL((qconv_bwd_weight_generic_kernel<T, 128, 64, 2, 2, 64, 4, false>), grid, block, 0, st,
+                               a);
+    }
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long ndw = (long long)g.O * a.KP;
