@@ -7,8 +7,12 @@
 //   dX[n,h,w,c] = sum_t sum_{r,q,o} G_t[n,i,j,o] W_t[o,r,q,c],  i*s - p + r = h, j*s - p + q = w
 //
 // ONE implicit GEMM reducing over (t, r, q, o):
-//   rows    : input channels c        (W_t pre-transposed to C x KH x KW x O)
+//   rows    : input channels c        (operand: W_t)
 //   columns : input pixels (n, h, w)  (G, T_a, T_b gathered at the output pixel of each tap)
+// With NATW (bf16, C a multiple of 8) each K step copies the weight rows
+// W_t[o, r, q, c0 .. c0 + BR) unchanged into natural LDS tiles and reads the
+// operand fragments with ds_read_b64_tr_b16; otherwise the weights come
+// pre-transposed to C x KH x KW x O and are staged K-contiguous.
 // Per K step the three weight tiles and the G, T_a and T_b tiles are copied
 // into the LDS ring (qpipe.h).  The products G o T_b and G o T_a are formed
 // in fp32 on the MFMA operand fragments right after they are read from LDS,
@@ -36,8 +40,9 @@ __device__ __forceinline__ void prologue_frag(const v4u &g, const v4u &ta, const
     gb = vpack<T>(fb);
 }
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool S1>
+template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool S1, bool NATW>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataArgs a) {
+    static_assert(!NATW || sizeof(T) == 2, "natural weight tiles need 16-bit elements");
     constexpr int VEC = Elem<T>::VEC;
     constexpr int KE = 64 / (int)sizeof(T);
     constexpr int ROWS = 3 * BR + 3 * BCOL;
@@ -67,6 +72,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
                       static_cast<const T *>(a.wt[2])};
 
     const int kcol = km_fill_col(lane);
+    // K-contiguous (pre-transposed) weight rows: row = input channel.
     int woff[NIW];
 #pragma unroll
     for (int i = 0; i < NIW; ++i) {
@@ -74,6 +80,13 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         const int c = rt * BR + (row - ((64 * i) / BR) * BR);
         woff[i] = c < a.C ? c * a.K : -1;
     }
+    // Natural weight tiles: KE rows (K indices) of BR channels per term.
+    constexpr int SW = BR / 8;          // 16-byte slots per weight row
+    constexpr int WT = KE * BR * 2;     // bytes of one term's weight tile
+    const int wslot = (lane % SW) ^ nat_swz<SW>(lane / SW);
+    const int wc0 = rt * BR + 8 * wslot;
+    const bool wc_ok = wc0 < a.C;
+    const int khkw = a.KH * a.KW;
     int goff[NIP], hh[NIP], ww[NIP];
 #pragma unroll
     for (int j = 0; j < NIP; ++j) {
@@ -101,10 +114,23 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         const int o = k - tap * a.O;
         const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
         const int q = tap - r * a.KW;
+        if constexpr (NATW) {
 #pragma unroll
-        for (int i = 0; i < NIW; ++i) {
-            const bool ok = kin && woff[i] >= 0;
-            dma16(dma_src(ok, wt[(64 * i) / BR] + woff[i] + k, a.zero), base + i * 4096);
+            for (int i = 0; i < NIW; ++i) {
+                const int t = (i * 4096) / WT;
+                const int row = ((i * 4096) % WT + wave * 1024) / (SW * 16) + lane / SW;
+                const int kr = s * KE + row;
+                const int tapr = (int)fdiv((uint32_t)kr, a.fd_o);
+                const int orow = kr - tapr * a.O;
+                const bool ok = wc_ok && kr < a.K;
+                dma16(dma_src(ok, wt[t] + ((size_t)(orow * khkw + tapr) * a.C + wc0), a.zero), base + i * 4096);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < NIW; ++i) {
+                const bool ok = kin && woff[i] >= 0;
+                dma16(dma_src(ok, wt[(64 * i) / BR] + woff[i] + k, a.zero), base + i * 4096);
+            }
         }
 #pragma unroll
         for (int j = 0; j < NIP; ++j) {
@@ -147,11 +173,20 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
 #pragma unroll
             for (int u = 0; u < 3; ++u) gr[set][u][mc] = lds_read16(base + (3 * BR + u * BCOL + prow) * 64);
         }
+        if constexpr (NATW) {
+            const char *wtile = smem + slot * STAGE;
 #pragma unroll
-        for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < 3; ++t)
 #pragma unroll
-            for (int mr = 0; mr < MR; ++mr)
-                af[set][t][mr] = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32) * 64);
+                for (int mr = 0; mr < MR; ++mr)
+                    af[set][t][mr] = nat_frag_bf16<SW>(wtile + t * WT, 16 * ch, wr * (BR / WGR) + mr * 32, lane);
+        } else {
+#pragma unroll
+            for (int t = 0; t < 3; ++t)
+#pragma unroll
+                for (int mr = 0; mr < MR; ++mr)
+                    af[set][t][mr] = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32) * 64);
+        }
     };
     // The prologue products are formed on the G-side fragments, then the MFMAs.
     auto mma = [&](int set) {

@@ -1,8 +1,7 @@
 // qconv_generic.h -- register-staged kernels of the quadratic layer for the
 // shapes the pipelined kernels do not take (channel counts that are not a
 // multiple of the 16-byte vector, e.g. 3-channel image inputs) and for the
-// fp32 weight gradient, plus the auxiliary kernels shared by both paths
-// (split-K combine/reductions and the weight transpose).
+// fp32 weight gradient.
 //
 // Forward (arXiv 2204.01701, section 3.1 eq:2ndneuron3): one implicit GEMM
 // for the three terms with the product and sum in the accumulator epilogue.
@@ -275,30 +274,6 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
     }
 }
 
-// Split-K epilogue: T_t = b_t + sum of the partials (in split order), then
-// Y = T_a o T_b + T_c.  One thread per output element.
-template <typename T>
-__global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float *__restrict__ ws, int splits,
-                                                                     long long MO, int O, const float *b0,
-                                                                     const float *b1, const float *b2, T *y, T *ta,
-                                                                     T *tb) {
-    for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < MO;
-         idx += (long long)gridDim.x * blockDim.x) {
-        const int o = (int)(idx % O);
-        float t3[3];
-        const float *bp[3] = {b0, b1, b2};
-#pragma unroll
-        for (int t = 0; t < 3; ++t) {
-            float s = 0.0f;
-            for (int sp = 0; sp < splits; ++sp) s += ws[((size_t)sp * 3 + t) * MO + idx];
-            t3[t] = (bp[t] ? bp[t][o] : 0.0f) + s;
-        }
-        if (y) y[idx] = from_f32<T>(t3[0] * t3[1] + t3[2]);
-        if (ta) ta[idx] = from_f32<T>(t3[0]);
-        if (tb) tb[idx] = from_f32<T>(t3[1]);
-    }
-}
-
 template <typename T, int BR, int BCOL, int WGR, int WGC, int BKB, bool VECK, bool S1>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const BwdDataArgs a) {
     constexpr int VEC = Elem<T>::VEC;
@@ -557,43 +532,6 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
                 }
             }
         }
-}
-
-// Split-K reduction of dX partials, in split order.
-template <typename T>
-__global__ __launch_bounds__(kThreads) void qconv_bwd_data_reduce_kernel(const float *__restrict__ ws, int splits,
-                                                                         long long total, T *__restrict__ dx) {
-    for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-         idx += (long long)gridDim.x * blockDim.x) {
-        float s = 0.0f;
-        for (int sp = 0; sp < splits; ++sp) s += ws[(size_t)sp * total + idx];
-        dx[idx] = from_f32<T>(s);
-    }
-}
-
-// Per-term weight transpose O x KH x KW x C -> C x KH x KW x O (LDS-tiled,
-// 32 x 32 tiles, both sides coalesced).  grid: (ceil(C/32), ceil(O/32), 3*KH*KW).
-template <typename T>
-__global__ __launch_bounds__(kThreads) void qconv_weight_transpose_kernel(const T *__restrict__ w0,
-                                                                          const T *__restrict__ w1,
-                                                                          const T *__restrict__ w2,
-                                                                          T *__restrict__ out, int O, int KHKW,
-                                                                          int C) {
-    __shared__ T tile[32][33];
-    const int t = blockIdx.z / KHKW, tap = blockIdx.z % KHKW;
-    const T *w = t == 0 ? w0 : (t == 1 ? w1 : w2);
-    T *dst = out + (size_t)t * O * KHKW * C;
-    const int c0 = blockIdx.x * 32, o0 = blockIdx.y * 32;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
-    for (int i = ty; i < 32; i += 8) {
-        const int o = o0 + i, c = c0 + tx;
-        if (o < O && c < C) tile[i][tx] = w[((size_t)o * KHKW + tap) * C + c];
-    }
-    __syncthreads();
-    for (int i = ty; i < 32; i += 8) {
-        const int c = c0 + i, o = o0 + tx;
-        if (o < O && c < C) dst[((size_t)c * KHKW + tap) * O + o] = tile[tx][i];
-    }
 }
 
 template <typename T, int BKP, int BO, int WGR, int WGC, int BKB, int PXG, bool VECK>
@@ -884,34 +822,6 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
                 a.db[t][o] = s;
             else
                 a.ws_db[((size_t)split * 3 + t) * a.O + o] = s;
-        }
-    }
-}
-
-// Split-K reduction of dW_t and db_t partials, in split order.
-__global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce_kernel(const float *__restrict__ ws_dw,
-                                                                           const float *__restrict__ ws_db,
-                                                                           int splits, long long ndw, int O,
-                                                                           float *dw0, float *dw1, float *dw2,
-                                                                           float *db0, float *db1, float *db2,
-                                                                           int want_db) {
-    const long long total = 3 * ndw + (want_db ? 3LL * O : 0LL);
-    for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-         idx += (long long)gridDim.x * blockDim.x) {
-        if (idx < 3 * ndw) {
-            const int t = (int)(idx / ndw);
-            const long long i = idx - t * ndw;
-            float s = 0.0f;
-            for (int sp = 0; sp < splits; ++sp) s += ws_dw[((size_t)sp * 3 + t) * ndw + i];
-            float *d = t == 0 ? dw0 : (t == 1 ? dw1 : dw2);
-            d[i] = s;
-        } else {
-            const long long j = idx - 3 * ndw;
-            const int t = (int)(j / O), o = (int)(j % O);
-            float s = 0.0f;
-            for (int sp = 0; sp < splits; ++sp) s += ws_db[((size_t)sp * 3 + t) * O + o];
-            float *d = t == 0 ? db0 : (t == 1 ? db1 : db2);
-            d[o] = s;
         }
     }
 }

@@ -9,6 +9,7 @@
 #include <cstdlib>
 
 #include "qlayer.h"
+#include "qconv_aux.h"
 #include "qconv_bwd_data.h"
 #include "qconv_bwd_weight.h"
 #include "qconv_fwd.h"
@@ -39,10 +40,10 @@ using namespace ql;
 namespace {
 
 constexpr int kNumCUs = 256;         // MI355X compute units
-constexpr int kTargetBlocks = 2 * kNumCUs;
+constexpr int kTargetBlocks = kNumCUs;  // split-K aims at one workgroup per CU
 constexpr size_t kAlign = 256;
 constexpr long long kMaxElems = (1LL << 31) - 1;  // 32-bit element offsets in the kernels
-constexpr size_t kMaxFwdSplitBytes = 48ull << 20;
+constexpr size_t kMaxSplitBytes = 32ull << 20;  // cap on split-K partial sums (written + read once)
 
 // Tuning override: QLAYER_<NAME>=<int> replaces a planner choice (for sweeps).
 int env_override(const char *name, int dflt) {
@@ -91,11 +92,14 @@ ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
     return make_geom(&c, g);
 }
 
-// Split-K planning: enough workgroups to fill the chip twice over.
-void plan_splits(int tiles, int stages_total, int min_stages, int &splits, int &sps) {
+// Split-K planning: enough workgroups for one per CU, at least min_stages K
+// steps per split, and at most max_bytes of partial sums (bytes_per_split each).
+void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int &splits, int &sps) {
     splits = 1;
-    if (tiles < kTargetBlocks && stages_total > min_stages) {
-        splits = std::min(cdiv(kTargetBlocks, tiles), std::max(1, stages_total / min_stages));
+    if (tiles < kTargetBlocks && stages_total >= 2 * min_stages) {
+        splits = std::min(cdiv(kTargetBlocks, tiles), stages_total / min_stages);
+        const int cap = (int)std::max<size_t>(1, kMaxSplitBytes / std::max<size_t>(bytes_per_split, 1));
+        splits = std::max(1, std::min(splits, cap));
     }
     sps = cdiv(stages_total, splits);
     splits = cdiv(stages_total, sps);
@@ -123,8 +127,8 @@ FwdPlan plan_fwd(const Geom &g) {
     const int M = g.N * g.HO * g.WO, K = g.KH * g.KW * g.C;
     p.veck = g.C % g.vec() == 0;
     if (p.veck) {
-        p.cfg = env_override("QLAYER_FWD_CFG", g.O <= 64 ? 1 : 0);
-        if (p.cfg < 0 || p.cfg > 3) p.cfg = 0;
+        p.cfg = env_override("QLAYER_FWD_CFG", 3);
+        if (p.cfg < 0 || p.cfg > 3) p.cfg = 3;
         p.BR = kFwdBR[p.cfg];
         p.BCOL = kFwdBCOL[p.cfg];
     } else {
@@ -136,12 +140,7 @@ FwdPlan plan_fwd(const Geom &g) {
     p.row_tiles = cdiv(g.O, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, p.splits, p.sps);
-    // Keep the split partials modest: they cost HBM/L2 traffic.
-    while (p.splits > 1 && (size_t)p.splits * 3 * M * g.O * 4 > kMaxFwdSplitBytes) {
-        p.sps = cdiv(p.stages_total, p.splits - 1);
-        p.splits = cdiv(p.stages_total, p.sps);
-    }
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)3 * M * g.O * 4, p.splits, p.sps);
     p.ws_bytes = p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0;
     return p;
 }
@@ -159,6 +158,7 @@ struct BwdDataPlan {
     int BR, BCOL, KE;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck, s1;
+    bool natw;  // weights read untransposed through natural LDS tiles (bf16, C % 8 == 0)
     size_t wt_bytes, part_bytes, ws_bytes;
 };
 
@@ -166,8 +166,11 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
     BwdDataPlan p{};
     const int M = g.N * g.H * g.W, K = g.KH * g.KW * g.O;
     p.veck = g.O % g.vec() == 0;
+    p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
     if (p.veck) {
-        p.cfg = env_override("QLAYER_BWD_DATA_CFG", g.C <= 64 ? 1 : 0);
+        int dflt = 1;
+        if (g.C > 64) dflt = (long long)cdiv(g.C, 128) * cdiv(M, 128) >= kNumCUs ? 0 : 2;
+        p.cfg = env_override("QLAYER_BWD_DATA_CFG", dflt);
         if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
         p.BR = kBdBR[p.cfg];
         p.BCOL = kBdBCOL[p.cfg];
@@ -181,8 +184,8 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
     p.row_tiles = cdiv(g.C, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, p.splits, p.sps);
-    p.wt_bytes = align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)M * g.C * 4, p.splits, p.sps);
+    p.wt_bytes = p.natw ? 0 : align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * M * g.C * sizeof(float)) : 0;
     p.ws_bytes = p.wt_bytes + p.part_bytes;
     return p;
@@ -211,7 +214,7 @@ BwdWeightPlan plan_bwd_weight(const Geom &g) {
     p.veck = g.C % g.vec() == 0 && g.O % g.vec() == 0;
     p.pipe = p.veck && g.dt == QL_BF16;
     if (p.pipe) {
-        p.cfg = env_override("QLAYER_BWD_WEIGHT_CFG", g.O <= 64 ? 0 : 1);
+        p.cfg = env_override("QLAYER_BWD_WEIGHT_CFG", 0);
         if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
         p.BKP = kBwBKP[p.cfg];
         p.BO = kBwBO[p.cfg];
@@ -224,7 +227,7 @@ BwdWeightPlan plan_bwd_weight(const Geom &g) {
     p.col_tiles = cdiv(g.O, p.BO);
     p.stages_total = cdiv(M, p.KE);
     plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16),
-                p.splits, p.sps);
+                (size_t)3 * g.O * KP * 4, p.splits, p.sps);
     if (p.splits > 1) {
         p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KP * sizeof(float));
         p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));
@@ -284,26 +287,36 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long MO = (long long)a.M * g.O;
-    hipLaunchKernelGGL((qconv_fwd_combine_kernel<T>), dim3(grid_1d(MO)), dim3(kThreads), 0, st,
-                       static_cast<const float *>(ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
-                       static_cast<T *>(ta), static_cast<T *>(tb));
+    if (g.O % 4 == 0)
+        hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, true>), dim3(grid_1d(MO / 4)), dim3(kThreads), 0, st,
+                           static_cast<const float *>(ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
+                           static_cast<T *>(ta), static_cast<T *>(tb));
+    else
+        hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, false>), dim3(grid_1d(MO)), dim3(kThreads), 0, st,
+                           static_cast<const float *>(ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
+                           static_cast<T *>(ta), static_cast<T *>(tb));
     return hip_status();
 }
 
 template <typename T>
 ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, const void *ta, const void *tb,
                           const void *wa, const void *wb, const void *wc, void *dx, void *ws, hipStream_t st) {
-    T *wt = static_cast<T *>(ws);
     const int khkw = g.KH * g.KW;
-    hipLaunchKernelGGL((qconv_weight_transpose_kernel<T>), dim3(cdiv(g.C, 32), cdiv(g.O, 32), 3 * khkw),
-                       dim3(kThreads), 0, st, static_cast<const T *>(wa), static_cast<const T *>(wb),
-                       static_cast<const T *>(wc), wt, g.O, khkw, g.C);
-    ql_status s = hip_status();
-    if (s != QL_OK) return s;
     BwdDataArgs a{};
+    ql_status s = QL_OK;
+    if (p.natw) {
+        a.wt[0] = wa; a.wt[1] = wb; a.wt[2] = wc;
+    } else {
+        T *wt = static_cast<T *>(ws);
+        hipLaunchKernelGGL((qconv_weight_transpose_kernel<T>), dim3(cdiv(g.C, 32), cdiv(g.O, 32), 3 * khkw),
+                           dim3(kThreads), 0, st, static_cast<const T *>(wa), static_cast<const T *>(wb),
+                           static_cast<const T *>(wc), wt, g.O, khkw, g.C);
+        s = hip_status();
+        if (s != QL_OK) return s;
+        const size_t wsz = (size_t)g.O * khkw * g.C;
+        a.wt[0] = wt; a.wt[1] = wt + wsz; a.wt[2] = wt + 2 * wsz;
+    }
     a.gy = gy; a.ta = ta; a.tb = tb;
-    const size_t wsz = (size_t)g.O * khkw * g.C;
-    a.wt[0] = wt; a.wt[1] = wt + wsz; a.wt[2] = wt + 2 * wsz;
     a.dx = dx;
     a.ws = reinterpret_cast<float *>(static_cast<char *>(ws) + p.wt_bytes);
     a.zero = zero_page();
@@ -321,12 +334,22 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.fd_sh = make_fastdiv(g.SH);
     a.fd_sw = make_fastdiv(g.SW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
-#define QL_BD_PIPE(BR, BCOL, NS)                                                                            \
-    do {                                                                                                    \
-        if (p.s1)                                                                                           \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true>), grid, block, 0, st, a);  \
-        else                                                                                                \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, false>), grid, block, 0, st, a); \
+#define QL_BD_PIPE_N(BR, BCOL, NS, NW)                                                                          \
+    do {                                                                                                        \
+        if (p.s1)                                                                                               \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true, NW>), grid, block, 0, st, a);  \
+        else                                                                                                    \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, false, NW>), grid, block, 0, st, a); \
+    } while (0)
+#define QL_BD_PIPE(BR, BCOL, NS)                                 \
+    do {                                                         \
+        if constexpr (sizeof(T) == 2) {                          \
+            if (p.natw) {                                        \
+                QL_BD_PIPE_N(BR, BCOL, NS, true);                \
+                break;                                           \
+            }                                                    \
+        }                                                        \
+        QL_BD_PIPE_N(BR, BCOL, NS, false);                       \
     } while (0)
 #define QL_BD_GEN(BR, BCOL)                                                                                      \
     do {                                                                                                         \
@@ -350,12 +373,17 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
         QL_BD_GEN(64, 128);
     }
 #undef QL_BD_PIPE
+#undef QL_BD_PIPE_N
 #undef QL_BD_GEN
     s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long total = (long long)a.M * g.C;
-    hipLaunchKernelGGL((qconv_bwd_data_reduce_kernel<T>), dim3(grid_1d(total)), dim3(kThreads), 0, st,
-                       static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx));
+    if (g.C % 4 == 0)
+        hipLaunchKernelGGL((qconv_sum_splits_kernel<T, true>), dim3(grid_1d(total / 4)), dim3(kThreads), 0, st,
+                           static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx));
+    else
+        hipLaunchKernelGGL((qconv_sum_splits_kernel<T, false>), dim3(grid_1d(total)), dim3(kThreads), 0, st,
+                           static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx));
     return hip_status();
 }
 
@@ -402,9 +430,16 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long ndw = (long long)g.O * a.KP;
-    hipLaunchKernelGGL(qconv_bwd_weight_reduce_kernel, dim3(grid_1d(3 * ndw)), dim3(kThreads), 0, st,
-                       static_cast<const float *>(a.ws_dw), static_cast<const float *>(a.ws_db), p.splits, ndw,
-                       g.O, dwa, dwb, dwc, dba, dbb, dbc, a.want_db);
+    if (ndw % 4 == 0)
+        hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<true>), dim3(grid_1d(3 * ndw / 4 + 3 * g.O)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db);
+    else
+        hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<false>), dim3(grid_1d(3 * ndw + 3 * g.O)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db);
     return hip_status();
 }
 
@@ -431,8 +466,8 @@ ql_status bwd_data_common(const Geom &g, const void *gy, const void *ta, const v
     for (const void *q : ptrs)
         if (!aligned16(q)) return QL_EINVAL;
     const BwdDataPlan p = plan_bwd_data(g);
-    if (ws_bytes < p.ws_bytes || !ws) return QL_EWORKSPACE;
-    if (!aligned16(ws)) return QL_EINVAL;
+    if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
+    if (ws && !aligned16(ws)) return QL_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     return g.dt == QL_BF16 ? launch_bwd_data<uint16_t>(g, p, gy, ta, tb, wa, wb, wc, dx, ws, st)
                            : launch_bwd_data<float>(g, p, gy, ta, tb, wa, wb, wc, dx, ws, st);

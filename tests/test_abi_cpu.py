@@ -123,9 +123,11 @@ def test_workspace_queries_are_consistent(L):
     assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(big)) == 0
     assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(small)) > 0
     assert L.qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(big)) > 0
+    # bf16 reads the weights untransposed; fp32 stages a transposed copy in the workspace
     dl = ql.linear_desc(8192, 4096, 4096, ql.QL_BF16)
-    need = L.qlayer_linear_bwd_workspace_size(ctypes.byref(dl))
-    assert need >= 3 * 4096 * 4096 * 2
+    assert L.qlayer_linear_bwd_workspace_size(ctypes.byref(dl)) % 256 == 0
+    dl32 = ql.linear_desc(8192, 4096, 4096, ql.QL_F32)
+    assert L.qlayer_linear_bwd_workspace_size(ctypes.byref(dl32)) >= 3 * 4096 * 4096 * 4
     for f in ("conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight"):
         assert getattr(L, f"qlayer_{f}_workspace_size")(ctypes.byref(big)) % 256 == 0
 
