@@ -46,6 +46,7 @@ struct BwdWeightArgs {
     int M, KP;  // M = N*HO*WO output pixels (reduction), KP = KH*KW*C
     int row_tiles, col_tiles, splits, stages_per_split, stages_total;
     int want_db;
+    int C_out;  // channels of dW_t as stored (< C when X arrives zero-padded to C channels)
     FastDiv fd_howo, fd_wo, fd_c, fd_kw;
 };
 

@@ -160,10 +160,12 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
     const int krow0 = rt * BKP + wr * (BKP / WGR);
     const int ocol0 = ct * BO + wc * (BO / WGC);
     const int lrow = lane & 31, lhi = lane >> 5;
-    const bool vec_out = (a.KP & 3) == 0;
+    const bool padded = a.C_out != a.C;  // dW_t stored with C_out < C channels
+    const int KPO = a.KH * a.KW * a.C_out;
+    const bool vec_out = (a.KP & 3) == 0 && !padded;
 #pragma unroll
     for (int t = 0; t < 3; ++t) {
-        float *__restrict__ dst = a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * a.KP;
+        float *__restrict__ dst = a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * KPO;
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
@@ -178,10 +180,19 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
                     if (vec_out) {
                         store4<float>(dst + off, acc[t][mr][mc][4 * g], acc[t][mr][mc][4 * g + 1],
                                       acc[t][mr][mc][4 * g + 2], acc[t][mr][mc][4 * g + 3]);
-                    } else {
+                    } else if (!padded) {
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
                             if (k + i < a.KP) dst[off + i] = acc[t][mr][mc][4 * g + i];
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int kk = k + i;
+                            const int tap = (int)fdiv((uint32_t)kk, a.fd_c);
+                            const int c = kk - tap * a.C;
+                            if (kk < a.KP && c < a.C_out)
+                                dst[(size_t)o * KPO + tap * a.C_out + c] = acc[t][mr][mc][4 * g + i];
+                        }
                     }
                 }
             }

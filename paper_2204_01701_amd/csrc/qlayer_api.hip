@@ -61,6 +61,10 @@ struct Geom {
     ql_dtype dt;
     size_t esize() const { return dt == QL_BF16 ? 2 : 4; }
     int vec() const { return dt == QL_BF16 ? 8 : 4; }
+    // Few input channels that are not a multiple of the 16-byte vector (e.g.
+    // 3-channel images): X and W_t are copied zero-padded to cpad() channels.
+    bool pad_small_c() const { return C % vec() != 0 && C < 2 * vec(); }
+    int cpad() const { return (C + vec() - 1) / vec() * vec(); }
 };
 
 ql_status make_geom(const ql_conv_desc *d, Geom &g) {
@@ -119,13 +123,22 @@ struct FwdPlan {
     int BR, BCOL, KE;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
+    bool pad;                      // X and W_t zero-padded to Cp channels first
+    int Cp;
+    size_t xpad_bytes, wpad_bytes;  // workspace: [X padded][W_a, W_b, W_c padded][split partials]
     size_t ws_bytes;
 };
 
 FwdPlan plan_fwd(const Geom &g) {
     FwdPlan p{};
-    const int M = g.N * g.HO * g.WO, K = g.KH * g.KW * g.C;
-    p.veck = g.C % g.vec() == 0;
+    p.pad = g.pad_small_c();
+    p.Cp = p.pad ? g.cpad() : g.C;
+    const int M = g.N * g.HO * g.WO, K = g.KH * g.KW * p.Cp;
+    p.veck = p.Cp % g.vec() == 0;
+    if (p.pad) {
+        p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
+        p.wpad_bytes = align_up((size_t)g.O * g.KH * g.KW * p.Cp * g.esize());
+    }
     if (p.veck) {
         p.cfg = env_override("QLAYER_FWD_CFG", 3);
         if (p.cfg < 0 || p.cfg > 3) p.cfg = 3;
@@ -141,7 +154,8 @@ FwdPlan plan_fwd(const Geom &g) {
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
     plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)3 * M * g.O * 4, p.splits, p.sps);
-    p.ws_bytes = p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0;
+    p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes +
+                 (p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0);
     return p;
 }
 
@@ -158,12 +172,19 @@ struct BwdDataPlan {
     int BR, BCOL, KE;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck, s1;
-    bool natw;  // weights read untransposed through natural LDS tiles (bf16, C % 8 == 0)
+    bool natw;    // weights read untransposed through natural LDS tiles (bf16, C % 8 == 0)
+    bool smallc;  // C <= 4: vector-ALU kernel (an MFMA tile would be mostly empty rows)
+    size_t smem;  // its dynamic LDS (the three weight tensors in fp32)
     size_t wt_bytes, part_bytes, ws_bytes;
 };
 
 BwdDataPlan plan_bwd_data(const Geom &g) {
     BwdDataPlan p{};
+    p.smem = (size_t)3 * g.O * g.KH * g.KW * 4 * sizeof(float);
+    const int gr = g.O / g.vec();  // lanes per input pixel in the small-C kernel
+    p.smallc = g.C <= 4 && g.O % g.vec() == 0 && gr <= 64 && (gr & (gr - 1)) == 0 && g.KH * g.KW <= 9 &&
+               p.smem <= 64 * 1024 && env_override("QLAYER_BWD_DATA_SMALLC", 1) != 0;
+    if (p.smallc) return p;
     const int M = g.N * g.H * g.W, K = g.KH * g.KW * g.O;
     p.veck = g.O % g.vec() == 0;
     p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
@@ -205,14 +226,19 @@ struct BwdWeightPlan {
     int BKP, BO, KE;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
-    size_t dw_bytes, db_bytes, ws_bytes;
+    bool pad;  // X zero-padded to Cp channels first (pipelined path only)
+    int Cp;
+    size_t xpad_bytes, dw_bytes, db_bytes, ws_bytes;  // workspace: [X padded][dW partials][db partials]
 };
 
 BwdWeightPlan plan_bwd_weight(const Geom &g) {
     BwdWeightPlan p{};
-    const int M = g.N * g.HO * g.WO, KP = g.KH * g.KW * g.C;
-    p.veck = g.C % g.vec() == 0 && g.O % g.vec() == 0;
+    p.pad = g.dt == QL_BF16 && g.pad_small_c() && g.O % g.vec() == 0;
+    p.Cp = p.pad ? g.cpad() : g.C;
+    const int M = g.N * g.HO * g.WO, KP = g.KH * g.KW * p.Cp, KPO = g.KH * g.KW * g.C;
+    p.veck = p.Cp % g.vec() == 0 && g.O % g.vec() == 0;
     p.pipe = p.veck && g.dt == QL_BF16;
+    if (p.pad) p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
     if (p.pipe) {
         p.cfg = env_override("QLAYER_BWD_WEIGHT_CFG", 0);
         if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
@@ -227,12 +253,12 @@ BwdWeightPlan plan_bwd_weight(const Geom &g) {
     p.col_tiles = cdiv(g.O, p.BO);
     p.stages_total = cdiv(M, p.KE);
     plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16),
-                (size_t)3 * g.O * KP * 4, p.splits, p.sps);
+                (size_t)3 * g.O * KPO * 4, p.splits, p.sps);
     if (p.splits > 1) {
-        p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KP * sizeof(float));
+        p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KPO * sizeof(float));
         p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));
     }
-    p.ws_bytes = p.dw_bytes + p.db_bytes;
+    p.ws_bytes = p.xpad_bytes + p.dw_bytes + p.db_bytes;
     return p;
 }
 
@@ -256,20 +282,40 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     FwdArgs a{};
     a.x = x;
     a.w[0] = wa; a.w[1] = wb; a.w[2] = wc;
+    char *wsb = static_cast<char *>(ws);
+    if (p.pad) {
+        // Zero-pad X and the three weights to Cp channels in the workspace.
+        PadSegments sg{};
+        const void *srcs[4] = {x, wa, wb, wc};
+        const long long rows[4] = {(long long)g.N * g.H * g.W, (long long)g.O * g.KH * g.KW,
+                                   (long long)g.O * g.KH * g.KW, (long long)g.O * g.KH * g.KW};
+        for (int i = 0; i < 4; ++i) {
+            sg.src[i] = srcs[i];
+            sg.dst[i] = wsb + (i == 0 ? 0 : p.xpad_bytes + (size_t)(i - 1) * p.wpad_bytes);
+            sg.rows[i] = rows[i];
+        }
+        hipLaunchKernelGGL((qconv_pad_channels_kernel<T>), dim3(grid_1d(rows[0] * p.Cp), 4), dim3(kThreads), 0, st,
+                           sg, g.C, p.Cp);
+        const ql_status s0 = hip_status();
+        if (s0 != QL_OK) return s0;
+        a.x = sg.dst[0];
+        a.w[0] = sg.dst[1]; a.w[1] = sg.dst[2]; a.w[2] = sg.dst[3];
+    }
+    const int C = p.Cp;  // channels the GEMM sees
     a.bias[0] = ba; a.bias[1] = bb; a.bias[2] = bc;
     a.y = y; a.ta = ta; a.tb = tb;
-    a.ws = static_cast<float *>(ws);
+    a.ws = reinterpret_cast<float *>(wsb + p.xpad_bytes + 3 * p.wpad_bytes);
     a.zero = zero_page();
     if (!a.zero) return QL_EHIP;
-    a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
+    a.N = g.N; a.H = g.H; a.W = g.W; a.C = C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
     a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
     a.M = g.N * g.HO * g.WO;
-    a.K = g.KH * g.KW * g.C;
+    a.K = g.KH * g.KW * C;
     a.row_tiles = p.row_tiles; a.col_tiles = p.col_tiles;
     a.splits = p.splits; a.stages_per_split = p.sps; a.stages_total = p.stages_total;
     a.fd_howo = make_fastdiv(g.HO * g.WO);
     a.fd_wo = make_fastdiv(g.WO);
-    a.fd_c = make_fastdiv(g.C);
+    a.fd_c = make_fastdiv(C);
     a.fd_kw = make_fastdiv(g.KW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     if (p.veck) {
@@ -289,11 +335,11 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     const long long MO = (long long)a.M * g.O;
     if (g.O % 4 == 0)
         hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, true>), dim3(grid_1d(MO / 4)), dim3(kThreads), 0, st,
-                           static_cast<const float *>(ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
+                           static_cast<const float *>(a.ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
                            static_cast<T *>(ta), static_cast<T *>(tb));
     else
         hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, false>), dim3(grid_1d(MO)), dim3(kThreads), 0, st,
-                           static_cast<const float *>(ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
+                           static_cast<const float *>(a.ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
                            static_cast<T *>(ta), static_cast<T *>(tb));
     return hip_status();
 }
@@ -301,6 +347,27 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
 template <typename T>
 ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, const void *ta, const void *tb,
                           const void *wa, const void *wb, const void *wc, void *dx, void *ws, hipStream_t st) {
+    if (p.smallc) {
+        const long long M = (long long)g.N * g.H * g.W;
+        const int gr = g.O / g.vec();
+#define QL_SMALLC(GR)                                                                                             \
+    hipLaunchKernelGGL((qconv_bwd_data_smallc_kernel<T, GR>), dim3(grid_1d(M * GR)), dim3(kThreads), p.smem, st, \
+                       static_cast<const T *>(gy), static_cast<const T *>(ta), static_cast<const T *>(tb),         \
+                       static_cast<const T *>(wa), static_cast<const T *>(wb), static_cast<const T *>(wc),          \
+                       static_cast<T *>(dx), g.N, g.H, g.W, g.C, g.O, g.KH, g.KW, g.SH, g.SW, g.PH, g.PW, g.HO,    \
+                       g.WO)
+        switch (gr) {
+            case 1: QL_SMALLC(1); break;
+            case 2: QL_SMALLC(2); break;
+            case 4: QL_SMALLC(4); break;
+            case 8: QL_SMALLC(8); break;
+            case 16: QL_SMALLC(16); break;
+            case 32: QL_SMALLC(32); break;
+            default: QL_SMALLC(64); break;
+        }
+#undef QL_SMALLC
+        return hip_status();
+    }
     const int khkw = g.KH * g.KW;
     BwdDataArgs a{};
     ql_status s = QL_OK;
@@ -393,22 +460,37 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
                             void *ws, hipStream_t st) {
     BwdWeightArgs a{};
     a.x = x; a.gy = gy; a.ta = ta; a.tb = tb;
+    char *wsb = static_cast<char *>(ws);
+    if (p.pad) {
+        // Zero-pad X to Cp channels in the workspace; dW_t is stored with the true C.
+        PadSegments sg{};
+        sg.src[0] = x;
+        sg.dst[0] = wsb;
+        sg.rows[0] = (long long)g.N * g.H * g.W;
+        hipLaunchKernelGGL((qconv_pad_channels_kernel<T>), dim3(grid_1d(sg.rows[0] * p.Cp), 1), dim3(kThreads), 0, st,
+                           sg, g.C, p.Cp);
+        const ql_status s0 = hip_status();
+        if (s0 != QL_OK) return s0;
+        a.x = wsb;
+    }
+    const int C = p.Cp;  // channels the GEMM sees
     a.dw[0] = dwa; a.dw[1] = dwb; a.dw[2] = dwc;
     a.db[0] = dba; a.db[1] = dbb; a.db[2] = dbc;
-    a.ws_dw = static_cast<float *>(ws);
-    a.ws_db = reinterpret_cast<float *>(static_cast<char *>(ws) + p.dw_bytes);
+    a.ws_dw = reinterpret_cast<float *>(wsb + p.xpad_bytes);
+    a.ws_db = reinterpret_cast<float *>(wsb + p.xpad_bytes + p.dw_bytes);
     a.zero = zero_page();
     if (!a.zero) return QL_EHIP;
-    a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
+    a.N = g.N; a.H = g.H; a.W = g.W; a.C = C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
     a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
     a.M = g.N * g.HO * g.WO;
-    a.KP = g.KH * g.KW * g.C;
+    a.KP = g.KH * g.KW * C;
+    a.C_out = g.C;
     a.row_tiles = p.row_tiles; a.col_tiles = p.col_tiles;
     a.splits = p.splits; a.stages_per_split = p.sps; a.stages_total = p.stages_total;
     a.want_db = dba != nullptr;
     a.fd_howo = make_fastdiv(g.HO * g.WO);
     a.fd_wo = make_fastdiv(g.WO);
-    a.fd_c = make_fastdiv(g.C);
+    a.fd_c = make_fastdiv(C);
     a.fd_kw = make_fastdiv(g.KW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     if constexpr (sizeof(T) == 2) {
@@ -429,8 +511,13 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     }
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
-    const long long ndw = (long long)g.O * a.KP;
-    if (ndw % 4 == 0)
+    const long long ndw = (long long)g.O * g.KH * g.KW * g.C;  // dW_t as stored
+    if (3 * ndw < (1LL << 20) && p.splits >= 16)
+        hipLaunchKernelGGL((qconv_bwd_weight_reduce2d_kernel<16>), dim3(grid_1d((3 * ndw + 3 * g.O) * 16)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db);
+    else if (ndw % 4 == 0)
         hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<true>), dim3(grid_1d(3 * ndw / 4 + 3 * g.O)),
                            dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
                            static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,

@@ -29,6 +29,8 @@ CONV_SHAPES = [
     (2, 16, 8, 8, 32, 3, 3, 2, 1),      # residual-stage transition
     (1, 8, 7, 9, 16, 3, 1, 1, 1),       # non-square kernel
     (2, 12, 6, 6, 20, 2, 2, 2, 0),      # even kernel, stride 2
+    (4, 3, 32, 32, 64, 3, 3, 1, 1),     # 3-channel image stem (channel padding, small-C input gradient)
+    (3, 5, 11, 9, 24, 3, 3, 2, 1),      # 5 channels, stride 2
 ]
 
 KEYS_FWD = ("y", "ta", "tb")
