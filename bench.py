@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing leg")
     ap.add_argument("--no-extra", action="store_true", help="skip the single-layer and dense workloads")
     ap.add_argument("--cpu-target-s", type=float, default=15.0, help="approximate oracle sample time")
+    ap.add_argument("--profile-summary", metavar="KERNEL_STATS_CSV",
+                    help="instead of running: summarise a rocprofv3 --stats kernel table per entry point")
     return ap.parse_args()
 
 
@@ -166,8 +168,61 @@ def cpu_baseline(layers_geom, target_s):
                       f"{t1:.1f} s for {f1 / 1e9:.1f} GFLOP)"}
 
 
+# Kernel symbol -> (entry point that launches it, whether it is that entry's one main kernel).
+# Every entry call launches exactly one main kernel, so main-kernel calls count entry calls.
+_KERNEL_FAMILY = [
+    (r"qconv_fwd_kernel<", "fwd", True),
+    (r"qconv_fwd_generic_kernel<", "fwd", True),
+    (r"qconv_fwd_combine_kernel<", "fwd", False),
+    (r"qconv_pad_channels_kernel<[^,>]+, 4>", "fwd", False),
+    (r"qconv_bwd_data_kernel<", "bwd_data", True),
+    (r"qconv_bwd_data_generic_kernel<", "bwd_data", True),
+    (r"qconv_bwd_data_smallc_kernel<", "bwd_data", True),
+    (r"qconv_sum_splits_kernel<", "bwd_data", False),
+    (r"qconv_weight_transpose_kernel<", "bwd_data", False),
+    (r"qconv_bwd_weight_kernel<", "bwd_weight", True),
+    (r"qconv_bwd_weight_generic_kernel<", "bwd_weight", True),
+    (r"qconv_bwd_weight_reduce_kernel<", "bwd_weight", False),
+    (r"qconv_bwd_weight_reduce2d_kernel<", "bwd_weight", False),
+    (r"qconv_pad_channels_kernel<[^,>]+, 1>", "bwd_weight", False),
+]
+
+
+def profile_summary(path):
+    """Markdown summary of a rocprofv3 kernel statistics table (--stats, csv output):
+    every kernel with its calls and average duration, then per entry point the total
+    kernel time divided by the number of entry calls (= calls of its main kernels)."""
+    import csv
+    import re
+
+    rows = list(csv.DictReader(open(path)))
+    fam_ns, fam_calls = {}, {}
+    lines = ["| kernel | entry point | calls | avg us | total ms |", "|---|---|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name, calls, tot = r["Name"], int(r["Calls"]), float(r["TotalDurationNs"])
+        fam, main = "-", False
+        for pat, f, m in _KERNEL_FAMILY:
+            if re.search(pat, name):
+                fam, main = f, m
+                break
+        if fam != "-":
+            fam_ns[fam] = fam_ns.get(fam, 0.0) + tot
+            if main:
+                fam_calls[fam] = fam_calls.get(fam, 0) + calls
+        short = name if len(name) < 110 else name[:107] + "..."
+        lines.append(f"| `{short}` | {fam} | {calls} | {tot / calls / 1e3:.1f} | {tot / 1e6:.2f} |")
+    lines += ["", "| entry point | entry calls | kernel time per call, us |", "|---|---:|---:|"]
+    for fam in ("fwd", "bwd_data", "bwd_weight"):
+        if fam_calls.get(fam):
+            lines.append(f"| qlayer_conv2d_{fam} | {fam_calls[fam]} | {fam_ns[fam] / fam_calls[fam] / 1e3:.1f} |")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
+    if args.profile_summary:
+        profile_summary(args.profile_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
                           "n_gpus": args.gpus}))

@@ -207,15 +207,18 @@ namespace ql {
 
 // Copy rows of C elements into rows of Cp >= C elements, zero-filling the
 // extra channels (lets 3-channel images use the 16-byte pipelined path).
-// blockIdx.y selects one of up to four (src, dst, rows) segments.
+// blockIdx.y selects one of the NSEG (src, dst, rows) segments: four for the
+// forward (X and the three weights), one for the weight gradient (X).
 struct PadSegments {
     const void *src[4];
     void *dst[4];
     long long rows[4];
 };
 
-template <typename T>
+template <typename T, int NSEG>
 __global__ __launch_bounds__(kThreads) void qconv_pad_channels_kernel(PadSegments sg, int C, int Cp) {
+    static_assert(NSEG >= 1 && NSEG <= 4, "segments");
+    if (blockIdx.y >= NSEG) return;
     const T *__restrict__ src = static_cast<const T *>(sg.src[blockIdx.y]);
     T *__restrict__ dst = static_cast<T *>(sg.dst[blockIdx.y]);
     const long long total = sg.rows[blockIdx.y] * Cp;
