@@ -230,79 +230,133 @@ __global__ __launch_bounds__(kThreads) void qconv_pad_channels_kernel(PadSegment
     }
 }
 
-// Input gradient for layers with few input channels (C <= 4), on the vector
-// ALUs: an MFMA tile would leave most of its rows empty.  GR = O / 8 adjacent
-// lanes share one input pixel, each lane taking 8 output channels; their
-// partial sums are combined with lane shuffles in a fixed order.  All taps'
-// loads of G, T_a, T_b (16 bytes each) are issued before any arithmetic.  The
-// weights sit in LDS as fp32, [tap][o][term][4].  Same arithmetic as the GEMM
-// path: dX[n,h,w,c] = sum_{r,q,o} (G o T_b) W_a + (G o T_a) W_b + G W_c over the
-// output pixels (i, j) with i*s - p + r = h, j*s - p + q = w.
-template <typename T, int GR>
-__global__ __launch_bounds__(kThreads) void qconv_bwd_data_smallc_kernel(
+// Input gradient for layers with few input channels (C <= 4, e.g. a network's
+// first layer on RGB images).  An MFMA tile with input channels as rows would
+// be nearly empty, so the contraction is split in two:
+//
+//   P[m, (r, q, c)] = sum_t sum_o G_t[m, o] W_t[o, r, q, c]      (m: output pixel)
+//   dX[n, h, w, c]  = sum_{r,q} P[(n, i, j), (r, q, c)],  i*s - p + r = h, j*s - p + q = w
+//
+// The first is a GEMM with output pixels as rows, (r, q, c) as columns
+// (KH*KW*C <= 32 * NJB) and K = (t, o).  Each wave takes 32 pixels, loads
+// G, T_a and T_b straight from global memory into MFMA fragments (16 bytes
+// per lane), forms the products G o T_b and G o T_a once per element, and
+// multiplies with weight fragments staged in LDS.  P is fp32 in the
+// workspace, tap-major ([r, q][m][c]), so that the second kernel, which
+// gathers it over the taps in a fixed order, reads consecutive pixels of one
+// tap plane from consecutive lanes.
+template <typename T, int NJB>
+__global__ __launch_bounds__(kThreads) void qconv_bwd_data_cols_kernel(
     const T *__restrict__ gy, const T *__restrict__ gta, const T *__restrict__ gtb, const T *__restrict__ w0,
-    const T *__restrict__ w1, const T *__restrict__ w2, T *__restrict__ dx, int N, int H, int W, int C, int O,
-    int KH, int KW, int SH, int SW, int PH, int PW, int HO, int WO) {
+    const T *__restrict__ w1, const T *__restrict__ w2, float *__restrict__ P, int M, int O, int C, int J) {
     constexpr int VEC = Elem<T>::VEC;
-    constexpr int MAXTAP = 9;
-    static_assert(GR >= 1 && GR <= 64 && (GR & (GR - 1)) == 0, "lane groups");
-    extern __shared__ __attribute__((aligned(16))) float wsm[];  // [KH*KW][O][3][4]
-    const int khkw = KH * KW;
-    const int nslots = khkw * O * 3;
-    for (int i = threadIdx.x; i < nslots * 4; i += blockDim.x) {
-        const int c = i & 3, slot = i >> 2;
-        const int t = slot % 3, to = slot / 3;
-        const int o = to % O, tap = to / O;
+    constexpr int KC = 2 * VEC;  // K elements (output channels) per MFMA chunk
+    constexpr int KB = 4;        // chunks whose loads are issued together
+    extern __shared__ __attribute__((aligned(16))) v4u wfr[];  // [t][nb][kc][lane]
+    const int nkc = O / KC;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int i = tid; i < 3 * NJB * nkc * 64; i += blockDim.x) {
+        const int l = i & 63, f = i >> 6;
+        const int kc = f % nkc, nb = (f / nkc) % NJB, t = f / (nkc * NJB);
         const T *w = t == 0 ? w0 : (t == 1 ? w1 : w2);
-        wsm[i] = c < C ? to_f32<T>(w[((size_t)o * khkw + tap) * C + c]) : 0.0f;
+        const int j = nb * 32 + (l & 31), o0 = kc * KC + VEC * (l >> 5);
+        float v[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[e] = j < J ? to_f32<T>(w[(size_t)(o0 + e) * J + j]) : 0.0f;
+        wfr[i] = vpack<T>(v);
     }
     __syncthreads();
-    const int grp = threadIdx.x % GR;  // which 8 output channels
-    const int o0 = grp * VEC;
+    // This lane's output column j = 32 nb + lane % 32 is (tap, c) = (j / C, j % C).
+    int ptap[NJB], pc[NJB];
+#pragma unroll
+    for (int nb = 0; nb < NJB; ++nb) {
+        const int j = nb * 32 + (lane & 31);
+        ptap[nb] = j < J ? j / C : -1;
+        pc[nb] = j < J ? j - (j / C) * C : 0;
+    }
+    const long long nblk = ((long long)M + 31) / 32;
+    for (long long mb = (long long)blockIdx.x * (kThreads / 64) + wave; mb < nblk;
+         mb += (long long)gridDim.x * (kThreads / 64)) {
+        const long long m = mb * 32 + (lane & 31);
+        const bool ok = m < M;
+        f32x16_t acc[NJB];
+#pragma unroll
+        for (int nb = 0; nb < NJB; ++nb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[nb][v] = 0.0f;
+        const size_t rowoff = (size_t)(ok ? m : 0) * O + VEC * (lane >> 5);
+        for (int kb = 0; kb < nkc; kb += KB) {
+            v4u g[KB], ta[KB], tb[KB];
+#pragma unroll
+            for (int u = 0; u < KB; ++u) {
+                const bool in = ok && kb + u < nkc;
+                const size_t off = rowoff + (size_t)(kb + u) * KC;
+                g[u] = ld16(gy + off, in);
+                ta[u] = ld16(gta + off, in);
+                tb[u] = ld16(gtb + off, in);
+            }
+#pragma unroll
+            for (int u = 0; u < KB; ++u) {
+                if (kb + u >= nkc) break;
+                const int kc = kb + u;
+                v4u ga, gb;
+                prologue_frag<T>(g[u], ta[u], tb[u], ga, gb);
+#pragma unroll
+                for (int nb = 0; nb < NJB; ++nb) {
+                    mfma_chunk<T>(ga, wfr[((0 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
+                    mfma_chunk<T>(gb, wfr[((1 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
+                    mfma_chunk<T>(g[u], wfr[((2 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
+                }
+            }
+        }
+        // Lane holds column j = 32 nb + lane % 32 of rows 8 (v / 4) + 4 (lane / 32) + v % 4.
+#pragma unroll
+        for (int nb = 0; nb < NJB; ++nb) {
+            if (ptap[nb] < 0) continue;
+            float *plane = P + (size_t)ptap[nb] * M * C + pc[nb];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const long long row = mb * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                if (row < M) plane[row * C] = acc[nb][v];
+            }
+        }
+    }
+}
+
+// dX[n, h, w, c] from the tap-major partial sums P ([KH*KW][Mo][C], Mo =
+// N*HO*WO): one thread per input pixel, taps summed in (r, q) order.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void qconv_bwd_data_col2im_kernel(const float *__restrict__ P, T *__restrict__ dx,
+                                                                         int N, int H, int W, int C, int KH, int KW,
+                                                                         int SH, int SW, int PH, int PW, int HO,
+                                                                         int WO) {
     const long long M = (long long)N * H * W;
-    const long long per_pass = (long long)gridDim.x * (blockDim.x / GR);
-    for (long long m = (long long)blockIdx.x * (blockDim.x / GR) + threadIdx.x / GR; m < M;
-         m += per_pass) {
+    const size_t plane = (size_t)N * HO * WO * C;
+    for (long long m = (long long)blockIdx.x * blockDim.x + threadIdx.x; m < M;
+         m += (long long)gridDim.x * blockDim.x) {
         const int n = (int)(m / ((long long)H * W));
         const int rem = (int)(m - (long long)n * H * W);
         const int h = rem / W, w = rem - (rem / W) * W;
-        v4u gv[MAXTAP], av[MAXTAP], bv[MAXTAP];
-        bool ok[MAXTAP];
-#pragma unroll
-        for (int tap = 0; tap < MAXTAP; ++tap) {
-            const int r = tap / KW, q = tap - (tap / KW) * KW;
-            const int hi = h + PH - r, wi = w + PW - q;
-            const int i = hi / SH, j = wi / SW;
-            ok[tap] = tap < khkw && hi >= 0 && wi >= 0 && i * SH == hi && j * SW == wi && i < HO && j < WO;
-            const size_t base = (((size_t)n * HO + (ok[tap] ? i : 0)) * WO + (ok[tap] ? j : 0)) * O + o0;
-            gv[tap] = ld16(gy + base, ok[tap]);
-            av[tap] = ld16(gta + base, ok[tap]);
-            bv[tap] = ld16(gtb + base, ok[tap]);
-        }
         float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int r = 0; r < KH; ++r) {
+            const int hi = h + PH - r;
+            if (hi < 0) break;
+            const int i = hi / SH;
+            if (i * SH != hi || i >= HO) continue;
+            for (int q = 0; q < KW; ++q) {
+                const int wi = w + PW - q;
+                if (wi < 0) break;
+                const int j = wi / SW;
+                if (j * SW != wi || j >= WO) continue;
+                const float *p = P + (size_t)(r * KW + q) * plane + (((size_t)n * HO + i) * WO + j) * C;
 #pragma unroll
-        for (int tap = 0; tap < MAXTAP; ++tap) {
-            if (!ok[tap]) continue;
-            const v4f *wt = reinterpret_cast<const v4f *>(wsm) + ((size_t)tap * O + o0) * 3;
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                const float g = vget<T>(gv[tap], e);
-                const float ga = g * vget<T>(bv[tap], e);
-                const float gb = g * vget<T>(av[tap], e);
-                const v4f wa = wt[e * 3 + 0], wb = wt[e * 3 + 1], wc = wt[e * 3 + 2];
-#pragma unroll
-                for (int c = 0; c < 4; ++c) acc[c] += ga * wa[c] + gb * wb[c] + g * wc[c];
+                for (int c = 0; c < 4; ++c)
+                    if (c < C) acc[c] += p[c];
             }
         }
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-#pragma unroll
-            for (int d = 1; d < GR; d <<= 1) acc[c] += __shfl_xor(acc[c], d);
-        if (grp == 0) {
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                if (c < C) dx[m * C + c] = from_f32<T>(acc[c]);
-        }
+            if (c < C) dx[m * C + c] = from_f32<T>(acc[c]);
     }
 }
 

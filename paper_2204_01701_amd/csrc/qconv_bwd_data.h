@@ -25,21 +25,6 @@
 
 namespace ql {
 
-// Products of the prologue on one 16-byte fragment: G o T_b and G o T_a.
-template <typename T>
-__device__ __forceinline__ void prologue_frag(const v4u &g, const v4u &ta, const v4u &tb, v4u &ga, v4u &gb) {
-    constexpr int VEC = Elem<T>::VEC;
-    float fa[VEC], fb[VEC];
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-        const float gv = vget<T>(g, e);
-        fa[e] = gv * vget<T>(tb, e);
-        fb[e] = gv * vget<T>(ta, e);
-    }
-    ga = vpack<T>(fa);
-    gb = vpack<T>(fb);
-}
-
 template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool S1, bool NATW>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataArgs a) {
     static_assert(!NATW || sizeof(T) == 2, "natural weight tiles need 16-bit elements");
@@ -106,10 +91,10 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         }
     }
 
-    auto issue = [&](int s, int slot) {
+    auto issue = [&](int s, int slot, bool live) {
         char *base = smem + slot * STAGE + wave * 1024;
         const int k = s * KE + kcol * VEC;
-        const bool kin = k < a.K;
+        const bool kin = live && k < a.K;
         const int tap = (int)fdiv((uint32_t)k, a.fd_o);
         const int o = k - tap * a.O;
         const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
@@ -122,7 +107,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
                 const int kr = s * KE + row;
                 const int tapr = (int)fdiv((uint32_t)kr, a.fd_o);
                 const int orow = kr - tapr * a.O;
-                const bool ok = wc_ok && kr < a.K;
+                const bool ok = live && wc_ok && kr < a.K;
                 dma16(dma_src(ok, wt[t] + ((size_t)(orow * khkw + tapr) * a.C + wc0), a.zero), base + i * 4096);
             }
         } else {

@@ -74,7 +74,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
     const int og = ct * BO + 8 * gslot;
     const bool og_ok = og < a.O;
 
-    auto issue = [&](int s, int slot) {
+    auto issue = [&](int s, int slot, bool live) {
         char *base = smem + slot * STAGE + wave * 1024;
 #pragma unroll
         for (int i = 0; i < NIX; ++i) {
@@ -84,13 +84,13 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
             const int oh = (int)fdiv((uint32_t)rem, a.fd_wo);
             const int ow = rem - oh * a.WO;
             const int ih = oh * a.SH - a.PH + xr, iw = ow * a.SW - a.PW + xq;
-            const bool ok = kp_ok && m < a.M && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+            const bool ok = live && kp_ok && m < a.M && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
             dma16(dma_src(ok, x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + xc, a.zero), base + i * 4096);
         }
 #pragma unroll
         for (int i = 0; i < NIG; ++i) {
             const int m = s * KE + RG * (4 * i + wave) + lane / SG;
-            const bool ok = og_ok && m < a.M;
+            const bool ok = live && og_ok && m < a.M;
             const size_t off = (size_t)m * a.O + og;
 #pragma unroll
             for (int u = 0; u < 3; ++u)

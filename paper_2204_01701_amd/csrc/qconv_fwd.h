@@ -83,10 +83,10 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
         }
     }
 
-    auto issue = [&](int s, int slot) {
+    auto issue = [&](int s, int slot, bool live) {
         char *base = smem + slot * STAGE + wave * 1024;
         const int k = s * KE + kcol * VEC;
-        const bool kin = k < a.K;
+        const bool kin = live && k < a.K;
         const int tap = (int)fdiv((uint32_t)k, a.fd_c);
         const int c = k - tap * a.C;
         const int r = (int)fdiv((uint32_t)tap, a.fd_kw);

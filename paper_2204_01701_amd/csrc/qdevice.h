@@ -118,6 +118,21 @@ template <> __device__ __forceinline__ void mfma_chunk<float>(const v4u &a, cons
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
 }
 
+// Products of the prologue on one 16-byte fragment: G o T_b and G o T_a.
+template <typename T>
+__device__ __forceinline__ void prologue_frag(const v4u &g, const v4u &ta, const v4u &tb, v4u &ga, v4u &gb) {
+    constexpr int VEC = Elem<T>::VEC;
+    float fa[VEC], fb[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+        const float gv = vget<T>(g, e);
+        fa[e] = gv * vget<T>(tb, e);
+        fb[e] = gv * vget<T>(ta, e);
+    }
+    ga = vpack<T>(fa);
+    gb = vpack<T>(fb);
+}
+
 // 16-byte global load, or zeros when !ok (the address is not touched then).
 template <typename P> __device__ __forceinline__ v4u ld16(const P *p, bool ok) {
     v4u v = {0u, 0u, 0u, 0u};

@@ -40,10 +40,16 @@ using namespace ql;
 namespace {
 
 constexpr int kNumCUs = 256;         // MI355X compute units
-constexpr int kTargetBlocks = kNumCUs;  // split-K aims at one workgroup per CU
 constexpr size_t kAlign = 256;
 constexpr long long kMaxElems = (1LL << 31) - 1;  // 32-bit element offsets in the kernels
-constexpr size_t kMaxSplitBytes = 32ull << 20;  // cap on split-K partial sums (written + read once)
+constexpr size_t kMaxSplitBytes = 128ull << 20;  // cap on split-K partial sums (written + read once)
+// Split-K cost model, in units of one K step of one workgroup alone on a CU:
+// a CU holding two co-resident workgroups finishes both in kSharedRound steps
+// per step each (the second one hides the first one's latency), and one unit
+// of time moves about kBytesPerStep bytes of partial sums through HBM.
+constexpr double kSharedRound = 1.25;
+constexpr double kBytesPerStep = 3.2e6;
+constexpr double kReduceSteps = 6.0;  // the reduction kernel's launch and ramp
 
 // Tuning override: QLAYER_<NAME>=<int> replaces a planner choice (for sweeps).
 int env_override(const char *name, int dflt) {
@@ -96,14 +102,34 @@ ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
     return make_geom(&c, g);
 }
 
-// Split-K planning: enough workgroups for one per CU, at least min_stages K
-// steps per split, and at most max_bytes of partial sums (bytes_per_split each).
-void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int &splits, int &sps) {
+// Split-K planning.  The workgroups run in rounds of kNumCUs * slots (slots =
+// workgroups one CU can hold at once); the split count minimises the modelled
+// time: K steps per split times the rounds' cost, plus the traffic of the
+// partial sums and the reduction.  A count that leaves a few CUs with a second
+// workgroup in the last round costs a whole shared round, which the search
+// avoids.  At least min_stages K steps per split, at most kMaxSplitBytes of
+// partial sums (bytes_per_split each).
+void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int slots, int &splits,
+                 int &sps) {
+    const int cap_bytes = (int)std::max<size_t>(1, kMaxSplitBytes / std::max<size_t>(bytes_per_split, 1));
+    const int s_max = std::max(1, std::min(stages_total / std::max(min_stages, 1), cap_bytes));
+    double best = 0.0;
     splits = 1;
-    if (tiles < kTargetBlocks && stages_total >= 2 * min_stages) {
-        splits = std::min(cdiv(kTargetBlocks, tiles), stages_total / min_stages);
-        const int cap = (int)std::max<size_t>(1, kMaxSplitBytes / std::max<size_t>(bytes_per_split, 1));
-        splits = std::max(1, std::min(splits, cap));
+    for (int s = 1; s <= s_max; ++s) {
+        const int per = cdiv(stages_total, s);
+        const int eff = cdiv(stages_total, per);
+        if (eff != s) continue;  // the same partition as a smaller count
+        const long long wgs = (long long)tiles * eff;
+        const long long round = (long long)kNumCUs * std::max(slots, 1);
+        const long long full = wgs / round, rest = wgs % round;
+        double rounds = (double)full * (slots > 1 ? kSharedRound : 1.0);
+        if (rest > 0) rounds += rest > kNumCUs ? kSharedRound : 1.0;
+        double t = per * rounds;
+        if (eff > 1) t += (double)eff * bytes_per_split * 2.0 / kBytesPerStep + kReduceSteps;
+        if (s == 1 || t < best) {
+            best = t;
+            splits = eff;
+        }
     }
     sps = cdiv(stages_total, splits);
     splits = cdiv(stages_total, sps);
@@ -117,10 +143,12 @@ void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_s
 //   0: 128 x 128 (32 x 128), 1: 64 x 256 (32 x 128), 2: 128 x 128 (64 x 64), 3: 64 x 128 (32 x 64).
 constexpr int kFwdBR[4] = {128, 64, 128, 64};
 constexpr int kFwdBCOL[4] = {128, 256, 128, 128};
+// Workgroups one CU holds at once (limited by LDS stages and registers).
+constexpr int kFwdSlots[4] = {1, 1, 1, 2};
 
 struct FwdPlan {
     int cfg;  // pipelined: index into kFwd*; generic: 0: 128 x 128, 1: 64 x 128
-    int BR, BCOL, KE;
+    int BR, BCOL, KE, slots;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
     bool pad;                      // X and W_t zero-padded to Cp channels first
@@ -144,16 +172,18 @@ FwdPlan plan_fwd(const Geom &g) {
         if (p.cfg < 0 || p.cfg > 3) p.cfg = 3;
         p.BR = kFwdBR[p.cfg];
         p.BCOL = kFwdBCOL[p.cfg];
+        p.slots = kFwdSlots[p.cfg];
     } else {
         p.cfg = g.O <= 64 ? 1 : 0;
         p.BR = p.cfg == 0 ? 128 : 64;
         p.BCOL = 128;
+        p.slots = 1;
     }
     p.KE = 64 / (int)g.esize();
     p.row_tiles = cdiv(g.O, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)3 * M * g.O * 4, p.splits, p.sps);
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)3 * M * g.O * 4, p.slots, p.splits, p.sps);
     p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes +
                  (p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0);
     return p;
@@ -169,22 +199,29 @@ constexpr int kBdBCOL[3] = {128, 128, 64};
 
 struct BwdDataPlan {
     int cfg;  // pipelined: index into kBd*; generic: 0: 128 x 128, 1: 64 x 128
-    int BR, BCOL, KE;
+    int BR, BCOL, KE, slots;  // slots: one workgroup per CU (the LDS ring takes 144 KB)
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck, s1;
     bool natw;    // weights read untransposed through natural LDS tiles (bf16, C % 8 == 0)
-    bool smallc;  // C <= 4: vector-ALU kernel (an MFMA tile would be mostly empty rows)
-    size_t smem;  // its dynamic LDS (the three weight tensors in fp32)
+    bool smallc;  // C <= 4: per-pixel partial sums by MFMA, then a gather over the taps
+    int njb;      // ... 32-column blocks of (r, q, c)
+    size_t smem;  // ... LDS of the weight fragments
     size_t wt_bytes, part_bytes, ws_bytes;
 };
 
 BwdDataPlan plan_bwd_data(const Geom &g) {
     BwdDataPlan p{};
-    p.smem = (size_t)3 * g.O * g.KH * g.KW * 4 * sizeof(float);
-    const int gr = g.O / g.vec();  // lanes per input pixel in the small-C kernel
-    p.smallc = g.C <= 4 && g.O % g.vec() == 0 && gr <= 64 && (gr & (gr - 1)) == 0 && g.KH * g.KW <= 9 &&
-               p.smem <= 64 * 1024 && env_override("QLAYER_BWD_DATA_SMALLC", 1) != 0;
-    if (p.smallc) return p;
+    {
+        const int J = g.KH * g.KW * g.C;  // columns (r, q, c) of the partial sums
+        p.njb = cdiv(J, 32);
+        p.smem = (size_t)3 * p.njb * (g.O / (2 * g.vec())) * 64 * 16;
+        p.smallc = g.C <= 4 && g.O % (2 * g.vec()) == 0 && p.njb <= 2 && p.smem <= 64 * 1024 &&
+                   env_override("QLAYER_BWD_DATA_SMALLC", 1) != 0;
+        if (p.smallc) {
+            p.ws_bytes = align_up((size_t)g.N * g.HO * g.WO * J * sizeof(float));
+            return p;
+        }
+    }
     const int M = g.N * g.H * g.W, K = g.KH * g.KW * g.O;
     p.veck = g.O % g.vec() == 0;
     p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
@@ -201,11 +238,12 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
         p.BCOL = 128;
     }
     p.KE = 64 / (int)g.esize();
+    p.slots = 1;
     p.s1 = g.SH == 1 && g.SW == 1;
     p.row_tiles = cdiv(g.C, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)M * g.C * 4, p.splits, p.sps);
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)M * g.C * 4, p.slots, p.splits, p.sps);
     p.wt_bytes = p.natw ? 0 : align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * M * g.C * sizeof(float)) : 0;
     p.ws_bytes = p.wt_bytes + p.part_bytes;
@@ -219,11 +257,12 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
 // output channels per term):  0: 128 x 64, 1: 128 x 128, 2: 64 x 64.
 constexpr int kBwBKP[3] = {128, 128, 64};
 constexpr int kBwBO[3] = {64, 128, 64};
+constexpr int kBwSlots[3] = {2, 1, 2};  // workgroups one CU holds at once
 
 struct BwdWeightPlan {
     int cfg;   // pipelined path only
     bool pipe; // bf16 and vectorizable: pipelined kernel; otherwise the generic one
-    int BKP, BO, KE;
+    int BKP, BO, KE, slots;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
     bool pad;  // X zero-padded to Cp channels first (pipelined path only)
@@ -244,16 +283,18 @@ BwdWeightPlan plan_bwd_weight(const Geom &g) {
         if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
         p.BKP = kBwBKP[p.cfg];
         p.BO = kBwBO[p.cfg];
+        p.slots = kBwSlots[p.cfg];
     } else {
         p.BKP = 128;
         p.BO = 64;
+        p.slots = 1;
     }
     p.KE = 64 / (int)g.esize();
     p.row_tiles = cdiv(KP, p.BKP);
     p.col_tiles = cdiv(g.O, p.BO);
     p.stages_total = cdiv(M, p.KE);
     plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16),
-                (size_t)3 * g.O * KPO * 4, p.splits, p.sps);
+                (size_t)3 * g.O * KPO * 4, p.slots, p.splits, p.sps);
     if (p.splits > 1) {
         p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KPO * sizeof(float));
         p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));
@@ -348,24 +389,26 @@ template <typename T>
 ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, const void *ta, const void *tb,
                           const void *wa, const void *wb, const void *wc, void *dx, void *ws, hipStream_t st) {
     if (p.smallc) {
+        const long long Mo = (long long)g.N * g.HO * g.WO;
+        const int J = g.KH * g.KW * g.C;
+        float *P = static_cast<float *>(ws);
+        const int nblk = cdiv(Mo, 32);
+        const dim3 grid(std::max(1, std::min(cdiv(nblk, kThreads / 64), 4 * kNumCUs)));
+        if (p.njb == 1)
+            hipLaunchKernelGGL((qconv_bwd_data_cols_kernel<T, 1>), grid, dim3(kThreads), p.smem, st,
+                               static_cast<const T *>(gy), static_cast<const T *>(ta), static_cast<const T *>(tb),
+                               static_cast<const T *>(wa), static_cast<const T *>(wb), static_cast<const T *>(wc), P,
+                               (int)Mo, g.O, g.C, J);
+        else
+            hipLaunchKernelGGL((qconv_bwd_data_cols_kernel<T, 2>), grid, dim3(kThreads), p.smem, st,
+                               static_cast<const T *>(gy), static_cast<const T *>(ta), static_cast<const T *>(tb),
+                               static_cast<const T *>(wa), static_cast<const T *>(wb), static_cast<const T *>(wc), P,
+                               (int)Mo, g.O, g.C, J);
+        const ql_status s0 = hip_status();
+        if (s0 != QL_OK) return s0;
         const long long M = (long long)g.N * g.H * g.W;
-        const int gr = g.O / g.vec();
-#define QL_SMALLC(GR)                                                                                             \
-    hipLaunchKernelGGL((qconv_bwd_data_smallc_kernel<T, GR>), dim3(grid_1d(M * GR)), dim3(kThreads), p.smem, st, \
-                       static_cast<const T *>(gy), static_cast<const T *>(ta), static_cast<const T *>(tb),         \
-                       static_cast<const T *>(wa), static_cast<const T *>(wb), static_cast<const T *>(wc),          \
-                       static_cast<T *>(dx), g.N, g.H, g.W, g.C, g.O, g.KH, g.KW, g.SH, g.SW, g.PH, g.PW, g.HO,    \
-                       g.WO)
-        switch (gr) {
-            case 1: QL_SMALLC(1); break;
-            case 2: QL_SMALLC(2); break;
-            case 4: QL_SMALLC(4); break;
-            case 8: QL_SMALLC(8); break;
-            case 16: QL_SMALLC(16); break;
-            case 32: QL_SMALLC(32); break;
-            default: QL_SMALLC(64); break;
-        }
-#undef QL_SMALLC
+        hipLaunchKernelGGL((qconv_bwd_data_col2im_kernel<T>), dim3(grid_1d(M)), dim3(kThreads), 0, st, P,
+                           static_cast<T *>(dx), g.N, g.H, g.W, g.C, g.KH, g.KW, g.SH, g.SW, g.PH, g.PW, g.HO, g.WO);
         return hip_status();
     }
     const int khkw = g.KH * g.KW;

@@ -51,12 +51,15 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 
 // Wait until at most N vector-memory operations of this thread are pending,
 // then barrier.  gfx9 s_waitcnt: vmcnt in bits [3:0] and [15:14], expcnt and
-// lgkmcnt left at their maxima (no wait on them).
+// lgkmcnt left at their maxima (no wait on them).  The wait goes through the
+// builtin, so the compiler's own wait insertion knows what has completed; the
+// barrier is asm with a memory clobber, so no LDS access moves across it.
 template <int N>
 __device__ __forceinline__ void wait_vm_barrier() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     constexpr int imm = (N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8);
-    asm volatile("s_waitcnt %0\n\ts_barrier" ::"n"(imm) : "memory");
+    __builtin_amdgcn_s_waitcnt(imm);
+    asm volatile("s_barrier" ::: "memory");
 }
 
 // The same, also waiting for this thread's outstanding LDS reads (so a ring
@@ -65,52 +68,60 @@ template <int N>
 __device__ __forceinline__ void wait_vm_barrier_lgkm() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     constexpr int imm = (N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8);
-    asm volatile("s_waitcnt %0\n\ts_barrier" ::"n"(imm) : "memory");
+    __builtin_amdgcn_s_waitcnt(imm);
+    asm volatile("s_barrier" ::: "memory");
 }
+
+// Waits for every outstanding global/DMA operation of this thread.
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // The software pipeline shared by the GEMM kernels.  A K step is two
 // 32-byte chunks; `read(slot, chunk, buf)` loads the MFMA fragments of one
 // chunk of the step held in ring slot `slot` into register set `buf` (0/1),
-// `mma(buf)` runs the MFMAs on a register set, and `issue(step, slot)` starts
-// the DMA of a K step into a ring slot.  Step j lives in slot j % NS.
+// `mma(buf)` runs the MFMAs on a register set, and `issue(step, slot, live)`
+// starts the DMA of a K step into a ring slot (every lane reading the zero
+// page when `live` is false).  Step j lives in slot j % NS.
 //
 // Iteration it (step it; chunk 0 already in register set 0):
 //   read chunk 1 of step it into set 1;
 //   issue step it + NS - 1 into the slot step it - 1 used, which every wave
-//     finished reading before the previous barrier (so these DMA
-//     instructions interleave with the MFMAs that follow);
+//     finished reading before the previous barrier;
 //   MFMAs on set 0;
 //   wait for step it + 1 and for this wave's LDS reads, barrier;
 //   read chunk 0 of step it + 1 into set 0;
 //   MFMAs on set 1.
-// NS - 1 steps are in flight while a step is being consumed.
+// The compiler interleaves the DMA address arithmetic, the LDS reads and
+// the MFMAs within each half.
+// Every iteration issues exactly NI DMA instructions per thread (past the
+// last step they fill a slot nobody reads again with zeros), so the loop body
+// is straight-line code and the vmcnt allowance is the same in every
+// iteration.  The last step issues nothing.  NS - 1 steps are in flight
+// while a step is being consumed.
 template <int NS, int NI, class Issue, class Read, class Mma>
 __device__ __forceinline__ void run_ring(int nst, int s_begin, Issue &&issue, Read &&read, Mma &&mma) {
     static_assert(NS >= 3 && (NS - 2) * NI < 64, "ring depth");
-#pragma unroll
-    for (int i = 0; i < NS - 1; ++i)
-        if (i < nst) issue(s_begin + i, i);
     if (nst <= 0) return;
-    if (nst >= NS - 1)
-        wait_vm_barrier<(NS - 2) * NI>();
-    else
-        wait_vm_barrier<0>();
+#pragma unroll
+    for (int i = 0; i < NS - 1; ++i) issue(s_begin + i, i, i < nst);
+    wait_vm_barrier<(NS - 2) * NI>();
     read(0, 0, 0);
     int slot = 0;
-    for (int it = 0; it < nst; ++it) {
+    // The last step is peeled off, so the loop body always takes the barrier
+    // path and the compiler's wait before the set-1 MFMAs is not widened by a
+    // merge with the barrier-less path.
+    for (int it = 0; it < nst - 1; ++it) {
         read(slot, 1, 1);
-        if (it + NS - 1 < nst) issue(s_begin + it + NS - 1, slot == 0 ? NS - 1 : slot - 1);
+        issue(s_begin + it + NS - 1, slot == 0 ? NS - 1 : slot - 1, it + NS - 1 < nst);
         mma(0);
-        if (it + 1 < nst) {
-            if (it + NS - 1 < nst)
-                wait_vm_barrier_lgkm<(NS - 2) * NI>();
-            else
-                wait_vm_barrier_lgkm<0>();
-            slot = slot + 1 == NS ? 0 : slot + 1;
-            read(slot, 0, 0);
-        }
+        wait_vm_barrier_lgkm<(NS - 2) * NI>();
+        slot = slot + 1 == NS ? 0 : slot + 1;
+        read(slot, 0, 0);
         mma(1);
     }
+    read(slot, 1, 1);
+    mma(0);
+    mma(1);
+    wait_vm_all();  // the zero-filling DMAs of the last iterations land before the LDS is released
 }
 
 // Plain barrier for LDS hand-offs that involve no DMA (epilogues).

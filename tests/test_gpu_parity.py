@@ -31,6 +31,9 @@ CONV_SHAPES = [
     (2, 12, 6, 6, 20, 2, 2, 2, 0),      # even kernel, stride 2
     (4, 3, 32, 32, 64, 3, 3, 1, 1),     # 3-channel image stem (channel padding, small-C input gradient)
     (3, 5, 11, 9, 24, 3, 3, 2, 1),      # 5 channels, stride 2
+    (2, 4, 10, 10, 32, 3, 3, 2, 1),     # 4 channels, stride 2: two column blocks of (r, q, c)
+    (3, 1, 7, 9, 16, 3, 3, 1, 0),       # 1 channel, no padding
+    (2, 2, 6, 7, 16, 5, 5, 1, 2),       # 2 channels, 5x5 kernel
 ]
 
 KEYS_FWD = ("y", "ta", "tb")
