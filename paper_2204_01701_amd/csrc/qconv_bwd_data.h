@@ -25,9 +25,10 @@
 
 namespace ql {
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool S1, bool NATW>
+template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool S1, bool NATW, bool CA>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataArgs a) {
     static_assert(!NATW || sizeof(T) == 2, "natural weight tiles need 16-bit elements");
+    static_assert(!CA || (S1 && NATW), "channel-aligned steps are implemented for stride 1, natural weight tiles");
     constexpr int VEC = Elem<T>::VEC;
     constexpr int KE = 64 / (int)sizeof(T);
     constexpr int ROWS = 3 * BR + 3 * BCOL;
@@ -91,8 +92,62 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         }
     }
 
+    // Channel-aligned K steps (CA: O a multiple of KE, stride 1): a K step lies
+    // within one tap, so tap and output-channel offset are wave-uniform and
+    // each DMA address is a per-lane base plus a scalar offset.  Weight
+    // columns past C and pixels past M re-read valid data (their results are
+    // never stored); taps whose output pixel lies outside the map are a
+    // per-lane bit mask.
+    const T *wrow[NATW ? NIW : 1];
+    long long go[NIP];
+    uint32_t gmask[NIP];
+    if constexpr (CA) {
+        const int wcc = min(wc0, a.C - 8);
+#pragma unroll
+        for (int i = 0; i < NIW; ++i) {
+            const int t = (i * 4096) / WT;
+            const int row = ((i * 4096) % WT + wave * 1024) / (SW * 16) + lane / SW;
+            wrow[i] = wt[t] + (size_t)row * khkw * a.C + wcc;
+        }
+#pragma unroll
+        for (int j = 0; j < NIP; ++j) {
+            const int m = min(ct * BCOL + 16 * (4 * j + wave) + (lane >> 2), a.M - 1);
+            const int n = (int)fdiv((uint32_t)m, a.fd_hw);
+            const int rem = m - n * a.H * a.W;
+            const int h = (int)fdiv((uint32_t)rem, a.fd_w);
+            const int w = rem - h * a.W;
+            const int i0 = h + a.PH, j0 = w + a.PW;  // output pixel of tap (0, 0)
+            go[j] = ((long long)n * a.HO * a.WO + (long long)i0 * a.WO + j0) * a.O + kcol * VEC;
+            uint32_t msk = 0;
+            for (int r = 0; r < a.KH; ++r)
+                for (int q = 0; q < a.KW; ++q)
+                    if ((unsigned)(i0 - r) < (unsigned)a.HO && (unsigned)(j0 - q) < (unsigned)a.WO)
+                        msk |= 1u << (r * a.KW + q);
+            gmask[j] = msk;
+        }
+    }
+
     auto issue = [&](int s, int slot, bool live) {
         char *base = smem + slot * STAGE + wave * 1024;
+        if constexpr (CA) {
+            const int k0 = min(s, a.stages_total - 1) * KE;
+            const int tap = (int)fdiv((uint32_t)k0, a.fd_o);
+            const int o0 = k0 - tap * a.O;
+            const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
+            const int q = tap - r * a.KW;
+            const long long sw = ((long long)o0 * khkw + tap) * a.C;
+#pragma unroll
+            for (int i = 0; i < NIW; ++i) dma16(wrow[i] + sw, base + i * 4096);
+            const long long sg = o0 - ((long long)r * a.WO + q) * a.O;
+#pragma unroll
+            for (int j = 0; j < NIP; ++j) {
+                const bool ok = live && ((gmask[j] >> tap) & 1u);
+#pragma unroll
+                for (int u = 0; u < 3; ++u)
+                    dma16(dma_src(ok, gsrc[u] + (go[j] + sg), a.zero), base + (NIW + u * NIP + j) * 4096);
+            }
+            return;
+        }
         const int k = s * KE + kcol * VEC;
         const bool kin = live && k < a.K;
         const int tap = (int)fdiv((uint32_t)k, a.fd_o);

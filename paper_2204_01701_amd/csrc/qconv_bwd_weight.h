@@ -132,17 +132,20 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
         for (int mc = 0; mc < MC; ++mc) {
             const v4u &g = gr[set][0][mc], &ta = gr[set][1][mc], &tb = gr[set][2][mc];
             float fa[8], fb[8];
-            float sa = 0.0f, sb = 0.0f, sc = 0.0f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float gv = vget<T>(g, e);
                 fa[e] = gv * vget<T>(tb, e);
                 fb[e] = gv * vget<T>(ta, e);
-                sa += fa[e];
-                sb += fb[e];
-                sc += gv;
             }
-            if (sum_db) {
+            if (sum_db) {  // wave-uniform: only the waves that own the bias sums add them up
+                float sa = 0.0f, sb = 0.0f, sc = 0.0f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    sa += fa[e];
+                    sb += fb[e];
+                    sc += vget<T>(g, e);
+                }
                 dsum[0][mc] += sa;
                 dsum[1][mc] += sb;
                 dsum[2][mc] += sc;

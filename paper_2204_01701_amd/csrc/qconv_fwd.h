@@ -20,7 +20,7 @@
 
 namespace ql {
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int NS>
+template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool CA>
 __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
     constexpr int VEC = Elem<T>::VEC;
     constexpr int KE = 64 / (int)sizeof(T);  // reduction elements per K step
@@ -83,8 +83,59 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
         }
     }
 
+    // Channel-aligned K steps (CA: C a multiple of KE, KH*KW <= 32): a K step
+    // lies within one tap, so tap and channel offset are wave-uniform and each
+    // DMA address is a per-lane base plus a scalar offset.  Weight rows past O
+    // and pixels past M re-read a valid row instead of zeros: their results are
+    // never stored.  Taps that land in the zero padding are a per-lane bit mask.
+    const T *wrow[NIW];
+    long long xo[NIX];
+    uint32_t xmask[NIX];
+    if constexpr (CA) {
+#pragma unroll
+        for (int i = 0; i < NIW; ++i) {
+            const int row = 16 * (4 * i + wave) + (lane >> 2);
+            const int t = row / BR;
+            const int o = min(rt * BR + (row - t * BR), a.O - 1);
+            wrow[i] = wp[t] + (size_t)o * a.K + kcol * VEC;
+        }
+#pragma unroll
+        for (int j = 0; j < NIX; ++j) {
+            const int p = 16 * (4 * (NIW + j) + wave) + (lane >> 2) - 3 * BR;
+            const int m = min(ct * BCOL + p, a.M - 1);
+            const int n = (int)fdiv((uint32_t)m, a.fd_howo);
+            const int rem = m - n * a.HO * a.WO;
+            const int oh = (int)fdiv((uint32_t)rem, a.fd_wo);
+            const int ow = rem - oh * a.WO;
+            const int h0 = oh * a.SH - a.PH, w0 = ow * a.SW - a.PW;
+            xo[j] = (long long)n * a.H * a.W * a.C + ((long long)h0 * a.W + w0) * a.C + kcol * VEC;
+            uint32_t msk = 0;
+            for (int r = 0; r < a.KH; ++r)
+                for (int q = 0; q < a.KW; ++q)
+                    if ((unsigned)(h0 + r) < (unsigned)a.H && (unsigned)(w0 + q) < (unsigned)a.W)
+                        msk |= 1u << (r * a.KW + q);
+            xmask[j] = msk;
+        }
+    }
+
     auto issue = [&](int s, int slot, bool live) {
         char *base = smem + slot * STAGE + wave * 1024;
+        if constexpr (CA) {
+            const int k0 = min(s, a.stages_total - 1) * KE;
+            const int tap = (int)fdiv((uint32_t)k0, a.fd_c);
+            const int c0 = k0 - tap * a.C;
+            const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
+            const int q = tap - r * a.KW;
+            const long long soff = ((long long)r * a.W + q) * a.C + c0;
+#pragma unroll
+            for (int i = 0; i < NIW; ++i) dma16(wrow[i] + k0, base + i * 4096);
+#pragma unroll
+            for (int j = 0; j < NIX; ++j) {
+                const bool ok = live && ((xmask[j] >> tap) & 1u);
+                dma16(dma_src(ok, x + (xo[j] + soff), a.zero), base + (NIW + j) * 4096);
+            }
+            return;
+        }
         const int k = s * KE + kcol * VEC;
         const bool kin = live && k < a.K;
         const int tap = (int)fdiv((uint32_t)k, a.fd_c);

@@ -360,12 +360,22 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     a.fd_kw = make_fastdiv(g.KW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     if (p.veck) {
+        // channel-aligned K steps: every step within one tap
+        const bool ca = C % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
+#define QL_FWD(BR, BC, WR, WC)                                                                                    \
+    do {                                                                                                          \
+        if (ca)                                                                                                   \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BC, WR, WC, 4, true>), grid, block, 0, st, a);           \
+        else                                                                                                      \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BC, WR, WC, 4, false>), grid, block, 0, st, a);          \
+    } while (0)
         switch (p.cfg) {
-            case 0: hipLaunchKernelGGL((qconv_fwd_kernel<T, 128, 128, 4, 1, 4>), grid, block, 0, st, a); break;
-            case 1: hipLaunchKernelGGL((qconv_fwd_kernel<T, 64, 256, 2, 2, 4>), grid, block, 0, st, a); break;
-            case 2: hipLaunchKernelGGL((qconv_fwd_kernel<T, 128, 128, 2, 2, 4>), grid, block, 0, st, a); break;
-            default: hipLaunchKernelGGL((qconv_fwd_kernel<T, 64, 128, 2, 2, 4>), grid, block, 0, st, a); break;
+            case 0: QL_FWD(128, 128, 4, 1); break;
+            case 1: QL_FWD(64, 256, 2, 2); break;
+            case 2: QL_FWD(128, 128, 2, 2); break;
+            default: QL_FWD(64, 128, 2, 2); break;
         }
+#undef QL_FWD
     } else if (p.cfg == 0) {
         hipLaunchKernelGGL((qconv_fwd_generic_kernel<T, 128, 128, 2, 2, 64, false>), grid, block, 0, st, a);
     } else {
@@ -444,22 +454,31 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.fd_sh = make_fastdiv(g.SH);
     a.fd_sw = make_fastdiv(g.SW);
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
-#define QL_BD_PIPE_N(BR, BCOL, NS, NW)                                                                          \
-    do {                                                                                                        \
-        if (p.s1)                                                                                               \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true, NW>), grid, block, 0, st, a);  \
-        else                                                                                                    \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, false, NW>), grid, block, 0, st, a); \
+    // channel-aligned K steps (each within one tap): stride 1, natural weight tiles, O a multiple of KE
+    const bool bd_ca = p.s1 && p.natw && g.O % p.KE == 0 && g.KH * g.KW <= 32 &&
+                       env_override("QLAYER_BWD_DATA_CA", 1) != 0;
+#define QL_BD_PIPE_N(BR, BCOL, NS, NW)                                                                              \
+    do {                                                                                                            \
+        if (p.s1)                                                                                                   \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true, NW, false>), grid, block, 0, st, a); \
+        else                                                                                                        \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, false, NW, false>), grid, block, 0, st, \
+                               a);                                                                                  \
     } while (0)
-#define QL_BD_PIPE(BR, BCOL, NS)                                 \
-    do {                                                         \
-        if constexpr (sizeof(T) == 2) {                          \
-            if (p.natw) {                                        \
-                QL_BD_PIPE_N(BR, BCOL, NS, true);                \
-                break;                                           \
-            }                                                    \
-        }                                                        \
-        QL_BD_PIPE_N(BR, BCOL, NS, false);                       \
+#define QL_BD_PIPE(BR, BCOL, NS)                                                                                     \
+    do {                                                                                                             \
+        if constexpr (sizeof(T) == 2) {                                                                              \
+            if (bd_ca) {                                                                                             \
+                hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true, true, true>), grid, block, 0, \
+                                   st, a);                                                                           \
+                break;                                                                                               \
+            }                                                                                                        \
+            if (p.natw) {                                                                                            \
+                QL_BD_PIPE_N(BR, BCOL, NS, true);                                                                    \
+                break;                                                                                               \
+            }                                                                                                        \
+        }                                                                                                            \
+        QL_BD_PIPE_N(BR, BCOL, NS, false);                                                                           \
     } while (0)
 #define QL_BD_GEN(BR, BCOL)                                                                                      \
     do {                                                                                                         \
