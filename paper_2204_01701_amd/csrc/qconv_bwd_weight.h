@@ -22,8 +22,11 @@
 
 namespace ql {
 
-template <int BKP, int BO, int WGR, int WGC, int NS>
-__global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWeightArgs a) {
+// The kernel body; SUM: this workgroup also accumulates the bias gradients
+// (row tile 0).  Instantiated twice so that the workgroups without bias sums
+// run code with no trace of them (fewer live registers in the main loop).
+template <int BKP, int BO, int WGR, int WGC, int NS, int NT, bool SUM>
+__device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *smem) {
     using T = uint16_t;                 // bf16 only: the transposed LDS read is 16-bit
     constexpr int KE = 32;              // output pixels per K step (two MFMA k-chunks)
     constexpr int SX = BKP / 8;         // 16-byte slots per X row
@@ -31,17 +34,16 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
     constexpr int XB = KE * BKP * 2;    // bytes of the X tile
     constexpr int GB = KE * BO * 2;     // bytes of each G-side tile
     constexpr int STAGE = XB + 3 * GB;
-    constexpr int NIX = XB / 4096;      // DMA instructions per thread per K step
-    constexpr int NIG = GB / 4096;
+    constexpr int NW = NT / 64;         // waves
+    constexpr int NIX = XB / (NT * 16); // DMA instructions per thread per K step
+    constexpr int NIG = GB / (NT * 16);
     constexpr int NI = NIX + 3 * NIG;
     constexpr int RX = 64 / SX;         // rows one wave-instruction fills
     constexpr int RG = 64 / SG;
     constexpr int MR = BKP / WGR / 32, MC = BO / WGC / 32;
-    static_assert(WGR * WGC == kThreads / 64, "one wave per wave-tile");
-    static_assert(XB % 4096 == 0 && GB % 4096 == 0 && SX <= 64 && SG <= 64, "whole DMA rounds");
+    static_assert(WGR * WGC == NW, "one wave per wave-tile");
+    static_assert(XB % (NT * 16) == 0 && GB % (NT * 16) == 0 && SX <= 64 && SG <= 64, "whole DMA rounds");
     static_assert(MR >= 1 && MC >= 1, "tile shape");
-
-    __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
     const int wr = wave / WGC, wc = wave % WGC;
@@ -57,9 +59,12 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
     const T *__restrict__ gsrc[3] = {static_cast<const T *>(a.gy), static_cast<const T *>(a.ta),
                                      static_cast<const T *>(a.tb)};
 
-    // X fill: instruction i of this wave writes rows RX * (4 i + wave) .. +RX;
-    // this lane fills row RX * (4 i + wave) + lane / SX at a fixed logical slot.
-    const int xslot = (lane % SX) ^ nat_swz<SX>(lane / SX);
+    // X fill: instruction i of this wave writes rows RX * (NW i + wave) .. +RX;
+    // this lane fills row RX * (NW i + wave) + lane / SX at a fixed logical slot.
+    // (the swizzle needs the tile row mod 4 (mod 8 for 8-slot rows); RX * NW * i
+    // is a multiple of that, so the row of instruction 0 gives it for all i)
+    static_assert((RX * NW) % 8 == 0 && (RG * NW) % 8 == 0, "swizzle phase");
+    const int xslot = (lane % SX) ^ nat_swz<SX>(RX * wave + lane / SX);
     const int kp = rt * BKP + 8 * xslot;  // first of the 8 k' this lane copies
     const bool kp_ok = kp < a.KP;
     int xr, xq, xc;
@@ -70,7 +75,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
         xq = tap - xr * a.KW;
     }
     // G fill: same scheme with rows of SG slots.
-    const int gslot = (lane % SG) ^ nat_swz<SG>(lane / SG);
+    const int gslot = (lane % SG) ^ nat_swz<SG>(RG * wave + lane / SG);
     const int og = ct * BO + 8 * gslot;
     const bool og_ok = og < a.O;
 
@@ -78,23 +83,23 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
         char *base = smem + slot * STAGE + wave * 1024;
 #pragma unroll
         for (int i = 0; i < NIX; ++i) {
-            const int m = s * KE + RX * (4 * i + wave) + lane / SX;
+            const int m = s * KE + RX * (NW * i + wave) + lane / SX;
             const int n = (int)fdiv((uint32_t)m, a.fd_howo);
             const int rem = m - n * a.HO * a.WO;
             const int oh = (int)fdiv((uint32_t)rem, a.fd_wo);
             const int ow = rem - oh * a.WO;
             const int ih = oh * a.SH - a.PH + xr, iw = ow * a.SW - a.PW + xq;
             const bool ok = live && kp_ok && m < a.M && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-            dma16(dma_src(ok, x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + xc, a.zero), base + i * 4096);
+            dma16(dma_src(ok, x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + xc, a.zero), base + i * (NT * 16));
         }
 #pragma unroll
         for (int i = 0; i < NIG; ++i) {
-            const int m = s * KE + RG * (4 * i + wave) + lane / SG;
+            const int m = s * KE + RG * (NW * i + wave) + lane / SG;
             const bool ok = live && og_ok && m < a.M;
             const size_t off = (size_t)m * a.O + og;
 #pragma unroll
             for (int u = 0; u < 3; ++u)
-                dma16(dma_src(ok, gsrc[u] + off, a.zero), base + XB + u * GB + i * 4096);
+                dma16(dma_src(ok, gsrc[u] + off, a.zero), base + XB + u * GB + i * (NT * 16));
         }
     };
 
@@ -112,9 +117,10 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
     for (int t = 0; t < 3; ++t)
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) dsum[t][mc] = 0.0f;
-    const bool sum_db = a.want_db && rt == 0 && wr == 0;
+    const bool sum_db = SUM && wr == 0;
 
-    v4u af[2][MR], gr[2][3][MC];  // two register sets: X and G, T_a, T_b fragments
+    constexpr int SETS = NT > 256 ? 1 : 2;  // fragment register sets (one when two waves share a SIMD)
+    v4u af[SETS][MR], gr[SETS][3][MC];      // X and G, T_a, T_b fragments
     auto read = [&](int slot, int ch, int set) {
         const char *xt = smem + slot * STAGE;
         const char *gt = xt + XB;
@@ -138,17 +144,19 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
                 fa[e] = gv * vget<T>(tb, e);
                 fb[e] = gv * vget<T>(ta, e);
             }
-            if (sum_db) {  // wave-uniform: only the waves that own the bias sums add them up
-                float sa = 0.0f, sb = 0.0f, sc = 0.0f;
+            if constexpr (SUM) {
+                if (sum_db) {  // wave-uniform: only the waves that own the bias sums add them up
+                    float sa = 0.0f, sb = 0.0f, sc = 0.0f;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    sa += fa[e];
-                    sb += fb[e];
-                    sc += vget<T>(g, e);
+                    for (int e = 0; e < 8; ++e) {
+                        sa += fa[e];
+                        sb += fb[e];
+                        sc += vget<T>(g, e);
+                    }
+                    dsum[0][mc] += sa;
+                    dsum[1][mc] += sb;
+                    dsum[2][mc] += sc;
                 }
-                dsum[0][mc] += sa;
-                dsum[1][mc] += sb;
-                dsum[2][mc] += sc;
             }
             const v4u bt[3] = {vpack<T>(fa), vpack<T>(fb), g};
 #pragma unroll
@@ -157,7 +165,10 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
                 for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[set][mr], bt[t], acc[t][mr][mc]);
         }
     };
-    run_ring<NS, NI>(nst, s_begin, issue, read, mma);
+    if constexpr (SETS == 2)
+        run_ring<NS, NI>(nst, s_begin, issue, read, mma);
+    else
+        run_ring_single<NS, NI>(nst, s_begin, issue, read, mma);
 
     // dW epilogue: rows k', columns o; lane holds 4 consecutive k' per group.
     const int krow0 = rt * BKP + wr * (BKP / WGR);
@@ -202,7 +213,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
     }
 
     // Bias gradients: lanes l and l + 32 hold the two pixel halves of channel l % 32.
-    if (sum_db) {
+    if (SUM && sum_db) {
 #pragma unroll
         for (int t = 0; t < 3; ++t)
 #pragma unroll
@@ -217,6 +228,20 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_kernel(const BwdWei
                 }
             }
     }
+}
+
+template <int BKP, int BO, int WGR, int WGC, int NS, int NT = kThreads>
+__global__ __launch_bounds__(NT) void qconv_bwd_weight_kernel(const BwdWeightArgs a) {
+    constexpr int STAGE = 32 * BKP * 2 + 3 * 32 * BO * 2;
+    __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+    // the same tile decomposition as the body: row tile 0 owns the bias sums
+    int bid = xcd_remap(blockIdx.x, gridDim.x);
+    const int tiles = a.row_tiles * a.col_tiles;
+    bid -= (bid / tiles) * tiles;
+    if (a.want_db && bid % a.row_tiles == 0)
+        bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true>(a, smem);
+    else
+        bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false>(a, smem);
 }
 
 }  // namespace ql

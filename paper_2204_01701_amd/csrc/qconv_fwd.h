@@ -20,18 +20,19 @@
 
 namespace ql {
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool CA>
-__global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
+template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool CA, int NT = kThreads>
+__global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     constexpr int VEC = Elem<T>::VEC;
     constexpr int KE = 64 / (int)sizeof(T);  // reduction elements per K step
     constexpr int ROWS = 3 * BR + BCOL;
     constexpr int STAGE = ROWS * 64;
-    constexpr int NIW = 3 * BR / 64;  // DMA instructions per thread per K step: weight rows
-    constexpr int NIX = BCOL / 64;    // ... pixel rows
+    constexpr int RPI = NT / 4;         // 64-byte tile rows one DMA instruction of the workgroup fills
+    constexpr int NIW = 3 * BR / RPI;   // DMA instructions per thread per K step: weight rows
+    constexpr int NIX = BCOL / RPI;     // ... pixel rows
     constexpr int NI = NIW + NIX;
     constexpr int MR = BR / WGR / 32, MC = BCOL / WGC / 32;
-    static_assert(WGR * WGC == kThreads / 64, "one wave per wave-tile");
-    static_assert(BR % 64 == 0 && BCOL % 64 == 0 && MR >= 1 && MC >= 1, "tile shape");
+    static_assert(WGR * WGC == NT / 64, "one wave per wave-tile");
+    static_assert((3 * BR) % RPI == 0 && BCOL % RPI == 0 && MR >= 1 && MC >= 1, "tile shape");
 
     __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
@@ -50,14 +51,14 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
                       static_cast<const T *>(a.w[2])};
 
     // Fill geometry: DMA instruction i of this wave writes tile rows
-    // 16 * (4 i + wave) .. +16; this lane fills row 16 * (4 i + wave) + lane / 4,
+    // RPI i + 16 wave .. +16; this lane fills row RPI i + 16 wave + lane / 4,
     // logical 16-byte column kcol (the same for every instruction).
     const int kcol = km_fill_col(lane);
     int woff[NIW];
     int wterm[NIW];
 #pragma unroll
     for (int i = 0; i < NIW; ++i) {
-        const int row = 16 * (4 * i + wave) + (lane >> 2);
+        const int row = RPI * i + 16 * wave + (lane >> 2);
         const int t = row / BR;
         const int o = rt * BR + (row - t * BR);
         wterm[i] = t;
@@ -66,7 +67,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
     int xoff[NIX], ih0[NIX], iw0[NIX];
 #pragma unroll
     for (int j = 0; j < NIX; ++j) {
-        const int p = 16 * (4 * (NIW + j) + wave) + (lane >> 2) - 3 * BR;
+        const int p = RPI * (NIW + j) + 16 * wave + (lane >> 2) - 3 * BR;
         const int m = ct * BCOL + p;
         if (m < a.M) {
             const int n = (int)fdiv((uint32_t)m, a.fd_howo);
@@ -94,14 +95,14 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
     if constexpr (CA) {
 #pragma unroll
         for (int i = 0; i < NIW; ++i) {
-            const int row = 16 * (4 * i + wave) + (lane >> 2);
+            const int row = RPI * i + 16 * wave + (lane >> 2);
             const int t = row / BR;
             const int o = min(rt * BR + (row - t * BR), a.O - 1);
             wrow[i] = wp[t] + (size_t)o * a.K + kcol * VEC;
         }
 #pragma unroll
         for (int j = 0; j < NIX; ++j) {
-            const int p = 16 * (4 * (NIW + j) + wave) + (lane >> 2) - 3 * BR;
+            const int p = RPI * (NIW + j) + 16 * wave + (lane >> 2) - 3 * BR;
             const int m = min(ct * BCOL + p, a.M - 1);
             const int n = (int)fdiv((uint32_t)m, a.fd_howo);
             const int rem = m - n * a.HO * a.WO;
@@ -128,11 +129,11 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
             const int q = tap - r * a.KW;
             const long long soff = ((long long)r * a.W + q) * a.C + c0;
 #pragma unroll
-            for (int i = 0; i < NIW; ++i) dma16(wrow[i] + k0, base + i * 4096);
+            for (int i = 0; i < NIW; ++i) dma16(wrow[i] + k0, base + i * (NT * 16));
 #pragma unroll
             for (int j = 0; j < NIX; ++j) {
                 const bool ok = live && ((xmask[j] >> tap) & 1u);
-                dma16(dma_src(ok, x + (xo[j] + soff), a.zero), base + (NIW + j) * 4096);
+                dma16(dma_src(ok, x + (xo[j] + soff), a.zero), base + (NIW + j) * (NT * 16));
             }
             return;
         }
@@ -145,13 +146,13 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
 #pragma unroll
         for (int i = 0; i < NIW; ++i) {
             const bool ok = kin && woff[i] >= 0;
-            dma16(dma_src(ok, wp[wterm[i]] + woff[i] + k, a.zero), base + i * 4096);
+            dma16(dma_src(ok, wp[wterm[i]] + woff[i] + k, a.zero), base + i * (NT * 16));
         }
 #pragma unroll
         for (int j = 0; j < NIX; ++j) {
             const int ih = ih0[j] + r, iw = iw0[j] + q;
             const bool ok = kin && xoff[j] >= 0 && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-            dma16(dma_src(ok, x + xoff[j] + (ih * a.W + iw) * a.C + c, a.zero), base + (NIW + j) * 4096);
+            dma16(dma_src(ok, x + xoff[j] + (ih * a.W + iw) * a.C + c, a.zero), base + (NIW + j) * (NT * 16));
         }
     };
 
@@ -178,7 +179,8 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
     // Fragment reads: row lrow of each 32-row block, logical column 2 * ch + lhi.
     const int swz = (lrow >> 2) & 3;
     const int colx0 = ((0 + lhi) ^ swz) << 4, colx1 = ((2 + lhi) ^ swz) << 4;
-    v4u bf[2][MC], af[2][3][MR];  // two register sets of fragments
+    constexpr int SETS = NT > 256 ? 1 : 2;  // fragment register sets (one when two waves share a SIMD)
+    v4u bf[SETS][MC], af[SETS][3][MR];
     auto read = [&](int slot, int ch, int set) {
         const char *base = smem + slot * STAGE + lrow * 64 + (ch == 0 ? colx0 : colx1);
 #pragma unroll
@@ -198,7 +200,10 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_kernel(const FwdArgs a) {
 #pragma unroll
                 for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af[set][t][mr], bf[set][mc], acc[t][mr][mc]);
     };
-    run_ring<NS, NI>(nst, s_begin, issue, read, mma);
+    if constexpr (SETS == 2)
+        run_ring<NS, NI>(nst, s_begin, issue, read, mma);
+    else
+        run_ring_single<NS, NI>(nst, s_begin, issue, read, mma);
 
     // Epilogue.
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);

@@ -139,12 +139,16 @@ void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_s
 // Forward planning.
 // ---------------------------------------------------------------------------
 // Pipelined forward tile configurations (rows = output channels per term,
-// columns = output pixels; per-wave tile in parentheses):
-//   0: 128 x 128 (32 x 128), 1: 64 x 256 (32 x 128), 2: 128 x 128 (64 x 64), 3: 64 x 128 (32 x 64).
-constexpr int kFwdBR[4] = {128, 64, 128, 64};
-constexpr int kFwdBCOL[4] = {128, 256, 128, 128};
+// columns = output pixels; per-wave tile in parentheses; 4 waves unless noted):
+//   0: 128 x 128 (32 x 128), 1: 64 x 256 (32 x 128), 2: 128 x 128 (64 x 64), 3: 64 x 128 (32 x 64),
+//   4: 128 x 256 (32 x 128, 8 waves), 5: 128 x 256 (64 x 64, 8 waves).
+// Larger workgroup tiles move fewer bytes through the vector-memory address
+// path per MFMA: 32768 (1/BCOL + 1/(3 BR)) bytes.
+constexpr int kFwdCfgs = 6;
+constexpr int kFwdBR[kFwdCfgs] = {128, 64, 128, 64, 128, 128};
+constexpr int kFwdBCOL[kFwdCfgs] = {128, 256, 128, 128, 256, 256};
 // Workgroups one CU holds at once (limited by LDS stages and registers).
-constexpr int kFwdSlots[4] = {1, 1, 1, 2};
+constexpr int kFwdSlots[kFwdCfgs] = {1, 1, 1, 2, 1, 1};
 
 struct FwdPlan {
     int cfg;  // pipelined: index into kFwd*; generic: 0: 128 x 128, 1: 64 x 128
@@ -168,8 +172,10 @@ FwdPlan plan_fwd(const Geom &g) {
         p.wpad_bytes = align_up((size_t)g.O * g.KH * g.KW * p.Cp * g.esize());
     }
     if (p.veck) {
-        p.cfg = env_override("QLAYER_FWD_CFG", 3);
-        if (p.cfg < 0 || p.cfg > 3) p.cfg = 3;
+        // 8-wave 128 x 256 tiles where there are enough of them to fill the GPU several times
+        const bool big = g.O >= 128 && (long long)cdiv(g.O, 128) * cdiv(M, 256) >= 4 * kNumCUs;
+        p.cfg = env_override("QLAYER_FWD_CFG", big ? 4 : 3);
+        if (p.cfg < 0 || p.cfg >= kFwdCfgs) p.cfg = 3;
         p.BR = kFwdBR[p.cfg];
         p.BCOL = kFwdBCOL[p.cfg];
         p.slots = kFwdSlots[p.cfg];
@@ -227,7 +233,7 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
     p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
     if (p.veck) {
         int dflt = 1;
-        if (g.C > 64) dflt = (long long)cdiv(g.C, 128) * cdiv(M, 128) >= kNumCUs ? 0 : 2;
+        if (g.C > 64) dflt = M >= 1024 ? 0 : 2;
         p.cfg = env_override("QLAYER_BWD_DATA_CFG", dflt);
         if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
         p.BR = kBdBR[p.cfg];
@@ -255,9 +261,10 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
 // ---------------------------------------------------------------------------
 // Pipelined (bf16) weight-gradient tile configurations (rows = k', columns =
 // output channels per term):  0: 128 x 64, 1: 128 x 128, 2: 64 x 64.
-constexpr int kBwBKP[3] = {128, 128, 64};
-constexpr int kBwBO[3] = {64, 128, 64};
-constexpr int kBwSlots[3] = {2, 1, 2};  // workgroups one CU holds at once
+constexpr int kBwCfgs = 3;
+constexpr int kBwBKP[kBwCfgs] = {128, 128, 64};
+constexpr int kBwBO[kBwCfgs] = {64, 128, 64};
+constexpr int kBwSlots[kBwCfgs] = {2, 1, 2};  // workgroups one CU holds at once
 
 struct BwdWeightPlan {
     int cfg;   // pipelined path only
@@ -280,7 +287,7 @@ BwdWeightPlan plan_bwd_weight(const Geom &g) {
     if (p.pad) p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
     if (p.pipe) {
         p.cfg = env_override("QLAYER_BWD_WEIGHT_CFG", 0);
-        if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
+        if (p.cfg < 0 || p.cfg >= kBwCfgs) p.cfg = 0;
         p.BKP = kBwBKP[p.cfg];
         p.BO = kBwBO[p.cfg];
         p.slots = kBwSlots[p.cfg];
@@ -362,18 +369,20 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     if (p.veck) {
         // channel-aligned K steps: every step within one tap
         const bool ca = C % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
-#define QL_FWD(BR, BC, WR, WC)                                                                                    \
+#define QL_FWD(BR, BC, WR, WC, NS, NT)                                                                           \
     do {                                                                                                          \
         if (ca)                                                                                                   \
-            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BC, WR, WC, 4, true>), grid, block, 0, st, a);           \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BC, WR, WC, NS, true, NT>), grid, dim3(NT), 0, st, a);   \
         else                                                                                                      \
-            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BC, WR, WC, 4, false>), grid, block, 0, st, a);          \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, BR, BC, WR, WC, NS, false, NT>), grid, dim3(NT), 0, st, a);  \
     } while (0)
         switch (p.cfg) {
-            case 0: QL_FWD(128, 128, 4, 1); break;
-            case 1: QL_FWD(64, 256, 2, 2); break;
-            case 2: QL_FWD(128, 128, 2, 2); break;
-            default: QL_FWD(64, 128, 2, 2); break;
+            case 0: QL_FWD(128, 128, 4, 1, 4, 256); break;
+            case 1: QL_FWD(64, 256, 2, 2, 4, 256); break;
+            case 2: QL_FWD(128, 128, 2, 2, 4, 256); break;
+            case 4: QL_FWD(128, 256, 4, 2, 3, 512); break;
+            case 5: QL_FWD(128, 256, 2, 4, 3, 512); break;
+            default: QL_FWD(64, 128, 2, 2, 4, 256); break;
         }
 #undef QL_FWD
     } else if (p.cfg == 0) {

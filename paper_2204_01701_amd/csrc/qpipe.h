@@ -124,6 +124,33 @@ __device__ __forceinline__ void run_ring(int nst, int s_begin, Issue &&issue, Re
     wait_vm_all();  // the zero-filling DMAs of the last iterations land before the LDS is released
 }
 
+// The same pipeline with ONE register set of fragments, for kernels that run
+// two waves per SIMD and need the registers for accumulators: each chunk is
+// read and then multiplied; the other wave on the SIMD covers the LDS latency.
+template <int NS, int NI, class Issue, class Read, class Mma>
+__device__ __forceinline__ void run_ring_single(int nst, int s_begin, Issue &&issue, Read &&read, Mma &&mma) {
+    static_assert(NS >= 3 && (NS - 2) * NI < 64, "ring depth");
+    if (nst <= 0) return;
+#pragma unroll
+    for (int i = 0; i < NS - 1; ++i) issue(s_begin + i, i, i < nst);
+    wait_vm_barrier<(NS - 2) * NI>();
+    int slot = 0;
+    for (int it = 0; it < nst - 1; ++it) {
+        issue(s_begin + it + NS - 1, slot == 0 ? NS - 1 : slot - 1, it + NS - 1 < nst);
+        read(slot, 0, 0);
+        mma(0);
+        read(slot, 1, 0);
+        mma(0);
+        wait_vm_barrier_lgkm<(NS - 2) * NI>();
+        slot = slot + 1 == NS ? 0 : slot + 1;
+    }
+    read(slot, 0, 0);
+    mma(0);
+    read(slot, 1, 0);
+    mma(0);
+    wait_vm_all();
+}
+
 // Plain barrier for LDS hand-offs that involve no DMA (epilogues).
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
