@@ -199,9 +199,11 @@ FwdPlan plan_fwd(const Geom &g) {
 // Input-gradient planning.  Workspace: transposed weights, then split partials.
 // ---------------------------------------------------------------------------
 // Pipelined input-gradient tile configurations (rows = input channels,
-// columns = input pixels):  0: 128 x 128, 1: 64 x 128, 2: 128 x 64.
-constexpr int kBdBR[3] = {128, 64, 128};
-constexpr int kBdBCOL[3] = {128, 128, 64};
+// columns = input pixels):  0: 128 x 128, 1: 64 x 128, 2: 128 x 64, 3: 128 x 128
+// with the four waves side by side (each 128 x 32: half the prologue
+// products per MFMA of configuration 0).
+constexpr int kBdBR[4] = {128, 64, 128, 128};
+constexpr int kBdBCOL[4] = {128, 128, 64, 128};
 
 struct BwdDataPlan {
     int cfg;  // pipelined: index into kBd*; generic: 0: 128 x 128, 1: 64 x 128
@@ -233,9 +235,9 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
     p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
     if (p.veck) {
         int dflt = 1;
-        if (g.C > 64) dflt = M >= 1024 ? 0 : 2;
+        if (g.C > 64) dflt = M >= 1024 ? 3 : 2;
         p.cfg = env_override("QLAYER_BWD_DATA_CFG", dflt);
-        if (p.cfg < 0 || p.cfg > 2) p.cfg = 0;
+        if (p.cfg < 0 || p.cfg > 3) p.cfg = 0;
         p.BR = kBdBR[p.cfg];
         p.BCOL = kBdBCOL[p.cfg];
     } else {
@@ -466,28 +468,28 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     // channel-aligned K steps (each within one tap): stride 1, natural weight tiles, O a multiple of KE
     const bool bd_ca = p.s1 && p.natw && g.O % p.KE == 0 && g.KH * g.KW <= 32 &&
                        env_override("QLAYER_BWD_DATA_CA", 1) != 0;
-#define QL_BD_PIPE_N(BR, BCOL, NS, NW)                                                                              \
-    do {                                                                                                            \
-        if (p.s1)                                                                                                   \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true, NW, false>), grid, block, 0, st, a); \
-        else                                                                                                        \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, false, NW, false>), grid, block, 0, st, \
-                               a);                                                                                  \
+#define QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, NW)                                                                        \
+    do {                                                                                                              \
+        if (p.s1)                                                                                                     \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, true, NW, false>), grid, block, 0, st, a); \
+        else                                                                                                          \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, false, NW, false>), grid, block, 0, st, \
+                               a);                                                                                    \
     } while (0)
-#define QL_BD_PIPE(BR, BCOL, NS)                                                                                     \
-    do {                                                                                                             \
-        if constexpr (sizeof(T) == 2) {                                                                              \
-            if (bd_ca) {                                                                                             \
-                hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, 2, 2, NS, true, true, true>), grid, block, 0, \
-                                   st, a);                                                                           \
-                break;                                                                                               \
-            }                                                                                                        \
-            if (p.natw) {                                                                                            \
-                QL_BD_PIPE_N(BR, BCOL, NS, true);                                                                    \
-                break;                                                                                               \
-            }                                                                                                        \
-        }                                                                                                            \
-        QL_BD_PIPE_N(BR, BCOL, NS, false);                                                                           \
+#define QL_BD_PIPE(BR, BCOL, WR, WC, NS)                                                                              \
+    do {                                                                                                              \
+        if constexpr (sizeof(T) == 2) {                                                                               \
+            if (bd_ca) {                                                                                              \
+                hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, true, true, true>), grid, block, 0, \
+                                   st, a);                                                                            \
+                break;                                                                                                \
+            }                                                                                                         \
+            if (p.natw) {                                                                                             \
+                QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, true);                                                             \
+                break;                                                                                                \
+            }                                                                                                         \
+        }                                                                                                             \
+        QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, false);                                                                    \
     } while (0)
 #define QL_BD_GEN(BR, BCOL)                                                                                      \
     do {                                                                                                         \
@@ -500,11 +502,13 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     } while (0)
     if (p.veck) {
         if (p.cfg == 0)
-            QL_BD_PIPE(128, 128, 3);
+            QL_BD_PIPE(128, 128, 2, 2, 3);
         else if (p.cfg == 1)
-            QL_BD_PIPE(64, 128, 4);
+            QL_BD_PIPE(64, 128, 2, 2, 4);
+        else if (p.cfg == 3)
+            QL_BD_PIPE(128, 128, 1, 4, 3);
         else
-            QL_BD_PIPE(128, 64, 4);
+            QL_BD_PIPE(128, 64, 2, 2, 4);
     } else if (p.cfg == 0) {
         QL_BD_GEN(128, 128);
     } else {
