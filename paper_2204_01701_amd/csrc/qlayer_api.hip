@@ -11,6 +11,7 @@
 #include "qlayer.h"
 #include "qconv_aux.h"
 #include "qconv_bwd_data.h"
+#include "qconv_bwd_data_wide.h"
 #include "qconv_bwd_weight.h"
 #include "qconv_fwd.h"
 #include "qconv_generic.h"
@@ -202,8 +203,8 @@ FwdPlan plan_fwd(const Geom &g) {
 // columns = input pixels):  0: 128 x 128, 1: 64 x 128, 2: 128 x 64, 3: 128 x 128
 // with the four waves side by side (each 128 x 32: half the prologue
 // products per MFMA of configuration 0).
-constexpr int kBdBR[4] = {128, 64, 128, 128};
-constexpr int kBdBCOL[4] = {128, 128, 64, 128};
+constexpr int kBdBR[5] = {128, 64, 128, 128, 256};
+constexpr int kBdBCOL[5] = {128, 128, 64, 128, 256};  // 4: the wide kernel (8 waves, 16-channel K steps)
 
 struct BwdDataPlan {
     int cfg;  // pipelined: index into kBd*; generic: 0: 128 x 128, 1: 64 x 128
@@ -233,11 +234,17 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
     const int M = g.N * g.H * g.W, K = g.KH * g.KW * g.O;
     p.veck = g.O % g.vec() == 0;
     p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
+    p.s1 = g.SH == 1 && g.SW == 1;
+    // the wide kernel: bf16, natural weight tiles, stride 1, 16-channel K steps within one tap
+    const bool wide_ok = p.natw && p.s1 && g.O % 16 == 0 && g.KH * g.KW <= 32;
     if (p.veck) {
         int dflt = 1;
         if (g.C > 64) dflt = M >= 1024 ? 3 : 2;
+        // (measured: faster for 1x1 layers such as the dense layer; for 3x3 layers the
+        // 4-wave tiles win, the wide kernel's 8 waves run their product arithmetic in step)
+        if (wide_ok && g.KH * g.KW == 1 && g.C >= 256 && M >= 1024) dflt = 4;
         p.cfg = env_override("QLAYER_BWD_DATA_CFG", dflt);
-        if (p.cfg < 0 || p.cfg > 3) p.cfg = 0;
+        if (p.cfg < 0 || p.cfg > 4 || (p.cfg == 4 && !wide_ok)) p.cfg = 0;
         p.BR = kBdBR[p.cfg];
         p.BCOL = kBdBCOL[p.cfg];
     } else {
@@ -245,9 +252,8 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
         p.BR = p.cfg == 0 ? 128 : 64;
         p.BCOL = 128;
     }
-    p.KE = 64 / (int)g.esize();
+    p.KE = p.cfg == 4 && p.veck ? 16 : 64 / (int)g.esize();
     p.slots = 1;
-    p.s1 = g.SH == 1 && g.SW == 1;
     p.row_tiles = cdiv(g.C, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
@@ -500,7 +506,10 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
             hipLaunchKernelGGL((qconv_bwd_data_generic_kernel<T, BR, BCOL, 2, 2, 64, false, false>), grid, block, \
                                0, st, a);                                                                        \
     } while (0)
-    if (p.veck) {
+    if (p.veck && p.cfg == 4) {
+        if constexpr (sizeof(T) == 2)
+            hipLaunchKernelGGL((qconv_bwd_data_wide_kernel<256, 256, 2, 4, 3>), grid, dim3(512), 0, st, a);
+    } else if (p.veck) {
         if (p.cfg == 0)
             QL_BD_PIPE(128, 128, 2, 2, 3);
         else if (p.cfg == 1)

@@ -125,9 +125,10 @@ __device__ __forceinline__ void run_ring(int nst, int s_begin, Issue &&issue, Re
 }
 
 // The same pipeline with ONE register set of fragments, for kernels that run
-// two waves per SIMD and need the registers for accumulators: each chunk is
-// read and then multiplied; the other wave on the SIMD covers the LDS latency.
-template <int NS, int NI, class Issue, class Read, class Mma>
+// two waves per SIMD and need the registers for accumulators: each of the CH
+// chunks of a step is read and then multiplied; the other wave on the SIMD
+// covers the LDS latency.
+template <int NS, int NI, int CH = 2, class Issue, class Read, class Mma>
 __device__ __forceinline__ void run_ring_single(int nst, int s_begin, Issue &&issue, Read &&read, Mma &&mma) {
     static_assert(NS >= 3 && (NS - 2) * NI < 64, "ring depth");
     if (nst <= 0) return;
@@ -137,17 +138,19 @@ __device__ __forceinline__ void run_ring_single(int nst, int s_begin, Issue &&is
     int slot = 0;
     for (int it = 0; it < nst - 1; ++it) {
         issue(s_begin + it + NS - 1, slot == 0 ? NS - 1 : slot - 1, it + NS - 1 < nst);
-        read(slot, 0, 0);
-        mma(0);
-        read(slot, 1, 0);
-        mma(0);
+#pragma unroll
+        for (int ch = 0; ch < CH; ++ch) {
+            read(slot, ch, 0);
+            mma(0);
+        }
         wait_vm_barrier_lgkm<(NS - 2) * NI>();
         slot = slot + 1 == NS ? 0 : slot + 1;
     }
-    read(slot, 0, 0);
-    mma(0);
-    read(slot, 1, 0);
-    mma(0);
+#pragma unroll
+    for (int ch = 0; ch < CH; ++ch) {
+        read(slot, ch, 0);
+        mma(0);
+    }
     wait_vm_all();
 }
 

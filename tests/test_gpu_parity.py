@@ -96,3 +96,27 @@ def test_no_bias_and_zero_product_weight(bf16):
             assert np.all(got[k] == 0), k  # G_b = G o T_a = 0
             continue
         assert qlh.relerr(got[k], d[k]) <= qlh.tol(bf16, True), k
+
+
+# Every tile configuration of the three convolution passes, forced through the
+# planner's override, on shapes with ragged tiles (the default planner picks
+# only some of them for the small shapes above).
+TILE_CONFIGS = ([("QLAYER_FWD_CFG", c) for c in range(6)] +
+                [("QLAYER_BWD_DATA_CFG", c) for c in range(5)] +
+                [("QLAYER_BWD_WEIGHT_CFG", c) for c in range(3)])
+TILE_SHAPES = [(2, 24, 10, 9, 48, 3, 3, 1, 1), (1, 264, 5, 7, 144, 3, 3, 1, 1), (2, 32, 9, 9, 16, 3, 3, 2, 1)]
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("shape", TILE_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("env,cfg", TILE_CONFIGS, ids=lambda v: str(v))
+def test_conv_tile_configs(env, cfg, shape, bf16, monkeypatch):
+    N, C, H, W, O, KH, KW, s, p = shape
+    print(f"tile config {env}={cfg} shape={shape} bf16={bf16}", flush=True)
+    monkeypatch.setenv(env, str(cfg))
+    inp = synth.random_conv_case([300] + list(shape), N, C, H, W, O, KH, KW, s, p, bf16=bf16)
+    got = qlh.conv_to_np(qlh.run_conv(inp, s, p, bf16))
+    ref = _oracle_all(inp, s, p)
+    for k in KEYS_FWD + KEYS_GRAD:
+        e = qlh.relerr(got[k], ref[k])
+        assert e <= qlh.tol(bf16, k in KEYS_GRAD), f"{k}: normwise relative error {e:.3e}"
