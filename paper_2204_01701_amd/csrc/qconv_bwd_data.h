@@ -229,19 +229,18 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         }
     };
     // The prologue products are formed on the G-side fragments, then the MFMAs.
+    // Column by column, so that the products of column mc + 1 can overlap the MFMAs of column mc.
     auto mma = [&](int set) {
-        v4u bt[3][MC];
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
-            prologue_frag<T>(gr[set][0][mc], gr[set][1][mc], gr[set][2][mc], bt[0][mc], bt[1][mc]);
-            bt[2][mc] = gr[set][0][mc];
+            v4u bt[3];
+            prologue_frag<T>(gr[set][0][mc], gr[set][1][mc], gr[set][2][mc], bt[0], bt[1]);
+            bt[2] = gr[set][0][mc];
+#pragma unroll
+            for (int t = 0; t < 3; ++t)
+#pragma unroll
+                for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[set][t][mr], bt[t], acc[mr][mc]);
         }
-#pragma unroll
-        for (int t = 0; t < 3; ++t)
-#pragma unroll
-            for (int mr = 0; mr < MR; ++mr)
-#pragma unroll
-                for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af[set][t][mr], bt[t][mc], acc[mr][mc]);
     };
     run_ring<NS, NI>(nst, s_begin, issue, read, mma);
 

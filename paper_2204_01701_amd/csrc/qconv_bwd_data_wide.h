@@ -132,18 +132,16 @@ __global__ __launch_bounds__(64 * WGR * WGC) void qconv_bwd_data_wide_kernel(con
         }
     };
     auto mma = [&](int) {
-        v4u bt[3][MC];
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
-            prologue_frag<T>(gr[0][mc], gr[1][mc], gr[2][mc], bt[0][mc], bt[1][mc]);
-            bt[2][mc] = gr[0][mc];
+            v4u bt[3];
+            prologue_frag<T>(gr[0][mc], gr[1][mc], gr[2][mc], bt[0], bt[1]);
+            bt[2] = gr[0][mc];
+#pragma unroll
+            for (int t = 0; t < 3; ++t)
+#pragma unroll
+                for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[t][mr], bt[t], acc[mr][mc]);
         }
-#pragma unroll
-        for (int t = 0; t < 3; ++t)
-#pragma unroll
-            for (int mr = 0; mr < MR; ++mr)
-#pragma unroll
-                for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af[t][mr], bt[t][mc], acc[mr][mc]);
     };
     run_ring_single<NS, NI, 1>(nst, s_begin, issue, read, mma);
 
