@@ -400,7 +400,66 @@ def extra_workloads(ql, torch, dev, stream, reps=10):
         "fwd_tflops": round(3 * u / (fam_ms["fwd"] / fam_n["fwd"] * 1e-3) / 1e12, 1),
         "bwd_tflops": round(6 * u / (fam_ms["bwd"] / fam_n["bwd"] * 1e-3) / 1e12, 1),
         "fwd_bwd_tflops": round(9 * u / (ms * 1e-3) / 1e12, 1)}
+    out["hybrid_bp_memory"] = hybrid_bp_memory(torch, dev)
     return out
+
+
+def hybrid_bp_memory(torch, dev, batch=256, reps=5):
+    """Peak device memory of one training step (forward + backward) of a small
+    quadratic ConvNet in the two memory modes of section 4.3: T_a, T_b saved by
+    the forward, or regenerated in the backward (hybrid back-propagation).  The
+    network stands in for the paper's memory experiment (3 quadratic conv layers
+    + 2 quadratic FC layers, batch 256, 32 x 32 inputs): qconv 3->64, 64->128,
+    128->256 (3x3, pad 1), each followed by ReLU and 2x2 max-pool, then qFC
+    4096->512, ReLU, qFC 512->10; bf16, synthetic N(0,1) inputs, He-scaled weights."""
+    from paper_2204_01701_amd.autograd import quad_conv2d, quad_linear
+
+    g = torch.Generator(device=dev).manual_seed(0)
+
+    def weights(shape, fan_in):
+        return [(torch.randn(shape, device=dev, generator=g) * (2.0 / fan_in) ** 0.5).to(torch.bfloat16)
+                .requires_grad_(True) for _ in range(3)]
+
+    convs = [weights((64, 3, 3, 3), 27), weights((128, 64, 3, 3), 576), weights((256, 128, 3, 3), 1152)]
+    fcs = [weights((512, 4096), 4096), weights((10, 512), 512)]
+    x = torch.randn(batch, 3, 32, 32, device=dev, generator=g).to(torch.bfloat16)
+    x = x.contiguous(memory_format=torch.channels_last)
+    gl = torch.randn(batch, 10, device=dev, generator=g).to(torch.bfloat16)
+
+    def step(recompute):
+        h = x
+        for w in convs:
+            h = torch.nn.functional.max_pool2d(torch.relu(quad_conv2d(h, *w, stride=1, pad=1, recompute=recompute)), 2)
+        h = h.flatten(1)
+        h = torch.relu(quad_linear(h, *fcs[0], recompute=recompute))
+        quad_linear(h, *fcs[1], recompute=recompute).backward(gl)
+
+    res = {"network": "qconv 3-64-128-256 (3x3, ReLU, max-pool) + qFC 4096-512-10, bf16, batch 256, 32x32"}
+    for mode in ("save", "recompute"):
+        rc = mode == "recompute"
+        for _ in range(3):  # warm-up (allocator growth, first launches)
+            step(rc)
+        torch.cuda.synchronize()
+        for ws in convs + fcs:
+            for w in ws:
+                w.grad = None
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats(dev)
+        base = torch.cuda.memory_allocated(dev)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(reps):
+            step(rc)
+        t1.record()
+        torch.cuda.synchronize()
+        res[f"{mode}_peak_mb"] = round((torch.cuda.max_memory_allocated(dev) - base) / 2**20, 1)
+        res[f"{mode}_step_ms"] = round(t0.elapsed_time(t1) / reps, 3)
+        for ws in convs + fcs:
+            for w in ws:
+                w.grad = None
+    res["memory_saving_pct"] = round(100 * (1 - res["recompute_peak_mb"] / res["save_peak_mb"]), 1)
+    return res
 
 
 if __name__ == "__main__":

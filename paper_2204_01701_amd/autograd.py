@@ -1,0 +1,163 @@
+"""Differentiable quadratic layers on top of the C ABI (arXiv 2204.01701).
+
+``quad_conv2d`` and ``quad_linear`` are torch autograd functions whose
+forward and backward run entirely in ``libqlayer.so``: the forward computes
+Y = (W_a*X + b_a) o (W_b*X + b_b) + (W_c*X + b_c) (section 3.1,
+eq:2ndneuron3), the backward the input, weight and bias gradients of
+section 4.3 (eq:SD).  They offer the two memory modes of section 4.3:
+
+* ``recompute=False`` (save): the forward keeps T_a = W_a*X + b_a and
+  T_b = W_b*X + b_b for the backward;
+* ``recompute=True`` (hybrid back-propagation): the forward keeps only X, and
+  the backward regenerates T_a and T_b with the forward kernel (Y not
+  written) before the gradient kernels.  The gradients are bitwise those of
+  save mode, since the same kernel produces T_a and T_b in both.
+
+Layouts.  Convolution tensors are NCHW-shaped torch tensors; they are used in
+channels_last memory format, whose memory is the library's NHWC (OHWI for
+weights), so channels_last inputs are not copied and the outputs come back
+channels_last.  X, the weights and Y share one dtype (bfloat16 or float32);
+biases are float32 or None (all three or none).  Weight gradients are
+returned in the weights' dtype, bias gradients in float32.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import (QL_BF16, QL_F32, conv_desc, linear_desc, qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_weight,
+               qlayer_conv2d_fwd, qlayer_linear_bwd, qlayer_linear_fwd)
+
+__all__ = ["quad_conv2d", "quad_linear", "QuadConv2dFunction", "QuadLinearFunction"]
+
+
+def _qdtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return QL_BF16
+    if t.dtype == torch.float32:
+        return QL_F32
+    raise TypeError(f"unsupported dtype {t.dtype}: use bfloat16 or float32")
+
+
+def _nhwc(t: torch.Tensor) -> torch.Tensor:
+    """NCHW-shaped tensor -> contiguous NHWC view of its channels_last memory."""
+    return t.contiguous(memory_format=torch.channels_last).permute(0, 2, 3, 1)
+
+
+def _biases(ba, bb, bc):
+    bs = (ba, bb, bc)
+    if all(b is None for b in bs):
+        return None
+    if any(b is None for b in bs):
+        raise ValueError("give all three biases or none")
+    return [b.contiguous().float() for b in bs]
+
+
+class QuadConv2dFunction(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, wa, wb, wc, ba, bb, bc, stride, pad, recompute):
+        N, C, H, W = x.shape
+        O, C2, KH, KW = wa.shape
+        if C2 != C or wb.shape != wa.shape or wc.shape != wa.shape:
+            raise ValueError("weight shapes must be (O, C, KH, KW) for all three terms")
+        d = conv_desc(N, C, H, W, O, KH, KW, stride, pad, _qdtype(x))
+        xn = _nhwc(x)
+        wn = [_nhwc(w.to(x.dtype)) for w in (wa, wb, wc)]
+        b = _biases(ba, bb, bc)
+        bl = b if b is not None else [None, None, None]
+        y = torch.empty((N, d.ho, d.wo, O), device=x.device, dtype=x.dtype)
+        if recompute:
+            qlayer_conv2d_fwd(d, xn, *wn, *bl, y)
+            ctx.save_for_backward(xn, *wn, *(b or []))
+        else:
+            ta, tb = torch.empty_like(y), torch.empty_like(y)
+            qlayer_conv2d_fwd(d, xn, *wn, *bl, y, ta, tb)
+            ctx.save_for_backward(xn, *wn, ta, tb)
+        ctx.desc, ctx.recompute, ctx.has_bias = d, recompute, b is not None
+        ctx.wdtype = wa.dtype
+        return y.permute(0, 3, 1, 2)
+
+    @staticmethod
+    def backward(ctx, gy):
+        d = ctx.desc
+        saved = ctx.saved_tensors
+        xn, wn = saved[0], list(saved[1:4])
+        if ctx.recompute:
+            bl = list(saved[4:7]) if ctx.has_bias else [None, None, None]
+            ta = torch.empty((d.n, d.ho, d.wo, d.o), device=xn.device, dtype=xn.dtype)
+            tb = torch.empty_like(ta)
+            qlayer_conv2d_fwd(d, xn, *wn, *bl, None, ta, tb)
+        else:
+            ta, tb = saved[4], saved[5]
+        gyn = _nhwc(gy.to(xn.dtype))
+        need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
+        need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
+        dx = dw = db = None
+        if need_x:
+            dxn = torch.empty_like(xn)
+            qlayer_conv2d_bwd_data(d, gyn, ta, tb, *wn, dxn)
+            dx = dxn.permute(0, 3, 1, 2)
+        if need_w or need_b:
+            dwn = [torch.empty(wn[0].shape, device=xn.device, dtype=torch.float32) for _ in range(3)]
+            db = [torch.empty(d.o, device=xn.device, dtype=torch.float32) for _ in range(3)] if need_b else None
+            qlayer_conv2d_bwd_weight(d, xn, gyn, ta, tb, *dwn, *(db or [None, None, None]))
+            dw = [g.permute(0, 3, 1, 2).to(ctx.wdtype) for g in dwn]
+        dw = dw or [None, None, None]
+        db = db or [None, None, None]
+        return (dx, *dw, *db, None, None, None)
+
+
+class QuadLinearFunction(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, wa, wb, wc, ba, bb, bc, recompute):
+        B, I = x.shape
+        O = wa.shape[0]
+        d = linear_desc(B, I, O, _qdtype(x))
+        xc = x.contiguous()
+        wl = [w.to(x.dtype).contiguous() for w in (wa, wb, wc)]
+        b = _biases(ba, bb, bc)
+        bl = b if b is not None else [None, None, None]
+        y = torch.empty((B, O), device=x.device, dtype=x.dtype)
+        if recompute:
+            qlayer_linear_fwd(d, xc, *wl, *bl, y)
+            ctx.save_for_backward(xc, *wl, *(b or []))
+        else:
+            ta, tb = torch.empty_like(y), torch.empty_like(y)
+            qlayer_linear_fwd(d, xc, *wl, *bl, y, ta, tb)
+            ctx.save_for_backward(xc, *wl, ta, tb)
+        ctx.desc, ctx.recompute, ctx.has_bias = d, recompute, b is not None
+        ctx.wdtype = wa.dtype
+        return y
+
+    @staticmethod
+    def backward(ctx, gy):
+        d = ctx.desc
+        saved = ctx.saved_tensors
+        xc, wl = saved[0], list(saved[1:4])
+        if ctx.recompute:
+            bl = list(saved[4:7]) if ctx.has_bias else [None, None, None]
+            ta = torch.empty((d.batch, d.out), device=xc.device, dtype=xc.dtype)
+            tb = torch.empty_like(ta)
+            qlayer_linear_fwd(d, xc, *wl, *bl, None, ta, tb)
+        else:
+            ta, tb = saved[4], saved[5]
+        gyc = gy.to(xc.dtype).contiguous()
+        need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
+        need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
+        dx = torch.empty_like(xc) if need_x else None
+        dw = [torch.empty(wl[0].shape, device=xc.device, dtype=torch.float32) for _ in range(3)] \
+            if (need_w or need_b) else None
+        db = [torch.empty(d.out, device=xc.device, dtype=torch.float32) for _ in range(3)] if need_b else None
+        qlayer_linear_bwd(d, xc, gyc, ta, tb, *wl, dx, *(dw or [None] * 3), *(db or [None] * 3))
+        dw = [g.to(ctx.wdtype) for g in dw] if dw is not None else [None, None, None]
+        db = db or [None, None, None]
+        return (dx, *dw, *db, None)
+
+
+def quad_conv2d(x, wa, wb, wc, ba=None, bb=None, bc=None, stride=1, pad=0, recompute=False):
+    """Quadratic 2-D convolution layer (NCHW-shaped tensors, channels_last memory)."""
+    return QuadConv2dFunction.apply(x, wa, wb, wc, ba, bb, bc, stride, pad, recompute)
+
+
+def quad_linear(x, wa, wb, wc, ba=None, bb=None, bc=None, recompute=False):
+    """Quadratic fully-connected layer: x (B, I), weights (O, I)."""
+    return QuadLinearFunction.apply(x, wa, wb, wc, ba, bb, bc, recompute)

@@ -1,0 +1,107 @@
+"""The autograd layer functions (save and recompute modes) against the fp64
+oracle, and the recompute mode's bitwise agreement with save mode and its
+lower peak memory (the hybrid back-propagation of section 4.3)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+import qlh  # noqa: E402
+from paper_2204_01701_amd.autograd import quad_conv2d, quad_linear  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def _t(a, dtype, grad=True):
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV, dtype)
+    return t.requires_grad_(grad)
+
+
+def _conv_run(inp, s, p, dtype, recompute):
+    x = _t(inp["x"], dtype).contiguous(memory_format=torch.channels_last).detach().requires_grad_(True)
+    w = [_t(inp[k], dtype) for k in ("wa", "wb", "wc")]
+    b = [_t(inp[k], torch.float32) for k in ("ba", "bb", "bc")]
+    y = quad_conv2d(x, *w, *b, stride=s, pad=p, recompute=recompute)
+    y.backward(_t(inp["gy"], dtype, grad=False))
+    torch.cuda.synchronize()
+    return {"y": y.detach(), "dx": x.grad, "dwa": w[0].grad, "dwb": w[1].grad, "dwc": w[2].grad,
+            "dba": b[0].grad, "dbb": b[1].grad, "dbc": b[2].grad}
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 16, 8, 8, 24, 3, 3, 1, 1), (3, 8, 9, 7, 16, 3, 3, 2, 1)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_conv_autograd_matches_oracle_in_both_modes(shape, bf16):
+    N, C, H, W, O, KH, KW, s, p = shape
+    dtype = torch.bfloat16 if bf16 else torch.float32
+    inp = synth.random_conv_case([400] + list(shape), N, C, H, W, O, KH, KW, s, p, bf16=bf16)
+    y, ta, tb = oracle.conv2d_fwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"], s, p)
+    ref = oracle.conv2d_bwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"],
+                            inp["gy"], s, p)
+    ref["y"] = y
+    got = {m: _conv_run(inp, s, p, dtype, m) for m in (False, True)}
+    for k in ref:
+        for m in (False, True):
+            e = qlh.relerr(got[m][k].double().cpu().numpy(), ref[k])
+            assert e <= qlh.tol(bf16, k != "y"), f"{k} recompute={m}: normwise relative error {e:.3e}"
+        # the same kernel makes T_a, T_b in both modes: identical gradients
+        assert torch.equal(got[False][k], got[True][k]), k
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+def test_linear_autograd_matches_oracle_in_both_modes(bf16):
+    B, I, O = 96, 72, 40
+    dtype = torch.bfloat16 if bf16 else torch.float32
+    inp = synth.random_dense_case([401, B, I, O], B, I, O, bf16=bf16)
+    y, _, _ = oracle.linear_fwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"])
+    ref = oracle.linear_bwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"], inp["gy"])
+    ref["y"] = y
+    got = {}
+    for m in (False, True):
+        x = _t(inp["x"], dtype)
+        w = [_t(inp[k], dtype) for k in ("wa", "wb", "wc")]
+        b = [_t(inp[k], torch.float32) for k in ("ba", "bb", "bc")]
+        out = quad_linear(x, *w, *b, recompute=m)
+        out.backward(_t(inp["gy"], dtype, grad=False))
+        got[m] = {"y": out.detach(), "dx": x.grad, "dwa": w[0].grad, "dwb": w[1].grad, "dwc": w[2].grad,
+                  "dba": b[0].grad, "dbb": b[1].grad, "dbc": b[2].grad}
+    for k in ref:
+        for m in (False, True):
+            e = qlh.relerr(got[m][k].double().cpu().numpy(), ref[k])
+            assert e <= qlh.tol(bf16, k != "y"), f"{k} recompute={m}: normwise relative error {e:.3e}"
+        assert torch.equal(got[False][k], got[True][k]), k
+
+
+def test_recompute_mode_lowers_peak_memory():
+    """A stack of quadratic layers: the recompute mode keeps no T_a, T_b between
+    forward and backward, so its peak memory is lower by about two output maps
+    per layer."""
+    torch.manual_seed(0)
+    N, C, H = 32, 32, 32
+    x0 = torch.randn(N, C, H, H, device=DEV, dtype=torch.bfloat16).contiguous(memory_format=torch.channels_last)
+    ws = [[(torch.randn(C, C, 3, 3, device=DEV) * 0.05).to(torch.bfloat16).requires_grad_(True) for _ in range(3)]
+          for _ in range(4)]
+    peaks, grads = {}, {}
+    for m in (False, True):
+        for layer in ws:
+            for w in layer:
+                w.grad = None
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        h = x0
+        for layer in ws:
+            h = quad_conv2d(h, *layer, stride=1, pad=1, recompute=m)
+        h.float().square().mean().backward()
+        torch.cuda.synchronize()
+        peaks[m] = torch.cuda.max_memory_allocated() - base
+        grads[m] = [w.grad.clone() for layer in ws for w in layer]
+    one_map = N * C * H * H * 2
+    assert peaks[True] < peaks[False], peaks
+    assert peaks[False] - peaks[True] >= 2 * one_map, (peaks, one_map)
+    for g0, g1 in zip(grads[False], grads[True]):
+        assert torch.equal(g0, g1)
