@@ -41,6 +41,11 @@ def parse():
     ap.add_argument("--cpu-target-s", type=float, default=15.0, help="approximate oracle sample time")
     ap.add_argument("--profile-summary", metavar="KERNEL_STATS_CSV",
                     help="instead of running: summarise a rocprofv3 --stats kernel table per entry point")
+    ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
+                    help="instead of running: one elementwise device copy of BYTES bytes (for counter scaling)")
+    ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
+                    help="instead of running: HBM bytes per entry call from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
+                         "counter tables of the benchmark and of --copy-calibration")
     return ap.parse_args()
 
 
@@ -212,7 +217,9 @@ _KERNEL_FAMILY = [
     (r"qconv_pad_channels_kernel<[^,>]+, 4>", "fwd", False),
     (r"qconv_bwd_data_kernel<", "bwd_data", True),
     (r"qconv_bwd_data_generic_kernel<", "bwd_data", True),
-    (r"qconv_bwd_data_smallc_kernel<", "bwd_data", True),
+    (r"qconv_bwd_data_wide_kernel<", "bwd_data", True),
+    (r"qconv_bwd_data_cols_kernel<", "bwd_data", True),
+    (r"qconv_bwd_data_col2im_kernel<", "bwd_data", False),
     (r"qconv_sum_splits_kernel<", "bwd_data", False),
     (r"qconv_weight_transpose_kernel<", "bwd_data", False),
     (r"qconv_bwd_weight_kernel<", "bwd_weight", True),
@@ -253,10 +260,104 @@ def profile_summary(path):
     print("\n".join(lines))
 
 
+def _family(name):
+    import re
+    for pat, f, m in _KERNEL_FAMILY:
+        if re.search(pat, name):
+            return f, m
+    return None, False
+
+
+def _counter_rows(path, counter):
+    """(kernel name, value) per dispatch of one counter in a rocprofv3 counter_collection table."""
+    import csv
+    out = []
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] == counter:
+            out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def sources_digest():
+    """sha256 of the kernel and host sources of the library (identifies the code counters were taken on)."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2204_01701_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".h", ".hip")):
+            h.update(f.encode())
+            h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_summary(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, cal_bytes):
+    """Markdown: HBM bytes per entry call per pass, from FETCH_SIZE / WRITE_SIZE (KiB per
+    dispatch) scaled so that the plain copy reads and writes exactly its size."""
+    # the calibration's multiply-by-one kernel (its buffer fill is another kernel)
+    cf = sum(v for k, v in _counter_rows(cal_fetch_csv, "FETCH_SIZE") if "MulFunctor" in k)
+    cw = sum(v for k, v in _counter_rows(cal_write_csv, "WRITE_SIZE") if "MulFunctor" in k)
+    sf = cal_bytes / (cf * 1024.0)
+    sw = cal_bytes / (cw * 1024.0)
+    lines = [f"copy calibration: {cal_bytes} bytes read and written; FETCH_SIZE read {cf:.0f} KiB, "
+             f"WRITE_SIZE {cw:.0f} KiB; scale factors fetch {sf:.4f}, write {sw:.4f}", "",
+             "| entry point | entry calls | read MB per call | written MB per call | traffic bytes per call |",
+             "|---|---:|---:|---:|---:|"]
+    tot = {}
+    for path, cnt, scale, key in ((fetch_csv, "FETCH_SIZE", sf, "r"), (write_csv, "WRITE_SIZE", sw, "w")):
+        for name, v in _counter_rows(path, cnt):
+            f, main = _family(name)
+            if f is None:
+                continue
+            d = tot.setdefault(f, {"r": 0.0, "w": 0.0, "calls_r": 0, "calls_w": 0})
+            d[key] += v * 1024.0 * scale
+            if main:
+                d["calls_" + key] += 1
+    for f in ("fwd", "bwd_data", "bwd_weight"):
+        if f in tot and tot[f]["calls_r"] and tot[f]["calls_w"]:
+            d = tot[f]
+            r, w = d["r"] / d["calls_r"], d["w"] / d["calls_w"]
+            lines.append(f"| qlayer_conv2d_{f} | {d['calls_r']} | {r / 1e6:.1f} | {w / 1e6:.1f} | {r + w:.0f} |")
+    lines += ["", f"sources: {sources_digest()}"]
+    print("\n".join(lines))
+
+
+def read_traffic(family):
+    """Traffic bytes per call of `family` from the committed counter summary, or None when
+    the summary is missing or was taken on other sources."""
+    import re
+    path = os.path.join(ROOT, "profiles", "vgg16_bf16_b128_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m = re.search(r"^sources: (\w+)$", txt, re.M)
+    if not m or m.group(1) != sources_digest():
+        return None
+    m = re.search(r"^\| qlayer_conv2d_%s \| \d+ \| [\d.]+ \| [\d.]+ \| (\d+) \|$" % family, txt, re.M)
+    return int(m.group(1)) if m else None
+
+
+def copy_calibration(nbytes):
+    import torch
+    dev = torch.device("cuda:0")
+    n = nbytes // 4
+    src = torch.ones(n, device=dev, dtype=torch.float32)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.mul(src, 1.0, out=dst)  # one elementwise kernel: reads and writes nbytes
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n * 4}))
+
+
 def main():
     args = parse()
     if args.profile_summary:
         profile_summary(args.profile_summary)
+        return
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary, cal_bytes=int(os.environ.get("QL_COPY_BYTES", 1 << 30)))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
@@ -316,7 +417,7 @@ def main():
     dom_flops = sum(3 * unit_flops(L) for L in geoms) / len(geoms)   # algorithmic flops per launch
     achieved = dom_flops / (dom_avg_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": read_traffic(dom),
                 "kernel": f"qlayer_conv2d_{dom} over the 13 layers (avg {dom_avg_ms * 1e3:.1f} us per launch, "
                           f"{dom_flops / 1e9:.2f} GFLOP per launch)"}
 
