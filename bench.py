@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--cpu-target-s", type=float, default=15.0, help="approximate oracle sample time")
     ap.add_argument("--profile-summary", metavar="KERNEL_STATS_CSV",
                     help="instead of running: summarise a rocprofv3 --stats kernel table per entry point")
+    ap.add_argument("--trace", metavar="KERNEL_TRACE_CSV",
+                    help="with --profile-summary: the run's kernel trace, to average the last --last-calls calls")
+    ap.add_argument("--last-calls", type=int, default=0,
+                    help="with --trace: entry calls per family in the final (roofline) region")
     ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
                     help="instead of running: one elementwise device copy of BYTES bytes (for counter scaling)")
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
@@ -230,7 +234,7 @@ _KERNEL_FAMILY = [
 ]
 
 
-def profile_summary(path):
+def profile_summary(path, trace=None, last_calls=0):
     """Markdown summary of a rocprofv3 kernel statistics table (--stats, csv output):
     every kernel with its calls and average duration, then per entry point the total
     kernel time divided by the number of entry calls (= calls of its main kernels)."""
@@ -257,7 +261,29 @@ def profile_summary(path):
     for fam in ("fwd", "bwd_data", "bwd_weight"):
         if fam_calls.get(fam):
             lines.append(f"| qlayer_conv2d_{fam} | {fam_calls[fam]} | {fam_ns[fam] / fam_calls[fam] / 1e3:.1f} |")
+    if trace and last_calls:
+        lines += ["", f"Final region only (the last {last_calls} calls of each entry point, from the kernel trace):", "",
+                  "| entry point | entry calls | kernel time per call, us |", "|---|---:|---:|"]
+        for fam, (n, ns) in region_times(trace, last_calls).items():
+            lines.append(f"| qlayer_conv2d_{fam} | {n} | {ns / n / 1e3:.1f} |")
     print("\n".join(lines))
+
+
+def region_times(trace_csv, last_calls):
+    """Per family: kernel time of its last `last_calls` entry calls in a rocprofv3 kernel trace
+    (from the first of those calls' main-kernel dispatch on, every kernel of the family)."""
+    import csv
+    rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Dispatch_Id"]))
+    out = {}
+    for fam in ("fwd", "bwd_data", "bwd_weight"):
+        mains = [i for i, r in enumerate(rows) if _family(r["Kernel_Name"]) == (fam, True)]
+        if len(mains) < last_calls:
+            continue
+        first = mains[-last_calls]
+        ns = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows[first:]
+                 if _family(r["Kernel_Name"])[0] == fam)
+        out[fam] = (last_calls, ns)
+    return out
 
 
 def _family(name):
@@ -351,7 +377,7 @@ def copy_calibration(nbytes):
 def main():
     args = parse()
     if args.profile_summary:
-        profile_summary(args.profile_summary)
+        profile_summary(args.profile_summary, args.trace, args.last_calls)
         return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
