@@ -47,6 +47,10 @@ struct BwdWeightArgs {
     int row_tiles, col_tiles, splits, stages_per_split, stages_total;
     int want_db;
     int C_out;  // channels of dW_t as stored (< C when X arrives zero-padded to C channels)
+    // Stride 1 with HO == H, WO == W: the X address of pixel m at a fixed tap is
+    // linear in m, and a K step advances each lane's (oh, ow) by lin_dq rows
+    // (mod HO) and lin_dr columns, with one carry.
+    int lin, lin_dq, lin_dr;
     FastDiv fd_howo, fd_wo, fd_c, fd_kw;
 };
 

@@ -25,7 +25,13 @@ namespace ql {
 // The kernel body; SUM: this workgroup also accumulates the bias gradients
 // (row tile 0).  Instantiated twice so that the workgroups without bias sums
 // run code with no trace of them (fewer live registers in the main loop).
-template <int BKP, int BO, int WGR, int WGC, int NS, int NT, bool SUM>
+//
+// LIN (stride 1, output map the size of the input map): each lane keeps the
+// element offset of its X and G rows at the first K step of its split plus
+// the (oh, ow) of its pixel, advanced by one K step (KE pixels) per issue
+// with a carry, instead of splitting the pixel index into (n, oh, ow) by
+// division at every step.
+template <int BKP, int BO, int WGR, int WGC, int NS, int NT, bool SUM, bool LIN>
 __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *smem) {
     using T = uint16_t;                 // bf16 only: the transposed LDS read is 16-bit
     constexpr int KE = 32;              // output pixels per K step (two MFMA k-chunks)
@@ -79,8 +85,57 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
     const int og = ct * BO + 8 * gslot;
     const bool og_ok = og < a.O;
 
+    // LIN state: per DMA instruction, the lane's pixel within a K step, its
+    // element offsets at step s_begin and the (oh, ow) of the step to issue next.
+    const int dh = xr - a.PH, dw = xq - a.PW;
+    long long xlin[NIX], glin[NIG];
+    int ohv[NIX], owv[NIX];
+    if constexpr (LIN) {
+#pragma unroll
+        for (int i = 0; i < NIX; ++i) {
+            const int m0 = s_begin * KE + RX * (NW * i + wave) + lane / SX;
+            const int n = (int)fdiv((uint32_t)m0, a.fd_howo);
+            const int rem = m0 - n * a.HO * a.WO;
+            ohv[i] = (int)fdiv((uint32_t)rem, a.fd_wo);
+            owv[i] = rem - ohv[i] * a.WO;
+            xlin[i] = ((long long)m0 + (long long)dh * a.W + dw) * a.C + xc;
+        }
+#pragma unroll
+        for (int i = 0; i < NIG; ++i)
+            glin[i] = (long long)(s_begin * KE + RG * (NW * i + wave) + lane / SG) * a.O + og;
+    }
+
     auto issue = [&](int s, int slot, bool live) {
         char *base = smem + slot * STAGE + wave * 1024;
+        if constexpr (LIN) {
+            const int ds = s - s_begin;
+            const int mleft = a.M - s * KE;  // pixels of this step that exist: lane pixel < mleft
+            const long long xs = (long long)ds * KE * a.C;
+#pragma unroll
+            for (int i = 0; i < NIX; ++i) {
+                const int p = RX * (NW * i + wave) + lane / SX;
+                const bool ok = live && kp_ok && p < mleft && (unsigned)(ohv[i] + dh) < (unsigned)a.H &&
+                                (unsigned)(owv[i] + dw) < (unsigned)a.W;
+                dma16(dma_src(ok, x + (xlin[i] + xs), a.zero), base + i * (NT * 16));
+                int ow = owv[i] + a.lin_dr;
+                const int carry = ow >= a.WO ? 1 : 0;
+                ow -= carry ? a.WO : 0;
+                int oh = ohv[i] + a.lin_dq + carry;
+                oh -= oh >= a.HO ? a.HO : 0;
+                owv[i] = ow;
+                ohv[i] = oh;
+            }
+            const long long gs = (long long)ds * KE * a.O;
+#pragma unroll
+            for (int i = 0; i < NIG; ++i) {
+                const int p = RG * (NW * i + wave) + lane / SG;
+                const bool ok = live && og_ok && p < mleft;
+#pragma unroll
+                for (int u = 0; u < 3; ++u)
+                    dma16(dma_src(ok, gsrc[u] + (glin[i] + gs), a.zero), base + XB + u * GB + i * (NT * 16));
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < NIX; ++i) {
             const int m = s * KE + RX * (NW * i + wave) + lane / SX;
@@ -238,10 +293,18 @@ __global__ __launch_bounds__(NT) void qconv_bwd_weight_kernel(const BwdWeightArg
     int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int tiles = a.row_tiles * a.col_tiles;
     bid -= (bid / tiles) * tiles;
-    if (a.want_db && bid % a.row_tiles == 0)
-        bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true>(a, smem);
-    else
-        bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false>(a, smem);
+    const bool sum = a.want_db && bid % a.row_tiles == 0;
+    if (a.lin) {
+        if (sum)
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true, true>(a, smem);
+        else
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false, true>(a, smem);
+    } else {
+        if (sum)
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true, false>(a, smem);
+        else
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false, false>(a, smem);
+    }
 }
 
 }  // namespace ql

@@ -202,9 +202,11 @@ FwdPlan plan_fwd(const Geom &g) {
 // Pipelined input-gradient tile configurations (rows = input channels,
 // columns = input pixels):  0: 128 x 128, 1: 64 x 128, 2: 128 x 64, 3: 128 x 128
 // with the four waves side by side (each 128 x 32: half the prologue
-// products per MFMA of configuration 0).
-constexpr int kBdBR[5] = {128, 64, 128, 128, 256};
-constexpr int kBdBCOL[5] = {128, 128, 64, 128, 256};  // 4: the wide kernel (8 waves, 16-channel K steps)
+// products per MFMA of configuration 0), 5: 64 x 128 with the waves side by
+// side (each 64 x 32: half the products per MFMA of configuration 1).
+constexpr int kBdCfgs = 6;
+constexpr int kBdBR[kBdCfgs] = {128, 64, 128, 128, 256, 64};
+constexpr int kBdBCOL[kBdCfgs] = {128, 128, 64, 128, 256, 128};  // 4: the wide kernel (8 waves, 16-channel K steps)
 
 struct BwdDataPlan {
     int cfg;  // pipelined: index into kBd*; generic: 0: 128 x 128, 1: 64 x 128
@@ -238,13 +240,13 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
     // the wide kernel: bf16, natural weight tiles, stride 1, 16-channel K steps within one tap
     const bool wide_ok = p.natw && p.s1 && g.O % 16 == 0 && g.KH * g.KW <= 32;
     if (p.veck) {
-        int dflt = 1;
+        int dflt = 5;
         if (g.C > 64) dflt = M >= 1024 ? 3 : 2;
         // (measured: faster for 1x1 layers such as the dense layer; for 3x3 layers the
         // 4-wave tiles win, the wide kernel's 8 waves run their product arithmetic in step)
         if (wide_ok && g.KH * g.KW == 1 && g.C >= 256 && M >= 1024) dflt = 4;
         p.cfg = env_override("QLAYER_BWD_DATA_CFG", dflt);
-        if (p.cfg < 0 || p.cfg > 4 || (p.cfg == 4 && !wide_ok)) p.cfg = 0;
+        if (p.cfg < 0 || p.cfg >= kBdCfgs || (p.cfg == 4 && !wide_ok)) p.cfg = 0;
         p.BR = kBdBR[p.cfg];
         p.BCOL = kBdBCOL[p.cfg];
     } else {
@@ -516,6 +518,8 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
             QL_BD_PIPE(64, 128, 2, 2, 4);
         else if (p.cfg == 3)
             QL_BD_PIPE(128, 128, 1, 4, 3);
+        else if (p.cfg == 5)
+            QL_BD_PIPE(64, 128, 1, 4, 4);
         else
             QL_BD_PIPE(128, 64, 2, 2, 4);
     } else if (p.cfg == 0) {
@@ -576,6 +580,9 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     a.fd_wo = make_fastdiv(g.WO);
     a.fd_c = make_fastdiv(C);
     a.fd_kw = make_fastdiv(g.KW);
+    a.lin = g.SH == 1 && g.SW == 1 && g.HO == g.H && g.WO == g.W && env_override("QLAYER_BWD_WEIGHT_LIN", 1) != 0;
+    a.lin_dq = (p.KE / g.WO) % g.HO;
+    a.lin_dr = p.KE % g.WO;
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     if constexpr (sizeof(T) == 2) {
         if (p.pipe) {

@@ -36,8 +36,16 @@ typedef short v4s_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 
 // Copy 16 bytes per lane from gptr into LDS at wave_base + 16 * lane.
+// Issued as inline asm, so the compiler's wait insertion does not see an LDS
+// write in flight: given the builtin, it puts a full vmcnt(0) drain in front
+// of every LDS read it cannot tell apart from the DMA target (the transposed
+// reads among them), which would leave one step in flight instead of NS - 1.
+// Ordering is explicit instead: each ring step waits for its own loads with
+// vmcnt and a barrier (below) before any wave reads them, and refills only a
+// slot every wave finished reading before the previous barrier.
 __device__ __forceinline__ void dma16(const void *gptr, char *wave_base) {
-    __builtin_amdgcn_global_load_lds(gptr, (lds_void_t *)wave_base, 16, 0, 0);
+    const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_void_t *)wave_base);
+    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gptr), "{m0}"(lds));
 }
 
 // Branch-free choice of a DMA source: the operand address when ok, else the zero page.
