@@ -212,6 +212,62 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         T *__restrict__ y = static_cast<T *>(a.y);
         T *__restrict__ ta = static_cast<T *>(a.ta);
         T *__restrict__ tb = static_cast<T *>(a.tb);
+        // Staged stores: each output map of the tile is written into the idle
+        // LDS ring as BCOL pixel rows of BR channels, then copied out in
+        // 16-byte chunks, consecutive lanes on consecutive addresses (one
+        // pixel's BR channels are contiguous in NHWC), instead of 4-channel
+        // pieces scattered over 32 pixel rows per store instruction.
+        constexpr int E = (int)sizeof(T);
+        constexpr int PITCH = BR * E + 16;  // LDS bytes per staged pixel row
+        constexpr int MAPB = BCOL * PITCH;
+        constexpr int PER = 3 * MAPB <= NS * STAGE ? 3 : 1;  // maps staged per round
+        constexpr int CPR = BR * E / 16;                       // 16-byte chunks per row
+        static_assert((CPR & (CPR - 1)) == 0, "staged epilogue tile");
+        if constexpr (MAPB <= NS * STAGE) {  // (otherwise, and for O not a multiple of 16 / E: direct stores)
+            if (a.O % (16 / E) == 0) {
+                T *outs[3] = {y, ta, tb};
+#pragma unroll
+                for (int r0 = 0; r0 < 3; r0 += PER) {
+                    lds_barrier();  // every wave is done with the ring (or the previous round's copy)
+#pragma unroll
+                    for (int j = r0; j < r0 + PER; ++j) {
+                        if (!outs[j]) continue;
+                        char *tile = smem + (j - r0) * MAPB;
+#pragma unroll
+                        for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+                            for (int mc = 0; mc < MC; ++mc) {
+                                const int p = wc * (BCOL / WGC) + mc * 32 + lrow;
+#pragma unroll
+                                for (int g = 0; g < 4; ++g) {
+                                    const int ol = wr * (BR / WGR) + mr * 32 + 8 * g + 4 * lhi;
+                                    float v[4];
+#pragma unroll
+                                    for (int i = 0; i < 4; ++i) {
+                                        const float fa = acc[0][mr][mc][4 * g + i], fb = acc[1][mr][mc][4 * g + i];
+                                        v[i] = j == 0 ? fa * fb + acc[2][mr][mc][4 * g + i] : (j == 1 ? fa : fb);
+                                    }
+                                    store4<T>(reinterpret_cast<T *>(tile + p * PITCH + ol * E), v[0], v[1], v[2], v[3]);
+                                }
+                            }
+                    }
+                    lds_barrier();
+#pragma unroll
+                    for (int j = r0; j < r0 + PER; ++j) {
+                        if (!outs[j]) continue;
+                        const char *tile = smem + (j - r0) * MAPB;
+                        for (int c = tid; c < BCOL * CPR; c += NT) {
+                            const int row = c / CPR, cc = c % CPR;
+                            const int m = ct * BCOL + row, o = rt * BR + cc * (16 / E);
+                            if (m < a.M && o < a.O)
+                                *reinterpret_cast<v4u *>(outs[j] + (size_t)m * a.O + o) =
+                                    lds_read16(tile + row * PITCH + cc * 16);
+                        }
+                    }
+                }
+                return;
+            }
+        }
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
