@@ -249,6 +249,41 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
     const bool vec_out = (a.C & 3) == 0;
     T *__restrict__ dx = static_cast<T *>(a.dx);
+
+    // Staged stores: the BCOL x BR block (pixel rows, channels contiguous in
+    // NHWC) goes through the idle LDS ring and out in 16-byte chunks with
+    // consecutive lanes on consecutive addresses; OT is T for dX, float for
+    // a split-K partial.
+    auto staged = [&](auto tag, auto *out) -> bool {
+        using OT = decltype(tag);
+        constexpr int E = (int)sizeof(OT);
+        constexpr int PITCH = BR * E + 16;
+        constexpr int CPR = BR * E / 16;
+        static_assert(BCOL * PITCH <= NS * STAGE, "staged tile fits the ring");
+        if (a.C % (16 / E) != 0) return false;
+        lds_barrier();  // every wave is done with the ring
+#pragma unroll
+        for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+            for (int mc = 0; mc < MC; ++mc) {
+                const int pl = wc * (BCOL / WGC) + mc * 32 + lrow;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int cl = wr * (BR / WGR) + mr * 32 + 8 * g + 4 * lhi;
+                    store4<OT>(reinterpret_cast<OT *>(smem + pl * PITCH + cl * E), acc[mr][mc][4 * g],
+                               acc[mr][mc][4 * g + 1], acc[mr][mc][4 * g + 2], acc[mr][mc][4 * g + 3]);
+                }
+            }
+        lds_barrier();
+        for (int c = tid; c < BCOL * CPR; c += kThreads) {
+            const int row = c / CPR, cc = c % CPR;
+            const int m = ct * BCOL + row, ch = rt * BR + cc * (16 / E);
+            if (m < a.M && ch < a.C)
+                *reinterpret_cast<v4u *>(out + (size_t)m * a.C + ch) = lds_read16(smem + row * PITCH + cc * 16);
+        }
+        return true;
+    };
+    if (a.splits == 1 ? staged(T{}, dx) : staged(float{}, a.ws + (size_t)split * a.M * a.C)) return;
 #pragma unroll
     for (int mr = 0; mr < MR; ++mr)
 #pragma unroll

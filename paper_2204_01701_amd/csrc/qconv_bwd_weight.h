@@ -232,8 +232,56 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
     const bool padded = a.C_out != a.C;  // dW_t stored with C_out < C channels
     const int KPO = a.KH * a.KW * a.C_out;
     const bool vec_out = (a.KP & 3) == 0 && !padded;
+    // Staged stores: each term's BO x BKP block of dW_t (o rows, k' contiguous
+    // in OHWI) goes through the idle LDS ring and out in 16-byte chunks with
+    // consecutive lanes on consecutive addresses.
+    constexpr int PITCH = BKP * 4 + 16;  // LDS bytes per staged o row
+    constexpr int MAPB = BO * PITCH;
+    constexpr int RING = NS * STAGE;
+    constexpr int PER = RING / MAPB >= 3 ? 3 : (RING / MAPB >= 1 ? RING / MAPB : 1);
+    constexpr int CPR = BKP / 4;  // 16-byte chunks per row
+    if constexpr (MAPB <= RING) {
+        if (vec_out) {
+#pragma unroll
+            for (int t0 = 0; t0 < 3; t0 += PER) {
+                lds_barrier();  // the ring (or the previous round's tiles) is no longer read
+#pragma unroll
+                for (int t = t0; t < t0 + PER && t < 3; ++t) {
+                    char *tile = smem + (t - t0) * MAPB;
+#pragma unroll
+                    for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+                        for (int mc = 0; mc < MC; ++mc) {
+                            const int ol = wc * (BO / WGC) + mc * 32 + lrow;
+#pragma unroll
+                            for (int g = 0; g < 4; ++g) {
+                                const int kl = wr * (BKP / WGR) + mr * 32 + 8 * g + 4 * lhi;
+                                store4<float>(reinterpret_cast<float *>(tile + ol * PITCH + kl * 4),
+                                              acc[t][mr][mc][4 * g], acc[t][mr][mc][4 * g + 1],
+                                              acc[t][mr][mc][4 * g + 2], acc[t][mr][mc][4 * g + 3]);
+                            }
+                        }
+                }
+                lds_barrier();
+#pragma unroll
+                for (int t = t0; t < t0 + PER && t < 3; ++t) {
+                    const char *tile = smem + (t - t0) * MAPB;
+                    float *__restrict__ dst =
+                        a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * KPO;
+                    for (int c = tid; c < BO * CPR; c += NT) {
+                        const int row = c / CPR, cc = c % CPR;
+                        const int o = ct * BO + row, k = rt * BKP + 4 * cc;
+                        if (o < a.O && k < a.KP)
+                            *reinterpret_cast<v4u *>(dst + (size_t)o * a.KP + k) =
+                                lds_read16(tile + row * PITCH + cc * 16);
+                    }
+                }
+            }
+        }
+    }
 #pragma unroll
     for (int t = 0; t < 3; ++t) {
+        if (MAPB <= RING && vec_out) break;  // stored above
         float *__restrict__ dst = a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * KPO;
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr)
