@@ -127,8 +127,9 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         }
     }
 
-    auto issue = [&](int s, int slot, bool live) {
+    auto issue = [&](int s, int slot, bool live, int lo, int hi) {
         char *base = smem + slot * STAGE + wave * 1024;
+        DmaPart part(lo, hi);
         if constexpr (CA) {
             const int k0 = min(s, a.stages_total - 1) * KE;
             const int tap = (int)fdiv((uint32_t)k0, a.fd_o);
@@ -137,14 +138,16 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
             const int q = tap - r * a.KW;
             const long long sw = ((long long)o0 * khkw + tap) * a.C;
 #pragma unroll
-            for (int i = 0; i < NIW; ++i) dma16(wrow[i] + sw, base + i * 4096);
+            for (int i = 0; i < NIW; ++i)
+                if (part.take()) dma16(wrow[i] + sw, base + i * 4096);
             const long long sg = o0 - ((long long)r * a.WO + q) * a.O;
 #pragma unroll
             for (int j = 0; j < NIP; ++j) {
                 const bool ok = live && ((gmask[j] >> tap) & 1u);
 #pragma unroll
                 for (int u = 0; u < 3; ++u)
-                    dma16(dma_src(ok, gsrc[u] + (go[j] + sg), a.zero), base + (NIW + u * NIP + j) * 4096);
+                    if (part.take())
+                        dma16(dma_src(ok, gsrc[u] + (go[j] + sg), a.zero), base + (NIW + u * NIP + j) * 4096);
             }
             return;
         }
@@ -163,13 +166,14 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
                 const int tapr = (int)fdiv((uint32_t)kr, a.fd_o);
                 const int orow = kr - tapr * a.O;
                 const bool ok = live && wc_ok && kr < a.K;
-                dma16(dma_src(ok, wt[t] + ((size_t)(orow * khkw + tapr) * a.C + wc0), a.zero), base + i * 4096);
+                if (part.take())
+                    dma16(dma_src(ok, wt[t] + ((size_t)(orow * khkw + tapr) * a.C + wc0), a.zero), base + i * 4096);
             }
         } else {
 #pragma unroll
             for (int i = 0; i < NIW; ++i) {
                 const bool ok = kin && woff[i] >= 0;
-                dma16(dma_src(ok, wt[(64 * i) / BR] + woff[i] + k, a.zero), base + i * 4096);
+                if (part.take()) dma16(dma_src(ok, wt[(64 * i) / BR] + woff[i] + k, a.zero), base + i * 4096);
             }
         }
 #pragma unroll
@@ -189,7 +193,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
             ok = ok && kin && goff[j] >= 0;
 #pragma unroll
             for (int u = 0; u < 3; ++u)
-                dma16(dma_src(ok, gsrc[u] + p, a.zero), base + (NIW + u * NIP + j) * 4096);
+                if (part.take()) dma16(dma_src(ok, gsrc[u] + p, a.zero), base + (NIW + u * NIP + j) * 4096);
         }
     };
 

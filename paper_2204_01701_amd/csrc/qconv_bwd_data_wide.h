@@ -91,8 +91,9 @@ __global__ __launch_bounds__(64 * WGR * WGC) void qconv_bwd_data_wide_kernel(con
                     gmask |= 1u << (r * a.KW + q);
     }
 
-    auto issue = [&](int s, int slot, bool live) {
+    auto issue = [&](int s, int slot, bool live, int lo, int hi) {
         char *base = smem + slot * STAGE + wave * 1024;
+        DmaPart part(lo, hi);
         const int k0 = min(s, a.stages_total - 1) * KE;
         const int tap = (int)fdiv((uint32_t)k0, a.fd_o);
         const int o0 = k0 - tap * a.O;
@@ -100,11 +101,13 @@ __global__ __launch_bounds__(64 * WGR * WGC) void qconv_bwd_data_wide_kernel(con
         const int q = tap - r * a.KW;
         const long long sw = ((long long)o0 * khkw + tap) * a.C;
 #pragma unroll
-        for (int t = 0; t < 3; ++t) dma16(wt[t] + (wbase + sw), base + t * WT);
+        for (int t = 0; t < 3; ++t)
+            if (part.take()) dma16(wt[t] + (wbase + sw), base + t * WT);
         const long long sg = o0 - ((long long)r * a.WO + q) * a.O;
         const bool ok = live && ((gmask >> tap) & 1u);
 #pragma unroll
-        for (int u = 0; u < 3; ++u) dma16(dma_src(ok, gsrc[u] + (go + sg), a.zero), base + 3 * WT + u * GT);
+        for (int u = 0; u < 3; ++u)
+            if (part.take()) dma16(dma_src(ok, gsrc[u] + (go + sg), a.zero), base + 3 * WT + u * GT);
     };
 
     f32x16_t acc[MR][MC];

@@ -105,8 +105,9 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
             glin[i] = (long long)(s_begin * KE + RG * (NW * i + wave) + lane / SG) * a.O + og;
     }
 
-    auto issue = [&](int s, int slot, bool live) {
+    auto issue = [&](int s, int slot, bool live, int lo, int hi) {
         char *base = smem + slot * STAGE + wave * 1024;
+        DmaPart part(lo, hi);
         if constexpr (LIN) {
             const int ds = s - s_begin;
             const int mleft = a.M - s * KE;  // pixels of this step that exist: lane pixel < mleft
@@ -116,6 +117,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
                 const int p = RX * (NW * i + wave) + lane / SX;
                 const bool ok = live && kp_ok && p < mleft && (unsigned)(ohv[i] + dh) < (unsigned)a.H &&
                                 (unsigned)(owv[i] + dw) < (unsigned)a.W;
+                if (!part.take()) continue;  // (its position advances in the part that issues it)
                 dma16(dma_src(ok, x + (xlin[i] + xs), a.zero), base + i * (NT * 16));
                 int ow = owv[i] + a.lin_dr;
                 const int carry = ow >= a.WO ? 1 : 0;
@@ -132,7 +134,8 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
                 const bool ok = live && og_ok && p < mleft;
 #pragma unroll
                 for (int u = 0; u < 3; ++u)
-                    dma16(dma_src(ok, gsrc[u] + (glin[i] + gs), a.zero), base + XB + u * GB + i * (NT * 16));
+                    if (part.take())
+                        dma16(dma_src(ok, gsrc[u] + (glin[i] + gs), a.zero), base + XB + u * GB + i * (NT * 16));
             }
             return;
         }
@@ -145,7 +148,8 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
             const int ow = rem - oh * a.WO;
             const int ih = oh * a.SH - a.PH + xr, iw = ow * a.SW - a.PW + xq;
             const bool ok = live && kp_ok && m < a.M && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-            dma16(dma_src(ok, x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + xc, a.zero), base + i * (NT * 16));
+            if (part.take())
+                dma16(dma_src(ok, x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + xc, a.zero), base + i * (NT * 16));
         }
 #pragma unroll
         for (int i = 0; i < NIG; ++i) {
@@ -154,7 +158,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
             const size_t off = (size_t)m * a.O + og;
 #pragma unroll
             for (int u = 0; u < 3; ++u)
-                dma16(dma_src(ok, gsrc[u] + off, a.zero), base + XB + u * GB + i * (NT * 16));
+                if (part.take()) dma16(dma_src(ok, gsrc[u] + off, a.zero), base + XB + u * GB + i * (NT * 16));
         }
     };
 

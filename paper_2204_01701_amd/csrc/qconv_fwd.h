@@ -119,8 +119,9 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         }
     }
 
-    auto issue = [&](int s, int slot, bool live) {
+    auto issue = [&](int s, int slot, bool live, int lo, int hi) {
         char *base = smem + slot * STAGE + wave * 1024;
+        DmaPart part(lo, hi);
         if constexpr (CA) {
             const int k0 = min(s, a.stages_total - 1) * KE;
             const int tap = (int)fdiv((uint32_t)k0, a.fd_c);
@@ -129,11 +130,12 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
             const int q = tap - r * a.KW;
             const long long soff = ((long long)r * a.W + q) * a.C + c0;
 #pragma unroll
-            for (int i = 0; i < NIW; ++i) dma16(wrow[i] + k0, base + i * (NT * 16));
+            for (int i = 0; i < NIW; ++i)
+                if (part.take()) dma16(wrow[i] + k0, base + i * (NT * 16));
 #pragma unroll
             for (int j = 0; j < NIX; ++j) {
                 const bool ok = live && ((xmask[j] >> tap) & 1u);
-                dma16(dma_src(ok, x + (xo[j] + soff), a.zero), base + (NIW + j) * (NT * 16));
+                if (part.take()) dma16(dma_src(ok, x + (xo[j] + soff), a.zero), base + (NIW + j) * (NT * 16));
             }
             return;
         }
@@ -146,13 +148,14 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
 #pragma unroll
         for (int i = 0; i < NIW; ++i) {
             const bool ok = kin && woff[i] >= 0;
-            dma16(dma_src(ok, wp[wterm[i]] + woff[i] + k, a.zero), base + i * (NT * 16));
+            if (part.take()) dma16(dma_src(ok, wp[wterm[i]] + woff[i] + k, a.zero), base + i * (NT * 16));
         }
 #pragma unroll
         for (int j = 0; j < NIX; ++j) {
             const int ih = ih0[j] + r, iw = iw0[j] + q;
             const bool ok = kin && xoff[j] >= 0 && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-            dma16(dma_src(ok, x + xoff[j] + (ih * a.W + iw) * a.C + c, a.zero), base + (NIW + j) * (NT * 16));
+            if (part.take())
+                dma16(dma_src(ok, x + xoff[j] + (ih * a.W + iw) * a.C + c, a.zero), base + (NIW + j) * (NT * 16));
         }
     };
 
@@ -202,8 +205,8 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     };
     if constexpr (SETS == 2)
         run_ring<NS, NI>(nst, s_begin, issue, read, mma);
-    else
-        run_ring_single<NS, NI>(nst, s_begin, issue, read, mma);
+    else  // 8 waves leave each barrier together: half the copies go out one chunk later (measured faster)
+        run_ring_single<NS, NI, 2, (NI + 1) / 2>(nst, s_begin, issue, read, mma);
 
     // Epilogue.
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);

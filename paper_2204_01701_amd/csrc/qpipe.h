@@ -48,6 +48,20 @@ __device__ __forceinline__ void dma16(const void *gptr, char *wave_base) {
     asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gptr), "{m0}"(lds));
 }
 
+// The DMA instructions of a K step are numbered 0 .. NI - 1 in issue order;
+// a ring may issue them in two parts, issue(step, slot, live, lo, hi) copying
+// those numbered lo .. hi - 1.  take() is called once per instruction in
+// order (the numbering folds to constants once the issue loops unroll).
+struct DmaPart {
+    int lo, hi, n;
+    __device__ __forceinline__ DmaPart(int l, int h) : lo(l), hi(h), n(0) {}
+    __device__ __forceinline__ bool take() {
+        const bool t = n >= lo && n < hi;
+        ++n;
+        return t;
+    }
+};
+
 // Branch-free choice of a DMA source: the operand address when ok, else the zero page.
 __device__ __forceinline__ const void *dma_src(bool ok, const void *p, const void *zero) {
     const uint64_t a = reinterpret_cast<uint64_t>(p), z = reinterpret_cast<uint64_t>(zero);
@@ -80,6 +94,9 @@ __device__ __forceinline__ void wait_vm_barrier_lgkm() {
     asm volatile("s_barrier" ::: "memory");
 }
 
+// Plain barrier for LDS hand-offs that involve no DMA (epilogues).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Waits for every outstanding global/DMA operation of this thread.
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -104,13 +121,15 @@ __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)
 // last step they fill a slot nobody reads again with zeros), so the loop body
 // is straight-line code and the vmcnt allowance is the same in every
 // iteration.  The last step issues nothing.  NS - 1 steps are in flight
-// while a step is being consumed.
-template <int NS, int NI, class Issue, class Read, class Mma>
+// while a step is being consumed.  With NI1 < NI only the first NI1
+// instructions of a step go out before the set-0 MFMAs and the rest after
+// the barrier (the wait allowance counts the part already issued).
+template <int NS, int NI, int NI1 = NI, class Issue, class Read, class Mma>
 __device__ __forceinline__ void run_ring(int nst, int s_begin, Issue &&issue, Read &&read, Mma &&mma) {
-    static_assert(NS >= 3 && (NS - 2) * NI < 64, "ring depth");
+    static_assert(NS >= 3 && (NS - 2) * NI < 64 && NI1 >= 1 && NI1 <= NI, "ring depth");
     if (nst <= 0) return;
 #pragma unroll
-    for (int i = 0; i < NS - 1; ++i) issue(s_begin + i, i, i < nst);
+    for (int i = 0; i < NS - 1; ++i) issue(s_begin + i, i, i < nst, 0, NI);
     wait_vm_barrier<(NS - 2) * NI>();
     read(0, 0, 0);
     int slot = 0;
@@ -118,10 +137,13 @@ __device__ __forceinline__ void run_ring(int nst, int s_begin, Issue &&issue, Re
     // path and the compiler's wait before the set-1 MFMAs is not widened by a
     // merge with the barrier-less path.
     for (int it = 0; it < nst - 1; ++it) {
+        const int s = s_begin + it + NS - 1, free = slot == 0 ? NS - 1 : slot - 1;
+        const bool live = it + NS - 1 < nst;
         read(slot, 1, 1);
-        issue(s_begin + it + NS - 1, slot == 0 ? NS - 1 : slot - 1, it + NS - 1 < nst);
+        issue(s, free, live, 0, NI1);
         mma(0);
-        wait_vm_barrier_lgkm<(NS - 2) * NI>();
+        wait_vm_barrier_lgkm<(NS - 3) * NI + NI1>();
+        if constexpr (NI1 < NI) issue(s, free, live, NI1, NI);
         slot = slot + 1 == NS ? 0 : slot + 1;
         read(slot, 0, 0);
         mma(1);
@@ -136,20 +158,24 @@ __device__ __forceinline__ void run_ring(int nst, int s_begin, Issue &&issue, Re
 // two waves per SIMD and need the registers for accumulators: each of the CH
 // chunks of a step is read and then multiplied; the other wave on the SIMD
 // covers the LDS latency.
-template <int NS, int NI, int CH = 2, class Issue, class Read, class Mma>
+template <int NS, int NI, int CH = 2, int NI1 = NI, class Issue, class Read, class Mma>
 __device__ __forceinline__ void run_ring_single(int nst, int s_begin, Issue &&issue, Read &&read, Mma &&mma) {
-    static_assert(NS >= 3 && (NS - 2) * NI < 64, "ring depth");
+    static_assert(NS >= 3 && (NS - 2) * NI < 64 && NI1 >= 1 && NI1 <= NI, "ring depth");
+    static_assert(CH >= 2 || NI1 == NI, "the second part goes out after the first half of the chunks");
     if (nst <= 0) return;
 #pragma unroll
-    for (int i = 0; i < NS - 1; ++i) issue(s_begin + i, i, i < nst);
+    for (int i = 0; i < NS - 1; ++i) issue(s_begin + i, i, i < nst, 0, NI);
     wait_vm_barrier<(NS - 2) * NI>();
     int slot = 0;
     for (int it = 0; it < nst - 1; ++it) {
-        issue(s_begin + it + NS - 1, slot == 0 ? NS - 1 : slot - 1, it + NS - 1 < nst);
+        const int s = s_begin + it + NS - 1, free = slot == 0 ? NS - 1 : slot - 1;
+        const bool live = it + NS - 1 < nst;
+        issue(s, free, live, 0, NI1);
 #pragma unroll
         for (int ch = 0; ch < CH; ++ch) {
             read(slot, ch, 0);
             mma(0);
+            if (ch == CH / 2 - 1 && NI1 < NI) issue(s, free, live, NI1, NI);
         }
         wait_vm_barrier_lgkm<(NS - 2) * NI>();
         slot = slot + 1 == NS ? 0 : slot + 1;
@@ -161,9 +187,6 @@ __device__ __forceinline__ void run_ring_single(int nst, int s_begin, Issue &&is
     }
     wait_vm_all();
 }
-
-// Plain barrier for LDS hand-offs that involve no DMA (epilogues).
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // --- KM layout ---------------------------------------------------------------
 // Byte offset of logical 16-byte column c (0..3) of row `row` in a KM tile.
