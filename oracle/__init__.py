@@ -60,6 +60,8 @@ def _load():
     lib.oracle_conv2d_fwd_at.argtypes = conv_geom + [_D] + w6 + [ctypes.c_longlong, _L, _D, _D, _D]
     lib.oracle_conv2d_dx_at.argtypes = conv_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
     lib.oracle_conv2d_dw_channel.argtypes = conv_geom + [_D] + w6 + [_D, _I] + [_D] * 6
+    lib.oracle_conv2d_fwd_neuron.argtypes = [_I] + conv_geom + [_D] + w6 + [_D, _D, _D]
+    lib.oracle_conv2d_bwd_neuron.argtypes = [_I] + conv_geom + [_D] + w6 + [_D] + [_D] * 7
     lib.oracle_conv2d_out_size.argtypes = [_I] * 4
     lib.oracle_conv2d_out_size.restype = _I
     fc_geom = [_I] * 3
@@ -68,7 +70,7 @@ def _load():
     lib.oracle_linear_fwd_at.argtypes = fc_geom + [_D] + w6 + [ctypes.c_longlong, _L, _D, _D, _D]
     lib.oracle_linear_dx_rows.argtypes = fc_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
     lib.oracle_linear_dw_row.argtypes = fc_geom + [_D] + w6 + [_D, _I] + [_D] * 6
-    for f in ("oracle_conv2d_fwd", "oracle_conv2d_bwd", "oracle_conv2d_fwd_at", "oracle_conv2d_dx_at",
+    for f in ("oracle_conv2d_fwd_neuron", "oracle_conv2d_bwd_neuron", "oracle_conv2d_fwd", "oracle_conv2d_bwd", "oracle_conv2d_fwd_at", "oracle_conv2d_dx_at",
               "oracle_conv2d_dw_channel", "oracle_linear_fwd", "oracle_linear_bwd",
               "oracle_linear_fwd_at", "oracle_linear_dx_rows", "oracle_linear_dw_row"):
         getattr(lib, f).restype = None
@@ -236,6 +238,62 @@ def linear_dw_row(x, wa, wb, wc, ba, bb, bc, gy, o):
     lib.oracle_linear_dw_row(B, I, O, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
                              int(o), *[_p(out[k]) for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
     return out
+
+
+# Neuron types (the proposed one and the earlier designs of Table 1 / Table 3).
+NEURON_QUADRA, NEURON_T4, NEURON_T4_IDENTITY, NEURON_T3, NEURON_T2 = 0, 1, 2, 3, 4
+NEURON_TERMS = {0: 3, 1: 2, 2: 2, 3: 1, 4: 1}  # first-order terms (weights) per type
+
+
+def conv2d_fwd_neuron(neuron, x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, stride=1, pad=0):
+    """Forward of neuron type `neuron`: returns (Y, T_a, T_b), N x O x Ho x Wo
+    (T_b is zeros for the one-term types, T_a is W_a*(X o X) + b_a for T2)."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc = map(_f64, (x, wa, wb, wc, ba, bb, bc))
+    g = _conv_geom(x, wa, stride, pad)
+    N, O = g[0], g[4]
+    Ho, Wo = out_size(g[2], g[5], g[7], g[9]), out_size(g[3], g[6], g[8], g[10])
+    if neuron == NEURON_T4_IDENTITY:
+        assert g[1] == O and Ho == g[2] and Wo == g[3], "the identity shortcut needs C == O and an unchanged map"
+    y, ta, tb = np.empty((N, O, Ho, Wo)), np.empty((N, O, Ho, Wo)), np.empty((N, O, Ho, Wo))
+    lib.oracle_conv2d_fwd_neuron(int(neuron), *g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc),
+                                 _p(y), _p(ta), _p(tb))
+    return y, ta, tb
+
+
+def conv2d_bwd_neuron(neuron, x, wa, wb, wc, ba, bb, bc, gy, stride=1, pad=0):
+    """Backward of neuron type `neuron`: dict dx and dw*/db* of the terms it has."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    g = _conv_geom(x, wa, stride, pad)
+    O = g[4]
+    nt = NEURON_TERMS[int(neuron)]
+    keys = [("dwa", "dba"), ("dwb", "dbb"), ("dwc", "dbc")][:nt]
+    out = {"dx": np.empty_like(x)}
+    for kw, kb in keys:
+        out[kw] = np.empty_like(wa)
+        out[kb] = np.empty(O)
+    lib.oracle_conv2d_bwd_neuron(int(neuron), *g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
+                                 *[_p(out.get(k)) for k in ("dx", "dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
+    return out
+
+
+def linear_fwd_neuron(neuron, x, wa, wb=None, wc=None, ba=None, bb=None, bc=None):
+    """Fully-connected layer of neuron type `neuron` (the 1x1 convolution of a 1x1 map): (Y, T_a, T_b), B x O."""
+    B, I = np.shape(x)
+    w4 = [None if w is None else np.asarray(w).reshape(np.shape(w)[0], I, 1, 1) for w in (wa, wb, wc)]
+    y, ta, tb = conv2d_fwd_neuron(neuron, np.asarray(x).reshape(B, I, 1, 1), *w4, ba, bb, bc)
+    return y.reshape(B, -1), ta.reshape(B, -1), tb.reshape(B, -1)
+
+
+def linear_bwd_neuron(neuron, x, wa, wb, wc, ba, bb, bc, gy):
+    B, I = np.shape(x)
+    O = np.shape(wa)[0]
+    w4 = [None if w is None else np.asarray(w).reshape(O, I, 1, 1) for w in (wa, wb, wc)]
+    out = conv2d_bwd_neuron(neuron, np.asarray(x).reshape(B, I, 1, 1), *w4, ba, bb, bc,
+                            np.asarray(gy).reshape(B, O, 1, 1))
+    return {k: (v.reshape(B, I) if k == "dx" else (v.reshape(O, I) if k.startswith("dw") else v))
+            for k, v in out.items()}
 
 
 def num_threads() -> int:

@@ -185,6 +185,179 @@ void oracle_conv2d_bwd(int N, int C, int H, int W, int O, int KH, int KW,
 }
 
 /* ---------------------------------------------------------------------------
+ * The earlier quadratic neuron types the paper compares its design with
+ * (Table 1 types and the Table 3 baselines), as convolution layers with the
+ * same geometry rules.  neuron: 0 the proposed one (as above), 1 T4, 2 T4 plus
+ * identity, 3 T3, 4 T2.  With T_t = W_t * X + b_t:
+ *   T4:            Y = T_a o T_b
+ *   T4 + identity: Y = T_a o T_b + X      (C == O, Ho == H, Wo == W: the
+ *                                          shortcut adds input channel o)
+ *   T3:            Y = T_a o T_a          (the square of one first-order neuron)
+ *   T2:            Y = W_a * (X o X) + b_a (a first-order neuron of the squared input)
+ * Unused weights and biases are ignored (may be NULL).  The saved maps:
+ * T_a and T_b (T4 types), T_a (T3), none (T2).
+ * ------------------------------------------------------------------------- */
+void oracle_conv2d_fwd_neuron(int neuron, int N, int C, int H, int W, int O, int KH, int KW,
+                              int sh, int sw, int ph, int pw,
+                              const double *x, const double *wa, const double *wb, const double *wc,
+                              const double *ba, const double *bb, const double *bc,
+                              double *y, double *ta, double *tb) {
+    if (neuron == 0) {
+        oracle_conv2d_fwd(N, C, H, W, O, KH, KW, sh, sw, ph, pw, x, wa, wb, wc, ba, bb, bc, y, ta, tb);
+        return;
+    }
+    int Ho = out_size(H, KH, sh, ph), Wo = out_size(W, KW, sw, pw);
+    if (Ho < 1 || Wo < 1) return;
+    if (neuron == 2 && (C != O || Ho != H || Wo != W)) return;
+    size_t nx = (size_t)N * C * H * W;
+    double *x2 = NULL;
+    if (neuron == 4) { /* the squared input, elementwise */
+        x2 = (double *)malloc(nx * sizeof(double));
+        if (!x2) return;
+        for (size_t e = 0; e < nx; ++e) x2[e] = x[e] * x[e];
+    }
+    long long total = (long long)N * O * Ho * Wo;
+#pragma omp parallel for schedule(static)
+    for (long long e = 0; e < total; ++e) {
+        int j = (int)(e % Wo), i = (int)((e / Wo) % Ho);
+        int o = (int)((e / ((long long)Wo * Ho)) % O), n = (int)(e / ((long long)Wo * Ho * O));
+        double Ta, Tb = 0.0, out;
+        if (neuron == 4) {
+            Ta = conv_term(C, H, W, KH, KW, sh, sw, ph, pw, x2, wa, ba, n, o, i, j);
+            out = Ta;
+        } else {
+            Ta = conv_term(C, H, W, KH, KW, sh, sw, ph, pw, x, wa, ba, n, o, i, j);
+            if (neuron == 3) {
+                out = Ta * Ta;
+            } else {
+                Tb = conv_term(C, H, W, KH, KW, sh, sw, ph, pw, x, wb, bb, n, o, i, j);
+                out = Ta * Tb;
+                if (neuron == 2) out += x[IDX4(n, o, i, j, C, H, W)];
+            }
+        }
+        if (y) y[e] = out;
+        if (ta) ta[e] = Ta;
+        if (tb) tb[e] = Tb;
+    }
+    free(x2);
+}
+
+/* Backward of the neuron types above: the per-term output gradients follow
+ * from the product rule on each Y,
+ *   T4, T4 + identity: G_a = G o T_b, G_b = G o T_a   (plus dX += G for the shortcut)
+ *   T3:                G_a = 2 G o T_a
+ *   T2:                G_a = G, the operand being X o X, so dW_a correlates G
+ *                      with X o X and dX = 2 X o (transposed convolution of G with W_a)
+ * and each term's weight, bias and input gradients are those of an ordinary
+ * convolution (the same loops as oracle_conv2d_bwd, written out again here). */
+void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int KH, int KW,
+                              int sh, int sw, int ph, int pw,
+                              const double *x, const double *wa, const double *wb, const double *wc,
+                              const double *ba, const double *bb, const double *bc,
+                              const double *gy,
+                              double *dx, double *dwa, double *dwb, double *dwc,
+                              double *dba, double *dbb, double *dbc) {
+    if (neuron == 0) {
+        oracle_conv2d_bwd(N, C, H, W, O, KH, KW, sh, sw, ph, pw, x, wa, wb, wc, ba, bb, bc, gy,
+                          dx, dwa, dwb, dwc, dba, dbb, dbc);
+        return;
+    }
+    int Ho = out_size(H, KH, sh, ph), Wo = out_size(W, KW, sw, pw);
+    if (Ho < 1 || Wo < 1) return;
+    if (neuron == 2 && (C != O || Ho != H || Wo != W)) return;
+    size_t P = (size_t)N * O * Ho * Wo, nx = (size_t)N * C * H * W;
+    double *ga = (double *)malloc(P * sizeof(double));
+    double *gb = (double *)malloc(P * sizeof(double));
+    double *ta = (double *)malloc(P * sizeof(double));
+    double *tb = (double *)malloc(P * sizeof(double));
+    double *xo = (double *)malloc(nx * sizeof(double)); /* the operand X (or X o X) */
+    if (!ga || !gb || !ta || !tb || !xo) { free(ga); free(gb); free(ta); free(tb); free(xo); return; }
+    oracle_conv2d_fwd_neuron(neuron, N, C, H, W, O, KH, KW, sh, sw, ph, pw, x, wa, wb, wc, ba, bb, bc,
+                             NULL, ta, tb);
+    int nterm = (neuron == 1 || neuron == 2) ? 2 : 1;
+    for (size_t e = 0; e < P; ++e) {
+        if (nterm == 2) {
+            ga[e] = gy[e] * tb[e];
+            gb[e] = gy[e] * ta[e];
+        } else if (neuron == 3) {
+            ga[e] = 2.0 * gy[e] * ta[e];
+        } else {
+            ga[e] = gy[e];
+        }
+    }
+    for (size_t e = 0; e < nx; ++e) xo[e] = neuron == 4 ? x[e] * x[e] : x[e];
+    const double *gt[2] = {ga, gb};
+    double *dwt[2] = {dwa, dwb};
+    double *dbt[2] = {dba, dbb};
+    const double *wt[2] = {wa, wb};
+    (void)wc; (void)bc; (void)dwc; (void)dbc;
+
+    long long nw = (long long)O * C * KH * KW;
+    for (int t = 0; t < nterm; ++t) {
+        if (!dwt[t]) continue;
+        const double *g = gt[t];
+        double *dw = dwt[t];
+#pragma omp parallel for schedule(static)
+        for (long long e = 0; e < nw; ++e) {
+            int q = (int)(e % KW), r = (int)((e / KW) % KH);
+            int c = (int)((e / ((long long)KW * KH)) % C), o = (int)(e / ((long long)KW * KH * C));
+            double acc = 0.0;
+            for (int n = 0; n < N; ++n)
+                for (int i = 0; i < Ho; ++i) {
+                    int ih = i * sh - ph + r;
+                    if (ih < 0 || ih >= H) continue;
+                    for (int j = 0; j < Wo; ++j) {
+                        int iw = j * sw - pw + q;
+                        if (iw < 0 || iw >= W) continue;
+                        acc += g[IDX4(n, o, i, j, O, Ho, Wo)] * xo[IDX4(n, c, ih, iw, C, H, W)];
+                    }
+                }
+            dw[e] = acc;
+        }
+    }
+    for (int t = 0; t < nterm; ++t) {
+        if (!dbt[t]) continue;
+        const double *g = gt[t];
+#pragma omp parallel for schedule(static)
+        for (int o = 0; o < O; ++o) {
+            double acc = 0.0;
+            for (int n = 0; n < N; ++n)
+                for (int i = 0; i < Ho; ++i)
+                    for (int j = 0; j < Wo; ++j) acc += g[IDX4(n, o, i, j, O, Ho, Wo)];
+            dbt[t][o] = acc;
+        }
+    }
+    if (dx) {
+        long long nxx = (long long)N * C * H * W;
+#pragma omp parallel for schedule(static)
+        for (long long e = 0; e < nxx; ++e) {
+            int w_ = (int)(e % W), h = (int)((e / W) % H);
+            int c = (int)((e / ((long long)W * H)) % C), n = (int)(e / ((long long)W * H * C));
+            double acc = 0.0;
+            for (int t = 0; t < nterm; ++t)
+                for (int o = 0; o < O; ++o)
+                    for (int r = 0; r < KH; ++r) {
+                        int hi = h + ph - r;
+                        if (hi < 0 || hi % sh) continue;
+                        int i = hi / sh;
+                        if (i >= Ho) continue;
+                        for (int q = 0; q < KW; ++q) {
+                            int wi = w_ + pw - q;
+                            if (wi < 0 || wi % sw) continue;
+                            int j = wi / sw;
+                            if (j >= Wo) continue;
+                            acc += gt[t][IDX4(n, o, i, j, O, Ho, Wo)] * wt[t][IDX4(o, c, r, q, C, KH, KW)];
+                        }
+                    }
+            if (neuron == 4) acc *= 2.0 * x[e];                 /* d(X o X)/dX */
+            if (neuron == 2) acc += gy[IDX4(n, c, h, w_, O, Ho, Wo)]; /* the identity shortcut */
+            dx[e] = acc;
+        }
+    }
+    free(ga); free(gb); free(ta); free(tb); free(xo);
+}
+
+/* ---------------------------------------------------------------------------
  * Sampled evaluation for full-size checks: the same definitions, evaluated
  * only at requested output positions.
  * ------------------------------------------------------------------------- */
