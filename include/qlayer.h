@@ -59,6 +59,30 @@ extern "C" {
 
 typedef enum { QL_F32 = 0, QL_BF16 = 1 } ql_dtype;
 
+/* Neuron type of a layer.  QL_NEURON_QUADRA is the design of section 3.1
+ * (eq:2ndneuron3); the others are the earlier quadratic neurons of Table 1
+ * that the paper evaluates against (Table 3), each built from the same
+ * first-order terms T_t = W_t * X + b_t:
+ *   QL_NEURON_QUADRA      Y = T_a o T_b + T_c            (weights a, b, c)
+ *   QL_NEURON_T4          Y = T_a o T_b                  (weights a, b)
+ *   QL_NEURON_T4_IDENTITY Y = T_a o T_b + X              (weights a, b; C == O and the
+ *                                                         output map the size of the input)
+ *   QL_NEURON_T3          Y = T_a o T_a                  (weight a)
+ *   QL_NEURON_T2          Y = W_a * (X o X) + b_a        (weight a)
+ * Backward, with G = dl/dY: G_a = G o T_b, G_b = G o T_a (T4 types; the
+ * shortcut adds G to dX), G_a = 2 G o T_a (T3), and for T2 dW_a correlates G
+ * with X o X while dX = 2 X o (the transposed convolution of G with W_a).
+ * Pointers of terms a type lacks are ignored (may be NULL); the saved maps
+ * are T_a, T_b (QUADRA, T4 types), T_a (T3), none (T2; its input gradient
+ * takes X itself in the `ta` argument). */
+typedef enum {
+    QL_NEURON_QUADRA = 0,
+    QL_NEURON_T4 = 1,
+    QL_NEURON_T4_IDENTITY = 2,
+    QL_NEURON_T3 = 3,
+    QL_NEURON_T2 = 4
+} ql_neuron;
+
 typedef enum {
     QL_OK = 0,
     QL_EINVAL = 1,       /* invalid argument */
@@ -74,12 +98,14 @@ typedef struct {
     int stride_h, stride_w; /* >= 1 */
     int pad_h, pad_w;       /* >= 0, symmetric zero padding */
     ql_dtype dtype;
+    ql_neuron neuron;       /* QL_NEURON_QUADRA (0) unless set */
 } ql_conv_desc;
 
 /* Geometry of a quadratic fully-connected layer. */
 typedef struct {
     int batch, in, out; /* X: batch x in, W_t: out x in, Y: batch x out */
     ql_dtype dtype;
+    ql_neuron neuron;   /* QL_NEURON_QUADRA (0) unless set */
 } ql_linear_desc;
 
 /* Human-readable name of a status code (static storage). */
@@ -91,14 +117,17 @@ int qlayer_version(void);
 /* ---------------------------------------------------------------------------
  * Convolution forward -- section 3.1 eq:2ndneuron3 applied as a conv layer.
  *   x          : X (N,H,W,C), required.
- *   wa, wb, wc : W_a, W_b, W_c (O,KH,KW,C), required.
+ *   wa, wb, wc : W_a, W_b, W_c (O,KH,KW,C), required for the terms the
+ *                neuron type has (all three for QL_NEURON_QUADRA).
  *   ba, bb, bc : b_a, b_b, b_c (O) float32; each may be NULL (= zero).
- *   y          : Y (N,Ho,Wo,O); may be NULL only when ta and tb are given
- *                (recompute mode of the hybrid back-propagation, section
- *                4.3: only the term maps are regenerated).
+ *   y          : Y (N,Ho,Wo,O); may be NULL only when the saved maps of the
+ *                type are given (recompute mode of the hybrid
+ *                back-propagation, section 4.3: only the term maps are
+ *                regenerated); required for QL_NEURON_T2.
  *   ta, tb     : if non-NULL, T_a and T_b (N,Ho,Wo,O) are written as well
- *                (the "saved" term maps the backward needs).  Recompute mode
- *                and saved mode produce bitwise identical T_a, T_b.
+ *                (the "saved" term maps the backward needs; tb only for the
+ *                two- and three-term types).  Recompute mode and saved mode
+ *                produce bitwise identical T_a, T_b.
  *   workspace  : qlayer_conv2d_fwd_workspace_size(desc) bytes (split-K
  *                partial sums for layers with few output pixels).
  * T_c is never written.
@@ -114,8 +143,10 @@ ql_status qlayer_conv2d_fwd(const ql_conv_desc *desc, const void *x,
  * Convolution input gradient -- section 4.3 (eq:AD chain rule, eq:SD):
  *   dX = sum_t  conv_transpose(G_t, W_t),  G_a = G o T_b, G_b = G o T_a, G_c = G.
  *   gy     : G = dl/dY (N,Ho,Wo,O), required.
- *   ta, tb : T_a, T_b (N,Ho,Wo,O) from a forward call, required.
- *   wa, wb, wc : weights (O,KH,KW,C), required.
+ *   ta, tb : the saved maps of the neuron type from a forward call: T_a and
+ *            T_b (N,Ho,Wo,O) for QUADRA and the T4 types, T_a for T3; for T2
+ *            `ta` is X (N,H,W,C) and tb is ignored.
+ *   wa, wb, wc : weights (O,KH,KW,C) of the terms the type has.
  *   dx     : dX (N,H,W,C), written (not accumulated).
  * The products G o T_b and G o T_a are formed on the fly and never stored.
  * ------------------------------------------------------------------------- */
@@ -130,9 +161,11 @@ ql_status qlayer_conv2d_bwd_data(const ql_conv_desc *desc, const void *gy,
  * Convolution weight and bias gradients -- section 4.3 eq:SD:
  *   dW_t[o,r,q,c] = sum_{n,i,j} G_t[n,i,j,o] X[n, i*s-p+r, j*s-p+q, c]
  *   db_t[o]       = sum_{n,i,j} G_t[n,i,j,o]
- *   x, gy, ta, tb  : required.
- *   dwa, dwb, dwc  : float32 (O,KH,KW,C), required, written (not accumulated).
- *   dba, dbb, dbc  : float32 (O); all three given or all three NULL (= skip).
+ *   x, gy          : required; ta, tb: the saved maps of the type (none for T2).
+ *   dwa, dwb, dwc  : float32 (O,KH,KW,C), required for the terms the type
+ *                    has, written (not accumulated).
+ *   dba, dbb, dbc  : float32 (O); given for every term of the type or all
+ *                    NULL (= skip).
  *   workspace      : qlayer_conv2d_bwd_weight_workspace_size(desc) bytes
  *                    (split-K partials, reduced in a fixed order, so results
  *                    are deterministic run to run).

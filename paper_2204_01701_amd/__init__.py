@@ -20,7 +20,8 @@ import ctypes
 import os
 
 __all__ = [
-    "QL_F32", "QL_BF16", "QLError", "ConvDesc", "LinearDesc", "conv_desc", "linear_desc", "lib",
+    "QL_F32", "QL_BF16", "QL_NEURON_QUADRA", "QL_NEURON_T4", "QL_NEURON_T4_IDENTITY", "QL_NEURON_T3",
+    "QL_NEURON_T2", "NEURON_TERMS", "QLError", "ConvDesc", "LinearDesc", "conv_desc", "linear_desc", "lib",
     "qlayer_version", "qlayer_status_string",
     "qlayer_conv2d_fwd_workspace_size", "qlayer_conv2d_fwd",
     "qlayer_conv2d_bwd_data_workspace_size", "qlayer_conv2d_bwd_data",
@@ -31,6 +32,9 @@ __all__ = [
 
 QL_F32 = 0
 QL_BF16 = 1
+# neuron types (qlayer.h ql_neuron): the proposed one and the earlier designs of Table 1
+QL_NEURON_QUADRA, QL_NEURON_T4, QL_NEURON_T4_IDENTITY, QL_NEURON_T3, QL_NEURON_T2 = 0, 1, 2, 3, 4
+NEURON_TERMS = {0: 3, 1: 2, 2: 2, 3: 1, 4: 1}  # first-order terms (weights) per type
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libqlayer.so")
@@ -44,7 +48,7 @@ class QLError(RuntimeError):
 
 class ConvDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in
-                ("n", "c", "h", "w", "o", "kh", "kw", "stride_h", "stride_w", "pad_h", "pad_w", "dtype")]
+                ("n", "c", "h", "w", "o", "kh", "kw", "stride_h", "stride_w", "pad_h", "pad_w", "dtype", "neuron")]
 
     @property
     def ho(self):
@@ -56,17 +60,18 @@ class ConvDesc(ctypes.Structure):
 
 
 class LinearDesc(ctypes.Structure):
-    _fields_ = [("batch", ctypes.c_int), ("in_", ctypes.c_int), ("out", ctypes.c_int), ("dtype", ctypes.c_int)]
+    _fields_ = [("batch", ctypes.c_int), ("in_", ctypes.c_int), ("out", ctypes.c_int), ("dtype", ctypes.c_int),
+                ("neuron", ctypes.c_int)]
 
 
-def conv_desc(n, c, h, w, o, kh, kw, stride=1, pad=0, dtype=QL_BF16) -> ConvDesc:
+def conv_desc(n, c, h, w, o, kh, kw, stride=1, pad=0, dtype=QL_BF16, neuron=QL_NEURON_QUADRA) -> ConvDesc:
     sh, sw = (stride, stride) if isinstance(stride, int) else stride
     ph, pw = (pad, pad) if isinstance(pad, int) else pad
-    return ConvDesc(n, c, h, w, o, kh, kw, sh, sw, ph, pw, dtype)
+    return ConvDesc(n, c, h, w, o, kh, kw, sh, sw, ph, pw, dtype, neuron)
 
 
-def linear_desc(batch, inp, out, dtype=QL_BF16) -> LinearDesc:
-    return LinearDesc(batch, inp, out, dtype)
+def linear_desc(batch, inp, out, dtype=QL_BF16, neuron=QL_NEURON_QUADRA) -> LinearDesc:
+    return LinearDesc(batch, inp, out, dtype, neuron)
 
 
 _lib = None

@@ -1,9 +1,29 @@
 // qargs.h -- kernel argument blocks (passed by value) of the quadratic-layer kernels.
 #pragma once
 
+#include <hip/hip_runtime.h>
+
 #include "qfastdiv.h"
 
 namespace ql {
+
+// Neuron types (arXiv 2204.01701: the proposed design, section 3.1, and the
+// earlier ones of Table 1 that Table 3 compares against), with T_t = W_t X + b_t:
+//   NEURON_QUADRA  Y = T_a o T_b + T_c      NEURON_T4  Y = T_a o T_b
+//   NEURON_T4I     Y = T_a o T_b + X        NEURON_T3  Y = T_a o T_a
+//   NEURON_T2      Y = W_a (X o X) + b_a
+enum { NEURON_QUADRA = 0, NEURON_T4 = 1, NEURON_T4I = 2, NEURON_T3 = 3, NEURON_T2 = 4 };
+// The kernels' compile-time operand mode: which first-order terms exist and
+// what feeds them.  OM_PAIR covers T4 and T4 + identity (they differ only in
+// the epilogue, a run-time switch).
+enum { OM_QUADRA = 0, OM_PAIR = 1, OM_SQUARE = 2, OM_SQIN = 3 };
+__host__ __device__ constexpr int om_of_neuron(int ne) {
+    return ne == NEURON_QUADRA ? OM_QUADRA : (ne <= NEURON_T4I ? OM_PAIR : (ne == NEURON_T3 ? OM_SQUARE : OM_SQIN));
+}
+// first-order terms (weights) of a mode
+__host__ __device__ constexpr int om_terms(int om) { return om == OM_QUADRA ? 3 : (om == OM_PAIR ? 2 : 1); }
+// output-side maps the backward stages: G, T_a, T_b / G, T_a / G
+__host__ __device__ constexpr int om_gmaps(int om) { return om == OM_SQIN ? 1 : (om == OM_SQUARE ? 2 : 3); }
 
 // Forward: ONE implicit GEMM, rows = output channels (three term blocks
 // W_a | W_b | W_c), columns = output pixels, K = (r, q, c).
@@ -17,6 +37,7 @@ struct FwdArgs {
     int N, H, W, C, O, KH, KW, SH, SW, PH, PW, HO, WO;
     int M, K;  // GEMM extents: M = N*HO*WO pixels, K = KH*KW*C
     int row_tiles, col_tiles, splits, stages_per_split, stages_total;
+    int neuron;  // NEURON_*: the epilogue (T4 + identity reads X at the output pixel)
     FastDiv fd_howo, fd_wo, fd_c, fd_kw;
 };
 
@@ -31,6 +52,8 @@ struct BwdDataArgs {
     int N, H, W, C, O, KH, KW, SH, SW, PH, PW, HO, WO;
     int M, K;  // M = N*H*W input pixels, K = KH*KW*O per term
     int row_tiles, col_tiles, splits, stages_per_split, stages_total;
+    int neuron;       // NEURON_*: the epilogue adds G (T4 + identity) or multiplies by 2 X (T2)
+    const void *xin;  // X (N x H x W x C) for T2, else unused
     FastDiv fd_hw, fd_w, fd_o, fd_kw, fd_sh, fd_sw;
 };
 
@@ -51,6 +74,7 @@ struct BwdWeightArgs {
     // linear in m, and a K step advances each lane's (oh, ow) by lin_dq rows
     // (mod HO) and lin_dr columns, with one carry.
     int lin, lin_dq, lin_dr;
+    int neuron;
     FastDiv fd_howo, fd_wo, fd_c, fd_kw;
 };
 

@@ -15,9 +15,10 @@ template <typename T, bool V4>
 __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float *__restrict__ ws, int splits,
                                                                      long long MO, int O, const float *b0,
                                                                      const float *b1, const float *b2, T *y, T *ta,
-                                                                     T *tb) {
+                                                                     T *tb, int neuron, const T *x) {
     constexpr int E = V4 ? 4 : 1;
     const float *bp[3] = {b0, b1, b2};
+    const int nt = neuron == NEURON_QUADRA ? 3 : (neuron <= NEURON_T4I ? 2 : 1);
     const long long n = MO / E;
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x) {
         const long long idx = i * E;
@@ -26,7 +27,8 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float
 #pragma unroll
         for (int t = 0; t < 3; ++t) {
 #pragma unroll
-            for (int e = 0; e < E; ++e) t3[t][e] = bp[t] ? bp[t][o + e] : 0.0f;
+            for (int e = 0; e < E; ++e) t3[t][e] = (t < nt && bp[t]) ? bp[t][o + e] : 0.0f;
+            if (t >= nt) continue;
             for (int sp = 0; sp < splits; ++sp) {
                 const float *src = ws + ((size_t)sp * 3 + t) * MO + idx;
                 if constexpr (V4) {
@@ -38,13 +40,24 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float
                 }
             }
         }
+        // the layer output of the neuron type (the shortcut of T4 + identity: C == O, same pixel)
+        float yv[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const float fa = t3[0][e], fb = t3[1][e];
+            if (neuron == NEURON_QUADRA) yv[e] = fa * fb + t3[2][e];
+            else if (neuron == NEURON_T4) yv[e] = fa * fb;
+            else if (neuron == NEURON_T4I) yv[e] = fa * fb + to_f32<T>(x[idx + e]);
+            else if (neuron == NEURON_T3) yv[e] = fa * fa;
+            else yv[e] = fa;
+        }
+        if (nt < 2) tb = nullptr;
         if constexpr (V4) {
-            if (y) store4<T>(y + idx, t3[0][0] * t3[1][0] + t3[2][0], t3[0][1] * t3[1][1] + t3[2][1],
-                             t3[0][2] * t3[1][2] + t3[2][2], t3[0][3] * t3[1][3] + t3[2][3]);
+            if (y) store4<T>(y + idx, yv[0], yv[1], yv[2], yv[3]);
             if (ta) store4<T>(ta + idx, t3[0][0], t3[0][1], t3[0][2], t3[0][3]);
             if (tb) store4<T>(tb + idx, t3[1][0], t3[1][1], t3[1][2], t3[1][3]);
         } else {
-            if (y) y[idx] = from_f32<T>(t3[0][0] * t3[1][0] + t3[2][0]);
+            if (y) y[idx] = from_f32<T>(yv[0]);
             if (ta) ta[idx] = from_f32<T>(t3[0][0]);
             if (tb) tb[idx] = from_f32<T>(t3[1][0]);
         }
@@ -52,10 +65,12 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float
 }
 
 // Sum of `splits` partial buffers of `total` floats each, in split order; the
-// result is converted to T.
+// result is converted to T.  mode 1 adds src (the shortcut gradient G of
+// T4 + identity), mode 2 multiplies by 2 src (X for T2); src has `total` elements.
 template <typename T, bool V4>
 __global__ __launch_bounds__(kThreads) void qconv_sum_splits_kernel(const float *__restrict__ ws, int splits,
-                                                                    long long total, T *__restrict__ out) {
+                                                                    long long total, T *__restrict__ out, int mode,
+                                                                    const T *__restrict__ src) {
     constexpr int E = V4 ? 4 : 1;
     const long long n = total / E;
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x) {
@@ -64,13 +79,20 @@ __global__ __launch_bounds__(kThreads) void qconv_sum_splits_kernel(const float 
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] = 0.0f;
         for (int sp = 0; sp < splits; ++sp) {
-            const float *src = ws + (size_t)sp * total + idx;
+            const float *p = ws + (size_t)sp * total + idx;
             if constexpr (V4) {
-                const v4f v = *reinterpret_cast<const v4f *>(src);
+                const v4f v = *reinterpret_cast<const v4f *>(p);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) acc[e] += v[e];
             } else {
-                acc[0] += src[0];
+                acc[0] += p[0];
+            }
+        }
+        if (mode != 0) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float v = to_f32<T>(src[idx + e]);
+                acc[e] = mode == 1 ? acc[e] + v : acc[e] * (2.0f * v);
             }
         }
         if constexpr (V4) {
@@ -88,10 +110,10 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce_kernel(const
                                                                            int splits, long long ndw, int O,
                                                                            float *dw0, float *dw1, float *dw2,
                                                                            float *db0, float *db1, float *db2,
-                                                                           int want_db) {
+                                                                           int want_db, int nterms) {
     constexpr int E = V4 ? 4 : 1;
-    const long long nv = 3 * ndw / E;
-    const long long total = nv + (want_db ? 3LL * O : 0LL);
+    const long long nv = nterms * ndw / E;
+    const long long total = nv + (want_db ? (long long)nterms * O : 0LL);
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (long long)gridDim.x * blockDim.x) {
         if (i < nv) {
@@ -136,21 +158,22 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce2d_kernel(con
                                                                              int splits, long long ndw, int O,
                                                                              float *dw0, float *dw1, float *dw2,
                                                                              float *db0, float *db1, float *db2,
-                                                                             int want_db) {
+                                                                             int want_db, int nterms) {
     constexpr int PER = kThreads / SG;
     __shared__ float part[SG][PER];
-    const long long total = 3 * ndw + (want_db ? 3LL * O : 0LL);
+    const long long nw = (long long)nterms * ndw;
+    const long long total = nw + (want_db ? (long long)nterms * O : 0LL);
     const int e = threadIdx.x % PER, sg = threadIdx.x / PER;
     for (long long base = (long long)blockIdx.x * PER; base < total; base += (long long)gridDim.x * PER) {
         const long long i = base + e;
         float s = 0.0f;
         if (i < total) {
-            if (i < 3 * ndw) {
+            if (i < nw) {
                 const int t = (int)(i / ndw);
                 const long long j = i - t * ndw;
                 for (int sp = sg; sp < splits; sp += SG) s += ws_dw[((size_t)sp * 3 + t) * ndw + j];
             } else {
-                const long long jj = i - 3 * ndw;
+                const long long jj = i - nw;
                 const int t = (int)(jj / O), o = (int)(jj % O);
                 for (int sp = sg; sp < splits; sp += SG) s += ws_db[((size_t)sp * 3 + t) * O + o];
             }
@@ -161,12 +184,12 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce2d_kernel(con
             float acc = 0.0f;
 #pragma unroll
             for (int k = 0; k < SG; ++k) acc += part[k][e];
-            if (i < 3 * ndw) {
+            if (i < nw) {
                 const int t = (int)(i / ndw);
                 float *d = t == 0 ? dw0 : (t == 1 ? dw1 : dw2);
                 d[i - t * ndw] = acc;
             } else {
-                const long long jj = i - 3 * ndw;
+                const long long jj = i - nw;
                 const int t = (int)(jj / O), o = (int)(jj % O);
                 float *d = t == 0 ? db0 : (t == 1 ? db1 : db2);
                 d[o] = acc;

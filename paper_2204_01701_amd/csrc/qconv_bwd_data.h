@@ -25,7 +25,13 @@
 
 namespace ql {
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool S1, bool NATW, bool CA>
+//
+// OM (qargs.h) selects the neuron type: only its terms' weight tiles and the
+// output-side maps its operands need (G, T_a, T_b / G, T_a / G) are copied,
+// the operands are formed per type (operands_frag), and the epilogue adds G
+// (T4 + identity) or multiplies by 2 X (T2).  The tile layout keeps room for
+// three terms and three maps.
+template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool S1, bool NATW, bool CA, int OM = OM_QUADRA>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataArgs a) {
     static_assert(!NATW || sizeof(T) == 2, "natural weight tiles need 16-bit elements");
     static_assert(!CA || (S1 && NATW), "channel-aligned steps are implemented for stride 1, natural weight tiles");
@@ -33,9 +39,11 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
     constexpr int KE = 64 / (int)sizeof(T);
     constexpr int ROWS = 3 * BR + 3 * BCOL;
     constexpr int STAGE = ROWS * 64;
-    constexpr int NIW = 3 * BR / 64;  // DMA instructions per thread per K step: weight rows
-    constexpr int NIP = BCOL / 64;    // ... rows of each of G, T_a, T_b
-    constexpr int NI = NIW + 3 * NIP;
+    constexpr int NTM = om_terms(OM), NGM = om_gmaps(OM);
+    constexpr int NIW3 = 3 * BR / 64;   // DMA instructions of the three weight tiles (layout)
+    constexpr int NIW = NTM * BR / 64;  // ... issued per thread per K step: the type's weight rows
+    constexpr int NIP = BCOL / 64;      // ... rows of each of G, T_a, T_b
+    constexpr int NI = NIW + NGM * NIP;
     constexpr int MR = BR / WGR / 32, MC = BCOL / WGC / 32;
     static_assert(WGR * WGC == kThreads / 64, "one wave per wave-tile");
     static_assert(BR % 64 == 0 && BCOL % 64 == 0 && MR >= 1 && MC >= 1, "tile shape");
@@ -145,9 +153,9 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
             for (int j = 0; j < NIP; ++j) {
                 const bool ok = live && ((gmask[j] >> tap) & 1u);
 #pragma unroll
-                for (int u = 0; u < 3; ++u)
+                for (int u = 0; u < NGM; ++u)
                     if (part.take())
-                        dma16(dma_src(ok, gsrc[u] + (go[j] + sg), a.zero), base + (NIW + u * NIP + j) * 4096);
+                        dma16(dma_src(ok, gsrc[u] + (go[j] + sg), a.zero), base + (NIW3 + u * NIP + j) * 4096);
             }
             return;
         }
@@ -192,8 +200,8 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
             }
             ok = ok && kin && goff[j] >= 0;
 #pragma unroll
-            for (int u = 0; u < 3; ++u)
-                if (part.take()) dma16(dma_src(ok, gsrc[u] + p, a.zero), base + (NIW + u * NIP + j) * 4096);
+            for (int u = 0; u < NGM; ++u)
+                if (part.take()) dma16(dma_src(ok, gsrc[u] + p, a.zero), base + (NIW3 + u * NIP + j) * 4096);
         }
     };
 
@@ -208,25 +216,25 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
     const int lrow = lane & 31, lhi = lane >> 5;
     const int swz = (lrow >> 2) & 3;
     const int colx0 = ((0 + lhi) ^ swz) << 4, colx1 = ((2 + lhi) ^ swz) << 4;
-    v4u gr[2][3][MC], af[2][3][MR];  // two register sets: G, T_a, T_b and weight fragments
+    v4u gr[2][3][MC], af[2][NTM][MR];  // two register sets: G, T_a, T_b and weight fragments
     auto read = [&](int slot, int ch, int set) {
         const char *base = smem + slot * STAGE + lrow * 64 + (ch == 0 ? colx0 : colx1);
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
             const int prow = wc * (BCOL / WGC) + mc * 32;
 #pragma unroll
-            for (int u = 0; u < 3; ++u) gr[set][u][mc] = lds_read16(base + (3 * BR + u * BCOL + prow) * 64);
+            for (int u = 0; u < NGM; ++u) gr[set][u][mc] = lds_read16(base + (3 * BR + u * BCOL + prow) * 64);
         }
         if constexpr (NATW) {
             const char *wtile = smem + slot * STAGE;
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int mr = 0; mr < MR; ++mr)
                     af[set][t][mr] = nat_frag_bf16<SW>(wtile + t * WT, 16 * ch, wr * (BR / WGR) + mr * 32, lane);
         } else {
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int mr = 0; mr < MR; ++mr)
                     af[set][t][mr] = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32) * 64);
@@ -238,10 +246,9 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
             v4u bt[3];
-            prologue_frag<T>(gr[set][0][mc], gr[set][1][mc], gr[set][2][mc], bt[0], bt[1]);
-            bt[2] = gr[set][0][mc];
+            operands_frag<T, OM>(gr[set][0][mc], gr[set][NGM >= 2 ? 1 : 0][mc], gr[set][NGM >= 3 ? 2 : 0][mc], bt);
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[set][t][mr], bt[t], acc[mr][mc]);
         }
@@ -251,6 +258,13 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
     // Epilogue: rows are input channels, columns input pixels.
     const int crow0 = rt * BR + wr * (BR / WGR);
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
+    // The neuron type's last step (whole K range only; split partials get it
+    // in the reduction): the shortcut of T4 + identity adds G at the same pixel
+    // and channel (C == O, unchanged map), T2's square contributes 2 X.
+    if constexpr (OM == OM_PAIR || OM == OM_SQIN) {
+        if (a.splits == 1 && (OM == OM_SQIN || a.neuron == NEURON_T4I))
+            neuron_dx_epilogue<T, OM, MR, MC>(acc, OM == OM_SQIN ? a.xin : a.gy, a.M, a.C, pcol0, crow0, lane);
+    }
     const bool vec_out = (a.C & 3) == 0;
     T *__restrict__ dx = static_cast<T *>(a.dx);
 

@@ -31,9 +31,14 @@ namespace ql {
 // the (oh, ow) of its pixel, advanced by one K step (KE pixels) per issue
 // with a carry, instead of splitting the pixel index into (n, oh, ow) by
 // division at every step.
-template <int BKP, int BO, int WGR, int WGC, int NS, int NT, bool SUM, bool LIN>
+//
+// OM (qargs.h) selects the neuron type: the output-side maps its operands
+// need, the operands themselves (operands_frag), its terms' accumulators,
+// and for T2 the X operand squared on its way to the MFMAs.
+template <int BKP, int BO, int WGR, int WGC, int NS, int NT, bool SUM, bool LIN, int OM>
 __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *smem) {
     using T = uint16_t;                 // bf16 only: the transposed LDS read is 16-bit
+    constexpr int NTM = om_terms(OM), NGM = om_gmaps(OM);
     constexpr int KE = 32;              // output pixels per K step (two MFMA k-chunks)
     constexpr int SX = BKP / 8;         // 16-byte slots per X row
     constexpr int SG = BO / 8;          // 16-byte slots per G / T_a / T_b row
@@ -43,7 +48,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
     constexpr int NW = NT / 64;         // waves
     constexpr int NIX = XB / (NT * 16); // DMA instructions per thread per K step
     constexpr int NIG = GB / (NT * 16);
-    constexpr int NI = NIX + 3 * NIG;
+    constexpr int NI = NIX + NGM * NIG;
     constexpr int RX = 64 / SX;         // rows one wave-instruction fills
     constexpr int RG = 64 / SG;
     constexpr int MR = BKP / WGR / 32, MC = BO / WGC / 32;
@@ -133,7 +138,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
                 const int p = RG * (NW * i + wave) + lane / SG;
                 const bool ok = live && og_ok && p < mleft;
 #pragma unroll
-                for (int u = 0; u < 3; ++u)
+                for (int u = 0; u < NGM; ++u)
                     if (part.take())
                         dma16(dma_src(ok, gsrc[u] + (glin[i] + gs), a.zero), base + XB + u * GB + i * (NT * 16));
             }
@@ -157,23 +162,23 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
             const bool ok = live && og_ok && m < a.M;
             const size_t off = (size_t)m * a.O + og;
 #pragma unroll
-            for (int u = 0; u < 3; ++u)
+            for (int u = 0; u < NGM; ++u)
                 if (part.take()) dma16(dma_src(ok, gsrc[u] + off, a.zero), base + XB + u * GB + i * (NT * 16));
         }
     };
 
-    f32x16_t acc[3][MR][MC];
+    f32x16_t acc[NTM][MR][MC];
 #pragma unroll
-    for (int t = 0; t < 3; ++t)
+    for (int t = 0; t < NTM; ++t)
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
             for (int mc = 0; mc < MC; ++mc)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[t][mr][mc][v] = 0.0f;
-    float dsum[3][MC];
+    float dsum[NTM][MC];
 #pragma unroll
-    for (int t = 0; t < 3; ++t)
+    for (int t = 0; t < NTM; ++t)
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) dsum[t][mc] = 0.0f;
     const bool sum_db = SUM && wr == 0;
@@ -188,38 +193,49 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc)
 #pragma unroll
-            for (int u = 0; u < 3; ++u)
+            for (int u = 0; u < NGM; ++u)
                 gr[set][u][mc] = nat_frag_bf16<SG>(gt + u * GB, 16 * ch, wc * (BO / WGC) + mc * 32, lane);
     };
     // Prologue products and bias sums in fp32, then the MFMAs.
     auto mma = [&](int set) {
+        if constexpr (OM == OM_SQIN) {
+#pragma unroll
+            for (int mr = 0; mr < MR; ++mr) af[set][mr] = square_frag<T>(af[set][mr]);
+        }
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
-            const v4u &g = gr[set][0][mc], &ta = gr[set][1][mc], &tb = gr[set][2][mc];
-            float fa[8], fb[8];
+            const v4u &g = gr[set][0][mc];
+            // the operands in fp32 (the bias sums use them before rounding)
+            float op[3][8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float gv = vget<T>(g, e);
-                fa[e] = gv * vget<T>(tb, e);
-                fb[e] = gv * vget<T>(ta, e);
+                if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+                    op[0][e] = gv * vget<T>(gr[set][NGM >= 3 ? 2 : 0][mc], e);
+                    op[1][e] = gv * vget<T>(gr[set][NGM >= 2 ? 1 : 0][mc], e);
+                    op[2][e] = gv;
+                } else if constexpr (OM == OM_SQUARE) {
+                    op[0][e] = 2.0f * gv * vget<T>(gr[set][NGM >= 2 ? 1 : 0][mc], e);
+                } else {
+                    op[0][e] = gv;
+                }
             }
             if constexpr (SUM) {
                 if (sum_db) {  // wave-uniform: only the waves that own the bias sums add them up
-                    float sa = 0.0f, sb = 0.0f, sc = 0.0f;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        sa += fa[e];
-                        sb += fb[e];
-                        sc += vget<T>(g, e);
+                    for (int t = 0; t < NTM; ++t) {
+                        float sacc = 0.0f;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) sacc += op[t][e];
+                        dsum[t][mc] += sacc;
                     }
-                    dsum[0][mc] += sa;
-                    dsum[1][mc] += sb;
-                    dsum[2][mc] += sc;
                 }
             }
-            const v4u bt[3] = {vpack<T>(fa), vpack<T>(fb), g};
+            v4u bt[NTM];
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t) bt[t] = (OM == OM_QUADRA && t == 2) || OM == OM_SQIN ? g : vpack<T>(op[t]);
+#pragma unroll
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[set][mr], bt[t], acc[t][mr][mc]);
         }
@@ -247,10 +263,10 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
     if constexpr (MAPB <= RING) {
         if (vec_out) {
 #pragma unroll
-            for (int t0 = 0; t0 < 3; t0 += PER) {
+            for (int t0 = 0; t0 < NTM; t0 += PER) {
                 lds_barrier();  // the ring (or the previous round's tiles) is no longer read
 #pragma unroll
-                for (int t = t0; t < t0 + PER && t < 3; ++t) {
+                for (int t = t0; t < t0 + PER && t < NTM; ++t) {
                     char *tile = smem + (t - t0) * MAPB;
 #pragma unroll
                     for (int mr = 0; mr < MR; ++mr)
@@ -268,7 +284,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
                 }
                 lds_barrier();
 #pragma unroll
-                for (int t = t0; t < t0 + PER && t < 3; ++t) {
+                for (int t = t0; t < t0 + PER && t < NTM; ++t) {
                     const char *tile = smem + (t - t0) * MAPB;
                     float *__restrict__ dst =
                         a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * KPO;
@@ -284,7 +300,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
         }
     }
 #pragma unroll
-    for (int t = 0; t < 3; ++t) {
+    for (int t = 0; t < NTM; ++t) {
         if (MAPB <= RING && vec_out) break;  // stored above
         float *__restrict__ dst = a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * KPO;
 #pragma unroll
@@ -322,7 +338,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
     // Bias gradients: lanes l and l + 32 hold the two pixel halves of channel l % 32.
     if (SUM && sum_db) {
 #pragma unroll
-        for (int t = 0; t < 3; ++t)
+        for (int t = 0; t < NTM; ++t)
 #pragma unroll
             for (int mc = 0; mc < MC; ++mc) {
                 const float tot = dsum[t][mc] + __shfl_xor(dsum[t][mc], 32);
@@ -337,7 +353,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
     }
 }
 
-template <int BKP, int BO, int WGR, int WGC, int NS, int NT = kThreads>
+template <int BKP, int BO, int WGR, int WGC, int NS, int NT = kThreads, int OM = OM_QUADRA>
 __global__ __launch_bounds__(NT) void qconv_bwd_weight_kernel(const BwdWeightArgs a) {
     constexpr int STAGE = 32 * BKP * 2 + 3 * 32 * BO * 2;
     __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
@@ -348,14 +364,14 @@ __global__ __launch_bounds__(NT) void qconv_bwd_weight_kernel(const BwdWeightArg
     const bool sum = a.want_db && bid % a.row_tiles == 0;
     if (a.lin) {
         if (sum)
-            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true, true>(a, smem);
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true, true, OM>(a, smem);
         else
-            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false, true>(a, smem);
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false, true, OM>(a, smem);
     } else {
         if (sum)
-            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true, false>(a, smem);
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, true, false, OM>(a, smem);
         else
-            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false, false>(a, smem);
+            bwd_weight_body<BKP, BO, WGR, WGC, NS, NT, false, false, OM>(a, smem);
     }
 }
 

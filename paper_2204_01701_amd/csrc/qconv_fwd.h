@@ -20,19 +20,27 @@
 
 namespace ql {
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool CA, int NT = kThreads>
+//
+// OM (qargs.h) selects the neuron type: the weight rows and MFMAs of the
+// terms it lacks are skipped (the tile layout keeps three term blocks), the
+// pixel operand is squared on its way to the MFMAs for T2, and the epilogue
+// forms the type's Y.
+template <typename T, int BR, int BCOL, int WGR, int WGC, int NS, bool CA, int NT = kThreads, int OM = OM_QUADRA>
 __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     constexpr int VEC = Elem<T>::VEC;
     constexpr int KE = 64 / (int)sizeof(T);  // reduction elements per K step
     constexpr int ROWS = 3 * BR + BCOL;
     constexpr int STAGE = ROWS * 64;
     constexpr int RPI = NT / 4;         // 64-byte tile rows one DMA instruction of the workgroup fills
-    constexpr int NIW = 3 * BR / RPI;   // DMA instructions per thread per K step: weight rows
+    constexpr int NTM = om_terms(OM);   // first-order terms
+    constexpr int NIW3 = 3 * BR / RPI;  // DMA instructions of the three weight blocks (tile layout)
+    constexpr int NIW = NTM * BR / RPI; // ... of the blocks this type has (issued per thread per K step)
     constexpr int NIX = BCOL / RPI;     // ... pixel rows
     constexpr int NI = NIW + NIX;
     constexpr int MR = BR / WGR / 32, MC = BCOL / WGC / 32;
     static_assert(WGR * WGC == NT / 64, "one wave per wave-tile");
     static_assert((3 * BR) % RPI == 0 && BCOL % RPI == 0 && MR >= 1 && MC >= 1, "tile shape");
+    static_assert(OM == OM_QUADRA || BR % RPI == 0, "each weight DMA instruction within one term block");
 
     __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
@@ -67,7 +75,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     int xoff[NIX], ih0[NIX], iw0[NIX];
 #pragma unroll
     for (int j = 0; j < NIX; ++j) {
-        const int p = RPI * (NIW + j) + 16 * wave + (lane >> 2) - 3 * BR;
+        const int p = RPI * (NIW3 + j) + 16 * wave + (lane >> 2) - 3 * BR;
         const int m = ct * BCOL + p;
         if (m < a.M) {
             const int n = (int)fdiv((uint32_t)m, a.fd_howo);
@@ -102,7 +110,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         }
 #pragma unroll
         for (int j = 0; j < NIX; ++j) {
-            const int p = RPI * (NIW + j) + 16 * wave + (lane >> 2) - 3 * BR;
+            const int p = RPI * (NIW3 + j) + 16 * wave + (lane >> 2) - 3 * BR;
             const int m = min(ct * BCOL + p, a.M - 1);
             const int n = (int)fdiv((uint32_t)m, a.fd_howo);
             const int rem = m - n * a.HO * a.WO;
@@ -135,7 +143,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
 #pragma unroll
             for (int j = 0; j < NIX; ++j) {
                 const bool ok = live && ((xmask[j] >> tap) & 1u);
-                if (part.take()) dma16(dma_src(ok, x + (xo[j] + soff), a.zero), base + (NIW + j) * (NT * 16));
+                if (part.take()) dma16(dma_src(ok, x + (xo[j] + soff), a.zero), base + (NIW3 + j) * (NT * 16));
             }
             return;
         }
@@ -155,16 +163,16 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
             const int ih = ih0[j] + r, iw = iw0[j] + q;
             const bool ok = kin && xoff[j] >= 0 && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
             if (part.take())
-                dma16(dma_src(ok, x + xoff[j] + (ih * a.W + iw) * a.C + c, a.zero), base + (NIW + j) * (NT * 16));
+                dma16(dma_src(ok, x + xoff[j] + (ih * a.W + iw) * a.C + c, a.zero), base + (NIW3 + j) * (NT * 16));
         }
     };
 
     // Accumulators, biases preloaded when this workgroup owns the whole K range.
-    f32x16_t acc[3][MR][MC];
+    f32x16_t acc[NTM][MR][MC];
     const int lrow = lane & 31, lhi = lane >> 5;
     const int orow0 = rt * BR + wr * (BR / WGR);
 #pragma unroll
-    for (int t = 0; t < 3; ++t) {
+    for (int t = 0; t < NTM; ++t) {
         const float *bp = a.bias[t];
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr) {
@@ -183,21 +191,25 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     const int swz = (lrow >> 2) & 3;
     const int colx0 = ((0 + lhi) ^ swz) << 4, colx1 = ((2 + lhi) ^ swz) << 4;
     constexpr int SETS = NT > 256 ? 1 : 2;  // fragment register sets (one when two waves share a SIMD)
-    v4u bf[SETS][MC], af[SETS][3][MR];
+    v4u bf[SETS][MC], af[SETS][NTM][MR];
     auto read = [&](int slot, int ch, int set) {
         const char *base = smem + slot * STAGE + lrow * 64 + (ch == 0 ? colx0 : colx1);
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc)
             bf[set][mc] = lds_read16(base + (3 * BR + wc * (BCOL / WGC) + mc * 32) * 64);
 #pragma unroll
-        for (int t = 0; t < 3; ++t)
+        for (int t = 0; t < NTM; ++t)
 #pragma unroll
             for (int mr = 0; mr < MR; ++mr)
                 af[set][t][mr] = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32) * 64);
     };
     auto mma = [&](int set) {
+        if constexpr (OM == OM_SQIN) {
 #pragma unroll
-        for (int t = 0; t < 3; ++t)
+            for (int mc = 0; mc < MC; ++mc) bf[set][mc] = square_frag<T>(bf[set][mc]);
+        }
+#pragma unroll
+        for (int t = 0; t < NTM; ++t)
 #pragma unroll
             for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
@@ -208,7 +220,29 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     else  // 8 waves leave each barrier together: half the copies go out one chunk later (measured faster)
         run_ring_single<NS, NI, 2, (NI + 1) / 2>(nst, s_begin, issue, read, mma);
 
-    // Epilogue.
+    // Epilogue.  Output j of a tile element: 0 the layer output Y of the
+    // neuron type, 1 and 2 the saved term maps T_a and T_b.  xs: the element
+    // of X the shortcut adds (T4 + identity, C == O, same pixel).
+    auto outv = [&](int j, int mr, int mc, int v, float xs) -> float {
+        const float fa = acc[0][mr][mc][v];
+        if (j == 1) return fa;
+        if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+            const float fb = acc[1][mr][mc][v];
+            if (j == 2) return fb;
+            if constexpr (OM == OM_QUADRA) return fa * fb + acc[2][mr][mc][v];
+            else return fa * fb + xs;
+        } else if constexpr (OM == OM_SQUARE) {
+            return fa * fa;
+        } else {
+            return fa;
+        }
+    };
+    const bool shortcut = OM == OM_PAIR && a.neuron == NEURON_T4I;
+    // the four shortcut values of a lane's group (channels o .. o + 3 of pixel m), or zeros
+    auto xs4 = [&](int m, int o, float *xv) {
+        xv[0] = xv[1] = xv[2] = xv[3] = 0.0f;
+        if (shortcut && m < a.M && o < a.O) load4<T>(x + (size_t)m * a.C + o, xv);
+    };
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
     const bool vec_out = (a.O & 3) == 0;
     if (a.splits == 1) {
@@ -228,7 +262,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         static_assert((CPR & (CPR - 1)) == 0, "staged epilogue tile");
         if constexpr (MAPB <= NS * STAGE) {  // (otherwise, and for O not a multiple of 16 / E: direct stores)
             if (a.O % (16 / E) == 0) {
-                T *outs[3] = {y, ta, tb};
+                T *outs[3] = {y, ta, NTM >= 2 ? tb : nullptr};
 #pragma unroll
                 for (int r0 = 0; r0 < 3; r0 += PER) {
                     lds_barrier();  // every wave is done with the ring (or the previous round's copy)
@@ -244,12 +278,10 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
 #pragma unroll
                                 for (int g = 0; g < 4; ++g) {
                                     const int ol = wr * (BR / WGR) + mr * 32 + 8 * g + 4 * lhi;
-                                    float v[4];
+                                    float v[4], xv[4];
+                                    if (j == 0) xs4(ct * BCOL + p, rt * BR + ol, xv);
 #pragma unroll
-                                    for (int i = 0; i < 4; ++i) {
-                                        const float fa = acc[0][mr][mc][4 * g + i], fb = acc[1][mr][mc][4 * g + i];
-                                        v[i] = j == 0 ? fa * fb + acc[2][mr][mc][4 * g + i] : (j == 1 ? fa : fb);
-                                    }
+                                    for (int i = 0; i < 4; ++i) v[i] = outv(j, mr, mc, 4 * g + i, j == 0 ? xv[i] : 0.0f);
                                     store4<T>(reinterpret_cast<T *>(tile + p * PITCH + ol * E), v[0], v[1], v[2], v[3]);
                                 }
                             }
@@ -281,13 +313,15 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                 for (int g = 0; g < 4; ++g) {
                     const int o = orow0 + mr * 32 + 8 * g + 4 * lhi;
                     if (o >= a.O) continue;
-                    float va[4], vb[4], vy[4];
+                    float va[4], vb[4], vy[4], xv[4];
+                    xs4(m, o, xv);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        va[i] = acc[0][mr][mc][4 * g + i];
-                        vb[i] = acc[1][mr][mc][4 * g + i];
-                        vy[i] = va[i] * vb[i] + acc[2][mr][mc][4 * g + i];
+                        va[i] = outv(1, mr, mc, 4 * g + i, 0.0f);
+                        vb[i] = NTM >= 2 ? outv(2, mr, mc, 4 * g + i, 0.0f) : 0.0f;
+                        vy[i] = outv(0, mr, mc, 4 * g + i, xv[i]);
                     }
+                    if (NTM < 2) tb = nullptr;
                     const size_t off = (size_t)m * a.O + o;
                     if (vec_out) {
                         if (y) store4<T>(y + off, vy[0], vy[1], vy[2], vy[3]);
@@ -306,7 +340,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
             }
     } else {
 #pragma unroll
-        for (int t = 0; t < 3; ++t) {
+        for (int t = 0; t < NTM; ++t) {
             float *__restrict__ ws = a.ws + ((size_t)split * 3 + t) * (size_t)a.M * a.O;
 #pragma unroll
             for (int mr = 0; mr < MR; ++mr)

@@ -18,9 +18,11 @@
 
 namespace ql {
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int BKB, bool VECK>
+// OM (qargs.h): the neuron type's terms; T2 squares the pixel operand while staging.
+template <typename T, int BR, int BCOL, int WGR, int WGC, int BKB, bool VECK, int OM = OM_QUADRA>
 __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdArgs a) {
     constexpr int VEC = Elem<T>::VEC;
+    constexpr int NTM = om_terms(OM);
     constexpr int NB = BKB / 16;  // 16-byte vectors per row per K step
     constexpr int KE = NB * VEC;  // reduction elements per K step
     constexpr int PITCH = BKB + 16;
@@ -79,7 +81,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
         }
     }
 
-    v4u rw[3][NVT], rx[NVP];
+    v4u rw[NTM][NVT], rx[NVP];
 
     auto load_stage = [&](int s) {
         const int k = s * KE + c16 * VEC;
@@ -94,8 +96,8 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
             for (int j = 0; j < NVT; ++j) {
                 const bool ok = kin && woff[j] >= 0;
                 rw[0][j] = ld16(w0 + woff[j] + k, ok);
-                rw[1][j] = ld16(w1 + woff[j] + k, ok);
-                rw[2][j] = ld16(w2 + woff[j] + k, ok);
+                if constexpr (NTM >= 2) rw[1][j] = ld16(w1 + woff[j] + k, ok);
+                if constexpr (NTM >= 3) rw[2][j] = ld16(w2 + woff[j] + k, ok);
             }
 #pragma unroll
             for (int j = 0; j < NVP; ++j) {
@@ -106,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
         } else {
             // General C: every element decodes its own (r, q, c).
             struct alignas(16) V { T e[VEC]; };
-            V vw[3][NVT], vx[NVP];
+            V vw[NTM][NVT], vx[NVP];
 #pragma unroll
             for (int e = 0; e < VEC; ++e) {
                 const int ke = k + e;
@@ -119,8 +121,8 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
                 for (int j = 0; j < NVT; ++j) {
                     const bool ok = kin && woff[j] >= 0;
                     vw[0][j].e[e] = ok ? w0[woff[j] + ke] : T(0);
-                    vw[1][j].e[e] = ok ? w1[woff[j] + ke] : T(0);
-                    vw[2][j].e[e] = ok ? w2[woff[j] + ke] : T(0);
+                    if constexpr (NTM >= 2) vw[1][j].e[e] = ok ? w1[woff[j] + ke] : T(0);
+                    if constexpr (NTM >= 3) vw[2][j].e[e] = ok ? w2[woff[j] + ke] : T(0);
                 }
 #pragma unroll
                 for (int j = 0; j < NVP; ++j) {
@@ -133,16 +135,20 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
 #pragma unroll
             for (int j = 0; j < NVT; ++j)
 #pragma unroll
-                for (int t = 0; t < 3; ++t) rw[t][j] = __builtin_bit_cast(v4u, vw[t][j]);
+                for (int t = 0; t < NTM; ++t) rw[t][j] = __builtin_bit_cast(v4u, vw[t][j]);
 #pragma unroll
             for (int j = 0; j < NVP; ++j) rx[j] = __builtin_bit_cast(v4u, vx[j]);
+        }
+        if constexpr (OM == OM_SQIN) {
+#pragma unroll
+            for (int j = 0; j < NVP; ++j) rx[j] = square_frag<T>(rx[j]);
         }
     };
 
     auto store_stage = [&](int b) {
         char *base = smem + b * ROWS * PITCH;
 #pragma unroll
-        for (int t = 0; t < 3; ++t)
+        for (int t = 0; t < NTM; ++t)
 #pragma unroll
             for (int j = 0; j < NVT; ++j)
                 lds_write16(base + (t * BR + rsub + j * RSTEP) * PITCH + c16 * 16, rw[t][j]);
@@ -152,11 +158,11 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
     };
 
     // Accumulators; the biases are preloaded when the whole K range is ours.
-    f32x16_t acc[3][MR][MC];
+    f32x16_t acc[NTM][MR][MC];
     const int lrow = lane & 31, lhi = lane >> 5;
     const int orow0 = rt * BR + wr * (BR / WGR);
 #pragma unroll
-    for (int t = 0; t < 3; ++t) {
+    for (int t = 0; t < NTM; ++t) {
         const float *bp = a.bias[t];
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr) {
@@ -181,7 +187,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
             for (int mc = 0; mc < MC; ++mc)
                 bf[mc] = lds_read16(base + (3 * BR + wc * (BCOL / WGC) + mc * 32 + lrow) * PITCH + coff);
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int mr = 0; mr < MR; ++mr) {
                     const v4u af = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32 + lrow) * PITCH + coff);
@@ -205,13 +211,28 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
         }
     }
 
-    // Epilogue.
+    // Epilogue: the neuron type's Y (j = 0) and the saved maps T_a, T_b (j = 1, 2).
+    auto outv = [&](int j, int mr, int mc, int v, float xs) -> float {
+        const float fa = acc[0][mr][mc][v];
+        if (j == 1) return fa;
+        if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+            const float fb = acc[1][mr][mc][v];
+            if (j == 2) return fb;
+            if constexpr (OM == OM_QUADRA) return fa * fb + acc[2][mr][mc][v];
+            else return fa * fb + xs;
+        } else if constexpr (OM == OM_SQUARE) {
+            return fa * fa;
+        } else {
+            return fa;
+        }
+    };
+    const bool shortcut = OM == OM_PAIR && a.neuron == NEURON_T4I;  // C == O: X at the output pixel
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
     const bool vec_out = (a.O & 3) == 0;
     if (a.splits == 1) {
         T *__restrict__ y = static_cast<T *>(a.y);
         T *__restrict__ ta = static_cast<T *>(a.ta);
-        T *__restrict__ tb = static_cast<T *>(a.tb);
+        T *__restrict__ tb = NTM >= 2 ? static_cast<T *>(a.tb) : nullptr;
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
@@ -225,9 +246,10 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
                     float va[4], vb[4], vy[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        va[i] = acc[0][mr][mc][4 * g + i];
-                        vb[i] = acc[1][mr][mc][4 * g + i];
-                        vy[i] = va[i] * vb[i] + acc[2][mr][mc][4 * g + i];
+                        const float xs = shortcut && o + i < a.O ? to_f32<T>(x[(size_t)m * a.C + o + i]) : 0.0f;
+                        va[i] = outv(1, mr, mc, 4 * g + i, 0.0f);
+                        vb[i] = NTM >= 2 ? outv(2, mr, mc, 4 * g + i, 0.0f) : 0.0f;
+                        vy[i] = outv(0, mr, mc, 4 * g + i, xs);
                     }
                     const size_t off = (size_t)m * a.O + o;
                     if (vec_out) {
@@ -247,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
             }
     } else {
 #pragma unroll
-        for (int t = 0; t < 3; ++t) {
+        for (int t = 0; t < NTM; ++t) {
             float *__restrict__ ws = a.ws + ((size_t)split * 3 + t) * (size_t)a.M * a.O;
 #pragma unroll
             for (int mr = 0; mr < MR; ++mr)
@@ -274,9 +296,11 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
     }
 }
 
-template <typename T, int BR, int BCOL, int WGR, int WGC, int BKB, bool VECK, bool S1>
+// OM (qargs.h): the neuron type's terms, output-side maps and operands.
+template <typename T, int BR, int BCOL, int WGR, int WGC, int BKB, bool VECK, bool S1, int OM = OM_QUADRA>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const BwdDataArgs a) {
     constexpr int VEC = Elem<T>::VEC;
+    constexpr int NTM = om_terms(OM), NGM = om_gmaps(OM);
     constexpr int NB = BKB / 16;
     constexpr int KE = NB * VEC;
     constexpr int PITCH = BKB + 16;
@@ -370,20 +394,17 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
             for (int j = 0; j < NVT; ++j) {
                 const bool ok = kin && woff[j] >= 0;
                 rw[0][j] = ld16(w0 + woff[j] + k, ok);
-                rw[1][j] = ld16(w1 + woff[j] + k, ok);
-                rw[2][j] = ld16(w2 + woff[j] + k, ok);
+                if constexpr (NTM >= 2) rw[1][j] = ld16(w1 + woff[j] + k, ok);
+                if constexpr (NTM >= 3) rw[2][j] = ld16(w2 + woff[j] + k, ok);
             }
 #pragma unroll
             for (int j = 0; j < NVP; ++j) {
                 const int p = kin ? out_pixel(j, r, q) : -1;
+                rg[0][j] = rg[1][j] = rg[2][j] = zero;
                 if (p >= 0) {
                     rg[0][j] = *reinterpret_cast<const v4u *>(gy + p + o);
-                    rg[1][j] = *reinterpret_cast<const v4u *>(gta + p + o);
-                    rg[2][j] = *reinterpret_cast<const v4u *>(gtb + p + o);
-                } else {
-                    rg[0][j] = zero;
-                    rg[1][j] = zero;
-                    rg[2][j] = zero;
+                    if constexpr (NGM >= 2) rg[1][j] = *reinterpret_cast<const v4u *>(gta + p + o);
+                    if constexpr (NGM >= 3) rg[2][j] = *reinterpret_cast<const v4u *>(gtb + p + o);
                 }
             }
         } else {
@@ -401,15 +422,15 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
                 for (int j = 0; j < NVT; ++j) {
                     const bool ok = kin && woff[j] >= 0;
                     vw[0][j].e[e] = ok ? w0[woff[j] + ke] : T(0);
-                    vw[1][j].e[e] = ok ? w1[woff[j] + ke] : T(0);
-                    vw[2][j].e[e] = ok ? w2[woff[j] + ke] : T(0);
+                    vw[1][j].e[e] = NTM >= 2 && ok ? w1[woff[j] + ke] : T(0);
+                    vw[2][j].e[e] = NTM >= 3 && ok ? w2[woff[j] + ke] : T(0);
                 }
 #pragma unroll
                 for (int j = 0; j < NVP; ++j) {
                     const int p = kin ? out_pixel(j, r, q) : -1;
                     vg[0][j].e[e] = p >= 0 ? gy[p + o] : T(0);
-                    vg[1][j].e[e] = p >= 0 ? gta[p + o] : T(0);
-                    vg[2][j].e[e] = p >= 0 ? gtb[p + o] : T(0);
+                    vg[1][j].e[e] = NGM >= 2 && p >= 0 ? gta[p + o] : T(0);
+                    vg[2][j].e[e] = NGM >= 3 && p >= 0 ? gtb[p + o] : T(0);
                 }
             }
 #pragma unroll
@@ -425,24 +446,18 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
     auto store_stage = [&](int b) {
         char *base = smem + b * ROWS * PITCH;
 #pragma unroll
-        for (int t = 0; t < 3; ++t)
+        for (int t = 0; t < NTM; ++t)
 #pragma unroll
             for (int j = 0; j < NVT; ++j)
                 lds_write16(base + (t * BR + rsub + j * RSTEP) * PITCH + c16 * 16, rw[t][j]);
-        // Prologue of eq:SD: G_a = G o T_b, G_b = G o T_a, G_c = G.
+        // Prologue of eq:SD (G_a = G o T_b, G_b = G o T_a, G_c = G) or the neuron type's operands.
 #pragma unroll
         for (int j = 0; j < NVP; ++j) {
-            float ga[VEC], gb[VEC];
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                const float g = vget<T>(rg[0][j], e);
-                ga[e] = g * vget<T>(rg[2][j], e);
-                gb[e] = g * vget<T>(rg[1][j], e);
-            }
+            v4u bt[3];
+            operands_frag<T, OM>(rg[0][j], rg[1][j], rg[2][j], bt);
             const int row = 3 * BR + rsub + j * RSTEP;
-            lds_write16(base + row * PITCH + c16 * 16, vpack<T>(ga));
-            lds_write16(base + (row + BCOL) * PITCH + c16 * 16, vpack<T>(gb));
-            lds_write16(base + (row + 2 * BCOL) * PITCH + c16 * 16, rg[0][j]);
+#pragma unroll
+            for (int t = 0; t < NTM; ++t) lds_write16(base + (row + t * BCOL) * PITCH + c16 * 16, bt[t]);
         }
     };
 
@@ -461,7 +476,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
         for (int ch = 0; ch < BKB / 32; ++ch) {
             const int coff = ch * 32 + lhi * 16;
 #pragma unroll
-            for (int t = 0; t < 3; ++t) {
+            for (int t = 0; t < NTM; ++t) {
                 v4u bf[MC];
 #pragma unroll
                 for (int mc = 0; mc < MC; ++mc)
@@ -495,6 +510,10 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
     // Epilogue: rows are input channels, columns input pixels.
     const int crow0 = rt * BR + wr * (BR / WGR);
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
+    if constexpr (OM == OM_PAIR || OM == OM_SQIN) {
+        if (a.splits == 1 && (OM == OM_SQIN || a.neuron == NEURON_T4I))
+            neuron_dx_epilogue<T, OM, MR, MC>(acc, OM == OM_SQIN ? a.xin : a.gy, a.M, a.C, pcol0, crow0, lane);
+    }
     const bool vec_out = (a.C & 3) == 0;
     T *__restrict__ dx = static_cast<T *>(a.dx);
     float *__restrict__ ws = a.ws + (size_t)split * a.M * a.C;
@@ -534,9 +553,11 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
         }
 }
 
-template <typename T, int BKP, int BO, int WGR, int WGC, int BKB, int PXG, bool VECK>
+// OM (qargs.h): the neuron type's maps, operands and terms; T2 stages X o X.
+template <typename T, int BKP, int BO, int WGR, int WGC, int BKB, int PXG, bool VECK, int OM = OM_QUADRA>
 __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(const BwdWeightArgs a) {
     constexpr int VEC = Elem<T>::VEC;
+    constexpr int NTM = om_terms(OM), NGM = om_gmaps(OM);
     constexpr int ES = (int)sizeof(T);
     constexpr int KE = BKB / ES;    // output pixels per K step
     constexpr int PXX = 16 / ES;    // pixels per X staging job (one 16-byte LDS write per channel)
@@ -626,6 +647,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
                     }
                     rx[p] = __builtin_bit_cast(v4u, v);
                 }
+                if constexpr (OM == OM_SQIN) rx[p] = square_frag<T>(rx[p]);
                 if (++ow == a.WO) {
                     ow = 0;
                     if (++oh == a.HO) {
@@ -643,16 +665,16 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
                 if constexpr (VECK) {
                     const bool ok = m < a.M && obase < a.O;
                     rg[0][p] = ld16(gy + off, ok);
-                    rg[1][p] = ld16(gta + off, ok);
-                    rg[2][p] = ld16(gtb + off, ok);
+                    rg[1][p] = ld16(gta + off, NGM >= 2 && ok);
+                    rg[2][p] = ld16(gtb + off, NGM >= 3 && ok);
                 } else {
                     struct alignas(16) V { T e[VEC]; } v0, v1, v2;
 #pragma unroll
                     for (int e = 0; e < VEC; ++e) {
                         const bool ok = m < a.M && obase + e < a.O;
                         v0.e[e] = ok ? gy[off + e] : T(0);
-                        v1.e[e] = ok ? gta[off + e] : T(0);
-                        v2.e[e] = ok ? gtb[off + e] : T(0);
+                        v1.e[e] = NGM >= 2 && ok ? gta[off + e] : T(0);
+                        v2.e[e] = NGM >= 3 && ok ? gtb[off + e] : T(0);
                     }
                     rg[0][p] = __builtin_bit_cast(v4u, v0);
                     rg[1][p] = __builtin_bit_cast(v4u, v1);
@@ -686,12 +708,18 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) {
                     const float g = vget<T>(rg[0][p], e);
-                    gv[0][p][e] = g * vget<T>(rg[2][p], e);
-                    gv[1][p][e] = g * vget<T>(rg[1][p], e);
-                    gv[2][p][e] = g;
+                    if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+                        gv[0][p][e] = g * vget<T>(rg[2][p], e);
+                        gv[1][p][e] = g * vget<T>(rg[1][p], e);
+                        gv[2][p][e] = g;
+                    } else if constexpr (OM == OM_SQUARE) {
+                        gv[0][p][e] = 2.0f * g * vget<T>(rg[1][p], e);
+                    } else {
+                        gv[0][p][e] = g;
+                    }
                 }
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) {
                     float sacc = 0.0f;
@@ -703,8 +731,9 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
                         uint32_t d[PXG / 2];
 #pragma unroll
                         for (int i = 0; i < PXG / 2; ++i)
-                            d[i] = (t == 2) ? (vraw<T>(rg[0][2 * i], e) | (vraw<T>(rg[0][2 * i + 1], e) << 16))
-                                            : pack_bf16x2(gv[t][2 * i][e], gv[t][2 * i + 1][e]);
+                            d[i] = ((OM == OM_QUADRA && t == 2) || OM == OM_SQIN)  // the operand is G itself
+                                       ? (vraw<T>(rg[0][2 * i], e) | (vraw<T>(rg[0][2 * i + 1], e) << 16))
+                                       : pack_bf16x2(gv[t][2 * i][e], gv[t][2 * i + 1][e]);
                         if constexpr (PXG == 4)
                             *reinterpret_cast<v2u *>(dst) = v2u{d[0], d[1]};
                         else
@@ -722,9 +751,9 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
         }
     };
 
-    f32x16_t acc[3][MR][MC];
+    f32x16_t acc[NTM][MR][MC];
 #pragma unroll
-    for (int t = 0; t < 3; ++t)
+    for (int t = 0; t < NTM; ++t)
 #pragma unroll
         for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
@@ -743,7 +772,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
             for (int mr = 0; mr < MR; ++mr)
                 af[mr] = lds_read16(base + (wr * (BKP / WGR) + mr * 32 + lrow) * PITCH + coff);
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int mc = 0; mc < MC; ++mc) {
                     const v4u bf =
@@ -773,7 +802,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
     const int ocol0 = ct * BO + wc * (BO / WGC);
     const bool vec_out = (a.KP & 3) == 0;
 #pragma unroll
-    for (int t = 0; t < 3; ++t) {
+    for (int t = 0; t < NTM; ++t) {
         float *__restrict__ dst =
             a.splits == 1 ? a.dw[t] : a.ws_dw + ((size_t)split * 3 + t) * (size_t)a.O * a.KP;
 #pragma unroll
@@ -807,12 +836,12 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
         static_assert(NPG * 3 * BO * 4 <= 2 * ROWS * PITCH, "bias scratch fits");
         if (is_g) {
 #pragma unroll
-            for (int t = 0; t < 3; ++t)
+            for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) red[(pgg * 3 + t) * BO + ov * VEC + e] = dsum[t][e];
         }
         __syncthreads();
-        for (int i = tid; i < 3 * BO; i += kThreads) {
+        for (int i = tid; i < NTM * BO; i += kThreads) {
             const int t = i / BO, ol = i % BO;
             const int o = ct * BO + ol;
             if (o >= a.O) continue;

@@ -13,6 +13,7 @@
 #include <stdint.h>
 
 #include "qfastdiv.h"
+#include "qargs.h"
 
 namespace ql {
 
@@ -131,6 +132,81 @@ __device__ __forceinline__ void prologue_frag(const v4u &g, const v4u &ta, const
     }
     ga = vpack<T>(fa);
     gb = vpack<T>(fb);
+}
+
+// Elementwise square of a 16-byte fragment (fp32 products rounded once to T):
+// the X o X operand of the T2 neuron.
+template <typename T> __device__ __forceinline__ v4u square_frag(const v4u &v) {
+    constexpr int VEC = Elem<T>::VEC;
+    float f[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+        const float x = vget<T>(v, e);
+        f[e] = x * x;
+    }
+    return vpack<T>(f);
+}
+
+// The output-side MFMA operands of a backward kernel for operand mode OM
+// (qargs.h), formed in fp32 on one 16-byte fragment of G, T_a, T_b and
+// rounded once to T:
+//   OM_QUADRA: G o T_b, G o T_a, G      OM_PAIR: G o T_b, G o T_a
+//   OM_SQUARE: 2 G o T_a                OM_SQIN: G
+template <typename T, int OM>
+__device__ __forceinline__ void operands_frag(const v4u &g, const v4u &ta, const v4u &tb, v4u *bt) {
+    constexpr int VEC = Elem<T>::VEC;
+    if constexpr (OM == OM_SQIN) {
+        bt[0] = g;
+    } else if constexpr (OM == OM_SQUARE) {
+        float f[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) f[e] = 2.0f * vget<T>(g, e) * vget<T>(ta, e);
+        bt[0] = vpack<T>(f);
+    } else {
+        prologue_frag<T>(g, ta, tb, bt[0], bt[1]);
+        if constexpr (OM == OM_QUADRA) bt[2] = g;
+    }
+}
+
+// Four consecutive elements of T as floats (8 bytes for bf16, 16 for fp32).
+template <typename T> __device__ __forceinline__ void load4(const T *p, float *f) {
+    if constexpr (sizeof(T) == 4) {
+        const v4f v = *reinterpret_cast<const v4f *>(p);
+        f[0] = v[0]; f[1] = v[1]; f[2] = v[2]; f[3] = v[3];
+    } else {
+        const v2u v = *reinterpret_cast<const v2u *>(p);
+        f[0] = bf2f(v.x & 0xffffu); f[1] = bf2f(v.x >> 16);
+        f[2] = bf2f(v.y & 0xffffu); f[3] = bf2f(v.y >> 16);
+    }
+}
+
+// Input-gradient epilogue of the T4 + identity and T2 neurons on a wave's
+// accumulator tile (rows: input channels c, columns: input pixels m, the MFMA
+// layout of mfma_chunk): acc += src[m, c] (src = G, the shortcut's gradient)
+// or acc *= 2 src[m, c] (src = X, the derivative of X o X).  src is M x C.
+template <typename T, int OM, int MR, int MC>
+__device__ __forceinline__ void neuron_dx_epilogue(f32x16_t (&acc)[MR][MC], const void *srcv, int M, int C,
+                                                   int pcol0, int crow0, int lane) {
+    const T *__restrict__ src = static_cast<const T *>(srcv);
+    const int lrow = lane & 31, lhi = lane >> 5;
+#pragma unroll
+    for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) {
+            const int m = pcol0 + mc * 32 + lrow;
+            if (m >= M) continue;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int c = crow0 + mr * 32 + 8 * g + 4 * lhi;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (c + i >= C) break;
+                    const float v = to_f32<T>(src[(size_t)m * C + c + i]);
+                    const float r = acc[mr][mc][4 * g + i];
+                    acc[mr][mc][4 * g + i] = OM == OM_SQIN ? r * (2.0f * v) : r + v;
+                }
+            }
+        }
 }
 
 // 16-byte global load, or zeros when !ok (the address is not touched then).

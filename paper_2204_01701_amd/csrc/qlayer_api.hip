@@ -66,6 +66,9 @@ int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 struct Geom {
     int N, C, H, W, O, KH, KW, SH, SW, PH, PW, HO, WO;
     ql_dtype dt;
+    int ne;  // neuron type (NEURON_*)
+    int om() const { return om_of_neuron(ne); }
+    int terms() const { return om_terms(om()); }
     size_t esize() const { return dt == QL_BF16 ? 2 : 4; }
     int vec() const { return dt == QL_BF16 ? 8 : 4; }
     // Few input channels that are not a multiple of the 16-byte vector (e.g.
@@ -80,6 +83,7 @@ ql_status make_geom(const ql_conv_desc *d, Geom &g) {
         return QL_EINVAL;
     if (d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0) return QL_EINVAL;
     if (d->dtype != QL_F32 && d->dtype != QL_BF16) return QL_EINVAL;
+    if ((int)d->neuron < NEURON_QUADRA || (int)d->neuron > NEURON_T2) return QL_EINVAL;
     const long long eh = (long long)d->h + 2LL * d->pad_h - d->kh;
     const long long ew = (long long)d->w + 2LL * d->pad_w - d->kw;
     if (eh < 0 || ew < 0) return QL_EINVAL;  // empty output
@@ -88,6 +92,9 @@ ql_status make_geom(const ql_conv_desc *d, Geom &g) {
     g.HO = (int)(eh / d->stride_h + 1);
     g.WO = (int)(ew / d->stride_w + 1);
     g.dt = d->dtype;
+    g.ne = (int)d->neuron;
+    // the shortcut of T4 + identity adds input channel o at the same pixel
+    if (g.ne == NEURON_T4I && (g.C != g.O || g.HO != g.H || g.WO != g.W)) return QL_EINVAL;
     const long long nx = (long long)g.N * g.H * g.W * g.C;
     const long long ny = (long long)g.N * g.HO * g.WO * g.O;
     const long long nw = (long long)g.O * g.KH * g.KW * g.C;
@@ -99,7 +106,7 @@ ql_status make_geom(const ql_conv_desc *d, Geom &g) {
 
 ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
     if (!d) return QL_EINVAL;
-    ql_conv_desc c{d->batch, d->in, 1, 1, d->out, 1, 1, 1, 1, 0, 0, d->dtype};
+    ql_conv_desc c{d->batch, d->in, 1, 1, d->out, 1, 1, 1, 1, 0, 0, d->dtype, d->neuron};
     return make_geom(&c, g);
 }
 
@@ -176,12 +183,12 @@ FwdPlan plan_fwd(const Geom &g) {
         // 8-wave 128 x 256 tiles where there are enough of them to fill the GPU several times
         const bool big = g.O >= 128 && (long long)cdiv(g.O, 128) * cdiv(M, 256) >= 4 * kNumCUs;
         p.cfg = env_override("QLAYER_FWD_CFG", big ? 4 : 3);
-        if (p.cfg < 0 || p.cfg >= kFwdCfgs) p.cfg = 3;
+        if (p.cfg < 0 || p.cfg >= kFwdCfgs || g.ne != NEURON_QUADRA) p.cfg = 3;  // (the other types: tile 3 only)
         p.BR = kFwdBR[p.cfg];
         p.BCOL = kFwdBCOL[p.cfg];
         p.slots = kFwdSlots[p.cfg];
     } else {
-        p.cfg = g.O <= 64 ? 1 : 0;
+        p.cfg = g.O <= 64 || g.ne != NEURON_QUADRA ? 1 : 0;
         p.BR = p.cfg == 0 ? 128 : 64;
         p.BCOL = 128;
         p.slots = 1;
@@ -227,7 +234,7 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
         p.njb = cdiv(J, 32);
         p.smem = (size_t)3 * p.njb * (g.O / (2 * g.vec())) * 64 * 16;
         p.smallc = g.C <= 4 && g.O % (2 * g.vec()) == 0 && p.njb <= 2 && p.smem <= 64 * 1024 &&
-                   env_override("QLAYER_BWD_DATA_SMALLC", 1) != 0;
+                   g.ne == NEURON_QUADRA && env_override("QLAYER_BWD_DATA_SMALLC", 1) != 0;
         if (p.smallc) {
             p.ws_bytes = align_up((size_t)g.N * g.HO * g.WO * J * sizeof(float));
             return p;
@@ -247,10 +254,11 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
         if (wide_ok && g.KH * g.KW == 1 && g.C >= 256 && M >= 1024) dflt = 4;
         p.cfg = env_override("QLAYER_BWD_DATA_CFG", dflt);
         if (p.cfg < 0 || p.cfg >= kBdCfgs || (p.cfg == 4 && !wide_ok)) p.cfg = 0;
+        if (g.ne != NEURON_QUADRA) p.cfg = g.C > 64 ? 3 : 5;  // (the other types: tiles 3 and 5 only)
         p.BR = kBdBR[p.cfg];
         p.BCOL = kBdBCOL[p.cfg];
     } else {
-        p.cfg = g.C <= 64 ? 1 : 0;
+        p.cfg = g.C <= 64 || g.ne != NEURON_QUADRA ? 1 : 0;
         p.BR = p.cfg == 0 ? 128 : 64;
         p.BCOL = 128;
     }
@@ -297,7 +305,7 @@ BwdWeightPlan plan_bwd_weight(const Geom &g) {
     if (p.pad) p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
     if (p.pipe) {
         p.cfg = env_override("QLAYER_BWD_WEIGHT_CFG", 0);
-        if (p.cfg < 0 || p.cfg >= kBwCfgs) p.cfg = 0;
+        if (p.cfg < 0 || p.cfg >= kBwCfgs || g.ne != NEURON_QUADRA) p.cfg = 0;  // (the other types: tile 0)
         p.BKP = kBwBKP[p.cfg];
         p.BO = kBwBO[p.cfg];
         p.slots = kBwSlots[p.cfg];
@@ -345,8 +353,9 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
         // Zero-pad X and the three weights to Cp channels in the workspace.
         PadSegments sg{};
         const void *srcs[4] = {x, wa, wb, wc};
-        const long long rows[4] = {(long long)g.N * g.H * g.W, (long long)g.O * g.KH * g.KW,
-                                   (long long)g.O * g.KH * g.KW, (long long)g.O * g.KH * g.KW};
+        const long long wrows = (long long)g.O * g.KH * g.KW;
+        const long long rows[4] = {(long long)g.N * g.H * g.W, wrows, g.terms() >= 2 ? wrows : 0,
+                                   g.terms() >= 3 ? wrows : 0};  // (terms the type lacks: nothing to pad)
         for (int i = 0; i < 4; ++i) {
             sg.src[i] = srcs[i];
             sg.dst[i] = wsb + (i == 0 ? 0 : p.xpad_bytes + (size_t)(i - 1) * p.wpad_bytes);
@@ -375,8 +384,31 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     a.fd_wo = make_fastdiv(g.WO);
     a.fd_c = make_fastdiv(C);
     a.fd_kw = make_fastdiv(g.KW);
+    a.neuron = g.ne;
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
-    if (p.veck) {
+    const int om = g.om();
+    if (p.veck && om != OM_QUADRA) {
+        const bool ca = C % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
+#define QL_FWD_OM(OM)                                                                                          \
+    do {                                                                                                        \
+        if (ca)                                                                                                 \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, 64, 128, 2, 2, 4, true, 256, OM>), grid, block, 0, st, a);  \
+        else                                                                                                    \
+            hipLaunchKernelGGL((qconv_fwd_kernel<T, 64, 128, 2, 2, 4, false, 256, OM>), grid, block, 0, st, a); \
+    } while (0)
+        if (om == OM_PAIR) QL_FWD_OM(OM_PAIR);
+        else if (om == OM_SQUARE) QL_FWD_OM(OM_SQUARE);
+        else QL_FWD_OM(OM_SQIN);
+#undef QL_FWD_OM
+    } else if (!p.veck && om != OM_QUADRA) {
+        if (om == OM_PAIR)
+            hipLaunchKernelGGL((qconv_fwd_generic_kernel<T, 64, 128, 2, 2, 64, false, OM_PAIR>), grid, block, 0, st, a);
+        else if (om == OM_SQUARE)
+            hipLaunchKernelGGL((qconv_fwd_generic_kernel<T, 64, 128, 2, 2, 64, false, OM_SQUARE>), grid, block, 0, st,
+                               a);
+        else
+            hipLaunchKernelGGL((qconv_fwd_generic_kernel<T, 64, 128, 2, 2, 64, false, OM_SQIN>), grid, block, 0, st, a);
+    } else if (p.veck) {
         // channel-aligned K steps: every step within one tap
         const bool ca = C % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
 #define QL_FWD(BR, BC, WR, WC, NS, NT)                                                                           \
@@ -406,11 +438,11 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     if (g.O % 4 == 0)
         hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, true>), dim3(grid_1d(MO / 4)), dim3(kThreads), 0, st,
                            static_cast<const float *>(a.ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
-                           static_cast<T *>(ta), static_cast<T *>(tb));
+                           static_cast<T *>(ta), static_cast<T *>(tb), g.ne, static_cast<const T *>(x));
     else
         hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, false>), dim3(grid_1d(MO)), dim3(kThreads), 0, st,
                            static_cast<const float *>(a.ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
-                           static_cast<T *>(ta), static_cast<T *>(tb));
+                           static_cast<T *>(ta), static_cast<T *>(tb), g.ne, static_cast<const T *>(x));
     return hip_status();
 }
 
@@ -447,7 +479,7 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
         a.wt[0] = wa; a.wt[1] = wb; a.wt[2] = wc;
     } else {
         T *wt = static_cast<T *>(ws);
-        hipLaunchKernelGGL((qconv_weight_transpose_kernel<T>), dim3(cdiv(g.C, 32), cdiv(g.O, 32), 3 * khkw),
+        hipLaunchKernelGGL((qconv_weight_transpose_kernel<T>), dim3(cdiv(g.C, 32), cdiv(g.O, 32), g.terms() * khkw),
                            dim3(kThreads), 0, st, static_cast<const T *>(wa), static_cast<const T *>(wb),
                            static_cast<const T *>(wc), wt, g.O, khkw, g.C);
         s = hip_status();
@@ -472,43 +504,64 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.fd_kw = make_fastdiv(g.KW);
     a.fd_sh = make_fastdiv(g.SH);
     a.fd_sw = make_fastdiv(g.SW);
+    a.neuron = g.ne;
+    a.xin = g.ne == NEURON_T2 ? ta : nullptr;  // (T2: the `ta` argument carries X)
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     // channel-aligned K steps (each within one tap): stride 1, natural weight tiles, O a multiple of KE
     const bool bd_ca = p.s1 && p.natw && g.O % p.KE == 0 && g.KH * g.KW <= 32 &&
                        env_override("QLAYER_BWD_DATA_CA", 1) != 0;
-#define QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, NW)                                                                        \
-    do {                                                                                                              \
-        if (p.s1)                                                                                                     \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, true, NW, false>), grid, block, 0, st, a); \
-        else                                                                                                          \
-            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, false, NW, false>), grid, block, 0, st, \
-                               a);                                                                                    \
+    const int om = g.om();
+#define QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, NW, OM)                                                                     \
+    do {                                                                                                               \
+        if (p.s1)                                                                                                      \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, true, NW, false, OM>), grid, block, 0, st, \
+                               a);                                                                                     \
+        else                                                                                                           \
+            hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, false, NW, false, OM>), grid, block, 0,  \
+                               st, a);                                                                                 \
     } while (0)
-#define QL_BD_PIPE(BR, BCOL, WR, WC, NS)                                                                              \
-    do {                                                                                                              \
-        if constexpr (sizeof(T) == 2) {                                                                               \
-            if (bd_ca) {                                                                                              \
-                hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, true, true, true>), grid, block, 0, \
-                                   st, a);                                                                            \
-                break;                                                                                                \
-            }                                                                                                         \
-            if (p.natw) {                                                                                             \
-                QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, true);                                                             \
-                break;                                                                                                \
-            }                                                                                                         \
-        }                                                                                                             \
-        QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, false);                                                                    \
+#define QL_BD_PIPE_OM(BR, BCOL, WR, WC, NS, OM)                                                                        \
+    do {                                                                                                               \
+        if constexpr (sizeof(T) == 2) {                                                                                \
+            if (bd_ca) {                                                                                               \
+                hipLaunchKernelGGL((qconv_bwd_data_kernel<T, BR, BCOL, WR, WC, NS, true, true, true, OM>), grid, block, \
+                                   0, st, a);                                                                          \
+                break;                                                                                                 \
+            }                                                                                                          \
+            if (p.natw) {                                                                                              \
+                QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, true, OM);                                                          \
+                break;                                                                                                 \
+            }                                                                                                          \
+        }                                                                                                              \
+        QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, false, OM);                                                                 \
     } while (0)
-#define QL_BD_GEN(BR, BCOL)                                                                                      \
-    do {                                                                                                         \
-        if (p.s1)                                                                                                \
-            hipLaunchKernelGGL((qconv_bwd_data_generic_kernel<T, BR, BCOL, 2, 2, 64, false, true>), grid, block, 0, \
-                               st, a);                                                                           \
-        else                                                                                                     \
-            hipLaunchKernelGGL((qconv_bwd_data_generic_kernel<T, BR, BCOL, 2, 2, 64, false, false>), grid, block, \
-                               0, st, a);                                                                        \
+#define QL_BD_PIPE(BR, BCOL, WR, WC, NS) QL_BD_PIPE_OM(BR, BCOL, WR, WC, NS, OM_QUADRA)
+#define QL_BD_GEN_OM(BR, BCOL, OM)                                                                                 \
+    do {                                                                                                           \
+        if (p.s1)                                                                                                  \
+            hipLaunchKernelGGL((qconv_bwd_data_generic_kernel<T, BR, BCOL, 2, 2, 64, false, true, OM>), grid, block, \
+                               0, st, a);                                                                          \
+        else                                                                                                       \
+            hipLaunchKernelGGL((qconv_bwd_data_generic_kernel<T, BR, BCOL, 2, 2, 64, false, false, OM>), grid,      \
+                               block, 0, st, a);                                                                   \
     } while (0)
-    if (p.veck && p.cfg == 4) {
+#define QL_BD_GEN(BR, BCOL) QL_BD_GEN_OM(BR, BCOL, OM_QUADRA)
+#define QL_BD_VARIANT(OM)                                                                                          \
+    do {                                                                                                           \
+        if (!p.veck)                                                                                               \
+            QL_BD_GEN_OM(64, 128, OM);                                                                             \
+        else if (p.cfg == 3)                                                                                       \
+            QL_BD_PIPE_OM(128, 128, 1, 4, 3, OM);                                                                  \
+        else                                                                                                       \
+            QL_BD_PIPE_OM(64, 128, 1, 4, 4, OM);                                                                   \
+    } while (0)
+    if (om == OM_PAIR) {
+        QL_BD_VARIANT(OM_PAIR);
+    } else if (om == OM_SQUARE) {
+        QL_BD_VARIANT(OM_SQUARE);
+    } else if (om == OM_SQIN) {
+        QL_BD_VARIANT(OM_SQIN);
+    } else if (p.veck && p.cfg == 4) {
         if constexpr (sizeof(T) == 2)
             hipLaunchKernelGGL((qconv_bwd_data_wide_kernel<256, 256, 2, 4, 3>), grid, dim3(512), 0, st, a);
     } else if (p.veck) {
@@ -527,18 +580,24 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     } else {
         QL_BD_GEN(64, 128);
     }
+#undef QL_BD_VARIANT
 #undef QL_BD_PIPE
+#undef QL_BD_PIPE_OM
 #undef QL_BD_PIPE_N
 #undef QL_BD_GEN
+#undef QL_BD_GEN_OM
     s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long total = (long long)a.M * g.C;
+    // the neuron type's last step on the summed partials: + G (T4 + identity), x 2 X (T2)
+    const int mode = g.ne == NEURON_T4I ? 1 : (g.ne == NEURON_T2 ? 2 : 0);
+    const T *src = static_cast<const T *>(mode == 1 ? gy : (mode == 2 ? ta : nullptr));
     if (g.C % 4 == 0)
         hipLaunchKernelGGL((qconv_sum_splits_kernel<T, true>), dim3(grid_1d(total / 4)), dim3(kThreads), 0, st,
-                           static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx));
+                           static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx), mode, src);
     else
         hipLaunchKernelGGL((qconv_sum_splits_kernel<T, false>), dim3(grid_1d(total)), dim3(kThreads), 0, st,
-                           static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx));
+                           static_cast<const float *>(a.ws), p.splits, total, static_cast<T *>(dx), mode, src);
     return hip_status();
 }
 
@@ -583,8 +642,29 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     a.lin = g.SH == 1 && g.SW == 1 && g.HO == g.H && g.WO == g.W && env_override("QLAYER_BWD_WEIGHT_LIN", 1) != 0;
     a.lin_dq = (p.KE / g.WO) % g.HO;
     a.lin_dr = p.KE % g.WO;
+    a.neuron = g.ne;
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
-    if constexpr (sizeof(T) == 2) {
+    const int om = g.om();
+    if (om != OM_QUADRA) {
+        // the other neuron types: the 128 x 64 pipelined tile (bf16) or the generic 128 x 64 kernel
+#define QL_BW_OM(OM)                                                                                               \
+    do {                                                                                                           \
+        if (p.pipe) {                                                                                              \
+            if constexpr (sizeof(T) == 2)                                                                          \
+                hipLaunchKernelGGL((qconv_bwd_weight_kernel<128, 64, 2, 2, 4, 256, OM>), grid, block, 0, st, a);   \
+        } else if (p.veck) {                                                                                       \
+            hipLaunchKernelGGL((qconv_bwd_weight_generic_kernel<T, 128, 64, 2, 2, 64, 4, true, OM>), grid, block, 0, \
+                               st, a);                                                                             \
+        } else {                                                                                                   \
+            hipLaunchKernelGGL((qconv_bwd_weight_generic_kernel<T, 128, 64, 2, 2, 64, 4, false, OM>), grid, block,   \
+                               0, st, a);                                                                          \
+        }                                                                                                          \
+    } while (0)
+        if (om == OM_PAIR) QL_BW_OM(OM_PAIR);
+        else if (om == OM_SQUARE) QL_BW_OM(OM_SQUARE);
+        else QL_BW_OM(OM_SQIN);
+#undef QL_BW_OM
+    } else if constexpr (sizeof(T) == 2) {
         if (p.pipe) {
             switch (p.cfg) {
                 case 0: hipLaunchKernelGGL((qconv_bwd_weight_kernel<128, 64, 2, 2, 4>), grid, block, 0, st, a); break;
@@ -593,7 +673,7 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
             }
         }
     }
-    if (!p.pipe) {
+    if (!p.pipe && om == OM_QUADRA) {
         if (p.veck)
             hipLaunchKernelGGL((qconv_bwd_weight_generic_kernel<T, 128, 64, 2, 2, 64, 4, true>), grid, block, 0, st, a);
         else
@@ -607,25 +687,31 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
         hipLaunchKernelGGL((qconv_bwd_weight_reduce2d_kernel<16>), dim3(grid_1d((3 * ndw + 3 * g.O) * 16)),
                            dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
                            static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
-                           a.want_db);
+                           a.want_db, g.terms());
     else if (ndw % 4 == 0)
         hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<true>), dim3(grid_1d(3 * ndw / 4 + 3 * g.O)),
                            dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
                            static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
-                           a.want_db);
+                           a.want_db, g.terms());
     else
         hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<false>), dim3(grid_1d(3 * ndw + 3 * g.O)),
                            dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
                            static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
-                           a.want_db);
+                           a.want_db, g.terms());
     return hip_status();
 }
 
 ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *wb, const void *wc, const float *ba,
                      const float *bb, const float *bc, void *y, void *ta, void *tb, void *ws, size_t ws_bytes,
                      void *stream) {
-    if (!x || !wa || !wb || !wc) return QL_EINVAL;
-    if (!y && !(ta && tb)) return QL_EINVAL;
+    const int nt = g.terms();
+    // pointers of terms the neuron type lacks are ignored
+    if (nt < 3) { wc = nullptr; bc = nullptr; }
+    if (nt < 2) { wb = nullptr; bb = nullptr; tb = nullptr; }
+    if (g.ne == NEURON_T2) ta = nullptr;  // (nothing is saved: its backward takes X)
+    if (!x || !wa || (nt >= 2 && !wb) || (nt >= 3 && !wc)) return QL_EINVAL;
+    const bool saved = g.ne == NEURON_T2 ? false : (nt >= 2 ? (ta && tb) : ta != nullptr);
+    if (!y && !saved) return QL_EINVAL;
     const void *ptrs[] = {x, wa, wb, wc, ba, bb, bc, y, ta, tb};
     for (const void *q : ptrs)
         if (q && !aligned16(q)) return QL_EINVAL;
@@ -639,10 +725,14 @@ ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *w
 
 ql_status bwd_data_common(const Geom &g, const void *gy, const void *ta, const void *tb, const void *wa,
                           const void *wb, const void *wc, void *dx, void *ws, size_t ws_bytes, void *stream) {
-    if (!gy || !ta || !tb || !wa || !wb || !wc || !dx) return QL_EINVAL;
+    const int nt = g.terms();
+    if (nt < 3) wc = nullptr;
+    if (nt < 2) wb = nullptr;
+    if (g.om() == OM_SQUARE || g.om() == OM_SQIN) tb = nullptr;  // (T2: `ta` is X)
+    if (!gy || !ta || !wa || !dx || (nt >= 2 && (!tb || !wb)) || (nt >= 3 && !wc)) return QL_EINVAL;
     const void *ptrs[] = {gy, ta, tb, wa, wb, wc, dx};
     for (const void *q : ptrs)
-        if (!aligned16(q)) return QL_EINVAL;
+        if (q && !aligned16(q)) return QL_EINVAL;
     const BwdDataPlan p = plan_bwd_data(g);
     if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
     if (ws && !aligned16(ws)) return QL_EINVAL;
@@ -654,9 +744,16 @@ ql_status bwd_data_common(const Geom &g, const void *gy, const void *ta, const v
 ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const void *ta, const void *tb,
                             float *dwa, float *dwb, float *dwc, float *dba, float *dbb, float *dbc, void *ws,
                             size_t ws_bytes, void *stream) {
-    if (!x || !gy || !ta || !tb || !dwa || !dwb || !dwc) return QL_EINVAL;
+    const int nt = g.terms(), ngm = om_gmaps(g.om());
+    // pointers of terms (and maps) the neuron type lacks are ignored
+    if (nt < 3) { dwc = nullptr; dbc = nullptr; }
+    if (nt < 2) { dwb = nullptr; dbb = nullptr; }
+    if (ngm < 3) tb = nullptr;
+    if (ngm < 2) ta = nullptr;
+    if (!x || !gy || (ngm >= 2 && !ta) || (ngm >= 3 && !tb) || !dwa || (nt >= 2 && !dwb) || (nt >= 3 && !dwc))
+        return QL_EINVAL;
     const int nb = (dba != nullptr) + (dbb != nullptr) + (dbc != nullptr);
-    if (nb != 0 && nb != 3) return QL_EINVAL;
+    if (nb != 0 && nb != nt) return QL_EINVAL;
     const void *ptrs[] = {x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc};
     for (const void *q : ptrs)
         if (q && !aligned16(q)) return QL_EINVAL;
@@ -759,11 +856,18 @@ ql_status qlayer_linear_bwd(const ql_linear_desc *desc, const void *x, const voi
     Geom g;
     ql_status s = linear_geom(desc, g);
     if (s != QL_OK) return s;
+    const int nt = g.terms(), ngm = om_gmaps(g.om());
+    // pointers of terms (and maps) the neuron type lacks are ignored
+    if (nt < 3) { wc = nullptr; dwc = nullptr; dbc = nullptr; }
+    if (nt < 2) { wb = nullptr; dwb = nullptr; dbb = nullptr; }
+    if (ngm < 3) tb = nullptr;
+    if (ngm < 2) ta = nullptr;
     const int nw = (dwa != nullptr) + (dwb != nullptr) + (dwc != nullptr);
     const int nb = (dba != nullptr) + (dbb != nullptr) + (dbc != nullptr);
-    if ((nw != 0 && nw != 3) || (nb != 0 && nb != 3) || (nb == 3 && nw == 0)) return QL_EINVAL;
+    if ((nw != 0 && nw != nt) || (nb != 0 && nb != nt) || (nb != 0 && nw == 0)) return QL_EINVAL;
     if (!dx && nw == 0) return QL_EINVAL;
-    if (!x || !gy || !ta || !tb || !wa || !wb || !wc) return QL_EINVAL;
+    if (!x || !gy || (ngm >= 2 && !ta) || (ngm >= 3 && !tb) || !wa || (nt >= 2 && !wb) || (nt >= 3 && !wc))
+        return QL_EINVAL;
     // Validate everything before the first launch.
     const void *ptrs[] = {x, gy, ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc};
     for (const void *q : ptrs)
@@ -771,7 +875,8 @@ ql_status qlayer_linear_bwd(const ql_linear_desc *desc, const void *x, const voi
     const size_t need = std::max(dx ? plan_bwd_data(g).ws_bytes : 0, nw ? plan_bwd_weight(g).ws_bytes : 0);
     if (workspace_bytes < need || (need && !workspace)) return QL_EWORKSPACE;
     if (dx) {
-        s = bwd_data_common(g, gy, ta, tb, wa, wb, wc, dx, workspace, workspace_bytes, stream);
+        // (T2: the input gradient takes X in place of the saved map)
+        s = bwd_data_common(g, gy, g.ne == NEURON_T2 ? x : ta, tb, wa, wb, wc, dx, workspace, workspace_bytes, stream);
         if (s != QL_OK) return s;
     }
     if (nw) s = bwd_weight_common(g, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, workspace, workspace_bytes, stream);

@@ -165,3 +165,35 @@ int main() {
                     str(src), "-o", str(exe)], check=True)
     out = subprocess.run([str(exe)], capture_output=True, text=True)
     assert out.returncode == 0 and out.stdout.strip() == "ok", out.stdout
+
+
+def test_neuron_type_validation(L):
+    # an unknown type, and the identity shortcut without C == O or with a changed map
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, 5)) == QL_EINVAL
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, -1)) == QL_EINVAL
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 32, 3, 3, 1, 1, ql.QL_F32, ql.QL_NEURON_T4_IDENTITY)) == QL_EINVAL
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 2, 1, ql.QL_F32, ql.QL_NEURON_T4_IDENTITY)) == QL_EINVAL
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 0, ql.QL_F32, ql.QL_NEURON_T4_IDENTITY)) == QL_EINVAL
+    # the weights a type has are required; recompute mode needs its saved maps; T2 saves none
+    t4 = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, ql.QL_NEURON_T4)
+    assert _fwd(L, t4, wb=None) == QL_EINVAL
+    assert _fwd(L, t4, y=None, ta=FAKE) == QL_EINVAL
+    t3 = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, ql.QL_NEURON_T3)
+    assert _fwd(L, t3, wa=None) == QL_EINVAL
+    assert _fwd(L, t3, y=None) == QL_EINVAL
+    t2 = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, ql.QL_NEURON_T2)
+    assert _fwd(L, t2, y=None, ta=FAKE, tb=FAKE) == QL_EINVAL
+    # backward: the saved maps of the type (T2's input gradient takes X in `ta`)
+    ws = 1 << 30
+    assert L.qlayer_conv2d_bwd_data(ctypes.byref(t3), FAKE, None, None, FAKE, None, None, FAKE, FAKE, ws,
+                                    None) == QL_EINVAL
+    assert L.qlayer_conv2d_bwd_data(ctypes.byref(t4), FAKE, FAKE, None, FAKE, FAKE, None, FAKE, FAKE, ws,
+                                    None) == QL_EINVAL
+    assert L.qlayer_conv2d_bwd_weight(ctypes.byref(t4), FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None,
+                                      None, FAKE, ws, None) == QL_EINVAL          # dW_b missing
+    assert L.qlayer_conv2d_bwd_weight(ctypes.byref(t4), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, None,
+                                      None, FAKE, ws, None) == QL_EINVAL          # biases of some terms only
+    # the workspace queries accept every type
+    for n in range(5):
+        d = ql.conv_desc(4, 256, 4, 4, 256, 3, 3, 1, 1, ql.QL_BF16, n)
+        assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d)) > 0
