@@ -56,12 +56,14 @@ def parse():
 class Layer:
     """Device tensors and call wrappers of one quadratic conv layer."""
 
-    def __init__(self, ql, torch, L, cfg_id, layer_id, dev, bf16=True):
+    def __init__(self, ql, torch, L, cfg_id, layer_id, dev, bf16=True, neuron=0):
         import numpy as np
         import synth
 
         self.L = L
         self.ql = ql
+        self.neuron = neuron
+        nt = ql.NEURON_TERMS[neuron]
         dt = torch.bfloat16 if bf16 else torch.float32
         inp = synth.conv_inputs(cfg_id, layer_id, L, bf16=bf16)
 
@@ -69,17 +71,19 @@ class Layer:
             return torch.from_numpy(np.ascontiguousarray(a)).permute(0, 2, 3, 1).contiguous().to(dev, dt)
 
         self.desc = ql.conv_desc(L.n, L.c, L.h, L.w, L.o, L.k, L.k, L.stride, L.pad,
-                                 ql.QL_BF16 if bf16 else ql.QL_F32)
+                                 ql.QL_BF16 if bf16 else ql.QL_F32, neuron)
         self.x = nhwc(inp["x"])
-        self.w = [nhwc(inp[k]) for k in ("wa", "wb", "wc")]
-        self.b = [torch.from_numpy(inp[k]).to(dev) for k in ("ba", "bb", "bc")]
+        self.w = [nhwc(inp[k]) if i < nt else None for i, k in enumerate(("wa", "wb", "wc"))]
+        self.b = [torch.from_numpy(inp[k]).to(dev) if i < nt else None for i, k in enumerate(("ba", "bb", "bc"))]
         self.gy = nhwc(inp["gy"])
         self.y = torch.empty((L.n, L.ho, L.wo, L.o), device=dev, dtype=dt)
-        self.ta = torch.empty_like(self.y)
-        self.tb = torch.empty_like(self.y)
+        # the saved maps of the neuron type (T2 saves none: its input gradient takes X)
+        self.ta = torch.empty_like(self.y) if neuron != ql.QL_NEURON_T2 else None
+        self.tb = torch.empty_like(self.y) if nt >= 2 else None
         self.dx = torch.empty_like(self.x)
-        self.dw = [torch.empty((L.o, L.k, L.k, L.c), device=dev, dtype=torch.float32) for _ in range(3)]
-        self.db = [torch.empty(L.o, device=dev, dtype=torch.float32) for _ in range(3)]
+        self.dw = [torch.empty((L.o, L.k, L.k, L.c), device=dev, dtype=torch.float32) if i < nt else None
+                   for i in range(3)]
+        self.db = [torch.empty(L.o, device=dev, dtype=torch.float32) if i < nt else None for i in range(3)]
         # forward and input gradient share one workspace (same stream); the weight
         # gradient has its own, so that it may run concurrently on a second stream
         need = max(ql.qlayer_conv2d_fwd_workspace_size(self.desc),
@@ -96,7 +100,8 @@ class Layer:
                                   workspace=self.wsp, stream=st)
 
     def bwd_data(self, st):
-        self.ql.qlayer_conv2d_bwd_data(self.desc, self.gy, self.ta, self.tb, *self.w, self.dx,
+        ta = self.x if self.neuron == self.ql.QL_NEURON_T2 else self.ta
+        self.ql.qlayer_conv2d_bwd_data(self.desc, self.gy, ta, self.tb, *self.w, self.dx,
                                        workspace=self.wsp, stream=st)
 
     def bwd_weight(self, st):
@@ -527,8 +532,34 @@ def extra_workloads(ql, torch, dev, stream, reps=10):
         "fwd_tflops": round(3 * u / (fam_ms["fwd"] / fam_n["fwd"] * 1e-3) / 1e12, 1),
         "bwd_tflops": round(6 * u / (fam_ms["bwd"] / fam_n["bwd"] * 1e-3) / 1e12, 1),
         "fwd_bwd_tflops": round(9 * u / (ms * 1e-3) / 1e12, 1)}
+    out["neuron_types"] = neuron_types(ql, torch, dev, stream, reps)
     out["hybrid_bp_memory"] = hybrid_bp_memory(torch, dev)
     return out
+
+
+def neuron_types(ql, torch, dev, stream, reps=10):
+    """The proposed neuron and the earlier types of Table 1 (T4, T4 + identity,
+    T3, T2) on the large layer (N=64, 256->256, 56x56, bf16), each pass timed
+    separately.  Algorithmic flops per pass: one first-order convolution (2 N
+    Ho Wo O C KH KW) per weighted term (3, 2, 2, 1, 1); the elementwise work
+    (products, the square of X for T2, the shortcut) is not counted."""
+    import synth
+
+    L = synth.LARGE_BF16
+    u = unit_flops(L)
+    names = {ql.QL_NEURON_QUADRA: "quadra", ql.QL_NEURON_T4: "t4", ql.QL_NEURON_T4_IDENTITY: "t4_identity",
+             ql.QL_NEURON_T3: "t3", ql.QL_NEURON_T2: "t2"}
+    res = {"shape": "N=64 C=256 56x56 -> 256, 3x3, bf16", "flops": "terms x 2 N Ho Wo O C KH KW per pass"}
+    for ne, name in names.items():
+        ly = Layer(ql, torch, L, 4, 0, dev, neuron=ne)
+        calls = [("fwd", ly.fwd), ("bwd_data", ly.bwd_data), ("bwd_weight", ly.bwd_weight)]
+        ms, _, fam_ms, fam_n = time_calls(torch, calls, reps, 3, stream)
+        nt = ql.NEURON_TERMS[ne]
+        r = {f"{f}_us": round(fam_ms[f] / fam_n[f] * 1e3, 1) for f in ("fwd", "bwd_data", "bwd_weight")}
+        r["fwd_bwd_tflops"] = round(3 * nt * u / (ms * 1e-3) / 1e12, 1)
+        res[name] = r
+        del ly
+    return res
 
 
 def hybrid_bp_memory(torch, dev, batch=256, reps=5):

@@ -13,6 +13,11 @@ section 4.3 (eq:SD).  They offer the two memory modes of section 4.3:
   written) before the gradient kernels.  The gradients are bitwise those of
   save mode, since the same kernel produces T_a and T_b in both.
 
+``neuron`` selects the layer type (``QL_NEURON_*``): the proposed neuron or
+one of the earlier designs of Table 1 (T4, T4 + identity, T3, T2).  Weights
+and biases of the terms a type lacks are passed as None.  T2 saves nothing
+but X in either mode (its backward needs only X).
+
 Layouts.  Convolution tensors are NCHW-shaped torch tensors; they are used in
 channels_last memory format, whose memory is the library's NHWC (OHWI for
 weights), so channels_last inputs are not copied and the outputs come back
@@ -24,8 +29,9 @@ from __future__ import annotations
 
 import torch
 
-from . import (QL_BF16, QL_F32, conv_desc, linear_desc, qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_weight,
-               qlayer_conv2d_fwd, qlayer_linear_bwd, qlayer_linear_fwd)
+from . import (NEURON_TERMS, QL_BF16, QL_F32, QL_NEURON_QUADRA, QL_NEURON_T2, conv_desc, linear_desc,
+               qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_weight, qlayer_conv2d_fwd, qlayer_linear_bwd,
+               qlayer_linear_fwd)
 
 __all__ = ["quad_conv2d", "quad_linear", "QuadConv2dFunction", "QuadLinearFunction"]
 
@@ -43,51 +49,65 @@ def _nhwc(t: torch.Tensor) -> torch.Tensor:
     return t.contiguous(memory_format=torch.channels_last).permute(0, 2, 3, 1)
 
 
-def _biases(ba, bb, bc):
-    bs = (ba, bb, bc)
+def _biases(ba, bb, bc, nt=3):
+    bs = (ba, bb, bc)[:nt]
     if all(b is None for b in bs):
         return None
     if any(b is None for b in bs):
-        raise ValueError("give all three biases or none")
-    return [b.contiguous().float() for b in bs]
+        raise ValueError("give the biases of every term of the neuron type or none")
+    return [b.contiguous().float() for b in bs] + [None] * (3 - nt)
+
+
+def _terms(ws, nt):
+    if any(w is None for w in ws[:nt]):
+        raise ValueError(f"the neuron type has {nt} weighted terms")
+    return list(ws[:nt]) + [None] * (3 - nt)
 
 
 class QuadConv2dFunction(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x, wa, wb, wc, ba, bb, bc, stride, pad, recompute):
+    def forward(ctx, x, wa, wb, wc, ba, bb, bc, stride, pad, recompute, neuron=QL_NEURON_QUADRA):
         N, C, H, W = x.shape
         O, C2, KH, KW = wa.shape
-        if C2 != C or wb.shape != wa.shape or wc.shape != wa.shape:
-            raise ValueError("weight shapes must be (O, C, KH, KW) for all three terms")
-        d = conv_desc(N, C, H, W, O, KH, KW, stride, pad, _qdtype(x))
+        nt = NEURON_TERMS[neuron]
+        ws = _terms((wa, wb, wc), nt)
+        if C2 != C or any(w.shape != wa.shape for w in ws[:nt]):
+            raise ValueError("weight shapes must be (O, C, KH, KW) for every term")
+        d = conv_desc(N, C, H, W, O, KH, KW, stride, pad, _qdtype(x), neuron)
         xn = _nhwc(x)
-        wn = [_nhwc(w.to(x.dtype)) for w in (wa, wb, wc)]
-        b = _biases(ba, bb, bc)
+        wn = [_nhwc(w.to(x.dtype)) if w is not None else None for w in ws]
+        b = _biases(ba, bb, bc, nt)
         bl = b if b is not None else [None, None, None]
         y = torch.empty((N, d.ho, d.wo, O), device=x.device, dtype=x.dtype)
+        recompute = recompute or neuron == QL_NEURON_T2  # (T2 saves nothing but X)
         if recompute:
             qlayer_conv2d_fwd(d, xn, *wn, *bl, y)
-            ctx.save_for_backward(xn, *wn, *(b or []))
         else:
-            ta, tb = torch.empty_like(y), torch.empty_like(y)
+            ta = torch.empty_like(y)
+            tb = torch.empty_like(y) if nt >= 2 else None
             qlayer_conv2d_fwd(d, xn, *wn, *bl, y, ta, tb)
-            ctx.save_for_backward(xn, *wn, ta, tb)
-        ctx.desc, ctx.recompute, ctx.has_bias = d, recompute, b is not None
+        ctx.maps = None if recompute else (ta, tb)
+        ctx.save_for_backward(xn, *[w for w in wn if w is not None], *[v for v in (b or []) if v is not None])
+        ctx.desc, ctx.recompute, ctx.has_bias, ctx.nt, ctx.neuron = d, recompute, b is not None, nt, neuron
         ctx.wdtype = wa.dtype
         return y.permute(0, 3, 1, 2)
 
     @staticmethod
     def backward(ctx, gy):
-        d = ctx.desc
+        d, nt = ctx.desc, ctx.nt
         saved = ctx.saved_tensors
-        xn, wn = saved[0], list(saved[1:4])
-        if ctx.recompute:
-            bl = list(saved[4:7]) if ctx.has_bias else [None, None, None]
+        xn = saved[0]
+        wn = list(saved[1:1 + nt]) + [None] * (3 - nt)
+        bl = (list(saved[1 + nt:1 + 2 * nt]) + [None] * (3 - nt)) if ctx.has_bias else [None, None, None]
+        ta = tb = None
+        if ctx.neuron == QL_NEURON_T2:
+            ta = xn  # its input gradient takes X in place of a saved map
+        elif ctx.recompute:
             ta = torch.empty((d.n, d.ho, d.wo, d.o), device=xn.device, dtype=xn.dtype)
-            tb = torch.empty_like(ta)
+            tb = torch.empty_like(ta) if nt >= 2 else None
             qlayer_conv2d_fwd(d, xn, *wn, *bl, None, ta, tb)
         else:
-            ta, tb = saved[4], saved[5]
+            ta, tb = ctx.maps
         gyn = _nhwc(gy.to(xn.dtype))
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
@@ -97,67 +117,79 @@ class QuadConv2dFunction(torch.autograd.Function):
             qlayer_conv2d_bwd_data(d, gyn, ta, tb, *wn, dxn)
             dx = dxn.permute(0, 3, 1, 2)
         if need_w or need_b:
-            dwn = [torch.empty(wn[0].shape, device=xn.device, dtype=torch.float32) for _ in range(3)]
-            db = [torch.empty(d.o, device=xn.device, dtype=torch.float32) for _ in range(3)] if need_b else None
-            qlayer_conv2d_bwd_weight(d, xn, gyn, ta, tb, *dwn, *(db or [None, None, None]))
-            dw = [g.permute(0, 3, 1, 2).to(ctx.wdtype) for g in dwn]
+            dwn = [torch.empty(wn[0].shape, device=xn.device, dtype=torch.float32) if i < nt else None
+                   for i in range(3)]
+            db = [torch.empty(d.o, device=xn.device, dtype=torch.float32) if i < nt else None
+                  for i in range(3)] if need_b else None
+            qlayer_conv2d_bwd_weight(d, xn, gyn, None if ctx.neuron == QL_NEURON_T2 else ta, tb, *dwn,
+                                     *(db or [None, None, None]))
+            dw = [g.permute(0, 3, 1, 2).to(ctx.wdtype) if g is not None else None for g in dwn]
         dw = dw or [None, None, None]
         db = db or [None, None, None]
-        return (dx, *dw, *db, None, None, None)
+        return (dx, *dw, *db, None, None, None, None)
 
 
 class QuadLinearFunction(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x, wa, wb, wc, ba, bb, bc, recompute):
+    def forward(ctx, x, wa, wb, wc, ba, bb, bc, recompute, neuron=QL_NEURON_QUADRA):
         B, I = x.shape
         O = wa.shape[0]
-        d = linear_desc(B, I, O, _qdtype(x))
+        nt = NEURON_TERMS[neuron]
+        d = linear_desc(B, I, O, _qdtype(x), neuron)
         xc = x.contiguous()
-        wl = [w.to(x.dtype).contiguous() for w in (wa, wb, wc)]
-        b = _biases(ba, bb, bc)
+        wl = [w.to(x.dtype).contiguous() if w is not None else None for w in _terms((wa, wb, wc), nt)]
+        b = _biases(ba, bb, bc, nt)
         bl = b if b is not None else [None, None, None]
         y = torch.empty((B, O), device=x.device, dtype=x.dtype)
+        recompute = recompute or neuron == QL_NEURON_T2
         if recompute:
             qlayer_linear_fwd(d, xc, *wl, *bl, y)
-            ctx.save_for_backward(xc, *wl, *(b or []))
         else:
-            ta, tb = torch.empty_like(y), torch.empty_like(y)
+            ta = torch.empty_like(y)
+            tb = torch.empty_like(y) if nt >= 2 else None
             qlayer_linear_fwd(d, xc, *wl, *bl, y, ta, tb)
-            ctx.save_for_backward(xc, *wl, ta, tb)
-        ctx.desc, ctx.recompute, ctx.has_bias = d, recompute, b is not None
+        ctx.maps = None if recompute else (ta, tb)
+        ctx.save_for_backward(xc, *[w for w in wl if w is not None], *[v for v in (b or []) if v is not None])
+        ctx.desc, ctx.recompute, ctx.has_bias, ctx.nt, ctx.neuron = d, recompute, b is not None, nt, neuron
         ctx.wdtype = wa.dtype
         return y
 
     @staticmethod
     def backward(ctx, gy):
-        d = ctx.desc
+        d, nt = ctx.desc, ctx.nt
         saved = ctx.saved_tensors
-        xc, wl = saved[0], list(saved[1:4])
-        if ctx.recompute:
-            bl = list(saved[4:7]) if ctx.has_bias else [None, None, None]
+        xc = saved[0]
+        wl = list(saved[1:1 + nt]) + [None] * (3 - nt)
+        bl = (list(saved[1 + nt:1 + 2 * nt]) + [None] * (3 - nt)) if ctx.has_bias else [None, None, None]
+        ta = tb = None
+        if ctx.neuron == QL_NEURON_T2:
+            pass  # the dense backward takes X itself
+        elif ctx.recompute:
             ta = torch.empty((d.batch, d.out), device=xc.device, dtype=xc.dtype)
-            tb = torch.empty_like(ta)
+            tb = torch.empty_like(ta) if nt >= 2 else None
             qlayer_linear_fwd(d, xc, *wl, *bl, None, ta, tb)
         else:
-            ta, tb = saved[4], saved[5]
+            ta, tb = ctx.maps
         gyc = gy.to(xc.dtype).contiguous()
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
         dx = torch.empty_like(xc) if need_x else None
-        dw = [torch.empty(wl[0].shape, device=xc.device, dtype=torch.float32) for _ in range(3)] \
-            if (need_w or need_b) else None
-        db = [torch.empty(d.out, device=xc.device, dtype=torch.float32) for _ in range(3)] if need_b else None
+        dw = [torch.empty(wl[0].shape, device=xc.device, dtype=torch.float32) if i < nt else None
+              for i in range(3)] if (need_w or need_b) else None
+        db = [torch.empty(d.out, device=xc.device, dtype=torch.float32) if i < nt else None
+              for i in range(3)] if need_b else None
         qlayer_linear_bwd(d, xc, gyc, ta, tb, *wl, dx, *(dw or [None] * 3), *(db or [None] * 3))
-        dw = [g.to(ctx.wdtype) for g in dw] if dw is not None else [None, None, None]
+        dw = [g.to(ctx.wdtype) if g is not None else None for g in dw] if dw is not None else [None, None, None]
         db = db or [None, None, None]
-        return (dx, *dw, *db, None)
+        return (dx, *dw, *db, None, None)
 
 
-def quad_conv2d(x, wa, wb, wc, ba=None, bb=None, bc=None, stride=1, pad=0, recompute=False):
+def quad_conv2d(x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, stride=1, pad=0, recompute=False,
+                neuron=QL_NEURON_QUADRA):
     """Quadratic 2-D convolution layer (NCHW-shaped tensors, channels_last memory)."""
-    return QuadConv2dFunction.apply(x, wa, wb, wc, ba, bb, bc, stride, pad, recompute)
+    return QuadConv2dFunction.apply(x, wa, wb, wc, ba, bb, bc, stride, pad, recompute, neuron)
 
 
-def quad_linear(x, wa, wb, wc, ba=None, bb=None, bc=None, recompute=False):
+def quad_linear(x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, recompute=False, neuron=QL_NEURON_QUADRA):
     """Quadratic fully-connected layer: x (B, I), weights (O, I)."""
-    return QuadLinearFunction.apply(x, wa, wb, wc, ba, bb, bc, recompute)
+    return QuadLinearFunction.apply(x, wa, wb, wc, ba, bb, bc, recompute, neuron)

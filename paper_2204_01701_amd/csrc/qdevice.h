@@ -198,12 +198,18 @@ __device__ __forceinline__ void neuron_dx_epilogue(f32x16_t (&acc)[MR][MC], cons
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int c = crow0 + mr * 32 + 8 * g + 4 * lhi;
+                float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                if ((C & 3) == 0 && c < C) {
+                    load4<T>(src + (size_t)m * C + c, v);  // four channels in one load
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (c + i < C) v[i] = to_f32<T>(src[(size_t)m * C + c + i]);
+                }
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    if (c + i >= C) break;
-                    const float v = to_f32<T>(src[(size_t)m * C + c + i]);
                     const float r = acc[mr][mc][4 * g + i];
-                    acc[mr][mc][4 * g + i] = OM == OM_SQIN ? r * (2.0f * v) : r + v;
+                    acc[mr][mc][4 * g + i] = OM == OM_SQIN ? r * (2.0f * v[i]) : r + v[i];
                 }
             }
         }

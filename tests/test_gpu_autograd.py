@@ -105,3 +105,65 @@ def test_recompute_mode_lowers_peak_memory():
     assert peaks[False] - peaks[True] >= 2 * one_map, (peaks, one_map)
     for g0, g1 in zip(grads[False], grads[True]):
         assert torch.equal(g0, g1)
+
+
+import paper_2204_01701_amd as ql  # noqa: E402
+
+NEURONS = [ql.QL_NEURON_T4, ql.QL_NEURON_T4_IDENTITY, ql.QL_NEURON_T3, ql.QL_NEURON_T2]
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("neuron", NEURONS, ids=["T4", "T4I", "T3", "T2"])
+def test_conv_autograd_neuron_types(neuron, bf16):
+    shape = (2, 16, 8, 8, 16, 3, 3, 1, 1)
+    N, C, H, W, O, KH, KW, s, p = shape
+    nt = ql.NEURON_TERMS[neuron]
+    dtype = torch.bfloat16 if bf16 else torch.float32
+    inp = synth.random_conv_case([403, neuron], N, C, H, W, O, KH, KW, s, p, bf16=bf16)
+    wl = [inp[k] if i < nt else None for i, k in enumerate(("wa", "wb", "wc"))]
+    bl = [inp[k] if i < nt else None for i, k in enumerate(("ba", "bb", "bc"))]
+    y, _, _ = oracle.conv2d_fwd_neuron(neuron, inp["x"], *wl, *bl, stride=s, pad=p)
+    ref = oracle.conv2d_bwd_neuron(neuron, inp["x"], *wl, *bl, inp["gy"], stride=s, pad=p)
+    ref["y"] = y
+    grads = {}
+    for m in (False, True):
+        x = _t(inp["x"], dtype).contiguous(memory_format=torch.channels_last).detach().requires_grad_(True)
+        w = [_t(inp[k], dtype) if i < nt else None for i, k in enumerate(("wa", "wb", "wc"))]
+        b = [_t(inp[k], torch.float32) if i < nt else None for i, k in enumerate(("ba", "bb", "bc"))]
+        out = quad_conv2d(x, *w, *b, stride=s, pad=p, recompute=m, neuron=neuron)
+        out.backward(_t(inp["gy"], dtype, grad=False))
+        torch.cuda.synchronize()
+        got = {"y": out.detach(), "dx": x.grad}
+        for i, (kw, kb) in enumerate((("dwa", "dba"), ("dwb", "dbb"))[:nt]):
+            got[kw], got[kb] = w[i].grad, b[i].grad
+        for k, v in got.items():
+            e = qlh.relerr(v.double().cpu().numpy(), ref[k])
+            assert e <= qlh.tol(bf16, k != "y"), f"{k} recompute={m}: normwise relative error {e:.3e}"
+        grads[m] = got
+    for k in grads[False]:
+        assert torch.equal(grads[False][k], grads[True][k]), k
+
+
+@pytest.mark.parametrize("neuron", NEURONS, ids=["T4", "T4I", "T3", "T2"])
+def test_linear_autograd_neuron_types(neuron):
+    B, I = 64, 48
+    O = I if neuron == ql.QL_NEURON_T4_IDENTITY else 40
+    nt = ql.NEURON_TERMS[neuron]
+    inp = synth.random_dense_case([404, neuron], B, I, O, bf16=True)
+    wl = [inp[k] if i < nt else None for i, k in enumerate(("wa", "wb", "wc"))]
+    bl = [inp[k] if i < nt else None for i, k in enumerate(("ba", "bb", "bc"))]
+    y, _, _ = oracle.linear_fwd_neuron(neuron, inp["x"], *wl, *bl)
+    ref = oracle.linear_bwd_neuron(neuron, inp["x"], *wl, *bl, inp["gy"])
+    ref["y"] = y
+    x = _t(inp["x"], torch.bfloat16)
+    w = [_t(v, torch.bfloat16) if v is not None else None for v in wl]
+    b = [_t(v, torch.float32) if v is not None else None for v in bl]
+    out = quad_linear(x, *w, *b, neuron=neuron)
+    out.backward(_t(inp["gy"], torch.bfloat16, grad=False))
+    torch.cuda.synchronize()
+    got = {"y": out.detach(), "dx": x.grad}
+    for i, (kw, kb) in enumerate((("dwa", "dba"), ("dwb", "dbb"))[:nt]):
+        got[kw], got[kb] = w[i].grad, b[i].grad
+    for k, v in got.items():
+        e = qlh.relerr(v.double().cpu().numpy(), ref[k])
+        assert e <= qlh.tol(True, k != "y"), f"{k}: normwise relative error {e:.3e}"
