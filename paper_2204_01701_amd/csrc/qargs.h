@@ -38,6 +38,7 @@ struct FwdArgs {
     int M, K;  // GEMM extents: M = N*HO*WO pixels, K = KH*KW*C
     int row_tiles, col_tiles, splits, stages_per_split, stages_total;
     int neuron;  // NEURON_*: the epilogue (T4 + identity reads X at the output pixel)
+    int xsq;     // T2: x already holds X o X (squared by a pre-pass), no squaring in the kernel
     FastDiv fd_howo, fd_wo, fd_c, fd_kw;
 };
 

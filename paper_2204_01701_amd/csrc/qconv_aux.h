@@ -232,6 +232,17 @@ namespace ql {
 // extra channels (lets 3-channel images use the 16-byte pipelined path).
 // blockIdx.y selects one of the NSEG (src, dst, rows) segments: four for the
 // forward (X and the three weights), one for the weight gradient (X).
+// Elementwise X o X (the operand of the T2 neuron), 16 bytes per thread and
+// step; n: elements, a multiple of the 16-byte vector.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void qconv_square_kernel(const T *__restrict__ src, T *__restrict__ dst,
+                                                                long long n) {
+    constexpr int VEC = Elem<T>::VEC;
+    const long long nv = n / VEC;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += (long long)gridDim.x * blockDim.x)
+        *reinterpret_cast<v4u *>(dst + i * VEC) = square_frag<T>(*reinterpret_cast<const v4u *>(src + i * VEC));
+}
+
 struct PadSegments {
     const void *src[4];
     void *dst[4];

@@ -205,8 +205,10 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     };
     auto mma = [&](int set) {
         if constexpr (OM == OM_SQIN) {
+            if (!a.xsq) {
 #pragma unroll
-            for (int mc = 0; mc < MC; ++mc) bf[set][mc] = square_frag<T>(bf[set][mc]);
+                for (int mc = 0; mc < MC; ++mc) bf[set][mc] = square_frag<T>(bf[set][mc]);
+            }
         }
 #pragma unroll
         for (int t = 0; t < NTM; ++t)

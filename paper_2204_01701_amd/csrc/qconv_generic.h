@@ -140,8 +140,10 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
             for (int j = 0; j < NVP; ++j) rx[j] = __builtin_bit_cast(v4u, vx[j]);
         }
         if constexpr (OM == OM_SQIN) {
+            if (!a.xsq) {
 #pragma unroll
-            for (int j = 0; j < NVP; ++j) rx[j] = square_frag<T>(rx[j]);
+                for (int j = 0; j < NVP; ++j) rx[j] = square_frag<T>(rx[j]);
+            }
         }
     };
 

@@ -165,7 +165,9 @@ struct FwdPlan {
     bool veck;
     bool pad;                      // X and W_t zero-padded to Cp channels first
     int Cp;
-    size_t xpad_bytes, wpad_bytes;  // workspace: [X padded][W_a, W_b, W_c padded][split partials]
+    size_t xpad_bytes, wpad_bytes;  // workspace: [X padded][W_a, W_b, W_c padded][split partials][X o X]
+    size_t part_bytes;
+    size_t xsq_bytes;               // T2 with 16-byte channel vectors: X o X formed once by a pre-pass
     size_t ws_bytes;
 };
 
@@ -198,8 +200,9 @@ FwdPlan plan_fwd(const Geom &g) {
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
     plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)3 * M * g.O * 4, p.slots, p.splits, p.sps);
-    p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes +
-                 (p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0);
+    p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0;
+    p.xsq_bytes = g.ne == NEURON_T2 && p.veck ? align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize()) : 0;
+    p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes + p.part_bytes + p.xsq_bytes;
     return p;
 }
 
@@ -385,6 +388,17 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     a.fd_c = make_fastdiv(C);
     a.fd_kw = make_fastdiv(g.KW);
     a.neuron = g.ne;
+    if (p.xsq_bytes) {
+        // T2: X o X once, instead of squaring every fragment in the MFMA loop
+        T *xsq = reinterpret_cast<T *>(wsb + p.xpad_bytes + 3 * p.wpad_bytes + p.part_bytes);
+        const long long n = (long long)g.N * g.H * g.W * C;
+        hipLaunchKernelGGL((qconv_square_kernel<T>), dim3(grid_1d(n / g.vec())), dim3(kThreads), 0, st,
+                           static_cast<const T *>(a.x), xsq, n);
+        const ql_status s0 = hip_status();
+        if (s0 != QL_OK) return s0;
+        a.x = xsq;
+        a.xsq = 1;
+    }
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     const int om = g.om();
     if (p.veck && om != OM_QUADRA) {
