@@ -62,6 +62,9 @@ def _load():
     lib.oracle_conv2d_dw_channel.argtypes = conv_geom + [_D] + w6 + [_D, _I] + [_D] * 6
     lib.oracle_conv2d_fwd_neuron.argtypes = [_I] + conv_geom + [_D] + w6 + [_D, _D, _D]
     lib.oracle_conv2d_bwd_neuron.argtypes = [_I] + conv_geom + [_D] + w6 + [_D] + [_D] * 7
+    dw_geom = [_I] * 11  # neuron, N, C, H, W, KH, KW, sh, sw, ph, pw
+    lib.oracle_dwconv2d_fwd.argtypes = dw_geom + [_D] + w6 + [_D, _D, _D]
+    lib.oracle_dwconv2d_bwd.argtypes = dw_geom + [_D] + w6 + [_D] + [_D] * 7
     lib.oracle_conv2d_out_size.argtypes = [_I] * 4
     lib.oracle_conv2d_out_size.restype = _I
     fc_geom = [_I] * 3
@@ -70,7 +73,7 @@ def _load():
     lib.oracle_linear_fwd_at.argtypes = fc_geom + [_D] + w6 + [ctypes.c_longlong, _L, _D, _D, _D]
     lib.oracle_linear_dx_rows.argtypes = fc_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
     lib.oracle_linear_dw_row.argtypes = fc_geom + [_D] + w6 + [_D, _I] + [_D] * 6
-    for f in ("oracle_conv2d_fwd_neuron", "oracle_conv2d_bwd_neuron", "oracle_conv2d_fwd", "oracle_conv2d_bwd", "oracle_conv2d_fwd_at", "oracle_conv2d_dx_at",
+    for f in ("oracle_dwconv2d_fwd", "oracle_dwconv2d_bwd", "oracle_conv2d_fwd_neuron", "oracle_conv2d_bwd_neuron", "oracle_conv2d_fwd", "oracle_conv2d_bwd", "oracle_conv2d_fwd_at", "oracle_conv2d_dx_at",
               "oracle_conv2d_dw_channel", "oracle_linear_fwd", "oracle_linear_bwd",
               "oracle_linear_fwd_at", "oracle_linear_dx_rows", "oracle_linear_dw_row"):
         getattr(lib, f).restype = None
@@ -294,6 +297,42 @@ def linear_bwd_neuron(neuron, x, wa, wb, wc, ba, bb, bc, gy):
                             np.asarray(gy).reshape(B, O, 1, 1))
     return {k: (v.reshape(B, I) if k == "dx" else (v.reshape(O, I) if k.startswith("dw") else v))
             for k, v in out.items()}
+
+
+def _dw_geom(neuron, x, w, stride, pad):
+    N, C, H, W = x.shape
+    C2, one, KH, KW = w.shape
+    assert C2 == C and one == 1, "depthwise weights are C x 1 x KH x KW"
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    return (int(neuron), N, C, H, W, KH, KW, sh, sw, ph, pw)
+
+
+def dwconv2d_fwd(neuron, x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, stride=1, pad=0):
+    """Depthwise quadratic convolution (groups = C), weights C x 1 x KH x KW: (Y, T_a, T_b), N x C x Ho x Wo."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc = map(_f64, (x, wa, wb, wc, ba, bb, bc))
+    g = _dw_geom(neuron, x, wa, stride, pad)
+    N, C = g[1], g[2]
+    Ho, Wo = out_size(g[3], g[5], g[7], g[9]), out_size(g[4], g[6], g[8], g[10])
+    y, ta, tb = np.empty((N, C, Ho, Wo)), np.zeros((N, C, Ho, Wo)), np.zeros((N, C, Ho, Wo))
+    lib.oracle_dwconv2d_fwd(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(y), _p(ta), _p(tb))
+    return y, ta, tb
+
+
+def dwconv2d_bwd(neuron, x, wa, wb, wc, ba, bb, bc, gy, stride=1, pad=0):
+    """Backward of the depthwise layer: dict dx and dw*/db* of the terms the type has."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    g = _dw_geom(neuron, x, wa, stride, pad)
+    nt = NEURON_TERMS[int(neuron)]
+    out = {"dx": np.empty_like(x)}
+    for kw, kb in [("dwa", "dba"), ("dwb", "dbb"), ("dwc", "dbc")][:nt]:
+        out[kw] = np.empty_like(wa)
+        out[kb] = np.empty(g[2])
+    lib.oracle_dwconv2d_bwd(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
+                            *[_p(out.get(k)) for k in ("dx", "dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
+    return out
 
 
 def num_threads() -> int:

@@ -358,6 +358,151 @@ void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int
 }
 
 /* ---------------------------------------------------------------------------
+ * Depthwise quadratic convolution (groups = C = O; section 4.2: the layer
+ * modules take the depth-wise setting of an ordinary convolution).  Each
+ * channel c has its own KH x KW filter per term, W_t[c, r, q], and
+ *   T_t[n,c,i,j] = b_t[c] + sum_{r,q} W_t[c,r,q] X[n, c, i*s-p+r, j*s-p+q]
+ * with the neuron type's Y as above (the shortcut of T4 + identity needs an
+ * unchanged map).  The backward is the same product rule per channel.
+ * ------------------------------------------------------------------------- */
+static double dw_term(int H, int W, int KH, int KW, int sh, int sw, int ph, int pw, const double *x,
+                      const double *w, const double *b, int C, int n, int c, int i, int j) {
+    double acc = b ? b[c] : 0.0;
+    for (int r = 0; r < KH; ++r) {
+        int ih = i * sh - ph + r;
+        if (ih < 0 || ih >= H) continue;
+        for (int q = 0; q < KW; ++q) {
+            int iw = j * sw - pw + q;
+            if (iw < 0 || iw >= W) continue;
+            acc += w[((size_t)c * KH + r) * KW + q] * x[IDX4(n, c, ih, iw, C, H, W)];
+        }
+    }
+    return acc;
+}
+
+void oracle_dwconv2d_fwd(int neuron, int N, int C, int H, int W, int KH, int KW, int sh, int sw, int ph, int pw,
+                         const double *x, const double *wa, const double *wb, const double *wc,
+                         const double *ba, const double *bb, const double *bc,
+                         double *y, double *ta, double *tb) {
+    int Ho = out_size(H, KH, sh, ph), Wo = out_size(W, KW, sw, pw);
+    if (Ho < 1 || Wo < 1) return;
+    if (neuron == 2 && (Ho != H || Wo != W)) return;
+    size_t nx = (size_t)N * C * H * W;
+    const double *xin = x;
+    double *x2 = NULL;
+    if (neuron == 4) {
+        x2 = (double *)malloc(nx * sizeof(double));
+        if (!x2) return;
+        for (size_t e = 0; e < nx; ++e) x2[e] = x[e] * x[e];
+        xin = x2;
+    }
+    long long total = (long long)N * C * Ho * Wo;
+#pragma omp parallel for schedule(static)
+    for (long long e = 0; e < total; ++e) {
+        int j = (int)(e % Wo), i = (int)((e / Wo) % Ho);
+        int c = (int)((e / ((long long)Wo * Ho)) % C), n = (int)(e / ((long long)Wo * Ho * C));
+        double Ta = dw_term(H, W, KH, KW, sh, sw, ph, pw, xin, wa, ba, C, n, c, i, j), Tb = 0.0, out;
+        if (neuron == 0 || neuron == 1 || neuron == 2)
+            Tb = dw_term(H, W, KH, KW, sh, sw, ph, pw, x, wb, bb, C, n, c, i, j);
+        if (neuron == 0) out = Ta * Tb + dw_term(H, W, KH, KW, sh, sw, ph, pw, x, wc, bc, C, n, c, i, j);
+        else if (neuron == 1) out = Ta * Tb;
+        else if (neuron == 2) out = Ta * Tb + x[IDX4(n, c, i, j, C, H, W)];
+        else if (neuron == 3) out = Ta * Ta;
+        else out = Ta;
+        if (y) y[e] = out;
+        if (ta) ta[e] = Ta;
+        if (tb) tb[e] = Tb;
+    }
+    free(x2);
+}
+
+void oracle_dwconv2d_bwd(int neuron, int N, int C, int H, int W, int KH, int KW, int sh, int sw, int ph, int pw,
+                         const double *x, const double *wa, const double *wb, const double *wc,
+                         const double *ba, const double *bb, const double *bc, const double *gy,
+                         double *dx, double *dwa, double *dwb, double *dwc,
+                         double *dba, double *dbb, double *dbc) {
+    int Ho = out_size(H, KH, sh, ph), Wo = out_size(W, KW, sw, pw);
+    if (Ho < 1 || Wo < 1) return;
+    if (neuron == 2 && (Ho != H || Wo != W)) return;
+    size_t P = (size_t)N * C * Ho * Wo, nx = (size_t)N * C * H * W;
+    int nterm = neuron == 0 ? 3 : (neuron <= 2 ? 2 : 1);
+    double *g3 = (double *)malloc(3 * P * sizeof(double));
+    double *ta = (double *)malloc(P * sizeof(double));
+    double *tb = (double *)malloc(P * sizeof(double));
+    double *xo = (double *)malloc(nx * sizeof(double));
+    if (!g3 || !ta || !tb || !xo) { free(g3); free(ta); free(tb); free(xo); return; }
+    oracle_dwconv2d_fwd(neuron, N, C, H, W, KH, KW, sh, sw, ph, pw, x, wa, wb, wc, ba, bb, bc, NULL, ta, tb);
+    for (size_t e = 0; e < P; ++e) {  /* the per-term output gradients (eq:SD and the types' product rule) */
+        if (nterm >= 2) {
+            g3[e] = gy[e] * tb[e];
+            g3[P + e] = gy[e] * ta[e];
+            g3[2 * P + e] = gy[e];
+        } else {
+            g3[e] = neuron == 3 ? 2.0 * gy[e] * ta[e] : gy[e];
+        }
+    }
+    for (size_t e = 0; e < nx; ++e) xo[e] = neuron == 4 ? x[e] * x[e] : x[e];
+    double *dwt[3] = {dwa, dwb, dwc};
+    double *dbt[3] = {dba, dbb, dbc};
+    const double *wt[3] = {wa, wb, wc};
+#pragma omp parallel for schedule(static)
+    for (int c = 0; c < C; ++c) {
+        for (int t = 0; t < nterm; ++t) {
+            const double *g = g3 + (size_t)t * P;
+            if (dbt[t]) {
+                double acc = 0.0;
+                for (int n = 0; n < N; ++n)
+                    for (int i = 0; i < Ho; ++i)
+                        for (int j = 0; j < Wo; ++j) acc += g[IDX4(n, c, i, j, C, Ho, Wo)];
+                dbt[t][c] = acc;
+            }
+            if (!dwt[t]) continue;
+            for (int r = 0; r < KH; ++r)
+                for (int q = 0; q < KW; ++q) {
+                    double acc = 0.0;
+                    for (int n = 0; n < N; ++n)
+                        for (int i = 0; i < Ho; ++i) {
+                            int ih = i * sh - ph + r;
+                            if (ih < 0 || ih >= H) continue;
+                            for (int j = 0; j < Wo; ++j) {
+                                int iw = j * sw - pw + q;
+                                if (iw < 0 || iw >= W) continue;
+                                acc += g[IDX4(n, c, i, j, C, Ho, Wo)] * xo[IDX4(n, c, ih, iw, C, H, W)];
+                            }
+                        }
+                    dwt[t][((size_t)c * KH + r) * KW + q] = acc;
+                }
+        }
+    }
+    if (dx) {
+#pragma omp parallel for schedule(static)
+        for (long long e = 0; e < (long long)nx; ++e) {
+            int w_ = (int)(e % W), h = (int)((e / W) % H);
+            int c = (int)((e / ((long long)W * H)) % C), n = (int)(e / ((long long)W * H * C));
+            double acc = 0.0;
+            for (int t = 0; t < nterm; ++t)
+                for (int r = 0; r < KH; ++r) {
+                    int hi = h + ph - r;
+                    if (hi < 0 || hi % sh) continue;
+                    int i = hi / sh;
+                    if (i >= Ho) continue;
+                    for (int q = 0; q < KW; ++q) {
+                        int wi = w_ + pw - q;
+                        if (wi < 0 || wi % sw) continue;
+                        int j = wi / sw;
+                        if (j >= Wo) continue;
+                        acc += g3[(size_t)t * P + IDX4(n, c, i, j, C, Ho, Wo)] * wt[t][((size_t)c * KH + r) * KW + q];
+                    }
+                }
+            if (neuron == 4) acc *= 2.0 * x[e];
+            if (neuron == 2) acc += gy[IDX4(n, c, h, w_, C, Ho, Wo)];
+            dx[e] = acc;
+        }
+    }
+    free(g3); free(ta); free(tb); free(xo);
+}
+
+/* ---------------------------------------------------------------------------
  * Sampled evaluation for full-size checks: the same definitions, evaluated
  * only at requested output positions.
  * ------------------------------------------------------------------------- */
