@@ -99,6 +99,10 @@ typedef struct {
     int pad_h, pad_w;       /* >= 0, symmetric zero padding */
     ql_dtype dtype;
     ql_neuron neuron;       /* QL_NEURON_QUADRA (0) unless set */
+    int groups;             /* 0 or 1: every output channel sees every input channel;
+                               C (with O == C): depthwise, each channel its own
+                               KH x KW filter per term, W_t (C,KH,KW,1), dW_t the same.
+                               Other group counts: QL_EUNSUPPORTED. */
 } ql_conv_desc;
 
 /* Geometry of a quadratic fully-connected layer. */

@@ -48,7 +48,8 @@ class QLError(RuntimeError):
 
 class ConvDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in
-                ("n", "c", "h", "w", "o", "kh", "kw", "stride_h", "stride_w", "pad_h", "pad_w", "dtype", "neuron")]
+                ("n", "c", "h", "w", "o", "kh", "kw", "stride_h", "stride_w", "pad_h", "pad_w", "dtype", "neuron",
+                 "groups")]
 
     @property
     def ho(self):
@@ -64,10 +65,12 @@ class LinearDesc(ctypes.Structure):
                 ("neuron", ctypes.c_int)]
 
 
-def conv_desc(n, c, h, w, o, kh, kw, stride=1, pad=0, dtype=QL_BF16, neuron=QL_NEURON_QUADRA) -> ConvDesc:
+def conv_desc(n, c, h, w, o, kh, kw, stride=1, pad=0, dtype=QL_BF16, neuron=QL_NEURON_QUADRA,
+              groups=1) -> ConvDesc:
+    """groups = c (with o == c) makes the layer depthwise: weights (c, kh, kw, 1)."""
     sh, sw = (stride, stride) if isinstance(stride, int) else stride
     ph, pw = (pad, pad) if isinstance(pad, int) else pad
-    return ConvDesc(n, c, h, w, o, kh, kw, sh, sw, ph, pw, dtype, neuron)
+    return ConvDesc(n, c, h, w, o, kh, kw, sh, sw, ph, pw, dtype, neuron, groups)
 
 
 def linear_desc(batch, inp, out, dtype=QL_BF16, neuron=QL_NEURON_QUADRA) -> LinearDesc:

@@ -13,6 +13,7 @@
 #include "qconv_bwd_data.h"
 #include "qconv_bwd_data_wide.h"
 #include "qconv_bwd_weight.h"
+#include "qconv_depthwise.h"
 #include "qconv_fwd.h"
 #include "qconv_generic.h"
 
@@ -67,6 +68,7 @@ struct Geom {
     int N, C, H, W, O, KH, KW, SH, SW, PH, PW, HO, WO;
     ql_dtype dt;
     int ne;  // neuron type (NEURON_*)
+    bool dw; // depthwise (groups == C == O)
     int om() const { return om_of_neuron(ne); }
     int terms() const { return om_terms(om()); }
     size_t esize() const { return dt == QL_BF16 ? 2 : 4; }
@@ -93,6 +95,10 @@ ql_status make_geom(const ql_conv_desc *d, Geom &g) {
     g.WO = (int)(ew / d->stride_w + 1);
     g.dt = d->dtype;
     g.ne = (int)d->neuron;
+    if (d->groups != 0 && d->groups != 1 && d->groups != d->c) return QL_EUNSUPPORTED;
+    g.dw = d->groups == d->c && d->c > 1;
+    if (g.dw && d->o != d->c) return QL_EINVAL;  // one output channel per group
+    if (g.dw && 3LL * d->kh * d->kw * kDwCB * 4 > 64 * 1024) return QL_EUNSUPPORTED;  // filters staged in LDS
     // the shortcut of T4 + identity adds input channel o at the same pixel
     if (g.ne == NEURON_T4I && (g.C != g.O || g.HO != g.H || g.WO != g.W)) return QL_EINVAL;
     const long long nx = (long long)g.N * g.H * g.W * g.C;
@@ -106,7 +112,7 @@ ql_status make_geom(const ql_conv_desc *d, Geom &g) {
 
 ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
     if (!d) return QL_EINVAL;
-    ql_conv_desc c{d->batch, d->in, 1, 1, d->out, 1, 1, 1, 1, 0, 0, d->dtype, d->neuron};
+    ql_conv_desc c{d->batch, d->in, 1, 1, d->out, 1, 1, 1, 1, 0, 0, d->dtype, d->neuron, 1};
     return make_geom(&c, g);
 }
 
@@ -715,6 +721,124 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     return hip_status();
 }
 
+// ---------------------------------------------------------------------------
+// Depthwise layers (groups == C == O): direct kernels of qconv_depthwise.h.
+// ---------------------------------------------------------------------------
+struct DwPlan {
+    int ct, tg;            // channel tiles of kDwCB, tap groups of 9
+    int splits, pps;       // weight gradient: pixel splits and pixels per split
+    size_t ws_dw, ws_db, ws_bytes;
+};
+
+DwPlan plan_dw(const Geom &g) {
+    DwPlan p{};
+    p.ct = cdiv(g.C, kDwCB);
+    const int taps = g.KH * g.KW;
+    p.tg = cdiv(taps, 9);
+    const long long M = (long long)g.N * g.HO * g.WO;
+    // about 8 workgroups per CU, each split at least 8 pixels per lane
+    p.splits = std::max(1, std::min(cdiv(8 * kNumCUs, (long long)p.ct * p.tg), cdiv(M, kDwPL * 8)));
+    p.pps = cdiv(M, p.splits);
+    p.splits = cdiv(M, p.pps);
+    if (p.splits > 1) {
+        p.ws_dw = align_up((size_t)p.splits * 3 * g.C * taps * sizeof(float));
+        p.ws_db = align_up((size_t)p.splits * 3 * g.C * sizeof(float));
+    }
+    p.ws_bytes = p.ws_dw + p.ws_db;
+    return p;
+}
+
+DwArgs dw_args(const Geom &g) {
+    DwArgs a{};
+    a.N = g.N; a.C = g.C; a.H = g.H; a.W = g.W; a.KH = g.KH; a.KW = g.KW;
+    a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
+    a.neuron = g.ne;
+    a.fd_howo = make_fastdiv(g.HO * g.WO);
+    a.fd_wo = make_fastdiv(g.WO);
+    a.fd_hw = make_fastdiv(g.H * g.W);
+    a.fd_w = make_fastdiv(g.W);
+    a.fd_sh = make_fastdiv(g.SH);
+    a.fd_sw = make_fastdiv(g.SW);
+    return a;
+}
+
+// dispatch a depthwise kernel template over (T, OM, V4)
+#define QL_DW_DISPATCH(KERNEL, EXTRA, GRID, SMEM)                                                              \
+    do {                                                                                                       \
+        const bool v4 = g.C % 4 == 0;                                                                          \
+        const int om = g.om();                                                                                 \
+        if (om == OM_QUADRA) {                                                                                 \
+            if (v4) hipLaunchKernelGGL((KERNEL<T, OM_QUADRA, true EXTRA>), GRID, dim3(kThreads), SMEM, st, a);    \
+            else hipLaunchKernelGGL((KERNEL<T, OM_QUADRA, false EXTRA>), GRID, dim3(kThreads), SMEM, st, a);      \
+        } else if (om == OM_PAIR) {                                                                            \
+            if (v4) hipLaunchKernelGGL((KERNEL<T, OM_PAIR, true EXTRA>), GRID, dim3(kThreads), SMEM, st, a);      \
+            else hipLaunchKernelGGL((KERNEL<T, OM_PAIR, false EXTRA>), GRID, dim3(kThreads), SMEM, st, a);        \
+        } else if (om == OM_SQUARE) {                                                                          \
+            if (v4) hipLaunchKernelGGL((KERNEL<T, OM_SQUARE, true EXTRA>), GRID, dim3(kThreads), SMEM, st, a);    \
+            else hipLaunchKernelGGL((KERNEL<T, OM_SQUARE, false EXTRA>), GRID, dim3(kThreads), SMEM, st, a);      \
+        } else {                                                                                               \
+            if (v4) hipLaunchKernelGGL((KERNEL<T, OM_SQIN, true EXTRA>), GRID, dim3(kThreads), SMEM, st, a);      \
+            else hipLaunchKernelGGL((KERNEL<T, OM_SQIN, false EXTRA>), GRID, dim3(kThreads), SMEM, st, a);        \
+        }                                                                                                      \
+    } while (0)
+#define QL_NOEXTRA
+#define QL_TAPS9 , 9
+
+template <typename T>
+ql_status launch_dw_fwd(const Geom &g, const void *x, const void *const *w, const float *const *b, void *y,
+                        void *ta, void *tb, hipStream_t st) {
+    DwArgs a = dw_args(g);
+    a.x = x;
+    for (int t = 0; t < 3; ++t) { a.w[t] = w[t]; a.bias[t] = b[t]; }
+    a.y = y; a.yta = ta; a.ytb = tb;
+    a.M = g.N * g.HO * g.WO;
+    const int ct = cdiv(g.C, kDwCB);
+    const dim3 grid(std::max(1, std::min(cdiv(a.M, kDwPL), cdiv(16 * kNumCUs, ct))), ct);
+    const size_t smem = (size_t)g.terms() * g.KH * g.KW * kDwCB * sizeof(float);
+    QL_DW_DISPATCH(qconv_dw_fwd_kernel, QL_NOEXTRA, grid, smem);
+    return hip_status();
+}
+
+template <typename T>
+ql_status launch_dw_bwd_data(const Geom &g, const void *gy, const void *ta, const void *tb, const void *const *w,
+                             void *dx, hipStream_t st) {
+    DwArgs a = dw_args(g);
+    a.gy = gy; a.ta = ta; a.tb = tb;
+    for (int t = 0; t < 3; ++t) a.w[t] = w[t];
+    a.dx = dx;
+    a.M = g.N * g.H * g.W;
+    const int ct = cdiv(g.C, kDwCB);
+    const dim3 grid(std::max(1, std::min(cdiv(a.M, kDwPL), cdiv(16 * kNumCUs, ct))), ct);
+    const size_t smem = (size_t)g.terms() * g.KH * g.KW * kDwCB * sizeof(float);
+    QL_DW_DISPATCH(qconv_dw_bwd_data_kernel, QL_NOEXTRA, grid, smem);
+    return hip_status();
+}
+
+template <typename T>
+ql_status launch_dw_bwd_weight(const Geom &g, const DwPlan &p, const void *x, const void *gy, const void *ta,
+                               const void *tb, float *const *dw, float *const *db, void *ws, hipStream_t st) {
+    DwArgs a = dw_args(g);
+    a.x = x; a.gy = gy; a.ta = ta; a.tb = tb;
+    for (int t = 0; t < 3; ++t) { a.dw[t] = dw[t]; a.db[t] = db[t]; }
+    a.ws_dw = static_cast<float *>(ws);
+    a.ws_db = reinterpret_cast<float *>(static_cast<char *>(ws) + p.ws_dw);
+    a.M = g.N * g.HO * g.WO;
+    a.splits = p.splits;
+    a.px_per_split = p.pps;
+    const dim3 grid(p.splits, p.ct, p.tg);
+    QL_DW_DISPATCH(qconv_dw_bwd_weight_kernel, QL_TAPS9, grid, 0);
+    ql_status s = hip_status();
+    if (s != QL_OK || p.splits == 1) return s;
+    const int taps = g.KH * g.KW, nt = g.terms();
+    const long long total = (long long)nt * g.C * taps + (db[0] ? (long long)nt * g.C : 0LL);
+    hipLaunchKernelGGL(qconv_dw_reduce_kernel, dim3(grid_1d(total)), dim3(kThreads), 0, st, a.ws_dw, a.ws_db,
+                       p.splits, g.C, taps, nt, dw[0], dw[1], dw[2], db[0], db[1], db[2], db[0] != nullptr);
+    return hip_status();
+}
+#undef QL_DW_DISPATCH
+#undef QL_NOEXTRA
+#undef QL_TAPS9
+
 ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *wb, const void *wc, const float *ba,
                      const float *bb, const float *bc, void *y, void *ta, void *tb, void *ws, size_t ws_bytes,
                      void *stream) {
@@ -729,6 +853,13 @@ ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *w
     const void *ptrs[] = {x, wa, wb, wc, ba, bb, bc, y, ta, tb};
     for (const void *q : ptrs)
         if (q && !aligned16(q)) return QL_EINVAL;
+    if (g.dw) {
+        const void *w[3] = {wa, wb, wc};
+        const float *b[3] = {ba, bb, bc};
+        hipStream_t st = static_cast<hipStream_t>(stream);
+        return g.dt == QL_BF16 ? launch_dw_fwd<uint16_t>(g, x, w, b, y, ta, tb, st)
+                               : launch_dw_fwd<float>(g, x, w, b, y, ta, tb, st);
+    }
     const FwdPlan p = plan_fwd(g);
     if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
     if (ws && !aligned16(ws)) return QL_EINVAL;
@@ -747,6 +878,12 @@ ql_status bwd_data_common(const Geom &g, const void *gy, const void *ta, const v
     const void *ptrs[] = {gy, ta, tb, wa, wb, wc, dx};
     for (const void *q : ptrs)
         if (q && !aligned16(q)) return QL_EINVAL;
+    if (g.dw) {
+        const void *w[3] = {wa, wb, wc};
+        hipStream_t st = static_cast<hipStream_t>(stream);
+        return g.dt == QL_BF16 ? launch_dw_bwd_data<uint16_t>(g, gy, ta, tb, w, dx, st)
+                               : launch_dw_bwd_data<float>(g, gy, ta, tb, w, dx, st);
+    }
     const BwdDataPlan p = plan_bwd_data(g);
     if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
     if (ws && !aligned16(ws)) return QL_EINVAL;
@@ -771,6 +908,16 @@ ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const 
     const void *ptrs[] = {x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc};
     for (const void *q : ptrs)
         if (q && !aligned16(q)) return QL_EINVAL;
+    if (g.dw) {
+        const DwPlan p = plan_dw(g);
+        if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
+        if (ws && !aligned16(ws)) return QL_EINVAL;
+        float *const dw[3] = {dwa, dwb, dwc};
+        float *const db[3] = {dba, dbb, dbc};
+        hipStream_t st = static_cast<hipStream_t>(stream);
+        return g.dt == QL_BF16 ? launch_dw_bwd_weight<uint16_t>(g, p, x, gy, ta, tb, dw, db, ws, st)
+                               : launch_dw_bwd_weight<float>(g, p, x, gy, ta, tb, dw, db, ws, st);
+    }
     const BwdWeightPlan p = plan_bwd_weight(g);
     if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
     if (ws && !aligned16(ws)) return QL_EINVAL;
@@ -800,6 +947,7 @@ int qlayer_version(void) { return 100; }
 size_t qlayer_conv2d_fwd_workspace_size(const ql_conv_desc *desc) {
     Geom g;
     if (make_geom(desc, g) != QL_OK) return 0;
+    if (g.dw) return 0;
     return plan_fwd(g).ws_bytes;
 }
 
@@ -815,6 +963,7 @@ ql_status qlayer_conv2d_fwd(const ql_conv_desc *desc, const void *x, const void 
 size_t qlayer_conv2d_bwd_data_workspace_size(const ql_conv_desc *desc) {
     Geom g;
     if (make_geom(desc, g) != QL_OK) return 0;
+    if (g.dw) return 0;
     return plan_bwd_data(g).ws_bytes;
 }
 
@@ -830,6 +979,7 @@ ql_status qlayer_conv2d_bwd_data(const ql_conv_desc *desc, const void *gy, const
 size_t qlayer_conv2d_bwd_weight_workspace_size(const ql_conv_desc *desc) {
     Geom g;
     if (make_geom(desc, g) != QL_OK) return 0;
+    if (g.dw) return plan_dw(g).ws_bytes;
     return plan_bwd_weight(g).ws_bytes;
 }
 

@@ -196,6 +196,32 @@ def random_conv_case(seed, N, C, H, W, O, KH, KW, stride=1, pad=0, bf16=False, w
     return out
 
 
+def random_dwconv_case(seed, N, C, H, W, KH, KW, stride=1, pad=0, bf16=False, w_var=None, b_var=0.01):
+    """Seeded inputs of a depthwise geometry (groups = C, one filter per channel).
+
+    X ~ N(0,1), W_t ~ N(0, w_var) (default 1/(KH*KW)) of shape C x 1 x KH x KW,
+    b_t ~ N(0, b_var), G ~ N(0,1).
+    """
+    wv = w_var if w_var is not None else 1.0 / (KH * KW)
+    Ho = (H + 2 * pad - KH) // stride + 1
+    Wo = (W + 2 * pad - KW) // stride + 1
+    s = list(seed) if isinstance(seed, (list, tuple)) else [seed]
+    out = {
+        "x": _normal(s + [X_ID], (N, C, H, W), 1.0),
+        "wa": _normal(s + [WA_ID], (C, 1, KH, KW), np.sqrt(wv)),
+        "wb": _normal(s + [WB_ID], (C, 1, KH, KW), np.sqrt(wv)),
+        "wc": _normal(s + [WC_ID], (C, 1, KH, KW), np.sqrt(wv)),
+        "ba": _normal(s + [BA_ID], (C,), np.sqrt(b_var)),
+        "bb": _normal(s + [BB_ID], (C,), np.sqrt(b_var)),
+        "bc": _normal(s + [BC_ID], (C,), np.sqrt(b_var)),
+        "gy": _normal(s + [G_ID], (N, C, Ho, Wo), 1.0),
+    }
+    if bf16:
+        for k in ("x", "wa", "wb", "wc", "gy"):
+            out[k] = round_bf16(out[k])
+    return out
+
+
 def random_dense_case(seed, B, I, O, bf16=False, w_var=None, b_var=0.01):
     """Seeded inputs of an arbitrary dense geometry: X ~ N(0,1), W_t ~ N(0, 1/I), b_t, G ~ N(0,1)."""
     wv = w_var if w_var is not None else 1.0 / I

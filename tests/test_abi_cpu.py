@@ -197,3 +197,28 @@ def test_neuron_type_validation(L):
     for n in range(5):
         d = ql.conv_desc(4, 256, 4, 4, 256, 3, 3, 1, 1, ql.QL_BF16, n)
         assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d)) > 0
+
+
+def test_depthwise_validation(L):
+    # groups: 1 (or 0) is dense, C with O == C is depthwise, anything else is not supported
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, 0, groups=2)) == QL_EUNSUPPORTED
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 32, 3, 3, 1, 1, ql.QL_F32, 0, groups=16)) == QL_EINVAL
+    # the filters of a channel slice are staged in 64 KiB of LDS: 15 x 15 is too large, 13 x 13 fits
+    assert _fwd(L, ql.conv_desc(2, 16, 16, 16, 16, 15, 15, 1, 7, ql.QL_F32, 0, groups=16)) == QL_EUNSUPPORTED
+    big = ql.conv_desc(2, 16, 16, 16, 16, 13, 13, 1, 6, ql.QL_F32, 0, groups=16)
+    assert L.qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(big)) >= 0
+    assert _fwd(L, big, wb=None) == QL_EINVAL  # the pointer checks of the dense path apply
+    # the forward and input gradient need no workspace; the weight gradient's
+    # split partials grow with the pixel count
+    for n in range(5):
+        d = ql.conv_desc(128, 64, 56, 56, 64, 3, 3, 1, 1, ql.QL_BF16, n, groups=64)
+        assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d)) == 0
+        assert L.qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(d)) == 0
+        nt = ql.NEURON_TERMS[n]
+        ws = L.qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(d))
+        assert ws >= 2 * nt * 64 * (9 + 1) * 4
+    tiny = ql.conv_desc(1, 8, 4, 4, 8, 3, 3, 1, 1, ql.QL_F32, 0, groups=8)
+    assert L.qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(tiny)) == 0  # one split writes dW directly
+    # a depthwise weight gradient with too small a workspace
+    assert L.qlayer_conv2d_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None,
+                                      None, FAKE, 16, None) == QL_EWORKSPACE

@@ -1,0 +1,138 @@
+"""Depthwise quadratic convolution (groups = C = O; the depth-wise setting of
+the layer modules, arXiv 2204.01701 section 4.2) through the C ABI against
+the fp64 oracle, element by element (normwise relative error), for every
+neuron type in fp32 and bf16: forward Y and saved maps, input gradient,
+weight and bias gradients."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+import qlh  # noqa: E402
+import paper_2204_01701_amd as ql  # noqa: E402
+
+DEV = qlh.DEV
+QUADRA, T4, T4I, T3, T2 = (ql.QL_NEURON_QUADRA, ql.QL_NEURON_T4, ql.QL_NEURON_T4_IDENTITY, ql.QL_NEURON_T3,
+                           ql.QL_NEURON_T2)
+NAMES = {QUADRA: "quadra", T4: "T4", T4I: "T4I", T3: "T3", T2: "T2"}
+TERMS = ql.NEURON_TERMS
+
+# N, C, H, W, K, stride, pad; same=True where the map keeps its size (the
+# shortcut of T4 + identity needs it).
+SHAPES = [
+    ((2, 32, 9, 7, 3, 1, 1), True),      # one channel slice, ragged pixel lanes
+    ((2, 72, 10, 9, 3, 2, 1), False),    # stride 2, ragged channel slice (72 = 2 * 32 + 8)
+    ((1, 13, 8, 6, 3, 1, 1), True),      # channels not a multiple of 4 (scalar channel path)
+    ((2, 48, 12, 12, 5, 1, 2), True),    # 5 x 5: three tap groups in the weight gradient
+    ((4, 256, 4, 4, 3, 1, 1), True),     # many channel slices, few pixels
+    ((3, 64, 20, 20, 3, 1, 1), True),    # several pixel splits and their reduction
+    ((2, 6, 7, 7, 7, 1, 3), True),       # 7 x 7 filters, six channels
+    ((2, 40, 11, 11, 3, 2, 0), False),   # stride 2 without padding
+]
+CASES = [(n, sh) for n in (QUADRA, T4, T4I, T3, T2) for sh, same in SHAPES if n != T4I or same]
+IDS = [f"{NAMES[n]}-{'x'.join(map(str, sh))}" for n, sh in CASES]
+
+
+def run_dw(neuron, inp, s, p, bf16, with_bias=True):
+    """Forward (saving the maps the type keeps), input and weight gradients on the GPU."""
+    N, C, H, W = inp["x"].shape
+    K = inp["wa"].shape[2]
+    nt = TERMS[neuron]
+    d = ql.conv_desc(N, C, H, W, C, K, K, s, p, qlh.qdtype(bf16), neuron, groups=C)
+    dt = qlh.tdtype(bf16)
+    x = qlh.nchw_to_dev(inp["x"], bf16)
+    w = [qlh.oihw_to_dev(inp[k], bf16) if i < nt else None for i, k in enumerate(("wa", "wb", "wc"))]
+    b = [qlh.vec_to_dev(inp[k]) if i < nt and with_bias else None for i, k in enumerate(("ba", "bb", "bc"))]
+    y = torch.empty((N, d.ho, d.wo, C), device=DEV, dtype=dt)
+    ta = torch.empty_like(y) if neuron != T2 else None
+    tb = torch.empty_like(y) if nt >= 2 else None
+    ql.qlayer_conv2d_fwd(d, x, *w, *b, y, ta, tb)
+    gy = qlh.nchw_to_dev(inp["gy"], bf16)
+    dx = torch.empty_like(x)
+    ql.qlayer_conv2d_bwd_data(d, gy, x if neuron == T2 else ta, tb, *w, dx)
+    dw = [torch.empty((C, K, K, 1), device=DEV, dtype=torch.float32) if i < nt else None for i in range(3)]
+    db = [torch.empty(C, device=DEV, dtype=torch.float32) if i < nt and with_bias else None for i in range(3)]
+    ql.qlayer_conv2d_bwd_weight(d, x, gy, ta, tb, *dw, *db)
+    torch.cuda.synchronize()
+    out = {"y": y, "dx": dx}
+    if ta is not None:
+        out["ta"] = ta
+    if tb is not None:
+        out["tb"] = tb
+    for i, (kw, kb) in enumerate((("dwa", "dba"), ("dwb", "dbb"), ("dwc", "dbc"))[:nt]):
+        out[kw] = dw[i]
+        if with_bias:
+            out[kb] = db[i]
+    return qlh.conv_to_np(out)
+
+
+def oracle_dw(neuron, inp, s, p, with_bias=True):
+    nt = TERMS[neuron]
+    w = [inp[k] if i < nt else None for i, k in enumerate(("wa", "wb", "wc"))]
+    b = [inp[k] if i < nt and with_bias else None for i, k in enumerate(("ba", "bb", "bc"))]
+    y, ta, tb = oracle.dwconv2d_fwd(neuron, inp["x"], *w, *b, stride=s, pad=p)
+    ref = oracle.dwconv2d_bwd(neuron, inp["x"], *w, *b, inp["gy"], stride=s, pad=p)
+    ref["y"] = y
+    if neuron != T2:
+        ref["ta"] = ta
+    if nt >= 2:
+        ref["tb"] = tb
+    if not with_bias:
+        for k in ("dba", "dbb", "dbc"):
+            ref.pop(k, None)
+    return ref
+
+
+def check(got, ref, bf16):
+    assert sorted(got) == sorted(ref)
+    for k in ref:
+        e = qlh.relerr(got[k], ref[k])
+        assert e <= qlh.tol(bf16, k not in ("y", "ta", "tb")), f"{k}: normwise relative error {e:.3e}"
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("neuron,shape", CASES, ids=IDS)
+def test_depthwise_matches_oracle(neuron, shape, bf16):
+    N, C, H, W, K, s, p = shape
+    print(f"depthwise {NAMES[neuron]} shape {shape} bf16={bf16}", flush=True)
+    inp = synth.random_dwconv_case([600, neuron] + list(shape), N, C, H, W, K, K, s, p, bf16=bf16)
+    check(run_dw(neuron, inp, s, p, bf16), oracle_dw(neuron, inp, s, p), bf16)
+
+
+@pytest.mark.parametrize("neuron", [QUADRA, T3, T2], ids=[NAMES[n] for n in (QUADRA, T3, T2)])
+def test_depthwise_without_bias(neuron):
+    shape = (2, 36, 9, 9, 3, 1, 1)
+    N, C, H, W, K, s, p = shape
+    print(f"depthwise without bias {NAMES[neuron]} shape {shape}", flush=True)
+    inp = synth.random_dwconv_case([601, neuron], N, C, H, W, K, K, s, p)
+    check(run_dw(neuron, inp, s, p, False, with_bias=False), oracle_dw(neuron, inp, s, p, with_bias=False), False)
+
+
+def test_depthwise_matches_library_grouped_conv():
+    """The forward maps against PyTorch's own grouped convolution on the GPU (fp32)."""
+    N, C, H, W, K = 2, 64, 14, 14, 3
+    print("depthwise vs torch grouped conv", flush=True)
+    inp = synth.random_dwconv_case([602], N, C, H, W, K, K, 1, 1)
+    got = run_dw(QUADRA, inp, 1, 1, False)
+    x = torch.from_numpy(inp["x"]).to(DEV)
+    ts = [torch.nn.functional.conv2d(x, torch.from_numpy(inp[w]).to(DEV), torch.from_numpy(inp[b]).to(DEV),
+                                     padding=1, groups=C) for w, b in (("wa", "ba"), ("wb", "bb"), ("wc", "bc"))]
+    ref = (ts[0] * ts[1] + ts[2]).double().cpu().numpy()
+    assert qlh.relerr(got["y"], ref) <= 1e-5
+    assert qlh.relerr(got["ta"], ts[0].double().cpu().numpy()) <= 1e-5
+
+
+def test_depthwise_repeat_is_bitwise_stable():
+    """Fixed summation order: two runs of every entry point give identical bits."""
+    shape = (4, 96, 16, 16, 3, 1, 1)
+    N, C, H, W, K, s, p = shape
+    print(f"depthwise repeat {shape}", flush=True)
+    inp = synth.random_dwconv_case([603], N, C, H, W, K, K, s, p, bf16=True)
+    a = run_dw(QUADRA, inp, s, p, True)
+    b = run_dw(QUADRA, inp, s, p, True)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
