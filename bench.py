@@ -56,7 +56,7 @@ def parse():
 class Layer:
     """Device tensors and call wrappers of one quadratic conv layer."""
 
-    def __init__(self, ql, torch, L, cfg_id, layer_id, dev, bf16=True, neuron=0):
+    def __init__(self, ql, torch, L, cfg_id, layer_id, dev, bf16=True, neuron=0, depthwise=False):
         import numpy as np
         import synth
 
@@ -65,13 +65,18 @@ class Layer:
         self.neuron = neuron
         nt = ql.NEURON_TERMS[neuron]
         dt = torch.bfloat16 if bf16 else torch.float32
-        inp = synth.conv_inputs(cfg_id, layer_id, L, bf16=bf16)
+        if depthwise:  # groups = C = O: one KH x KW filter per channel and term
+            inp = synth.random_dwconv_case([cfg_id, layer_id], L.n, L.c, L.h, L.w, L.k, L.k, L.stride, L.pad,
+                                           bf16=bf16)
+        else:
+            inp = synth.conv_inputs(cfg_id, layer_id, L, bf16=bf16)
+        cw = 1 if depthwise else L.c
 
         def nhwc(a):
             return torch.from_numpy(np.ascontiguousarray(a)).permute(0, 2, 3, 1).contiguous().to(dev, dt)
 
         self.desc = ql.conv_desc(L.n, L.c, L.h, L.w, L.o, L.k, L.k, L.stride, L.pad,
-                                 ql.QL_BF16 if bf16 else ql.QL_F32, neuron)
+                                 ql.QL_BF16 if bf16 else ql.QL_F32, neuron, groups=L.c if depthwise else 1)
         self.x = nhwc(inp["x"])
         self.w = [nhwc(inp[k]) if i < nt else None for i, k in enumerate(("wa", "wb", "wc"))]
         self.b = [torch.from_numpy(inp[k]).to(dev) if i < nt else None for i, k in enumerate(("ba", "bb", "bc"))]
@@ -81,7 +86,7 @@ class Layer:
         self.ta = torch.empty_like(self.y) if neuron != ql.QL_NEURON_T2 else None
         self.tb = torch.empty_like(self.y) if nt >= 2 else None
         self.dx = torch.empty_like(self.x)
-        self.dw = [torch.empty((L.o, L.k, L.k, L.c), device=dev, dtype=torch.float32) if i < nt else None
+        self.dw = [torch.empty((L.o, L.k, L.k, cw), device=dev, dtype=torch.float32) if i < nt else None
                    for i in range(3)]
         self.db = [torch.empty(L.o, device=dev, dtype=torch.float32) if i < nt else None for i in range(3)]
         # forward and input gradient share one workspace (same stream); the weight
@@ -533,6 +538,7 @@ def extra_workloads(ql, torch, dev, stream, reps=10):
         "bwd_tflops": round(6 * u / (fam_ms["bwd"] / fam_n["bwd"] * 1e-3) / 1e12, 1),
         "fwd_bwd_tflops": round(9 * u / (ms * 1e-3) / 1e12, 1)}
     out["neuron_types"] = neuron_types(ql, torch, dev, stream, reps)
+    out["depthwise"] = depthwise(ql, torch, dev, stream, reps)
     out["hybrid_bp_memory"] = hybrid_bp_memory(torch, dev)
     return out
 
@@ -559,6 +565,64 @@ def neuron_types(ql, torch, dev, stream, reps=10):
         r["fwd_bwd_tflops"] = round(3 * nt * u / (ms * 1e-3) / 1e12, 1)
         res[name] = r
         del ly
+    return res
+
+
+def dw_bytes(L, fam, esize=2, nterms=3):
+    """Algorithmic HBM bytes of one pass of a depthwise layer of the proposed
+    neuron: every input and output tensor once (X, the maps Y / T_a / T_b or G /
+    T_a / T_b, dX; the fp32 weight and bias gradients), nothing re-read."""
+    X = L.n * L.h * L.w * L.c
+    P = L.n * L.ho * L.wo * L.o
+    Wt = nterms * L.c * L.k * L.k
+    if fam == "fwd":
+        return esize * (X + 3 * P + Wt) + 4 * nterms * L.c
+    if fam == "bwd_data":
+        return esize * (3 * P + X + Wt)
+    return esize * (X + 3 * P) + 4 * (Wt + nterms * L.c)
+
+
+def depthwise(ql, torch, dev, stream, reps=10):
+    """Depthwise quadratic layers (groups = C, the pair layers of MobileNet-V1,
+    section 4.2 and Table 3), bf16, the proposed neuron: the 13 depthwise /
+    pointwise pairs of a CIFAR MobileNet-V1 at batch 128 (summed over the
+    layers), and one large depthwise layer (N=64, C=256, 56x56, 3x3) where the
+    direct kernels meet the HBM roofline; each pass timed separately."""
+    import synth
+
+    fams = ("fwd", "bwd_data", "bwd_weight")
+    res = {}
+    pairs = synth.mobilenet_v1_pairs(128)
+    dws = [Layer(ql, torch, d, 7, i, dev, depthwise=True) for i, (d, _) in enumerate(pairs)]
+    pws = [Layer(ql, torch, p, 8, i, dev) for i, (_, p) in enumerate(pairs)]
+    calls = [((f, "dw", i), getattr(ly, f)) for i, ly in enumerate(dws) for f in fams]
+    calls += [((f, "pw", i), getattr(ly, f)) for i, ly in enumerate(pws) for f in fams]
+    ms, _, fam_ms, fam_n = time_calls(torch, calls, reps, 3, stream)
+    r = {"shape": "CIFAR MobileNet-V1, batch 128, 13 pairs of 3x3 depthwise + 1x1 pointwise, bf16",
+         "pair_step_us": round(ms * 1e3, 1)}
+    for kind, lys in (("dw", dws), ("pw", pws)):
+        for f in fams:
+            t = sum(fam_ms[(f, kind, i)] / fam_n[(f, kind, i)] for i in range(len(lys)))
+            r[f"{kind}_{f}_us"] = round(t * 1e3, 1)
+            if kind == "dw":
+                r[f"{kind}_{f}_gbs"] = round(sum(dw_bytes(ly.L, f) for ly in lys) / (t * 1e-3) / 1e9, 1)
+            else:
+                r[f"{kind}_{f}_tflops"] = round(3 * sum(unit_flops(ly.L) for ly in lys) / (t * 1e-3) / 1e12, 1)
+    res["mobilenet_v1_cifar_b128"] = r
+    del dws, pws, calls
+
+    L = synth.ConvLayer(n=64, c=256, h=56, w=56, o=256, k=3, stride=1, pad=1)
+    ly = Layer(ql, torch, L, 9, 0, dev, depthwise=True)
+    calls = [(f, getattr(ly, f)) for f in fams]
+    ms, _, fam_ms, fam_n = time_calls(torch, calls, reps, 3, stream)
+    r = {"shape": "N=64 C=256 56x56, 3x3 depthwise, bf16", "peak_gbs": HBM_PEAK_GBS}
+    for f in fams:
+        t = fam_ms[f] / fam_n[f]
+        gbs = dw_bytes(L, f) / (t * 1e-3) / 1e9
+        r[f"{f}_us"] = round(t * 1e3, 1)
+        r[f"{f}_gbs"] = round(gbs, 1)
+        r[f"{f}_frac"] = round(gbs / HBM_PEAK_GBS, 3)
+    res["large_dw"] = r
     return res
 
 

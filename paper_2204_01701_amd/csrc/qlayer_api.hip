@@ -723,46 +723,135 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
 
 // ---------------------------------------------------------------------------
 // Depthwise layers (groups == C == O): direct kernels of qconv_depthwise.h.
+// 3 x 3 filters at stride 1 or 2 take the column kernels (the input gradient
+// at stride 2 the gathering one); other shapes take the generic kernels.
 // ---------------------------------------------------------------------------
+// Rows per thread of the column kernels and whether they prefetch the next
+// column (chosen by measurement on the N=64, C=256, 56x56 layer: the
+// configurations that fit the registers without spilling).
+constexpr int kDwRowsFwd = 4, kDwRowsBd = 4, kDwRowsBw = 2;
+
 struct DwPlan {
-    int ct, tg;            // channel tiles of kDwCB, tap groups of 9
-    int splits, pps;       // weight gradient: pixel splits and pixels per split
-    size_t ws_dw, ws_db, ws_bytes;
+    bool fast;             // 3 x 3 kernels for this pass
+    bool col;              // column kernel (else the gathering input-gradient kernel)
+    int V;                 // channels per thread (8 or 4)
+    bool vec;              // C % V == 0: vector loads
+    int lanes, lsh, tiles; // channel lanes per pixel, log2, channel slices
+    int R;                 // column kernels: rows per thread
+    long long items;       // work items: columns, or input pixels for the gathering kernel
+    int ng, iwid;          // column kernels: row groups per image, columns per row
+    int ct, tg;            // generic kernels: channel tiles of kDwCB, tap groups of 9
+    int splits, pps;       // weight gradient: splits and work items per split
+    int grid;              // 3 x 3 forward / input gradient: workgroups (tiles x blocks per slice)
+    size_t ws_bytes;
 };
 
-DwPlan plan_dw(const Geom &g) {
+int dw_lanes(int C, int V) {
+    int l = 1;
+    while (l < 8 && l * V < C) l *= 2;
+    return l;
+}
+
+// pass: 0 forward, 1 input gradient, 2 weight gradient
+DwPlan plan_dw(const Geom &g, int pass) {
     DwPlan p{};
-    p.ct = cdiv(g.C, kDwCB);
     const int taps = g.KH * g.KW;
+    // (the 3 x 3 kernels address each tensor with 32-bit buffer offsets)
+    const long long xbytes = (long long)g.N * g.H * g.W * g.C * g.esize();
+    const long long pbytes = (long long)g.N * g.HO * g.WO * g.C * g.esize();
+    p.fast = g.KH == 3 && g.KW == 3 && g.SH == g.SW && g.SH <= 2 && xbytes < (1LL << 31) && pbytes < (1LL << 31);
+    p.col = p.fast && (pass != 1 || g.SH == 1);
+    // bf16 channel vectors: 16 bytes for the gathering input gradient, else 8
+    // (the column kernels' registers; the weight gradient's 27 V accumulators)
+    p.V = (g.dt == QL_BF16 && g.C % 8 == 0 && pass == 1 && !p.col) ? 8 : 4;
+    p.vec = g.C % p.V == 0;
+    p.lanes = dw_lanes(g.C, p.V);
+    p.lsh = p.lanes == 1 ? 0 : (p.lanes == 2 ? 1 : (p.lanes == 4 ? 2 : 3));
+    p.tiles = cdiv(g.C, p.lanes * p.V);
+    p.ct = cdiv(g.C, kDwCB);
     p.tg = cdiv(taps, 9);
-    const long long M = (long long)g.N * g.HO * g.WO;
-    // about 8 workgroups per CU, each split at least 8 pixels per lane
-    p.splits = std::max(1, std::min(cdiv(8 * kNumCUs, (long long)p.ct * p.tg), cdiv(M, kDwPL * 8)));
-    p.pps = cdiv(M, p.splits);
-    p.splits = cdiv(M, p.pps);
-    if (p.splits > 1) {
-        p.ws_dw = align_up((size_t)p.splits * 3 * g.C * taps * sizeof(float));
-        p.ws_db = align_up((size_t)p.splits * 3 * g.C * sizeof(float));
+    p.R = pass == 0 ? kDwRowsFwd : (pass == 1 ? kDwRowsBd : kDwRowsBw);
+    const int rows = pass == 1 ? g.H : g.HO;
+    p.iwid = pass == 1 ? g.W : g.WO;
+    p.ng = cdiv(rows, p.R);
+    p.items = p.col ? (long long)g.N * p.ng * p.iwid : (long long)g.N * (pass == 1 ? g.H * g.W : g.HO * g.WO);
+    const int PL = kThreads / p.lanes;
+    if (pass != 2) {
+        const int chunks = cdiv(p.items, PL);
+        const int target = env_override("QLAYER_DW_BLOCKS", 2 * kNumCUs);
+        p.grid = p.fast ? std::max(1, std::min(chunks, cdiv(target, p.tiles))) * p.tiles : 0;
+        return p;
     }
-    p.ws_bytes = p.ws_dw + p.ws_db;
+    // weight gradient: about 2 workgroups per CU, at least 4 items per lane and split
+    const long long blocks_per_split = p.fast ? p.tiles : (long long)p.ct * p.tg;
+    const int lanes_px = p.fast ? PL : kDwPL;
+    p.splits = std::max(1, std::min(cdiv(env_override("QLAYER_DW_BW_BLOCKS", 2 * kNumCUs), blocks_per_split),
+                                    cdiv(p.items, (long long)lanes_px * 4)));
+    p.pps = cdiv(p.items, p.splits);
+    p.splits = cdiv(p.items, p.pps);
+    if (p.splits > 1) p.ws_bytes = align_up((size_t)p.splits * 3 * g.C * (taps + 1) * sizeof(float));
     return p;
 }
 
-DwArgs dw_args(const Geom &g) {
+DwArgs dw_args(const Geom &g, const DwPlan &p) {
     DwArgs a{};
     a.N = g.N; a.C = g.C; a.H = g.H; a.W = g.W; a.KH = g.KH; a.KW = g.KW;
     a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
     a.neuron = g.ne;
+    a.J = 3 * g.C * (g.KH * g.KW + 1);
+    a.lanes = p.lanes; a.lsh = p.lsh; a.tiles = p.tiles;
+    a.ng = p.ng; a.iwid = p.iwid;
     a.fd_howo = make_fastdiv(g.HO * g.WO);
     a.fd_wo = make_fastdiv(g.WO);
     a.fd_hw = make_fastdiv(g.H * g.W);
     a.fd_w = make_fastdiv(g.W);
     a.fd_sh = make_fastdiv(g.SH);
     a.fd_sw = make_fastdiv(g.SW);
+    a.fd_item = make_fastdiv(p.ng * p.iwid);
+    a.fd_iw = make_fastdiv(p.iwid);
+    a.xbytes = (int)std::min<long long>((long long)g.N * g.H * g.W * g.C * g.esize(), INT32_MAX);
+    a.pbytes = (int)std::min<long long>((long long)g.N * g.HO * g.WO * g.C * g.esize(), INT32_MAX);
     return a;
 }
 
-// dispatch a depthwise kernel template over (T, OM, V4)
+// 3 x 3 kernels of one operand mode and channel vector.
+template <typename T, int OM, int V, bool VEC>
+void dw_launch_k(const DwPlan &p, int pass, int S, const DwArgs &a, dim3 grid, size_t smem, hipStream_t st) {
+    if (pass == 0) {
+        if constexpr (V == 4) {
+            if (S == 1) hipLaunchKernelGGL((qconv_dw_fwd_col_kernel<T, OM, V, VEC, 3, 1, kDwRowsFwd, true>), grid, dim3(kThreads), smem, st, a);
+            else hipLaunchKernelGGL((qconv_dw_fwd_col_kernel<T, OM, V, VEC, 3, 2, kDwRowsFwd, true>), grid, dim3(kThreads), smem, st, a);
+        }
+    } else if (pass == 1) {
+        // prefetching the next column fits the registers with bf16 only
+        constexpr bool PF = sizeof(T) == 2 && V == 4;
+        if (!p.col) hipLaunchKernelGGL((qconv_dw_bwd_data_k_kernel<T, OM, V, VEC, 3, 2>), grid, dim3(kThreads), smem, st, a);
+        else if constexpr (V == 4) hipLaunchKernelGGL((qconv_dw_bwd_data_col_kernel<T, OM, V, VEC, 3, kDwRowsBd, PF>), grid, dim3(kThreads), smem, st, a);
+    } else if constexpr (V == 4) {
+        if (S == 1) hipLaunchKernelGGL((qconv_dw_bwd_weight_col_kernel<T, OM, V, VEC, 3, 1, kDwRowsBw>), grid, dim3(kThreads), 0, st, a);
+        else hipLaunchKernelGGL((qconv_dw_bwd_weight_col_kernel<T, OM, V, VEC, 3, 2, kDwRowsBw>), grid, dim3(kThreads), 0, st, a);
+    }
+}
+template <typename T, int OM>
+void dw_launch_om(const DwPlan &p, int pass, int S, const DwArgs &a, dim3 grid, size_t smem, hipStream_t st) {
+    if constexpr (sizeof(T) == 2) {
+        if (p.V == 8) return dw_launch_k<T, OM, 8, true>(p, pass, S, a, grid, smem, st);
+    }
+    if (p.vec) dw_launch_k<T, OM, 4, true>(p, pass, S, a, grid, smem, st);
+    else dw_launch_k<T, OM, 4, false>(p, pass, S, a, grid, smem, st);
+}
+template <typename T>
+void dw_launch_fast(const Geom &g, const DwPlan &p, int pass, const DwArgs &a, dim3 grid, size_t smem,
+                    hipStream_t st) {
+    switch (g.om()) {
+        case OM_QUADRA: dw_launch_om<T, OM_QUADRA>(p, pass, g.SH, a, grid, smem, st); break;
+        case OM_PAIR: dw_launch_om<T, OM_PAIR>(p, pass, g.SH, a, grid, smem, st); break;
+        case OM_SQUARE: dw_launch_om<T, OM_SQUARE>(p, pass, g.SH, a, grid, smem, st); break;
+        default: dw_launch_om<T, OM_SQIN>(p, pass, g.SH, a, grid, smem, st); break;
+    }
+}
+
+// generic kernels: dispatch a template over (T, OM, V4)
 #define QL_DW_DISPATCH(KERNEL, EXTRA, GRID, SMEM)                                                              \
     do {                                                                                                       \
         const bool v4 = g.C % 4 == 0;                                                                          \
@@ -787,13 +876,21 @@ DwArgs dw_args(const Geom &g) {
 template <typename T>
 ql_status launch_dw_fwd(const Geom &g, const void *x, const void *const *w, const float *const *b, void *y,
                         void *ta, void *tb, hipStream_t st) {
-    DwArgs a = dw_args(g);
+    const DwPlan p = plan_dw(g, 0);
+    DwArgs a = dw_args(g, p);
     a.x = x;
     for (int t = 0; t < 3; ++t) { a.w[t] = w[t]; a.bias[t] = b[t]; }
     a.y = y; a.yta = ta; a.ytb = tb;
+    if (p.fast) {
+        a.zero = zero_page();
+        if (!a.zero) return QL_EHIP;
+        a.M = (int)p.items;
+        const size_t smem = (size_t)g.terms() * (9 + 1) * p.lanes * p.V * sizeof(float);  // filters, biases
+        dw_launch_fast<T>(g, p, 0, a, dim3(p.grid), smem, st);
+        return hip_status();
+    }
     a.M = g.N * g.HO * g.WO;
-    const int ct = cdiv(g.C, kDwCB);
-    const dim3 grid(std::max(1, std::min(cdiv(a.M, kDwPL), cdiv(16 * kNumCUs, ct))), ct);
+    const dim3 grid(std::max(1, std::min(cdiv(a.M, kDwPL), cdiv(16 * kNumCUs, p.ct))), p.ct);
     const size_t smem = (size_t)g.terms() * g.KH * g.KW * kDwCB * sizeof(float);
     QL_DW_DISPATCH(qconv_dw_fwd_kernel, QL_NOEXTRA, grid, smem);
     return hip_status();
@@ -802,13 +899,21 @@ ql_status launch_dw_fwd(const Geom &g, const void *x, const void *const *w, cons
 template <typename T>
 ql_status launch_dw_bwd_data(const Geom &g, const void *gy, const void *ta, const void *tb, const void *const *w,
                              void *dx, hipStream_t st) {
-    DwArgs a = dw_args(g);
+    const DwPlan p = plan_dw(g, 1);
+    DwArgs a = dw_args(g, p);
     a.gy = gy; a.ta = ta; a.tb = tb;
     for (int t = 0; t < 3; ++t) a.w[t] = w[t];
     a.dx = dx;
+    if (p.fast) {
+        a.zero = zero_page();
+        if (!a.zero) return QL_EHIP;
+        a.M = (int)p.items;
+        const size_t smem = (size_t)g.terms() * 9 * p.lanes * p.V * sizeof(float);
+        dw_launch_fast<T>(g, p, 1, a, dim3(p.grid), smem, st);
+        return hip_status();
+    }
     a.M = g.N * g.H * g.W;
-    const int ct = cdiv(g.C, kDwCB);
-    const dim3 grid(std::max(1, std::min(cdiv(a.M, kDwPL), cdiv(16 * kNumCUs, ct))), ct);
+    const dim3 grid(std::max(1, std::min(cdiv(a.M, kDwPL), cdiv(16 * kNumCUs, p.ct))), p.ct);
     const size_t smem = (size_t)g.terms() * g.KH * g.KW * kDwCB * sizeof(float);
     QL_DW_DISPATCH(qconv_dw_bwd_data_kernel, QL_NOEXTRA, grid, smem);
     return hip_status();
@@ -817,22 +922,27 @@ ql_status launch_dw_bwd_data(const Geom &g, const void *gy, const void *ta, cons
 template <typename T>
 ql_status launch_dw_bwd_weight(const Geom &g, const DwPlan &p, const void *x, const void *gy, const void *ta,
                                const void *tb, float *const *dw, float *const *db, void *ws, hipStream_t st) {
-    DwArgs a = dw_args(g);
+    DwArgs a = dw_args(g, p);
     a.x = x; a.gy = gy; a.ta = ta; a.tb = tb;
     for (int t = 0; t < 3; ++t) { a.dw[t] = dw[t]; a.db[t] = db[t]; }
-    a.ws_dw = static_cast<float *>(ws);
-    a.ws_db = reinterpret_cast<float *>(static_cast<char *>(ws) + p.ws_dw);
-    a.M = g.N * g.HO * g.WO;
+    a.ws = static_cast<float *>(ws);
     a.splits = p.splits;
     a.px_per_split = p.pps;
-    const dim3 grid(p.splits, p.ct, p.tg);
-    QL_DW_DISPATCH(qconv_dw_bwd_weight_kernel, QL_TAPS9, grid, 0);
+    a.M = (int)p.items;
+    if (p.fast) {
+        a.zero = zero_page();
+        if (!a.zero) return QL_EHIP;
+        dw_launch_fast<T>(g, p, 2, a, dim3(p.splits, p.tiles), 0, st);
+    } else {
+        const dim3 grid(p.splits, p.ct, p.tg);
+        QL_DW_DISPATCH(qconv_dw_bwd_weight_kernel, QL_TAPS9, grid, 0);
+    }
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const int taps = g.KH * g.KW, nt = g.terms();
-    const long long total = (long long)nt * g.C * taps + (db[0] ? (long long)nt * g.C : 0LL);
-    hipLaunchKernelGGL(qconv_dw_reduce_kernel, dim3(grid_1d(total)), dim3(kThreads), 0, st, a.ws_dw, a.ws_db,
-                       p.splits, g.C, taps, nt, dw[0], dw[1], dw[2], db[0], db[1], db[2], db[0] != nullptr);
+    const int jn = nt * g.C * taps + (db[0] ? nt * g.C : 0);
+    hipLaunchKernelGGL(qconv_dw_reduce_kernel, dim3(cdiv(jn, 16)), dim3(kThreads), 0, st, a.ws, p.splits, a.J, g.C,
+                       taps, nt, dw[0], dw[1], dw[2], db[0], db[1], db[2], db[0] != nullptr);
     return hip_status();
 }
 #undef QL_DW_DISPATCH
@@ -909,7 +1019,7 @@ ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const 
     for (const void *q : ptrs)
         if (q && !aligned16(q)) return QL_EINVAL;
     if (g.dw) {
-        const DwPlan p = plan_dw(g);
+        const DwPlan p = plan_dw(g, 2);
         if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
         if (ws && !aligned16(ws)) return QL_EINVAL;
         float *const dw[3] = {dwa, dwb, dwc};
@@ -979,7 +1089,7 @@ ql_status qlayer_conv2d_bwd_data(const ql_conv_desc *desc, const void *gy, const
 size_t qlayer_conv2d_bwd_weight_workspace_size(const ql_conv_desc *desc) {
     Geom g;
     if (make_geom(desc, g) != QL_OK) return 0;
-    if (g.dw) return plan_dw(g).ws_bytes;
+    if (g.dw) return plan_dw(g, 2).ws_bytes;
     return plan_bwd_weight(g).ws_bytes;
 }
 

@@ -164,6 +164,23 @@ def resnet20_layers(batch: int = 256):
     return layers
 
 
+def mobilenet_v1_pairs(batch: int = 128):
+    """The 13 depthwise / pointwise pairs of a CIFAR MobileNet-V1 (a 3->32 stem at
+    32x32, then blocks of a 3x3 depthwise layer, stride 1 or 2, and a 1x1
+    pointwise layer to 64, 128, 128, 256, 256, 512 x 6, 1024, 1024 channels;
+    stride 2 in the blocks to 128, 256, 512 and the first 1024).  Returns
+    (depthwise, pointwise) ConvLayer pairs; a depthwise layer has o == c."""
+    cfg = [64, (128, 2), 128, (256, 2), 256, (512, 2), 512, 512, 512, 512, 512, (1024, 2), 1024]
+    pairs, c, hw = [], 32, 32
+    for v in cfg:
+        o, s = (v, 1) if isinstance(v, int) else v
+        dw = ConvLayer(n=batch, c=c, h=hw, w=hw, o=c, k=3, stride=s, pad=1)
+        hw = dw.ho
+        pairs.append((dw, ConvLayer(n=batch, c=c, h=hw, w=hw, o=o, k=1, stride=1, pad=0)))
+        c = o
+    return pairs
+
+
 # 4: one large bf16 layer, N=64, C=O=256, 56x56, 3x3, s1 p1.
 LARGE_BF16 = ConvLayer(n=64, c=256, h=56, w=56, o=256, k=3, stride=1, pad=1)
 

@@ -32,6 +32,10 @@ SHAPES = [
     ((3, 64, 20, 20, 3, 1, 1), True),    # several pixel splits and their reduction
     ((2, 6, 7, 7, 7, 1, 3), True),       # 7 x 7 filters, six channels
     ((2, 40, 11, 11, 3, 2, 0), False),   # stride 2 without padding
+    ((4, 64, 2, 2, 3, 1, 1), True),      # 2 x 2 maps: columns wrap across images
+    ((3, 32, 1, 1, 3, 1, 1), True),      # 1 x 1 maps: only the centre tap is inside
+    ((2, 24, 3, 5, 3, 2, 1), False),     # stride 2 on a small map, odd row count
+    ((3, 16, 5, 3, 3, 1, 1), True),      # odd rows per column group, three columns
 ]
 CASES = [(n, sh) for n in (QUADRA, T4, T4I, T3, T2) for sh, same in SHAPES if n != T4I or same]
 IDS = [f"{NAMES[n]}-{'x'.join(map(str, sh))}" for n, sh in CASES]
