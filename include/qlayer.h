@@ -10,8 +10,8 @@
  * three terms T_t = W_t * X + b_t is an ordinary first-order layer (section
  * 3.2, P4), which is why each keeps its own bias.  As a convolution "*" is the
  * cross-correlation of a PyTorch nn.Conv2d (section 4.2: zero padding, floor
- * output size, dilation 1, groups 1, kernel/stride/padding shared by the
- * three terms).  As a fully-connected layer (section 3.2, P3) "*" is a
+ * output size, dilation 1, kernel/stride/padding/groups shared by the three
+ * terms; groups 1, or groups = C for the depth-wise setting of section 4.2).  As a fully-connected layer (section 3.2, P3) "*" is a
  * matrix product.  The backward pass follows section 4.3 (eq:AD, eq:SD):
  * with G = dl/dY, the per-term output gradients are
  *
@@ -28,6 +28,7 @@
  *  - Layouts (row-major, innermost last):
  *      conv X, dX       : N x H x W x C          (NHWC)
  *      conv W_t         : O x KH x KW x C        (OHWI), dW_t the same
+ *                         (depthwise, groups = C = O: C x KH x KW x 1)
  *      conv Y, G, T_a, T_b : N x Ho x Wo x O     (NHWC),
  *                          Ho = (H + 2*pad_h - KH) / stride_h + 1 (floor), Wo likewise
  *      dense X, dX      : B x I;  W_t, dW_t : O x I;  Y, G, T_a, T_b : B x O
@@ -101,8 +102,11 @@ typedef struct {
     ql_neuron neuron;       /* QL_NEURON_QUADRA (0) unless set */
     int groups;             /* 0 or 1: every output channel sees every input channel;
                                C (with O == C): depthwise, each channel its own
-                               KH x KW filter per term, W_t (C,KH,KW,1), dW_t the same.
-                               Other group counts: QL_EUNSUPPORTED. */
+                               KH x KW filter per term, W_t (C,KH,KW,1), dW_t the same;
+                               its forward and input gradient need no workspace.
+                               Other group counts, or depthwise filters above
+                               13 x 13 (three terms staged per channel slice):
+                               QL_EUNSUPPORTED. */
 } ql_conv_desc;
 
 /* Geometry of a quadratic fully-connected layer. */
