@@ -65,6 +65,7 @@ def _load():
     dw_geom = [_I] * 11  # neuron, N, C, H, W, KH, KW, sh, sw, ph, pw
     lib.oracle_dwconv2d_fwd.argtypes = dw_geom + [_D] + w6 + [_D, _D, _D]
     lib.oracle_dwconv2d_bwd.argtypes = dw_geom + [_D] + w6 + [_D] + [_D] * 7
+    lib.oracle_epilogue.argtypes = [_I, _I, ctypes.c_longlong, _D, _D, _D, _I, _D, _D, _D]
     lib.oracle_conv2d_out_size.argtypes = [_I] * 4
     lib.oracle_conv2d_out_size.restype = _I
     fc_geom = [_I] * 3
@@ -333,6 +334,22 @@ def dwconv2d_bwd(neuron, x, wa, wb, wc, ba, bb, bc, gy, stride=1, pad=0):
     lib.oracle_dwconv2d_bwd(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy),
                             *[_p(out.get(k)) for k in ("dx", "dwa", "dwb", "dwc", "dba", "dbb", "dbc")])
     return out
+
+
+def epilogue(y, scale=None, shift=None, relu=False):
+    """Forward epilogue of a layer output y (N x O x H x W, or B x O for a dense
+    layer): y' = relu(scale * y + shift) per channel, and the per-channel sum
+    and sum of squares of y' over every other axis.  Returns (y', sum, sumsq)."""
+    lib = _load()
+    y = _f64(y)
+    shp = y.shape
+    N, O = shp[0], shp[1]
+    P = int(np.prod(shp[2:])) if len(shp) > 2 else 1
+    scale, shift = _f64(scale), _f64(shift)
+    yo, s, s2 = np.empty_like(y), np.empty(O), np.empty(O)
+    lib.oracle_epilogue(N, O, ctypes.c_longlong(P), _p(y), _p(scale), _p(shift), int(bool(relu)), _p(yo), _p(s),
+                        _p(s2))
+    return yo, s, s2
 
 
 def num_threads() -> int:

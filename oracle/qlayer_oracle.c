@@ -796,3 +796,36 @@ void oracle_linear_dw_row(int B, int I, int O,
     if (dbc) *dbc = sc;
     free(ga); free(gb);
 }
+
+/* ------------------------------------------------------------------------
+ * Forward epilogue of a layer output (section 4.2, model construction:
+ * batch normalization regulates the quadratic layers' output values, and
+ * deeper networks put an activation after them).  y is N x O x P (P = Ho*Wo;
+ * a dense output has P = 1).  Per channel o, with optional scale/shift
+ * (a batch normalization with fixed statistics folded to y' = s y + t) and
+ * an optional ReLU:
+ *     y'[n,o,p] = relu(scale[o] * y[n,o,p] + shift[o])
+ * and the statistics a training-mode batch normalization of y' needs:
+ *     sum[o] = sum_{n,p} y'[n,o,p],   sumsq[o] = sum_{n,p} y'[n,o,p]^2
+ * ------------------------------------------------------------------------ */
+void oracle_epilogue(int N, int O, long long P, const double *y, const double *scale, const double *shift, int relu,
+                     double *yo, double *sum, double *sumsq) {
+#pragma omp parallel for schedule(static)
+    for (int o = 0; o < O; ++o) {
+        double s = 0.0, s2 = 0.0;
+        for (int n = 0; n < N; ++n) {
+            for (long long p = 0; p < P; ++p) {
+                size_t i = ((size_t)n * O + o) * (size_t)P + (size_t)p;
+                double v = y[i];
+                if (scale) v = scale[o] * v;
+                if (shift) v = v + shift[o];
+                if (relu && v < 0.0) v = 0.0;
+                yo[i] = v;
+                s += v;
+                s2 += v * v;
+            }
+        }
+        sum[o] = s;
+        sumsq[o] = s2;
+    }
+}
