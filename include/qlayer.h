@@ -214,6 +214,53 @@ ql_status qlayer_linear_bwd(const ql_linear_desc *desc, const void *x, const voi
                             float *dba, float *dbb, float *dbc,
                             void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Forward with a fused epilogue -- section 4.2, model construction: batch
+ * normalization after the quadratic layers regulates the extreme values the
+ * second-order term produces, and deeper networks put an activation (ReLU)
+ * after them.  The forward kernel transforms Y before storing it:
+ *
+ *     y'[m, o] = relu( scale[o] * Y[m, o] + shift[o] )     (per output channel o)
+ *
+ * (a batch normalization with fixed statistics folds into scale and shift),
+ * stores y' in y, and gathers the statistics a training-mode batch
+ * normalization of y' needs, over the N x Ho x Wo pixels (B rows of a dense
+ * layer) of each channel, from the values as stored (rounded to the dtype):
+ *
+ *     sum[o] = sum_m y'[m, o],    sumsq[o] = sum_m y'[m, o]^2
+ *
+ * Every member is optional: scale NULL = 1, shift NULL = 0, relu 0 = none,
+ * sum and sumsq both NULL = no statistics (both or neither, else QL_EINVAL).
+ * T_a and T_b are stored untransformed (the backward takes dl/dY, the
+ * gradient before the epilogue, which the caller forms).  An epilogue that
+ * does anything needs y != NULL (recompute mode has no Y): QL_EINVAL.  The
+ * statistics are summed in a fixed order: repeated calls give identical bits.
+ * The pointers are float32 device pointers of O values, 16-byte aligned.
+ * epi == NULL is the plain forward.  The workspace query takes the same epi
+ * (the statistics need per-tile partial sums); other arguments and errors as
+ * for qlayer_conv2d_fwd / qlayer_linear_fwd.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    const float *scale;  /* O per-channel factors, or NULL */
+    const float *shift;  /* O per-channel offsets, or NULL */
+    int relu;            /* nonzero: clamp y' at 0 */
+    float *sum;          /* O: per-channel sum of y', or NULL */
+    float *sumsq;        /* O: per-channel sum of y'^2, or NULL */
+} ql_epilogue;
+
+size_t qlayer_conv2d_fwd_ex_workspace_size(const ql_conv_desc *desc, const ql_epilogue *epi);
+ql_status qlayer_conv2d_fwd_ex(const ql_conv_desc *desc, const void *x,
+                               const void *wa, const void *wb, const void *wc,
+                               const float *ba, const float *bb, const float *bc,
+                               void *y, void *ta, void *tb, const ql_epilogue *epi,
+                               void *workspace, size_t workspace_bytes, void *stream);
+size_t qlayer_linear_fwd_ex_workspace_size(const ql_linear_desc *desc, const ql_epilogue *epi);
+ql_status qlayer_linear_fwd_ex(const ql_linear_desc *desc, const void *x,
+                               const void *wa, const void *wb, const void *wc,
+                               const float *ba, const float *bb, const float *bc,
+                               void *y, void *ta, void *tb, const ql_epilogue *epi,
+                               void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -65,6 +65,18 @@ class LinearDesc(ctypes.Structure):
                 ("neuron", ctypes.c_int)]
 
 
+class Epilogue(ctypes.Structure):
+    """ql_epilogue: y' = relu(scale * Y + shift) per output channel, and the
+    per-channel sum / sum of squares of the stored y' (every member optional)."""
+    _fields_ = [("scale", ctypes.c_void_p), ("shift", ctypes.c_void_p), ("relu", ctypes.c_int),
+                ("sum", ctypes.c_void_p), ("sumsq", ctypes.c_void_p)]
+
+
+def epilogue(scale=None, shift=None, relu=False, stat_sum=None, stat_sumsq=None) -> Epilogue:
+    """An Epilogue over float32 device tensors of O values (or None); the tensors must outlive the call."""
+    return Epilogue(_ptr(scale), _ptr(shift), int(bool(relu)), _ptr(stat_sum), _ptr(stat_sumsq))
+
+
 def conv_desc(n, c, h, w, o, kh, kw, stride=1, pad=0, dtype=QL_BF16, neuron=QL_NEURON_QUADRA,
               groups=1) -> ConvDesc:
     """groups = c (with o == c) makes the layer depthwise: weights (c, kh, kw, 1)."""
@@ -104,6 +116,13 @@ def lib():
     L.qlayer_conv2d_bwd_weight.argtypes = [cd] + [_vp] * 10 + [_vp, _sz, _vp]
     L.qlayer_linear_fwd.argtypes = [ld] + [_vp] * 10 + [_vp, _sz, _vp]
     L.qlayer_linear_bwd.argtypes = [ld] + [_vp] * 14 + [_vp, _sz, _vp]
+    ep = ctypes.POINTER(Epilogue)
+    for name, d in (("conv2d_fwd_ex", cd), ("linear_fwd_ex", ld)):
+        f = getattr(L, f"qlayer_{name}_workspace_size")
+        f.argtypes = [d, ep]
+        f.restype = _sz
+        getattr(L, f"qlayer_{name}").argtypes = [d] + [_vp] * 10 + [ep, _vp, _sz, _vp]
+        getattr(L, f"qlayer_{name}").restype = ctypes.c_int
     for name in ("conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight", "linear_fwd", "linear_bwd"):
         getattr(L, f"qlayer_{name}").restype = ctypes.c_int
     _lib = L
@@ -220,6 +239,38 @@ def qlayer_linear_fwd(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None, ta
     _check("qlayer_linear_fwd", lib().qlayer_linear_fwd(
         ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
         _ptr(y), _ptr(ta), _ptr(tb), wp, wn, _stream(stream, dev)))
+
+
+def _epi_ref(epi):
+    return ctypes.byref(epi) if epi is not None else None
+
+
+def qlayer_conv2d_fwd_ex_workspace_size(desc: ConvDesc, epi=None) -> int:
+    return lib().qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(desc), _epi_ref(epi))
+
+
+def qlayer_conv2d_fwd_ex(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None, ta=None, tb=None, epi=None,
+                         workspace=None, stream=None):
+    """qlayer_conv2d_fwd with a fused epilogue (an Epilogue, see epilogue())."""
+    dev = _device(x, wa)
+    wp, wn = _workspace(workspace, qlayer_conv2d_fwd_ex_workspace_size(desc, epi), dev)
+    _check("qlayer_conv2d_fwd_ex", lib().qlayer_conv2d_fwd_ex(
+        ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
+        _ptr(y), _ptr(ta), _ptr(tb), _epi_ref(epi), wp, wn, _stream(stream, dev)))
+
+
+def qlayer_linear_fwd_ex_workspace_size(desc: LinearDesc, epi=None) -> int:
+    return lib().qlayer_linear_fwd_ex_workspace_size(ctypes.byref(desc), _epi_ref(epi))
+
+
+def qlayer_linear_fwd_ex(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None, ta=None, tb=None, epi=None,
+                         workspace=None, stream=None):
+    """qlayer_linear_fwd with a fused epilogue (an Epilogue, see epilogue())."""
+    dev = _device(x, wa)
+    wp, wn = _workspace(workspace, qlayer_linear_fwd_ex_workspace_size(desc, epi), dev)
+    _check("qlayer_linear_fwd_ex", lib().qlayer_linear_fwd_ex(
+        ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
+        _ptr(y), _ptr(ta), _ptr(tb), _epi_ref(epi), wp, wn, _stream(stream, dev)))
 
 
 def qlayer_linear_bwd_workspace_size(desc: LinearDesc) -> int:

@@ -25,6 +25,25 @@ __host__ __device__ constexpr int om_terms(int om) { return om == OM_QUADRA ? 3 
 // output-side maps the backward stages: G, T_a, T_b / G, T_a / G
 __host__ __device__ constexpr int om_gmaps(int om) { return om == OM_SQIN ? 1 : (om == OM_SQUARE ? 2 : 3); }
 
+// Forward epilogue of the layer output (section 4.2, model construction:
+// batch normalization after the quadratic layers, an activation in deeper
+// networks): y' = relu(scale[o] y + shift[o]) per output channel o (a batch
+// normalization with fixed statistics folded to scale and shift), stored in
+// place of y; the per-channel sums of y' and y'^2 (training-mode statistics)
+// are gathered from the stored values.
+struct EpiArgs {
+    const float *scale, *shift;  // per output channel, or NULL (1 and 0)
+    int relu;
+};
+
+// Whether the forward kernel of a tile configuration writes its output tiles
+// through the LDS ring (the path that also gathers the epilogue statistics):
+// one staged map of BCOL pixel rows of BR channels (padded by 16 bytes) fits
+// the ring of NS stages of 3 BR + BCOL 64-byte rows.
+__host__ __device__ constexpr bool fwd_staged_fits(int BR, int BCOL, int NS, int E) {
+    return BCOL * (BR * E + 16) <= NS * (3 * BR + BCOL) * 64;
+}
+
 // Forward: ONE implicit GEMM, rows = output channels (three term blocks
 // W_a | W_b | W_c), columns = output pixels, K = (r, q, c).
 struct FwdArgs {
@@ -39,6 +58,8 @@ struct FwdArgs {
     int row_tiles, col_tiles, splits, stages_per_split, stages_total;
     int neuron;  // NEURON_*: the epilogue (T4 + identity reads X at the output pixel)
     int xsq;     // T2: x already holds X o X (squared by a pre-pass), no squaring in the kernel
+    EpiArgs epi;
+    float *stat_part;  // staged epilogue: per pixel tile ct, partial sums of y' [ct][O] and y'^2 [ct][O]; or NULL
     FastDiv fd_howo, fd_wo, fd_c, fd_kw;
 };
 

@@ -15,7 +15,7 @@ template <typename T, bool V4>
 __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float *__restrict__ ws, int splits,
                                                                      long long MO, int O, const float *b0,
                                                                      const float *b1, const float *b2, T *y, T *ta,
-                                                                     T *tb, int neuron, const T *x) {
+                                                                     T *tb, int neuron, const T *x, EpiArgs epi) {
     constexpr int E = V4 ? 4 : 1;
     const float *bp[3] = {b0, b1, b2};
     const int nt = neuron == NEURON_QUADRA ? 3 : (neuron <= NEURON_T4I ? 2 : 1);
@@ -50,6 +50,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float
             else if (neuron == NEURON_T4I) yv[e] = fa * fb + to_f32<T>(x[idx + e]);
             else if (neuron == NEURON_T3) yv[e] = fa * fa;
             else yv[e] = fa;
+            yv[e] = epi_apply(epi, o + e, yv[e]);
         }
         if (nt < 2) tb = nullptr;
         if constexpr (V4) {
@@ -391,6 +392,77 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_col2im_kernel(const f
 #pragma unroll
         for (int c = 0; c < 4; ++c)
             if (c < C) dx[m * C + c] = from_f32<T>(acc[c]);
+    }
+}
+
+// Per-channel statistics of a stored layer output y' (M rows of O channels,
+// the forward epilogue's sums when its kernel did not gather them): part p
+// takes rows [p rpp, (p + 1) rpp); a thread takes 4 channels of every 16th
+// row of the part, and the 16 row lanes are summed in lane order.  Writes
+// part[p][0][o] = sum of y', part[p][1][o] = sum of y'^2.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void qconv_channel_stats_kernel(const T *__restrict__ y, int M, int O,
+                                                                        int rpp, float *__restrict__ part) {
+    __shared__ float red[2][16][65];
+    const int cl = threadIdx.x & 15, rl = threadIdx.x >> 4;
+    const int c = blockIdx.y * 64 + 4 * cl;
+    const int r0 = blockIdx.x * rpp, r1 = min(M, r0 + rpp);
+    float s1[4] = {0.0f, 0.0f, 0.0f, 0.0f}, s2[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    const bool v4 = (O & 3) == 0;
+    if (c < O) {
+        for (int r = r0 + rl; r < r1; r += 16) {
+            float v[4];
+            const T *p = y + (size_t)r * O + c;
+            if (v4) {
+                load4<T>(p, v);
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] = c + k < O ? to_f32<T>(p[k]) : 0.0f;
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                s1[k] += v[k];
+                s2[k] += v[k] * v[k];
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        red[0][rl][4 * cl + k] = s1[k];
+        red[1][rl][4 * cl + k] = s2[k];
+    }
+    __syncthreads();
+    if (threadIdx.x < 128) {
+        const int st = threadIdx.x >> 6, ch = threadIdx.x & 63;
+        float t = 0.0f;
+#pragma unroll
+        for (int l = 0; l < 16; ++l) t += red[st][l][ch];
+        const int o = blockIdx.y * 64 + ch;
+        if (o < O) part[((size_t)blockIdx.x * 2 + st) * O + o] = t;
+    }
+}
+
+// Sum of the per-part statistics [part][2][O] in part order: sum[o] and sumsq[o].
+// A block takes 16 indices j of [2][O]; 16 lanes sum every 16th part and the
+// lane sums are added in lane order.
+__global__ __launch_bounds__(kThreads) void qconv_stats_reduce_kernel(const float *__restrict__ part, int nparts,
+                                                                       int O, float *sum, float *sumsq) {
+    __shared__ float red[16][17];
+    const int jl = threadIdx.x & 15, sl = threadIdx.x >> 4;
+    const int j = blockIdx.x * 16 + jl;
+    float s = 0.0f;
+    if (j < 2 * O) {
+#pragma unroll 4
+        for (int p = sl; p < nparts; p += 16) s += part[(size_t)p * 2 * O + j];
+    }
+    red[sl][jl] = s;
+    __syncthreads();
+    if (sl == 0 && j < 2 * O) {
+        float t = 0.0f;
+#pragma unroll
+        for (int l = 0; l < 16; ++l) t += red[l][jl];
+        if (j < O) sum[j] = t;
+        else sumsq[j - O] = t;
     }
 }
 

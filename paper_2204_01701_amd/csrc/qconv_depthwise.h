@@ -43,6 +43,7 @@ struct DwArgs {
     int ng, iwid;
     const void *zero;  // 16 zero bytes: the source of out-of-range taps (generic kernels)
     int xbytes, pbytes;  // 3 x 3 kernels: bytes of X (and dX) and of an output-side map (< 2^31)
+    EpiArgs epi;         // forward epilogue of Y (qargs.h)
     FastDiv fd_howo, fd_wo, fd_hw, fd_w, fd_sh, fd_sw, fd_item, fd_iw;
 };
 
@@ -148,6 +149,7 @@ __global__ __launch_bounds__(kThreads) void qconv_dw_fwd_kernel(const DwArgs a) 
             else if constexpr (OM == OM_PAIR) yv[k] = fa * acc[1][k] + xs[k];
             else if constexpr (OM == OM_SQUARE) yv[k] = fa * fa;
             else yv[k] = fa;
+            if (k < cleft) yv[k] = epi_apply(a.epi, c + k, yv[k]);
         }
         if (a.y) dw_st4<T, V4>(static_cast<T *>(a.y) + off, cleft, yv);
         if (a.yta) dw_st4<T, V4>(static_cast<T *>(a.yta) + off, cleft, acc[0]);
@@ -625,6 +627,7 @@ __device__ __forceinline__ void dw_fwd_col_compute(const DwArgs &a, const DwFwdC
             else if constexpr (OM == OM_PAIR) yv[k] = fa * acc[rr][1][k] + xs[k];
             else if constexpr (OM == OM_SQUARE) yv[k] = fa * fa;
             else yv[k] = fa;
+            if (k < cleft) yv[k] = epi_apply(a.epi, c + k, yv[k]);
         }
         if (a.y) dw_stv<T, V, VEC>(static_cast<T *>(a.y) + off, cleft, yv);
         if (a.yta) dw_stv<T, V, VEC>(static_cast<T *>(a.yta) + off, cleft, acc[rr][0]);

@@ -261,10 +261,19 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         constexpr int MAPB = BCOL * PITCH;
         constexpr int PER = 3 * MAPB <= NS * STAGE ? 3 : 1;  // maps staged per round
         constexpr int CPR = BR * E / 16;                       // 16-byte chunks per row
-        static_assert((CPR & (CPR - 1)) == 0, "staged epilogue tile");
+        constexpr int VE = 16 / E;                             // channels per chunk
+        static_assert((CPR & (CPR - 1)) == 0 && NT % CPR == 0, "staged epilogue tile");
+        static_assert(fwd_staged_fits(BR, BCOL, NS, E) == (MAPB <= NS * STAGE), "staged epilogue predicate");
         if constexpr (MAPB <= NS * STAGE) {  // (otherwise, and for O not a multiple of 16 / E: direct stores)
             if (a.O % (16 / E) == 0) {
                 T *outs[3] = {y, ta, NTM >= 2 ? tb : nullptr};
+                // Epilogue statistics: a thread copies chunks of one channel
+                // group (its chunk index mod CPR is fixed), so it sums its VE
+                // channels of y' over its pixel rows in registers.
+                const bool stats = a.stat_part != nullptr;
+                float ssum[VE], ssq[VE];
+#pragma unroll
+                for (int k = 0; k < VE; ++k) ssum[k] = ssq[k] = 0.0f;
 #pragma unroll
                 for (int r0 = 0; r0 < 3; r0 += PER) {
                     lds_barrier();  // every wave is done with the ring (or the previous round's copy)
@@ -283,7 +292,11 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                                     float v[4], xv[4];
                                     if (j == 0) xs4(ct * BCOL + p, rt * BR + ol, xv);
 #pragma unroll
-                                    for (int i = 0; i < 4; ++i) v[i] = outv(j, mr, mc, 4 * g + i, j == 0 ? xv[i] : 0.0f);
+                                    for (int i = 0; i < 4; ++i) {
+                                        v[i] = outv(j, mr, mc, 4 * g + i, j == 0 ? xv[i] : 0.0f);
+                                        const int o = rt * BR + ol + i;
+                                        if (j == 0 && o < a.O) v[i] = epi_apply(a.epi, o, v[i]);
+                                    }
                                     store4<T>(reinterpret_cast<T *>(tile + p * PITCH + ol * E), v[0], v[1], v[2], v[3]);
                                 }
                             }
@@ -296,9 +309,42 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                         for (int c = tid; c < BCOL * CPR; c += NT) {
                             const int row = c / CPR, cc = c % CPR;
                             const int m = ct * BCOL + row, o = rt * BR + cc * (16 / E);
-                            if (m < a.M && o < a.O)
-                                *reinterpret_cast<v4u *>(outs[j] + (size_t)m * a.O + o) =
-                                    lds_read16(tile + row * PITCH + cc * 16);
+                            if (m < a.M && o < a.O) {
+                                const v4u val = lds_read16(tile + row * PITCH + cc * 16);
+                                *reinterpret_cast<v4u *>(outs[j] + (size_t)m * a.O + o) = val;
+                                if (j == 0 && stats) {
+#pragma unroll
+                                    for (int k = 0; k < VE; ++k) {
+                                        const float f = vget<T>(val, k);  // the stored value
+                                        ssum[k] += f;
+                                        ssq[k] += f * f;
+                                    }
+                                }
+                            }
+                        }
+                    }
+                }
+                if (stats) {
+                    // channel ol = cc VE + k of the tile: threads tid = cc (mod CPR), summed in tid order
+                    lds_barrier();
+                    float *red = reinterpret_cast<float *>(smem);
+#pragma unroll
+                    for (int k = 0; k < VE; ++k) {
+                        red[tid * 2 * VE + k] = ssum[k];
+                        red[tid * 2 * VE + VE + k] = ssq[k];
+                    }
+                    lds_barrier();
+                    if (tid < BR) {
+                        const int cc = tid / VE, k = tid - cc * VE;
+                        float s1 = 0.0f, s2 = 0.0f;
+                        for (int u = cc; u < NT; u += CPR) {
+                            s1 += red[u * 2 * VE + k];
+                            s2 += red[u * 2 * VE + VE + k];
+                        }
+                        const int o = rt * BR + tid;
+                        if (o < a.O) {
+                            a.stat_part[(size_t)ct * 2 * a.O + o] = s1;
+                            a.stat_part[(size_t)ct * 2 * a.O + a.O + o] = s2;
                         }
                     }
                 }
@@ -322,6 +368,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                         va[i] = outv(1, mr, mc, 4 * g + i, 0.0f);
                         vb[i] = NTM >= 2 ? outv(2, mr, mc, 4 * g + i, 0.0f) : 0.0f;
                         vy[i] = outv(0, mr, mc, 4 * g + i, xv[i]);
+                        if (o + i < a.O) vy[i] = epi_apply(a.epi, o + i, vy[i]);
                     }
                     if (NTM < 2) tb = nullptr;
                     const size_t off = (size_t)m * a.O + o;

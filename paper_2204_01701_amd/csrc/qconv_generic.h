@@ -252,6 +252,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
                         va[i] = outv(1, mr, mc, 4 * g + i, 0.0f);
                         vb[i] = NTM >= 2 ? outv(2, mr, mc, 4 * g + i, 0.0f) : 0.0f;
                         vy[i] = outv(0, mr, mc, 4 * g + i, xs);
+                        if (o + i < a.O) vy[i] = epi_apply(a.epi, o + i, vy[i]);
                     }
                     const size_t off = (size_t)m * a.O + o;
                     if (vec_out) {

@@ -82,6 +82,13 @@ template <typename T> __device__ __forceinline__ uint32_t vraw(const v4u &v, int
     }
 }
 
+// The forward epilogue of output channel o (EpiArgs): scale, shift, ReLU.
+__device__ __forceinline__ float epi_apply(const EpiArgs &e, int o, float v) {
+    if (e.scale) v *= e.scale[o];
+    if (e.shift) v += e.shift[o];
+    return e.relu ? fmaxf(v, 0.0f) : v;
+}
+
 template <typename T> __device__ __forceinline__ float to_f32(T v);
 template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ float to_f32<uint16_t>(uint16_t v) { return bf2f(v); }

@@ -353,8 +353,10 @@ int grid_1d(long long total) {
 template <typename T>
 ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void *wa, const void *wb, const void *wc,
                      const float *ba, const float *bb, const float *bc, void *y, void *ta, void *tb, void *ws,
-                     hipStream_t st) {
+                     const EpiArgs &epi, float *stat_part, hipStream_t st) {
     FwdArgs a{};
+    a.epi = epi;
+    a.stat_part = stat_part;  // (set by the caller only where the kernel's staged epilogue runs)
     a.x = x;
     a.w[0] = wa; a.w[1] = wb; a.w[2] = wc;
     char *wsb = static_cast<char *>(ws);
@@ -458,12 +460,20 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     if (g.O % 4 == 0)
         hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, true>), dim3(grid_1d(MO / 4)), dim3(kThreads), 0, st,
                            static_cast<const float *>(a.ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
-                           static_cast<T *>(ta), static_cast<T *>(tb), g.ne, static_cast<const T *>(x));
+                           static_cast<T *>(ta), static_cast<T *>(tb), g.ne, static_cast<const T *>(x), epi);
     else
         hipLaunchKernelGGL((qconv_fwd_combine_kernel<T, false>), dim3(grid_1d(MO)), dim3(kThreads), 0, st,
                            static_cast<const float *>(a.ws), p.splits, MO, g.O, ba, bb, bc, static_cast<T *>(y),
-                           static_cast<T *>(ta), static_cast<T *>(tb), g.ne, static_cast<const T *>(x));
+                           static_cast<T *>(ta), static_cast<T *>(tb), g.ne, static_cast<const T *>(x), epi);
     return hip_status();
+}
+
+// Whether launch_fwd's kernel writes Y through its staged epilogue, the path
+// that gathers the epilogue statistics itself (qconv_fwd.h).
+bool fwd_stats_fused(const Geom &g, const FwdPlan &p) {
+    if (!p.veck || p.splits != 1 || g.O % (16 / (int)g.esize()) != 0) return false;
+    const int ns = (g.ne == NEURON_QUADRA && (p.cfg == 4 || p.cfg == 5)) ? 3 : 4;
+    return fwd_staged_fits(p.BR, p.BCOL, ns, (int)g.esize());
 }
 
 template <typename T>
@@ -875,9 +885,10 @@ void dw_launch_fast(const Geom &g, const DwPlan &p, int pass, const DwArgs &a, d
 
 template <typename T>
 ql_status launch_dw_fwd(const Geom &g, const void *x, const void *const *w, const float *const *b, void *y,
-                        void *ta, void *tb, hipStream_t st) {
+                        void *ta, void *tb, const EpiArgs &epi, hipStream_t st) {
     const DwPlan p = plan_dw(g, 0);
     DwArgs a = dw_args(g, p);
+    a.epi = epi;
     a.x = x;
     for (int t = 0; t < 3; ++t) { a.w[t] = w[t]; a.bias[t] = b[t]; }
     a.y = y; a.yta = ta; a.ytb = tb;
@@ -949,9 +960,40 @@ ql_status launch_dw_bwd_weight(const Geom &g, const DwPlan &p, const void *x, co
 #undef QL_NOEXTRA
 #undef QL_TAPS9
 
+// The forward epilogue's statistics: partial sums per pixel tile (gathered by
+// the staged forward kernel) or per part of rows (a pass over the stored Y'),
+// then one reduction in part order.
+struct StatPlan {
+    bool on, fused;
+    int nparts, rpp;  // parts; rows per part of the separate pass
+    size_t bytes;
+};
+
+StatPlan plan_stats(const Geom &g, const ql_epilogue *e) {
+    StatPlan s{};
+    s.on = e && e->sum;
+    if (!s.on) return s;
+    const int M = g.N * g.HO * g.WO;
+    FwdPlan p{};
+    if (!g.dw) p = plan_fwd(g);
+    s.fused = !g.dw && fwd_stats_fused(g, p);
+    if (s.fused) {
+        s.nparts = p.col_tiles;
+    } else {
+        s.rpp = std::max(64, cdiv(M, 1024));
+        s.nparts = cdiv(M, s.rpp);
+    }
+    s.bytes = align_up((size_t)s.nparts * 2 * g.O * sizeof(float));
+    return s;
+}
+
+size_t fwd_ws_bytes(const Geom &g, const ql_epilogue *e) {
+    return (g.dw ? 0 : plan_fwd(g).ws_bytes) + plan_stats(g, e).bytes;
+}
+
 ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *wb, const void *wc, const float *ba,
-                     const float *bb, const float *bc, void *y, void *ta, void *tb, void *ws, size_t ws_bytes,
-                     void *stream) {
+                     const float *bb, const float *bc, void *y, void *ta, void *tb, const ql_epilogue *e, void *ws,
+                     size_t ws_bytes, void *stream) {
     const int nt = g.terms();
     // pointers of terms the neuron type lacks are ignored
     if (nt < 3) { wc = nullptr; bc = nullptr; }
@@ -960,22 +1002,57 @@ ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *w
     if (!x || !wa || (nt >= 2 && !wb) || (nt >= 3 && !wc)) return QL_EINVAL;
     const bool saved = g.ne == NEURON_T2 ? false : (nt >= 2 ? (ta && tb) : ta != nullptr);
     if (!y && !saved) return QL_EINVAL;
+    EpiArgs epi{};
+    if (e) {
+        // the epilogue transforms Y: it needs Y; the statistics come as a pair
+        const bool any = e->scale || e->shift || e->relu || e->sum || e->sumsq;
+        if (any && !y) return QL_EINVAL;
+        if ((e->sum == nullptr) != (e->sumsq == nullptr)) return QL_EINVAL;
+        const void *eps[] = {e->scale, e->shift, e->sum, e->sumsq};
+        for (const void *q : eps)
+            if (q && !aligned16(q)) return QL_EINVAL;
+        epi.scale = e->scale;
+        epi.shift = e->shift;
+        epi.relu = e->relu != 0;
+    }
     const void *ptrs[] = {x, wa, wb, wc, ba, bb, bc, y, ta, tb};
     for (const void *q : ptrs)
         if (q && !aligned16(q)) return QL_EINVAL;
+    const StatPlan sp = plan_stats(g, e);
+    const size_t main_bytes = g.dw ? 0 : plan_fwd(g).ws_bytes;
+    if (ws_bytes < main_bytes + sp.bytes || (main_bytes + sp.bytes && !ws)) return QL_EWORKSPACE;
+    if (ws && !aligned16(ws)) return QL_EINVAL;
+    float *stat_part = sp.on ? reinterpret_cast<float *>(static_cast<char *>(ws) + main_bytes) : nullptr;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    ql_status s;
     if (g.dw) {
         const void *w[3] = {wa, wb, wc};
         const float *b[3] = {ba, bb, bc};
-        hipStream_t st = static_cast<hipStream_t>(stream);
-        return g.dt == QL_BF16 ? launch_dw_fwd<uint16_t>(g, x, w, b, y, ta, tb, st)
-                               : launch_dw_fwd<float>(g, x, w, b, y, ta, tb, st);
+        s = g.dt == QL_BF16 ? launch_dw_fwd<uint16_t>(g, x, w, b, y, ta, tb, epi, st)
+                            : launch_dw_fwd<float>(g, x, w, b, y, ta, tb, epi, st);
+    } else {
+        const FwdPlan p = plan_fwd(g);
+        float *fused_part = sp.fused ? stat_part : nullptr;
+        s = g.dt == QL_BF16
+                ? launch_fwd<uint16_t>(g, p, x, wa, wb, wc, ba, bb, bc, y, ta, tb, ws, epi, fused_part, st)
+                : launch_fwd<float>(g, p, x, wa, wb, wc, ba, bb, bc, y, ta, tb, ws, epi, fused_part, st);
     }
-    const FwdPlan p = plan_fwd(g);
-    if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
-    if (ws && !aligned16(ws)) return QL_EINVAL;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    return g.dt == QL_BF16 ? launch_fwd<uint16_t>(g, p, x, wa, wb, wc, ba, bb, bc, y, ta, tb, ws, st)
-                           : launch_fwd<float>(g, p, x, wa, wb, wc, ba, bb, bc, y, ta, tb, ws, st);
+    if (s != QL_OK || !sp.on) return s;
+    const int M = g.N * g.HO * g.WO;
+    if (!sp.fused) {
+        const dim3 grid(sp.nparts, cdiv(g.O, 64));
+        if (g.dt == QL_BF16)
+            hipLaunchKernelGGL(qconv_channel_stats_kernel<uint16_t>, grid, dim3(kThreads), 0, st,
+                               static_cast<const uint16_t *>(y), M, g.O, sp.rpp, stat_part);
+        else
+            hipLaunchKernelGGL(qconv_channel_stats_kernel<float>, grid, dim3(kThreads), 0, st,
+                               static_cast<const float *>(y), M, g.O, sp.rpp, stat_part);
+        s = hip_status();
+        if (s != QL_OK) return s;
+    }
+    hipLaunchKernelGGL(qconv_stats_reduce_kernel, dim3(cdiv(2 * g.O, 16)), dim3(kThreads), 0, st, stat_part,
+                       sp.nparts, g.O, e->sum, e->sumsq);
+    return hip_status();
 }
 
 ql_status bwd_data_common(const Geom &g, const void *gy, const void *ta, const void *tb, const void *wa,
@@ -1057,8 +1134,7 @@ int qlayer_version(void) { return 100; }
 size_t qlayer_conv2d_fwd_workspace_size(const ql_conv_desc *desc) {
     Geom g;
     if (make_geom(desc, g) != QL_OK) return 0;
-    if (g.dw) return 0;
-    return plan_fwd(g).ws_bytes;
+    return fwd_ws_bytes(g, nullptr);
 }
 
 ql_status qlayer_conv2d_fwd(const ql_conv_desc *desc, const void *x, const void *wa, const void *wb, const void *wc,
@@ -1067,7 +1143,7 @@ ql_status qlayer_conv2d_fwd(const ql_conv_desc *desc, const void *x, const void 
     Geom g;
     const ql_status s = make_geom(desc, g);
     if (s != QL_OK) return s;
-    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, workspace, workspace_bytes, stream);
+    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, nullptr, workspace, workspace_bytes, stream);
 }
 
 size_t qlayer_conv2d_bwd_data_workspace_size(const ql_conv_desc *desc) {
@@ -1105,7 +1181,39 @@ ql_status qlayer_conv2d_bwd_weight(const ql_conv_desc *desc, const void *x, cons
 size_t qlayer_linear_fwd_workspace_size(const ql_linear_desc *desc) {
     Geom g;
     if (linear_geom(desc, g) != QL_OK) return 0;
-    return plan_fwd(g).ws_bytes;
+    return fwd_ws_bytes(g, nullptr);
+}
+
+size_t qlayer_conv2d_fwd_ex_workspace_size(const ql_conv_desc *desc, const ql_epilogue *epi) {
+    Geom g;
+    if (make_geom(desc, g) != QL_OK) return 0;
+    return fwd_ws_bytes(g, epi);
+}
+
+ql_status qlayer_conv2d_fwd_ex(const ql_conv_desc *desc, const void *x, const void *wa, const void *wb,
+                               const void *wc, const float *ba, const float *bb, const float *bc, void *y, void *ta,
+                               void *tb, const ql_epilogue *epi, void *workspace, size_t workspace_bytes,
+                               void *stream) {
+    Geom g;
+    const ql_status s = make_geom(desc, g);
+    if (s != QL_OK) return s;
+    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, epi, workspace, workspace_bytes, stream);
+}
+
+size_t qlayer_linear_fwd_ex_workspace_size(const ql_linear_desc *desc, const ql_epilogue *epi) {
+    Geom g;
+    if (linear_geom(desc, g) != QL_OK) return 0;
+    return fwd_ws_bytes(g, epi);
+}
+
+ql_status qlayer_linear_fwd_ex(const ql_linear_desc *desc, const void *x, const void *wa, const void *wb,
+                               const void *wc, const float *ba, const float *bb, const float *bc, void *y, void *ta,
+                               void *tb, const ql_epilogue *epi, void *workspace, size_t workspace_bytes,
+                               void *stream) {
+    Geom g;
+    const ql_status s = linear_geom(desc, g);
+    if (s != QL_OK) return s;
+    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, epi, workspace, workspace_bytes, stream);
 }
 
 ql_status qlayer_linear_fwd(const ql_linear_desc *desc, const void *x, const void *wa, const void *wb,
@@ -1114,7 +1222,7 @@ ql_status qlayer_linear_fwd(const ql_linear_desc *desc, const void *x, const voi
     Geom g;
     const ql_status s = linear_geom(desc, g);
     if (s != QL_OK) return s;
-    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, workspace, workspace_bytes, stream);
+    return fwd_common(g, x, wa, wb, wc, ba, bb, bc, y, ta, tb, nullptr, workspace, workspace_bytes, stream);
 }
 
 size_t qlayer_linear_bwd_workspace_size(const ql_linear_desc *desc) {

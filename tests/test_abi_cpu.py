@@ -222,3 +222,35 @@ def test_depthwise_validation(L):
     # a depthwise weight gradient with too small a workspace
     assert L.qlayer_conv2d_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None,
                                       None, FAKE, 16, None) == QL_EWORKSPACE
+
+
+def test_epilogue_validation(L):
+    d = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32)
+    ld = ql.linear_desc(32, 64, 64, ql.QL_BF16)
+
+    def fwd_ex(epi, y=FAKE, ta=None, tb=None, ws=FAKE, wsb=1 << 30):
+        return L.qlayer_conv2d_fwd_ex(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, None, None, y, ta, tb,
+                                      ctypes.byref(epi) if epi is not None else None, ws, wsb, None)
+
+    # recompute mode (no Y) with an epilogue that does anything; half of the statistics pair
+    assert fwd_ex(ql.Epilogue(None, None, 1, None, None), y=None, ta=FAKE, tb=FAKE) == QL_EINVAL
+    assert fwd_ex(ql.Epilogue(None, None, 0, FAKE, FAKE), y=None, ta=FAKE, tb=FAKE) == QL_EINVAL
+    assert fwd_ex(ql.Epilogue(None, None, 0, FAKE, None)) == QL_EINVAL
+    assert fwd_ex(ql.Epilogue(None, None, 0, None, FAKE)) == QL_EINVAL
+    assert fwd_ex(ql.Epilogue(FAKE + 4, None, 0, None, None)) == QL_EINVAL  # 16-byte alignment
+    # the statistics need partial sums in the workspace; the affine and ReLU alone need none
+    plain = L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d))
+    none_epi = L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), None)
+    relu = ql.Epilogue(FAKE, FAKE, 1, None, None)
+    stats = ql.Epilogue(None, None, 0, FAKE, FAKE)
+    assert none_epi == plain
+    assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(relu)) == plain
+    need = L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(stats))
+    assert need >= plain + 2 * 16 * 4
+    assert fwd_ex(stats, ws=FAKE, wsb=need - 1) == QL_EWORKSPACE
+    assert L.qlayer_linear_fwd_ex_workspace_size(ctypes.byref(ld), ctypes.byref(stats)) >= \
+        L.qlayer_linear_fwd_workspace_size(ctypes.byref(ld)) + 2 * 64 * 4
+    # depthwise: no workspace but the statistics' partial sums
+    dd = ql.conv_desc(2, 32, 8, 8, 32, 3, 3, 1, 1, ql.QL_BF16, 0, groups=32)
+    assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(dd), ctypes.byref(relu)) == 0
+    assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(dd), ctypes.byref(stats)) >= 2 * 32 * 4
