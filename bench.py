@@ -539,6 +539,7 @@ def extra_workloads(ql, torch, dev, stream, reps=10):
         "fwd_bwd_tflops": round(9 * u / (ms * 1e-3) / 1e12, 1)}
     out["neuron_types"] = neuron_types(ql, torch, dev, stream, reps)
     out["depthwise"] = depthwise(ql, torch, dev, stream, reps)
+    out["epilogue"] = epilogue_cost(ql, torch, dev, stream, reps)
     out["hybrid_bp_memory"] = hybrid_bp_memory(torch, dev)
     return out
 
@@ -623,6 +624,51 @@ def depthwise(ql, torch, dev, stream, reps=10):
         r[f"{f}_gbs"] = round(gbs, 1)
         r[f"{f}_frac"] = round(gbs / HBM_PEAK_GBS, 3)
     res["large_dw"] = r
+    return res
+
+
+def epilogue_cost(ql, torch, dev, stream, reps=10):
+    """The fused forward epilogue on the 13 VGG-16 layers (bf16, batch 128), the
+    forward of each layer summed: plain; with the batch-normalization sums of
+    Y (training); with a per-channel scale / shift and ReLU (a batch
+    normalization with fixed statistics, then the activation; section 4.2).
+    For comparison, the sums taken by a separate torch reduction over the
+    stored Y (torch.var_mean over N, H, W)."""
+    import synth
+
+    geoms = synth.vgg16_layers(128)
+    layers = [Layer(ql, torch, L, 2, i, dev) for i, L in enumerate(geoms)]
+    stats, affs, wss = [], [], []
+    for ly in layers:
+        O = ly.L.o
+        ssum, ssq = torch.empty(O, device=dev), torch.empty(O, device=dev)
+        sc, sh = torch.rand(O, device=dev) + 0.5, torch.randn(O, device=dev)
+        e_stat = ql.epilogue(None, None, False, ssum, ssq)
+        e_aff = ql.epilogue(sc, sh, True)
+        need = max(ql.qlayer_conv2d_fwd_ex_workspace_size(ly.desc, e_stat), 256)
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        stats.append((e_stat, ssum, ssq))
+        affs.append((e_aff, sc, sh))
+        wss.append(ws)
+
+    def fwd_ex(i, e):
+        ly = layers[i]
+        return lambda st: ql.qlayer_conv2d_fwd_ex(ly.desc, ly.x, *ly.w, *ly.b, ly.y, ly.ta, ly.tb, epi=e,
+                                                  workspace=(wss[i].data_ptr(), wss[i].numel()), stream=st)
+
+    def torch_stats(i):
+        ly = layers[i]
+        return lambda st: torch.var_mean(ly.y.float(), dim=(0, 1, 2), unbiased=False)
+
+    res = {"shape": "13 VGG-16 layers, bf16, batch 128, forward only, us summed over the layers"}
+    for name, calls in (("plain", [(i, layers[i].fwd) for i in range(len(layers))]),
+                        ("bn_sums", [(i, fwd_ex(i, stats[i][0])) for i in range(len(layers))]),
+                        ("scale_shift_relu", [(i, fwd_ex(i, affs[i][0])) for i in range(len(layers))]),
+                        ("plain_then_torch_sums", [c for i in range(len(layers))
+                                                   for c in ((i, layers[i].fwd), (("t", i), torch_stats(i)))])):
+        _, _, fam_ms, fam_n = time_calls(torch, calls, reps, 2, stream)
+        res[f"{name}_us"] = round(sum(fam_ms[k] / fam_n[k] for k in fam_ms) * 1e3, 1)
+    del layers
     return res
 
 

@@ -410,6 +410,7 @@ __global__ __launch_bounds__(kThreads) void qconv_channel_stats_kernel(const T *
     float s1[4] = {0.0f, 0.0f, 0.0f, 0.0f}, s2[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     const bool v4 = (O & 3) == 0;
     if (c < O) {
+#pragma unroll 4
         for (int r = r0 + rl; r < r1; r += 16) {
             float v[4];
             const T *p = y + (size_t)r * O + c;
@@ -443,24 +444,23 @@ __global__ __launch_bounds__(kThreads) void qconv_channel_stats_kernel(const T *
 }
 
 // Sum of the per-part statistics [part][2][O] in part order: sum[o] and sumsq[o].
-// A block takes 16 indices j of [2][O]; 16 lanes sum every 16th part and the
-// lane sums are added in lane order.
+// A block takes 4 indices j of [2][O]; 64 lanes per index sum every 64th
+// part, and the lane sums are added in lane order.
 __global__ __launch_bounds__(kThreads) void qconv_stats_reduce_kernel(const float *__restrict__ part, int nparts,
                                                                        int O, float *sum, float *sumsq) {
-    __shared__ float red[16][17];
-    const int jl = threadIdx.x & 15, sl = threadIdx.x >> 4;
-    const int j = blockIdx.x * 16 + jl;
+    __shared__ float red[4][65];
+    const int jl = threadIdx.x >> 6, sl = threadIdx.x & 63;
+    const int j = blockIdx.x * 4 + jl;
     float s = 0.0f;
     if (j < 2 * O) {
 #pragma unroll 4
-        for (int p = sl; p < nparts; p += 16) s += part[(size_t)p * 2 * O + j];
+        for (int p = sl; p < nparts; p += 64) s += part[(size_t)p * 2 * O + j];
     }
-    red[sl][jl] = s;
+    red[jl][sl] = s;
     __syncthreads();
     if (sl == 0 && j < 2 * O) {
         float t = 0.0f;
-#pragma unroll
-        for (int l = 0; l < 16; ++l) t += red[l][jl];
+        for (int l = 0; l < 64; ++l) t += red[jl][l];
         if (j < O) sum[j] = t;
         else sumsq[j - O] = t;
     }

@@ -1050,7 +1050,7 @@ ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *w
         s = hip_status();
         if (s != QL_OK) return s;
     }
-    hipLaunchKernelGGL(qconv_stats_reduce_kernel, dim3(cdiv(2 * g.O, 16)), dim3(kThreads), 0, st, stat_part,
+    hipLaunchKernelGGL(qconv_stats_reduce_kernel, dim3(cdiv(2 * g.O, 4)), dim3(kThreads), 0, st, stat_part,
                        sp.nparts, g.O, e->sum, e->sumsq);
     return hip_status();
 }

@@ -239,18 +239,21 @@ def test_epilogue_validation(L):
     assert fwd_ex(ql.Epilogue(None, None, 0, None, FAKE)) == QL_EINVAL
     assert fwd_ex(ql.Epilogue(FAKE + 4, None, 0, None, None)) == QL_EINVAL  # 16-byte alignment
     # the statistics need partial sums in the workspace; the affine and ReLU alone need none
-    plain = L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d))
-    none_epi = L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), None)
     relu = ql.Epilogue(FAKE, FAKE, 1, None, None)
     stats = ql.Epilogue(None, None, 0, FAKE, FAKE)
-    assert none_epi == plain
+    plain = L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d))
+    assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), None) == plain
     assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(relu)) == plain
+    assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(stats)) <= plain + 256  # 128 rows
+    d = ql.conv_desc(8, 64, 32, 32, 64, 3, 3, 1, 1, ql.QL_BF16)
+    plain = L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d))
     need = L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(stats))
-    assert need >= plain + 2 * 16 * 4
+    assert need >= plain + 2 * 64 * 4
     assert fwd_ex(stats, ws=FAKE, wsb=need - 1) == QL_EWORKSPACE
+    ld = ql.linear_desc(8192, 64, 64, ql.QL_BF16)
     assert L.qlayer_linear_fwd_ex_workspace_size(ctypes.byref(ld), ctypes.byref(stats)) >= \
         L.qlayer_linear_fwd_workspace_size(ctypes.byref(ld)) + 2 * 64 * 4
     # depthwise: no workspace but the statistics' partial sums
-    dd = ql.conv_desc(2, 32, 8, 8, 32, 3, 3, 1, 1, ql.QL_BF16, 0, groups=32)
+    dd = ql.conv_desc(8, 32, 32, 32, 32, 3, 3, 1, 1, ql.QL_BF16, 0, groups=32)
     assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(dd), ctypes.byref(relu)) == 0
     assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(dd), ctypes.byref(stats)) >= 2 * 32 * 4
