@@ -18,6 +18,12 @@ one of the earlier designs of Table 1 (T4, T4 + identity, T3, T2).  Weights
 and biases of the terms a type lacks are passed as None.  T2 saves nothing
 but X in either mode (its backward needs only X).
 
+``relu=True`` applies the activation deeper networks put after each
+quadratic layer (section 4.2, model construction) in the forward kernel's
+epilogue; the backward masks the incoming gradient with y' > 0 before the
+layer's own gradients.  ``groups`` (convolution): 1, or C for the
+depth-wise setting (weights (C, 1, KH, KW)).
+
 Layouts.  Convolution tensors are NCHW-shaped torch tensors; they are used in
 channels_last memory format, whose memory is the library's NHWC (OHWI for
 weights), so channels_last inputs are not copied and the outputs come back
@@ -29,9 +35,9 @@ from __future__ import annotations
 
 import torch
 
-from . import (NEURON_TERMS, QL_BF16, QL_F32, QL_NEURON_QUADRA, QL_NEURON_T2, conv_desc, linear_desc,
-               qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_weight, qlayer_conv2d_fwd, qlayer_linear_bwd,
-               qlayer_linear_fwd)
+from . import (NEURON_TERMS, QL_BF16, QL_F32, QL_NEURON_QUADRA, QL_NEURON_T2, conv_desc, epilogue, linear_desc,
+               qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_weight, qlayer_conv2d_fwd, qlayer_conv2d_fwd_ex,
+               qlayer_linear_bwd, qlayer_linear_fwd, qlayer_linear_fwd_ex)
 
 __all__ = ["quad_conv2d", "quad_linear", "QuadConv2dFunction", "QuadLinearFunction"]
 
@@ -66,27 +72,29 @@ def _terms(ws, nt):
 
 class QuadConv2dFunction(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x, wa, wb, wc, ba, bb, bc, stride, pad, recompute, neuron=QL_NEURON_QUADRA):
+    def forward(ctx, x, wa, wb, wc, ba, bb, bc, stride, pad, recompute, neuron=QL_NEURON_QUADRA, relu=False,
+                groups=1):
         N, C, H, W = x.shape
         O, C2, KH, KW = wa.shape
         nt = NEURON_TERMS[neuron]
         ws = _terms((wa, wb, wc), nt)
-        if C2 != C or any(w.shape != wa.shape for w in ws[:nt]):
-            raise ValueError("weight shapes must be (O, C, KH, KW) for every term")
-        d = conv_desc(N, C, H, W, O, KH, KW, stride, pad, _qdtype(x), neuron)
+        if C2 * groups != C or any(w.shape != wa.shape for w in ws[:nt]):
+            raise ValueError("weight shapes must be (O, C / groups, KH, KW) for every term")
+        d = conv_desc(N, C, H, W, O, KH, KW, stride, pad, _qdtype(x), neuron, groups=groups)
         xn = _nhwc(x)
         wn = [_nhwc(w.to(x.dtype)) if w is not None else None for w in ws]
         b = _biases(ba, bb, bc, nt)
         bl = b if b is not None else [None, None, None]
         y = torch.empty((N, d.ho, d.wo, O), device=x.device, dtype=x.dtype)
         recompute = recompute or neuron == QL_NEURON_T2  # (T2 saves nothing but X)
-        if recompute:
-            qlayer_conv2d_fwd(d, xn, *wn, *bl, y)
+        ta = torch.empty_like(y) if not recompute else None
+        tb = torch.empty_like(y) if not recompute and nt >= 2 else None
+        if relu:
+            qlayer_conv2d_fwd_ex(d, xn, *wn, *bl, y, ta, tb, epi=epilogue(relu=True))
         else:
-            ta = torch.empty_like(y)
-            tb = torch.empty_like(y) if nt >= 2 else None
             qlayer_conv2d_fwd(d, xn, *wn, *bl, y, ta, tb)
         ctx.maps = None if recompute else (ta, tb)
+        ctx.relu_out = y if relu else None  # the mask y' > 0 of the backward
         ctx.save_for_backward(xn, *[w for w in wn if w is not None], *[v for v in (b or []) if v is not None])
         ctx.desc, ctx.recompute, ctx.has_bias, ctx.nt, ctx.neuron = d, recompute, b is not None, nt, neuron
         ctx.wdtype = wa.dtype
@@ -109,6 +117,8 @@ class QuadConv2dFunction(torch.autograd.Function):
         else:
             ta, tb = ctx.maps
         gyn = _nhwc(gy.to(xn.dtype))
+        if ctx.relu_out is not None:
+            gyn = gyn * (ctx.relu_out > 0).to(gyn.dtype)
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
         dx = dw = db = None
@@ -126,12 +136,12 @@ class QuadConv2dFunction(torch.autograd.Function):
             dw = [g.permute(0, 3, 1, 2).to(ctx.wdtype) if g is not None else None for g in dwn]
         dw = dw or [None, None, None]
         db = db or [None, None, None]
-        return (dx, *dw, *db, None, None, None, None)
+        return (dx, *dw, *db, None, None, None, None, None, None)
 
 
 class QuadLinearFunction(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x, wa, wb, wc, ba, bb, bc, recompute, neuron=QL_NEURON_QUADRA):
+    def forward(ctx, x, wa, wb, wc, ba, bb, bc, recompute, neuron=QL_NEURON_QUADRA, relu=False):
         B, I = x.shape
         O = wa.shape[0]
         nt = NEURON_TERMS[neuron]
@@ -142,13 +152,14 @@ class QuadLinearFunction(torch.autograd.Function):
         bl = b if b is not None else [None, None, None]
         y = torch.empty((B, O), device=x.device, dtype=x.dtype)
         recompute = recompute or neuron == QL_NEURON_T2
-        if recompute:
-            qlayer_linear_fwd(d, xc, *wl, *bl, y)
+        ta = torch.empty_like(y) if not recompute else None
+        tb = torch.empty_like(y) if not recompute and nt >= 2 else None
+        if relu:
+            qlayer_linear_fwd_ex(d, xc, *wl, *bl, y, ta, tb, epi=epilogue(relu=True))
         else:
-            ta = torch.empty_like(y)
-            tb = torch.empty_like(y) if nt >= 2 else None
             qlayer_linear_fwd(d, xc, *wl, *bl, y, ta, tb)
         ctx.maps = None if recompute else (ta, tb)
+        ctx.relu_out = y if relu else None
         ctx.save_for_backward(xc, *[w for w in wl if w is not None], *[v for v in (b or []) if v is not None])
         ctx.desc, ctx.recompute, ctx.has_bias, ctx.nt, ctx.neuron = d, recompute, b is not None, nt, neuron
         ctx.wdtype = wa.dtype
@@ -171,6 +182,8 @@ class QuadLinearFunction(torch.autograd.Function):
         else:
             ta, tb = ctx.maps
         gyc = gy.to(xc.dtype).contiguous()
+        if ctx.relu_out is not None:
+            gyc = gyc * (ctx.relu_out > 0).to(gyc.dtype)
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
         dx = torch.empty_like(xc) if need_x else None
@@ -181,15 +194,16 @@ class QuadLinearFunction(torch.autograd.Function):
         qlayer_linear_bwd(d, xc, gyc, ta, tb, *wl, dx, *(dw or [None] * 3), *(db or [None] * 3))
         dw = [g.to(ctx.wdtype) if g is not None else None for g in dw] if dw is not None else [None, None, None]
         db = db or [None, None, None]
-        return (dx, *dw, *db, None, None)
+        return (dx, *dw, *db, None, None, None)
 
 
 def quad_conv2d(x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, stride=1, pad=0, recompute=False,
-                neuron=QL_NEURON_QUADRA):
+                neuron=QL_NEURON_QUADRA, relu=False, groups=1):
     """Quadratic 2-D convolution layer (NCHW-shaped tensors, channels_last memory)."""
-    return QuadConv2dFunction.apply(x, wa, wb, wc, ba, bb, bc, stride, pad, recompute, neuron)
+    return QuadConv2dFunction.apply(x, wa, wb, wc, ba, bb, bc, stride, pad, recompute, neuron, relu, groups)
 
 
-def quad_linear(x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, recompute=False, neuron=QL_NEURON_QUADRA):
+def quad_linear(x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, recompute=False, neuron=QL_NEURON_QUADRA,
+                relu=False):
     """Quadratic fully-connected layer: x (B, I), weights (O, I)."""
-    return QuadLinearFunction.apply(x, wa, wb, wc, ba, bb, bc, recompute, neuron)
+    return QuadLinearFunction.apply(x, wa, wb, wc, ba, bb, bc, recompute, neuron, relu)

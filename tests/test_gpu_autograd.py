@@ -167,3 +167,66 @@ def test_linear_autograd_neuron_types(neuron):
     for k, v in got.items():
         e = qlh.relerr(v.double().cpu().numpy(), ref[k])
         assert e <= qlh.tol(True, k != "y"), f"{k}: normwise relative error {e:.3e}"
+
+
+@pytest.mark.parametrize("recompute", [False, True], ids=["save", "recompute"])
+def test_conv_autograd_fused_relu(recompute):
+    """relu=True: y' = relu(Y) from the forward epilogue; the backward masks G with y' > 0
+    (oracle: the layer's gradients of the masked G), fp32."""
+    N, C, H, W, O, s, p = 2, 16, 8, 8, 24, 1, 1
+    inp = synth.random_conv_case([420], N, C, H, W, O, 3, 3, s, p)
+    y, _, _ = oracle.conv2d_fwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"], s, p)
+    yr, _, _ = oracle.epilogue(y, relu=True)
+    gm = inp["gy"] * (yr > 0)
+    ref = oracle.conv2d_bwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"], gm, s, p)
+    x = _t(inp["x"], torch.float32).contiguous(memory_format=torch.channels_last).detach().requires_grad_(True)
+    w = [_t(inp[k], torch.float32) for k in ("wa", "wb", "wc")]
+    b = [_t(inp[k], torch.float32) for k in ("ba", "bb", "bc")]
+    out = quad_conv2d(x, *w, *b, stride=s, pad=p, recompute=recompute, relu=True)
+    out.backward(_t(inp["gy"], torch.float32, grad=False))
+    torch.cuda.synchronize()
+    assert qlh.relerr(out.detach().double().cpu().numpy(), yr) <= qlh.tol(False, False)
+    got = {"dx": x.grad, "dwa": w[0].grad, "dwb": w[1].grad, "dwc": w[2].grad, "dba": b[0].grad,
+           "dbb": b[1].grad, "dbc": b[2].grad}
+    for k, v in got.items():
+        assert qlh.relerr(v.double().cpu().numpy(), ref[k]) <= qlh.tol(False, True), k
+
+
+def test_linear_autograd_fused_relu():
+    B, I, O = 64, 48, 40
+    inp = synth.random_dense_case([421], B, I, O)
+    y = oracle.linear_fwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"])[0]
+    yr, _, _ = oracle.epilogue(y, relu=True)
+    ref = oracle.linear_bwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"],
+                            inp["gy"] * (yr > 0))
+    x = _t(inp["x"], torch.float32)
+    w = [_t(inp[k], torch.float32) for k in ("wa", "wb", "wc")]
+    b = [_t(inp[k], torch.float32) for k in ("ba", "bb", "bc")]
+    out = quad_linear(x, *w, *b, relu=True)
+    out.backward(_t(inp["gy"], torch.float32, grad=False))
+    torch.cuda.synchronize()
+    assert qlh.relerr(out.detach().double().cpu().numpy(), yr) <= qlh.tol(False, False)
+    for k, v in (("dx", x.grad), ("dwa", w[0].grad), ("dwc", w[2].grad), ("dbb", b[1].grad)):
+        assert qlh.relerr(v.double().cpu().numpy(), ref[k]) <= qlh.tol(False, True), k
+
+
+@pytest.mark.parametrize("recompute", [False, True], ids=["save", "recompute"])
+def test_conv_autograd_depthwise(recompute):
+    """groups = C through the autograd function against the depthwise oracle (bf16)."""
+    N, C, H, W, K, s, p = 2, 32, 9, 7, 3, 1, 1
+    inp = synth.random_dwconv_case([422], N, C, H, W, K, K, s, p, bf16=True)
+    y, _, _ = oracle.dwconv2d_fwd(0, inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"],
+                                  stride=s, pad=p)
+    ref = oracle.dwconv2d_bwd(0, inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"],
+                              inp["gy"], stride=s, pad=p)
+    ref["y"] = y
+    x = _t(inp["x"], torch.bfloat16).contiguous(memory_format=torch.channels_last).detach().requires_grad_(True)
+    w = [_t(inp[k], torch.bfloat16) for k in ("wa", "wb", "wc")]
+    b = [_t(inp[k], torch.float32) for k in ("ba", "bb", "bc")]
+    out = quad_conv2d(x, *w, *b, stride=s, pad=p, recompute=recompute, groups=C)
+    out.backward(_t(inp["gy"], torch.bfloat16, grad=False))
+    torch.cuda.synchronize()
+    got = {"y": out.detach(), "dx": x.grad, "dwa": w[0].grad, "dwb": w[1].grad, "dwc": w[2].grad,
+           "dba": b[0].grad, "dbb": b[1].grad, "dbc": b[2].grad}
+    for k in ref:
+        assert qlh.relerr(got[k].double().cpu().numpy(), ref[k]) <= qlh.tol(True, k != "y"), k
