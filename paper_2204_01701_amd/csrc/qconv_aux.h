@@ -29,6 +29,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float
 #pragma unroll
             for (int e = 0; e < E; ++e) t3[t][e] = (t < nt && bp[t]) ? bp[t][o + e] : 0.0f;
             if (t >= nt) continue;
+#pragma unroll 4
             for (int sp = 0; sp < splits; ++sp) {
                 const float *src = ws + ((size_t)sp * 3 + t) * MO + idx;
                 if constexpr (V4) {
@@ -79,6 +80,7 @@ __global__ __launch_bounds__(kThreads) void qconv_sum_splits_kernel(const float 
         float acc[E];
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+#pragma unroll 4
         for (int sp = 0; sp < splits; ++sp) {
             const float *p = ws + (size_t)sp * total + idx;
             if constexpr (V4) {
@@ -124,6 +126,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce_kernel(const
             float acc[E];
 #pragma unroll
             for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+#pragma unroll 4
             for (int sp = 0; sp < splits; ++sp) {
                 const float *src = ws_dw + ((size_t)sp * 3 + t) * ndw + j;
                 if constexpr (V4) {
@@ -147,6 +150,58 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce_kernel(const
             float *d = t == 0 ? db0 : (t == 1 ? db1 : db2);
             d[o] = s;
         }
+    }
+}
+
+// The same reduction for small outputs with many splits, 16-byte vectors
+// (ndw % 4 == 0): a block takes 16 items (an item is 4 consecutive dW_t
+// values, or one bias value after the nterms ndw / 4 vectors); 16 split
+// lanes per item sum every 16th split (unrolled, the loads independent) and
+// the lane sums are added in lane order, the same order as the scalar kernel.
+__global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce2dv_kernel(const float *__restrict__ ws_dw,
+                                                                              const float *__restrict__ ws_db,
+                                                                              int splits, long long ndw, int O,
+                                                                              float *dw0, float *dw1, float *dw2,
+                                                                              float *db0, float *db1, float *db2,
+                                                                              int want_db, int nterms) {
+    __shared__ v4f part[16][17];
+    const long long nv = (long long)nterms * ndw / 4;
+    const long long total = nv + (want_db ? (long long)nterms * O : 0LL);
+    const int it = threadIdx.x & 15, sl = threadIdx.x >> 4;
+    for (long long base = (long long)blockIdx.x * 16; base < total; base += (long long)gridDim.x * 16) {
+        const long long i = base + it;
+        v4f s = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (i < nv) {
+            const long long idx = i * 4;
+            const int t = (int)(idx / ndw);
+            const long long j = idx - t * ndw;
+#pragma unroll 4
+            for (int sp = sl; sp < splits; sp += 16) s += *reinterpret_cast<const v4f *>(ws_dw + ((size_t)sp * 3 + t) * ndw + j);
+        } else if (i < total) {
+            const long long jj = i - nv;
+            const int t = (int)(jj / O), o = (int)(jj % O);
+#pragma unroll 4
+            for (int sp = sl; sp < splits; sp += 16) s[0] += ws_db[((size_t)sp * 3 + t) * O + o];
+        }
+        part[sl][it] = s;
+        __syncthreads();
+        if (sl == 0 && i < total) {
+            v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int k = 0; k < 16; ++k) acc += part[k][it];
+            if (i < nv) {
+                const long long idx = i * 4;
+                const int t = (int)(idx / ndw);
+                float *d = t == 0 ? dw0 : (t == 1 ? dw1 : dw2);
+                *reinterpret_cast<v4f *>(d + (idx - t * ndw)) = acc;
+            } else {
+                const long long jj = i - nv;
+                const int t = (int)(jj / O), o = (int)(jj % O);
+                float *d = t == 0 ? db0 : (t == 1 ? db1 : db2);
+                d[o] = acc[0];
+            }
+        }
+        __syncthreads();
     }
 }
 

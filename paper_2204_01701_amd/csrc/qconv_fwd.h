@@ -15,6 +15,8 @@
 // qconv_fwd_combine_kernel applies the biases and the product.
 #pragma once
 
+#include <type_traits>
+
 #include "qargs.h"
 #include "qpipe.h"
 
@@ -247,146 +249,161 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     };
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
     const bool vec_out = (a.O & 3) == 0;
-    if (a.splits == 1) {
-        T *__restrict__ y = static_cast<T *>(a.y);
-        T *__restrict__ ta = static_cast<T *>(a.ta);
-        T *__restrict__ tb = static_cast<T *>(a.tb);
-        // Staged stores: each output map of the tile is written into the idle
-        // LDS ring as BCOL pixel rows of BR channels, then copied out in
-        // 16-byte chunks, consecutive lanes on consecutive addresses (one
-        // pixel's BR channels are contiguous in NHWC), instead of 4-channel
-        // pieces scattered over 32 pixel rows per store instruction.
-        constexpr int E = (int)sizeof(T);
-        constexpr int PITCH = BR * E + 16;  // LDS bytes per staged pixel row
-        constexpr int MAPB = BCOL * PITCH;
-        constexpr int PER = 3 * MAPB <= NS * STAGE ? 3 : 1;  // maps staged per round
-        constexpr int CPR = BR * E / 16;                       // 16-byte chunks per row
-        constexpr int VE = 16 / E;                             // channels per chunk
-        static_assert((CPR & (CPR - 1)) == 0 && NT % CPR == 0, "staged epilogue tile");
-        static_assert(fwd_staged_fits(BR, BCOL, NS, E) == (MAPB <= NS * STAGE), "staged epilogue predicate");
-        if constexpr (MAPB <= NS * STAGE) {  // (otherwise, and for O not a multiple of 16 / E: direct stores)
-            if (a.O % (16 / E) == 0) {
-                T *outs[3] = {y, ta, NTM >= 2 ? tb : nullptr};
-                // Epilogue statistics: a thread copies chunks of one channel
-                // group (its chunk index mod CPR is fixed), so it sums its VE
-                // channels of y' over its pixel rows in registers.
-                const bool stats = a.stat_part != nullptr;
-                float ssum[VE], ssq[VE];
-#pragma unroll
-                for (int k = 0; k < VE; ++k) ssum[k] = ssq[k] = 0.0f;
-#pragma unroll
-                for (int r0 = 0; r0 < 3; r0 += PER) {
-                    lds_barrier();  // every wave is done with the ring (or the previous round's copy)
-#pragma unroll
-                    for (int j = r0; j < r0 + PER; ++j) {
-                        if (!outs[j]) continue;
-                        char *tile = smem + (j - r0) * MAPB;
-#pragma unroll
-                        for (int mr = 0; mr < MR; ++mr)
-#pragma unroll
-                            for (int mc = 0; mc < MC; ++mc) {
-                                const int p = wc * (BCOL / WGC) + mc * 32 + lrow;
-#pragma unroll
-                                for (int g = 0; g < 4; ++g) {
-                                    const int ol = wr * (BR / WGR) + mr * 32 + 8 * g + 4 * lhi;
-                                    float v[4], xv[4];
-                                    if (j == 0) xs4(ct * BCOL + p, rt * BR + ol, xv);
-#pragma unroll
-                                    for (int i = 0; i < 4; ++i) {
-                                        v[i] = outv(j, mr, mc, 4 * g + i, j == 0 ? xv[i] : 0.0f);
-                                        const int o = rt * BR + ol + i;
-                                        if (j == 0 && o < a.O) v[i] = epi_apply(a.epi, o, v[i]);
-                                    }
-                                    store4<T>(reinterpret_cast<T *>(tile + p * PITCH + ol * E), v[0], v[1], v[2], v[3]);
-                                }
-                            }
-                    }
-                    lds_barrier();
-#pragma unroll
-                    for (int j = r0; j < r0 + PER; ++j) {
-                        if (!outs[j]) continue;
-                        const char *tile = smem + (j - r0) * MAPB;
-                        for (int c = tid; c < BCOL * CPR; c += NT) {
-                            const int row = c / CPR, cc = c % CPR;
-                            const int m = ct * BCOL + row, o = rt * BR + cc * (16 / E);
-                            if (m < a.M && o < a.O) {
-                                const v4u val = lds_read16(tile + row * PITCH + cc * 16);
-                                *reinterpret_cast<v4u *>(outs[j] + (size_t)m * a.O + o) = val;
-                                if (j == 0 && stats) {
-#pragma unroll
-                                    for (int k = 0; k < VE; ++k) {
-                                        const float f = vget<T>(val, k);  // the stored value
-                                        ssum[k] += f;
-                                        ssq[k] += f * f;
+    // The single-split epilogue, compiled twice: EPI adds the fused forward
+    // epilogue (EpiArgs, the statistics); without it the code is the plain one.
+    auto single = [&](auto epi_c) {
+        constexpr bool EPI = decltype(epi_c)::value;
+            T *__restrict__ y = static_cast<T *>(a.y);
+            T *__restrict__ ta = static_cast<T *>(a.ta);
+            T *__restrict__ tb = static_cast<T *>(a.tb);
+            // Staged stores: each output map of the tile is written into the idle
+            // LDS ring as BCOL pixel rows of BR channels, then copied out in
+            // 16-byte chunks, consecutive lanes on consecutive addresses (one
+            // pixel's BR channels are contiguous in NHWC), instead of 4-channel
+            // pieces scattered over 32 pixel rows per store instruction.
+            constexpr int E = (int)sizeof(T);
+            constexpr int PITCH = BR * E + 16;  // LDS bytes per staged pixel row
+            constexpr int MAPB = BCOL * PITCH;
+            constexpr int PER = 3 * MAPB <= NS * STAGE ? 3 : 1;  // maps staged per round
+            constexpr int CPR = BR * E / 16;                       // 16-byte chunks per row
+            constexpr int VE = 16 / E;                             // channels per chunk
+            static_assert((CPR & (CPR - 1)) == 0 && NT % CPR == 0, "staged epilogue tile");
+            static_assert(fwd_staged_fits(BR, BCOL, NS, E) == (MAPB <= NS * STAGE), "staged epilogue predicate");
+            if constexpr (MAPB <= NS * STAGE) {  // (otherwise, and for O not a multiple of 16 / E: direct stores)
+                if (a.O % (16 / E) == 0) {
+                    T *outs[3] = {y, ta, NTM >= 2 ? tb : nullptr};
+                    // Epilogue statistics: a thread copies chunks of one channel
+                    // group (its chunk index mod CPR is fixed), so it sums its VE
+                    // channels of y' over its pixel rows in registers.
+                    const bool stats = EPI && a.stat_part != nullptr;
+                    float ssum[VE], ssq[VE];
+    #pragma unroll
+                    for (int k = 0; k < VE; ++k) ssum[k] = ssq[k] = 0.0f;
+    #pragma unroll
+                    for (int r0 = 0; r0 < 3; r0 += PER) {
+                        lds_barrier();  // every wave is done with the ring (or the previous round's copy)
+    #pragma unroll
+                        for (int j = r0; j < r0 + PER; ++j) {
+                            if (!outs[j]) continue;
+                            char *tile = smem + (j - r0) * MAPB;
+    #pragma unroll
+                            for (int mr = 0; mr < MR; ++mr)
+    #pragma unroll
+                                for (int mc = 0; mc < MC; ++mc) {
+                                    const int p = wc * (BCOL / WGC) + mc * 32 + lrow;
+    #pragma unroll
+                                    for (int g = 0; g < 4; ++g) {
+                                        const int ol = wr * (BR / WGR) + mr * 32 + 8 * g + 4 * lhi;
+                                        float v[4], xv[4];
+                                        if (j == 0) xs4(ct * BCOL + p, rt * BR + ol, xv);
+    #pragma unroll
+                                        for (int i = 0; i < 4; ++i) {
+                                            v[i] = outv(j, mr, mc, 4 * g + i, j == 0 ? xv[i] : 0.0f);
+                                            if constexpr (EPI) {
+                                                const int o = rt * BR + ol + i;
+                                                if (j == 0 && o < a.O) v[i] = epi_apply(a.epi, o, v[i]);
+                                            }
+                                        }
+                                        store4<T>(reinterpret_cast<T *>(tile + p * PITCH + ol * E), v[0], v[1], v[2], v[3]);
                                     }
                                 }
+                        }
+                        lds_barrier();
+    #pragma unroll
+                        for (int j = r0; j < r0 + PER; ++j) {
+                            if (!outs[j]) continue;
+                            const char *tile = smem + (j - r0) * MAPB;
+                            for (int c = tid; c < BCOL * CPR; c += NT) {
+                                const int row = c / CPR, cc = c % CPR;
+                                const int m = ct * BCOL + row, o = rt * BR + cc * (16 / E);
+                                if (m < a.M && o < a.O) {
+                                    const v4u val = lds_read16(tile + row * PITCH + cc * 16);
+                                    *reinterpret_cast<v4u *>(outs[j] + (size_t)m * a.O + o) = val;
+                                    if constexpr (EPI) {
+                                        if (j == 0 && stats) {
+    #pragma unroll
+                                            for (int k = 0; k < VE; ++k) {
+                                                const float f = vget<T>(val, k);  // the stored value
+                                                ssum[k] += f;
+                                                ssq[k] += f * f;
+                                            }
+                                        }
+                                    }
+                                }
                             }
                         }
                     }
-                }
-                if (stats) {
-                    // channel ol = cc VE + k of the tile: threads tid = cc (mod CPR), summed in tid order
-                    lds_barrier();
-                    float *red = reinterpret_cast<float *>(smem);
-#pragma unroll
-                    for (int k = 0; k < VE; ++k) {
-                        red[tid * 2 * VE + k] = ssum[k];
-                        red[tid * 2 * VE + VE + k] = ssq[k];
-                    }
-                    lds_barrier();
-                    if (tid < BR) {
-                        const int cc = tid / VE, k = tid - cc * VE;
-                        float s1 = 0.0f, s2 = 0.0f;
-                        for (int u = cc; u < NT; u += CPR) {
-                            s1 += red[u * 2 * VE + k];
-                            s2 += red[u * 2 * VE + VE + k];
+                    if (EPI && stats) {
+                        // channel ol = cc VE + k of the tile: threads tid = cc (mod CPR), summed in tid order
+                        lds_barrier();
+                        float *red = reinterpret_cast<float *>(smem);
+    #pragma unroll
+                        for (int k = 0; k < VE; ++k) {
+                            red[tid * 2 * VE + k] = ssum[k];
+                            red[tid * 2 * VE + VE + k] = ssq[k];
                         }
-                        const int o = rt * BR + tid;
-                        if (o < a.O) {
-                            a.stat_part[(size_t)ct * 2 * a.O + o] = s1;
-                            a.stat_part[(size_t)ct * 2 * a.O + a.O + o] = s2;
+                        lds_barrier();
+                        if (tid < BR) {
+                            const int cc = tid / VE, k = tid - cc * VE;
+                            float s1 = 0.0f, s2 = 0.0f;
+                            for (int u = cc; u < NT; u += CPR) {
+                                s1 += red[u * 2 * VE + k];
+                                s2 += red[u * 2 * VE + VE + k];
+                            }
+                            const int o = rt * BR + tid;
+                            if (o < a.O) {
+                                a.stat_part[(size_t)ct * 2 * a.O + o] = s1;
+                                a.stat_part[(size_t)ct * 2 * a.O + a.O + o] = s2;
+                            }
                         }
                     }
+                    return;
                 }
-                return;
             }
-        }
-#pragma unroll
-        for (int mr = 0; mr < MR; ++mr)
-#pragma unroll
-            for (int mc = 0; mc < MC; ++mc) {
-                const int m = pcol0 + mc * 32 + lrow;
-                if (m >= a.M) continue;
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int o = orow0 + mr * 32 + 8 * g + 4 * lhi;
-                    if (o >= a.O) continue;
-                    float va[4], vb[4], vy[4], xv[4];
-                    xs4(m, o, xv);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        va[i] = outv(1, mr, mc, 4 * g + i, 0.0f);
-                        vb[i] = NTM >= 2 ? outv(2, mr, mc, 4 * g + i, 0.0f) : 0.0f;
-                        vy[i] = outv(0, mr, mc, 4 * g + i, xv[i]);
-                        if (o + i < a.O) vy[i] = epi_apply(a.epi, o + i, vy[i]);
-                    }
-                    if (NTM < 2) tb = nullptr;
-                    const size_t off = (size_t)m * a.O + o;
-                    if (vec_out) {
-                        if (y) store4<T>(y + off, vy[0], vy[1], vy[2], vy[3]);
-                        if (ta) store4<T>(ta + off, va[0], va[1], va[2], va[3]);
-                        if (tb) store4<T>(tb + off, vb[0], vb[1], vb[2], vb[3]);
-                    } else {
-#pragma unroll
+    #pragma unroll
+            for (int mr = 0; mr < MR; ++mr)
+    #pragma unroll
+                for (int mc = 0; mc < MC; ++mc) {
+                    const int m = pcol0 + mc * 32 + lrow;
+                    if (m >= a.M) continue;
+    #pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int o = orow0 + mr * 32 + 8 * g + 4 * lhi;
+                        if (o >= a.O) continue;
+                        float va[4], vb[4], vy[4], xv[4];
+                        xs4(m, o, xv);
+    #pragma unroll
                         for (int i = 0; i < 4; ++i) {
-                            if (o + i >= a.O) break;
-                            if (y) y[off + i] = from_f32<T>(vy[i]);
-                            if (ta) ta[off + i] = from_f32<T>(va[i]);
-                            if (tb) tb[off + i] = from_f32<T>(vb[i]);
+                            va[i] = outv(1, mr, mc, 4 * g + i, 0.0f);
+                            vb[i] = NTM >= 2 ? outv(2, mr, mc, 4 * g + i, 0.0f) : 0.0f;
+                            vy[i] = outv(0, mr, mc, 4 * g + i, xv[i]);
+                            if constexpr (EPI) {
+                                if (o + i < a.O) vy[i] = epi_apply(a.epi, o + i, vy[i]);
+                            }
+                        }
+                        if (NTM < 2) tb = nullptr;
+                        const size_t off = (size_t)m * a.O + o;
+                        if (vec_out) {
+                            if (y) store4<T>(y + off, vy[0], vy[1], vy[2], vy[3]);
+                            if (ta) store4<T>(ta + off, va[0], va[1], va[2], va[3]);
+                            if (tb) store4<T>(tb + off, vb[0], vb[1], vb[2], vb[3]);
+                        } else {
+    #pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                if (o + i >= a.O) break;
+                                if (y) y[off + i] = from_f32<T>(vy[i]);
+                                if (ta) ta[off + i] = from_f32<T>(va[i]);
+                                if (tb) tb[off + i] = from_f32<T>(vb[i]);
+                            }
                         }
                     }
                 }
-            }
+    };
+    if (a.splits == 1) {
+        if (a.epi.scale || a.epi.shift || a.epi.relu || a.stat_part)
+            single(std::true_type{});
+        else
+            single(std::false_type{});
     } else {
 #pragma unroll
         for (int t = 0; t < NTM; ++t) {

@@ -713,7 +713,12 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
     const long long ndw = (long long)g.O * g.KH * g.KW * g.C;  // dW_t as stored
-    if (3 * ndw < (1LL << 20) && p.splits >= 16)
+    if (3 * ndw < (1LL << 20) && p.splits >= 16 && ndw % 4 == 0)
+        hipLaunchKernelGGL(qconv_bwd_weight_reduce2dv_kernel, dim3(grid_1d((3 * ndw / 4 + 3 * g.O) * 16)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db, g.terms());
+    else if (3 * ndw < (1LL << 20) && p.splits >= 16)
         hipLaunchKernelGGL((qconv_bwd_weight_reduce2d_kernel<16>), dim3(grid_1d((3 * ndw + 3 * g.O) * 16)),
                            dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
                            static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
