@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
                     help="instead of running: HBM bytes per entry call from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
                          "counter tables of the benchmark and of --copy-calibration")
+    ap.add_argument("--leg", choices=("depthwise", "epilogue", "neuron_types"),
+                    help="instead of the benchmark: run one extra leg alone and print its JSON (for profiling)")
     return ap.parse_args()
 
 
@@ -411,6 +413,10 @@ def main():
     ql.lib()  # fail loudly if the HIP library is missing
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
+    if args.leg:
+        legs = {"depthwise": depthwise, "epilogue": epilogue_cost, "neuron_types": neuron_types}
+        print(json.dumps({args.leg: legs[args.leg](ql, torch, dev, stream)}), flush=True)
+        return
 
     geoms = synth.vgg16_layers(128)
     layers = [Layer(ql, torch, L, 2, i, dev) for i, L in enumerate(geoms)]
