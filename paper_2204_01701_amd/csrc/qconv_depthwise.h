@@ -969,7 +969,7 @@ template <typename T, int OM, int V, bool VEC, int K, int S, int R>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(QL_DW_WAVES_BW)))
 void qconv_dw_bwd_weight_col_kernel(const DwArgs a) {
     constexpr int NTM = om_terms(OM), TAPS = K * K;
-    __shared__ float red[kThreads * V];
+    __shared__ float wsum[(kThreads / 64) * 8 * NTM * (TAPS + 1) * V];  // [wave][channel group][...]
     const int CB = a.lanes * V;
     const int split = blockIdx.x, c0 = blockIdx.y * CB;
     const int cg = threadIdx.x & (a.lanes - 1), pl = threadIdx.x >> a.lsh, PL = kThreads >> a.lsh;
@@ -1009,31 +1009,51 @@ void qconv_dw_bwd_weight_col_kernel(const DwArgs a) {
             if (item >= i_end) break;
         }
     }
-    // Sum over the pixel lanes in lane order: thread i < CB owns channel c0 + i.
-    auto reduce_out = [&](const float *v, float *dst, size_t stride_c) {
-        __syncthreads();
+    // Sum over the pixel lanes in a fixed order: a butterfly over the lanes of
+    // each wave that share the channel group (lane bits lsh .. 5; every
+    // value's exchange of one step issued together), then the four waves in
+    // wave order through LDS.
+    constexpr int NV = NTM * (TAPS + 1) * V;  // per thread: every tap, then the bias sum
+    for (int m = a.lanes; m < 64; m <<= 1) {
 #pragma unroll
-        for (int k = 0; k < V; ++k) red[threadIdx.x * V + k] = v[k];
-        __syncthreads();
-        if (threadIdx.x < CB) {
-            const int g2 = threadIdx.x / V, k = threadIdx.x - g2 * V;
-            float s = 0.0f;
-            for (int l = 0; l < PL; ++l) s += red[((l << a.lsh) + g2) * V + k];
-            const int cc = c0 + threadIdx.x;
-            if (cc < a.C) dst[(size_t)cc * stride_c] = s;
-        }
-    };
+        for (int t = 0; t < NTM; ++t)
 #pragma unroll
-    for (int t = 0; t < NTM; ++t) {
+            for (int k = 0; k < V; ++k) {
 #pragma unroll
-        for (int tap = 0; tap < TAPS; ++tap) {
-            float *dst = a.splits == 1 ? a.dw[t] + tap : a.ws + (size_t)split * a.J + (size_t)t * a.C * TAPS + tap;
-            reduce_out(acc[t][tap], dst, TAPS);
-        }
-        if (a.db[t]) {
-            float *dst = a.splits == 1 ? a.db[t] : a.ws + (size_t)split * a.J + (size_t)(NTM * TAPS + t) * a.C;
-            reduce_out(dsum[t], dst, 1);
-        }
+                for (int u = 0; u < TAPS; ++u) acc[t][u][k] += __shfl_xor(acc[t][u][k], m);
+                dsum[t][k] += __shfl_xor(dsum[t][k], m);
+            }
+    }
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane < a.lanes) {  // one lane per channel group and wave holds the wave's sums
+        float *r = wsum + (wave * 8 + cg) * NV;
+#pragma unroll
+        for (int t = 0; t < NTM; ++t)
+#pragma unroll
+            for (int k = 0; k < V; ++k) {
+#pragma unroll
+                for (int u = 0; u < TAPS; ++u) r[(t * (TAPS + 1) + u) * V + k] = acc[t][u][k];
+                r[(t * (TAPS + 1) + TAPS) * V + k] = dsum[t][k];
+            }
+    }
+    __syncthreads();
+    // output (t, u, channel c0 + cc) for u < TAPS a weight tap, u = TAPS the bias
+    for (int i = threadIdx.x; i < NTM * (TAPS + 1) * CB; i += kThreads) {
+        const int t = i / ((TAPS + 1) * CB), rem = i - t * (TAPS + 1) * CB;
+        const int u = rem / CB, cc = rem - u * CB;
+        const int g2 = cc / V, k = cc - g2 * V;
+        const int ch = c0 + cc;
+        if (ch >= a.C || (u == TAPS && !a.db[t])) continue;
+        float sum = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kThreads / 64; ++w) sum += wsum[(w * 8 + g2) * NV + (t * (TAPS + 1) + u) * V + k];
+        float *dst;
+        if (u < TAPS)
+            dst = a.splits == 1 ? a.dw[t] + (size_t)ch * TAPS + u
+                                : a.ws + (size_t)split * a.J + ((size_t)t * a.C + ch) * TAPS + u;
+        else
+            dst = a.splits == 1 ? a.db[t] + ch : a.ws + (size_t)split * a.J + (size_t)(NTM * TAPS + t) * a.C + ch;
+        *dst = sum;
     }
 }
 
