@@ -201,3 +201,45 @@ def test_epilogue_full_size_layer_and_repeatability():
                                stride=L.stride, pad=L.pad)[0]
     got = np.array([y[n, i, j, o].float().item() for n, o, i, j in idx])
     assert qlh.relerr(got, ref) <= qlh.tol(True, False)
+
+
+@pytest.mark.parametrize("case", [CONV_CASES[0], CONV_CASES[3], CONV_CASES[6]], ids=["staged", "split-k", "depthwise"])
+def test_epilogue_invariants(case, env):
+    """fwd_ex with no epilogue (or an empty one) writes the plain forward's bits; the sums
+    taken with the epilogue equal those of the plain output stored by it; scale = 1, shift = 0
+    changes nothing."""
+    name, N, C, H, W, O, K, s, p, groups, over = case
+    print(f"epilogue invariants {name}", flush=True)
+    env(over)
+    if groups > 1:
+        inp = synth.random_dwconv_case([708], N, C, H, W, K, K, s, p, bf16=True)
+    else:
+        inp = synth.random_conv_case([708], N, C, H, W, O, K, K, s, p, bf16=True)
+    d = ql.conv_desc(N, C, H, W, O, K, K, s, p, ql.QL_BF16, groups=groups)
+    x = qlh.nchw_to_dev(inp["x"], True)
+    w = [qlh.oihw_to_dev(inp[k], True) for k in ("wa", "wb", "wc")]
+    b = [qlh.vec_to_dev(inp[k]) for k in ("ba", "bb", "bc")]
+    outs = []
+    for epi in (None, ql.epilogue(), "stats", "unit"):
+        y = torch.empty((N, d.ho, d.wo, O), device=DEV, dtype=torch.bfloat16)
+        ta, tb = torch.empty_like(y), torch.empty_like(y)
+        sums = None
+        if epi is None:
+            ql.qlayer_conv2d_fwd(d, x, *w, *b, y, ta, tb)
+        elif epi == "stats":
+            sums = (torch.empty(O, device=DEV), torch.empty(O, device=DEV))
+            ql.qlayer_conv2d_fwd_ex(d, x, *w, *b, y, ta, tb, epi=ql.epilogue(None, None, False, *sums))
+        elif epi == "unit":
+            one, zero = torch.ones(O, device=DEV), torch.zeros(O, device=DEV)
+            ql.qlayer_conv2d_fwd_ex(d, x, *w, *b, y, ta, tb, epi=ql.epilogue(one, zero, False))
+        else:
+            ql.qlayer_conv2d_fwd_ex(d, x, *w, *b, y, ta, tb, epi=epi)
+        torch.cuda.synchronize()
+        outs.append((y, ta, tb, sums))
+    for y, ta, tb, _ in outs[1:]:
+        assert torch.equal(y, outs[0][0]) and torch.equal(ta, outs[0][1]) and torch.equal(tb, outs[0][2])
+    yd = outs[0][0].double()
+    s1 = yd.sum(dim=(0, 1, 2)).cpu().numpy()
+    a1 = yd.abs().sum(dim=(0, 1, 2)).cpu().numpy()
+    got = outs[2][3][0].double().cpu().numpy()
+    assert np.all(np.abs(got - s1) <= 3e-5 * a1 + 1e-30)
