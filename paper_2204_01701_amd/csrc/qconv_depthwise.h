@@ -508,29 +508,11 @@ __device__ __forceinline__ void dw_stage_bias(const DwArgs &a, int c0, int CB, f
     }
 }
 
-#ifndef QL_DW_WAVES_FWD
-#define QL_DW_WAVES_FWD 1
-#endif
-#ifndef QL_DW_WAVES_BD
-#define QL_DW_WAVES_BD 1
-#endif
-#ifndef QL_DW_WAVES_BW
-#define QL_DW_WAVES_BW 1
-#endif
-// Filter values are read from LDS inside the chunk loop; without a fence the
-// compiler hoists them into registers (27 V of them), which bounds occupancy.
-#ifdef QL_DW_HOIST
-#define QL_DW_CHUNK_FENCE()
-#else
+// A compiler fence at the top of each chunk: the filter values are then read
+// from LDS within the chunk instead of being hoisted out of the chunk loop
+// into registers (27 V of them), which would bound the occupancy.
 #define QL_DW_CHUNK_FENCE() asm volatile("" ::: "memory")
-#endif
-// Between taps: keeps each tap's filter reads next to its arithmetic (the
-// scheduler would otherwise issue all of them first and hold them in registers).
-#ifdef QL_DW_TAP_FENCE_ON
-#define QL_DW_TAP_FENCE() asm volatile("" ::: "memory")
-#else
-#define QL_DW_TAP_FENCE()
-#endif
+
 // One column of the forward: its position and the raw input rows it sees.
 template <typename T, int V, bool VEC, int K, int S, int R>
 struct DwFwdCol {
@@ -588,7 +570,6 @@ __device__ __forceinline__ void dw_fwd_col_compute(const DwArgs &a, const DwFwdC
     for (int r = 0; r < K; ++r) {
 #pragma unroll
         for (int q = 0; q < K; ++q) {
-            QL_DW_TAP_FENCE();
             float xs[R][V];
 #pragma unroll
             for (int rr = 0; rr < R; ++rr)
@@ -638,7 +619,7 @@ __device__ __forceinline__ void dw_fwd_col_compute(const DwArgs &a, const DwFwdC
 }
 
 template <typename T, int OM, int V, bool VEC, int K, int S, int R, bool PF>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(QL_DW_WAVES_FWD)))
+__global__ __launch_bounds__(kThreads)
 void qconv_dw_fwd_col_kernel(const DwArgs a) {
     constexpr int NTM = om_terms(OM), TAPS = K * K;
     extern __shared__ float wl[];  // [NTM][TAPS][CB], then the biases [NTM][CB]
@@ -760,7 +741,6 @@ __device__ __forceinline__ void dw_bd_col_compute(const DwArgs &a, const DwBdCol
     for (int e = 0; e < NOR; ++e) {
 #pragma unroll
         for (int q = 0; q < K; ++q) {
-            QL_DW_TAP_FENCE();
             float op[3][V];
             dw_ops<OM, V>(b.gv[e][q], op);
 #pragma unroll
@@ -786,7 +766,7 @@ __device__ __forceinline__ void dw_bd_col_compute(const DwArgs &a, const DwBdCol
 // PF: the next column's loads are issued before the current column's
 // arithmetic.  a.M counts the columns N x ceil(H / R) x W.
 template <typename T, int OM, int V, bool VEC, int K, int R, bool PF>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(QL_DW_WAVES_BD)))
+__global__ __launch_bounds__(kThreads)
 void qconv_dw_bwd_data_col_kernel(const DwArgs a) {
     constexpr int NTM = om_terms(OM), NGM = om_gmaps(OM), TAPS = K * K;
     extern __shared__ float wl[];
@@ -833,7 +813,7 @@ void qconv_dw_bwd_data_col_kernel(const DwArgs a) {
 // others read the zero page.  One input pixel of V channels per thread and
 // chunk; a.M counts the input pixels.
 template <typename T, int OM, int V, bool VEC, int K, int S>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(QL_DW_WAVES_BD)))
+__global__ __launch_bounds__(kThreads)
 void qconv_dw_bwd_data_k_kernel(const DwArgs a) {
     constexpr int NTM = om_terms(OM), NGM = om_gmaps(OM), TAPS = K * K, NR = (K + S - 1) / S;
     extern __shared__ float wl[];
@@ -884,7 +864,6 @@ void qconv_dw_bwd_data_k_kernel(const DwArgs a) {
         for (int k = 0; k < V; ++k) acc[k] = 0.0f;
 #pragma unroll
         for (int slot = 0; slot < NR * NR; ++slot) {
-            QL_DW_TAP_FENCE();
             float op[3][V];
             dw_ops<OM, V>(gv[slot], op);
 #pragma unroll
@@ -966,7 +945,7 @@ struct DwBwCol {
 };
 
 template <typename T, int OM, int V, bool VEC, int K, int S, int R>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(QL_DW_WAVES_BW)))
+__global__ __launch_bounds__(kThreads)
 void qconv_dw_bwd_weight_col_kernel(const DwArgs a) {
     constexpr int NTM = om_terms(OM), TAPS = K * K;
     __shared__ float wsum[(kThreads / 64) * 8 * NTM * (TAPS + 1) * V];  // [wave][channel group][...]
