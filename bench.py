@@ -44,7 +44,9 @@ def parse():
     ap.add_argument("--trace", metavar="KERNEL_TRACE_CSV",
                     help="with --profile-summary: the run's kernel trace, to average the last --last-calls calls")
     ap.add_argument("--last-calls", type=int, default=0,
-                    help="with --trace: entry calls per family in the final (roofline) region")
+                    help="with --trace: entry calls per family in the roofline region")
+    ap.add_argument("--skip-calls", type=int, default=0,
+                    help="with --trace: entry calls per family after the roofline region (the timed steps)")
     ap.add_argument("--copy-calibration", type=int, metavar="BYTES",
                     help="instead of running: one elementwise device copy of BYTES bytes (for counter scaling)")
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
@@ -116,6 +118,52 @@ class Layer:
                                          workspace=self.wsp_w, stream=st)
 
 
+class DevEvent:
+    """A HIP event recorded with device-scope release and acquire
+    (hipEventDisableSystemFence), created on the HIP runtime that torch loaded.
+
+    The benchmark's events only order kernels on one GPU and time them; a
+    system-scope fence (what torch's events use) makes every record write the
+    caches back for the host, an idle gap of several microseconds between two
+    launches.  The host reads results only after torch.cuda.synchronize()."""
+    _hip = None
+    DISABLE_TIMING = 0x2
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, timing=True):
+        import ctypes
+        if DevEvent._hip is None:
+            DevEvent._hip = ctypes.CDLL("libamdhip64.so.7")   # same soname as torch's runtime: same instance
+        self._ct = ctypes
+        self.ev = ctypes.c_void_p()
+        flags = self.DISABLE_SYSTEM_FENCE | (0 if timing else self.DISABLE_TIMING)
+        self._check(DevEvent._hip.hipEventCreateWithFlags(ctypes.byref(self.ev), ctypes.c_uint(flags)),
+                    "hipEventCreateWithFlags")
+
+    @staticmethod
+    def _check(rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} failed with HIP error {rc}")
+
+    def record(self, stream):
+        self._check(DevEvent._hip.hipEventRecord(self.ev, self._ct.c_void_p(stream.cuda_stream)), "hipEventRecord")
+
+    def wait(self, stream):
+        """Make `stream` wait for this event (device side)."""
+        self._check(DevEvent._hip.hipStreamWaitEvent(self._ct.c_void_p(stream.cuda_stream), self.ev,
+                                                      self._ct.c_uint(0)), "hipStreamWaitEvent")
+
+    def elapsed_time(self, end):
+        """Milliseconds from this event to `end` (both complete)."""
+        ms = self._ct.c_float()
+        self._check(DevEvent._hip.hipEventElapsedTime(self._ct.byref(ms), self.ev, end.ev), "hipEventElapsedTime")
+        return ms.value
+
+    def __del__(self):
+        if DevEvent._hip is not None and self.ev:
+            DevEvent._hip.hipEventDestroy(self.ev)
+
+
 def unit_flops(L):
     return 2 * L.n * L.ho * L.wo * L.o * L.c * L.k * L.k
 
@@ -124,8 +172,9 @@ def time_calls(torch, calls, steps, warmup, stream, timed_families=None):
     """Run `calls` (list of (family, fn)) warmup + steps times.
 
     Returns (device ms per step, wall ms per step, {family: summed event ms}, {family: launches}).
-    HIP events bracket every launch whose family is in `timed_families` (all when None); the
-    events are recorded on `stream`, the stream the library launches on.
+    HIP events (device-scope, DevEvent) bracket every launch whose family is in
+    `timed_families` (all when None); the events are recorded on `stream`, the stream
+    the library launches on.
     """
     for _ in range(warmup):
         for _, fn in calls:
@@ -133,14 +182,14 @@ def time_calls(torch, calls, steps, warmup, stream, timed_families=None):
     torch.cuda.synchronize()
     evs = []
     t0 = time.perf_counter()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
+    start = DevEvent()
+    stop = DevEvent()
     start.record(stream)
     for _ in range(steps):
         for fam, fn in calls:
             if timed_families is None or fam in timed_families:
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
+                e0 = DevEvent()
+                e1 = DevEvent()
                 e0.record(stream)
                 fn(stream)
                 e1.record(stream)
@@ -163,23 +212,26 @@ def time_overlapped(torch, layers, steps, warmup, s1, s2):
     """Run the step `warmup` + `steps` times with each layer's weight gradient on a
     second stream: it depends only on the layer's forward (T_a, T_b), so it overlaps
     with the input gradient on the first stream.  Returns (device ms per step, wall
-    ms per step), timed with events on s1 at the two ends of the timed steps."""
-    fwd_done = [torch.cuda.Event() for _ in layers]
+    ms per step), timed with events on s1 at the two ends of the timed steps.  The
+    cross-stream dependencies are device-scope events (DevEvent)."""
+    fwd_done = [DevEvent(timing=False) for _ in layers]
+    s2_done = DevEvent(timing=False)
 
     def step():
         for ly, ev in zip(layers, fwd_done):
             ly.fwd(s1)
             ev.record(s1)
-            s2.wait_event(ev)
+            ev.wait(s2)
             ly.bwd_weight(s2)
             ly.bwd_data(s1)
-        s1.wait_stream(s2)  # the next step's forward overwrites T_a, T_b
+        s2_done.record(s2)
+        s2_done.wait(s1)  # the next step's forward overwrites T_a, T_b
 
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
+    start = DevEvent()
+    stop = DevEvent()
     t0 = time.perf_counter()
     start.record(s1)
     for _ in range(steps):
@@ -246,7 +298,7 @@ _KERNEL_FAMILY = [
 ]
 
 
-def profile_summary(path, trace=None, last_calls=0):
+def profile_summary(path, trace=None, last_calls=0, skip_calls=0):
     """Markdown summary of a rocprofv3 kernel statistics table (--stats, csv output):
     every kernel with its calls and average duration, then per entry point the total
     kernel time divided by the number of entry calls (= calls of its main kernels)."""
@@ -274,25 +326,28 @@ def profile_summary(path, trace=None, last_calls=0):
         if fam_calls.get(fam):
             lines.append(f"| qlayer_conv2d_{fam} | {fam_calls[fam]} | {fam_ns[fam] / fam_calls[fam] / 1e3:.1f} |")
     if trace and last_calls:
-        lines += ["", f"Final region only (the last {last_calls} calls of each entry point, from the kernel trace):", "",
+        where = f"before its last {skip_calls}" if skip_calls else "its last"
+        lines += ["", f"One region only ({last_calls} calls of each entry point, {where}, from the kernel trace):", "",
                   "| entry point | entry calls | kernel time per call, us |", "|---|---:|---:|"]
-        for fam, (n, ns) in region_times(trace, last_calls).items():
+        for fam, (n, ns) in region_times(trace, last_calls, skip_calls).items():
             lines.append(f"| qlayer_conv2d_{fam} | {n} | {ns / n / 1e3:.1f} |")
     print("\n".join(lines))
 
 
-def region_times(trace_csv, last_calls):
-    """Per family: kernel time of its last `last_calls` entry calls in a rocprofv3 kernel trace
-    (from the first of those calls' main-kernel dispatch on, every kernel of the family)."""
+def region_times(trace_csv, last_calls, skip_calls=0):
+    """Per family: kernel time of `last_calls` entry calls in a rocprofv3 kernel trace, those
+    that precede the family's last `skip_calls` calls (every kernel of the family from the
+    first selected call's main-kernel dispatch up to the next unselected one)."""
     import csv
     rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Dispatch_Id"]))
     out = {}
     for fam in ("fwd", "bwd_data", "bwd_weight"):
         mains = [i for i, r in enumerate(rows) if _family(r["Kernel_Name"]) == (fam, True)]
-        if len(mains) < last_calls:
+        if len(mains) < last_calls + skip_calls:
             continue
-        first = mains[-last_calls]
-        ns = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows[first:]
+        first = mains[len(mains) - skip_calls - last_calls]
+        end = mains[len(mains) - skip_calls] if skip_calls else len(rows)
+        ns = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows[first:end]
                  if _family(r["Kernel_Name"])[0] == fam)
         out[fam] = (last_calls, ns)
     return out
@@ -389,7 +444,7 @@ def copy_calibration(nbytes):
 def main():
     args = parse()
     if args.profile_summary:
-        profile_summary(args.profile_summary, args.trace, args.last_calls)
+        profile_summary(args.profile_summary, args.trace, args.last_calls, args.skip_calls)
         return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -441,15 +496,19 @@ def main():
         per_layer.append(row)
     dom = max(fam_tot, key=fam_tot.get)
 
-    # Timed region: K steps with events only at its two ends (an event between
-    # two launches serialises them, so per-launch events would slow the step);
-    # each layer's weight gradient runs on a second stream beside its input gradient.
-    stream2 = torch.cuda.Stream(dev)  # default priority
-    ms_step, wall = time_overlapped(torch, layers, args.steps, 2, stream, stream2)
+    # Single-stream steps, then the roofline region: K more steps, events bracketing each
+    # launch of the dominant family.  Both run before the timed region, so that it
+    # starts on a GPU that has been busy for a while (the first tens of steps after
+    # start-up run several per cent slower).
     ms_serial, _, _, _ = time_calls(torch, calls, args.steps, 1, stream, timed_families=set())
-    # Roofline region: K more steps, events bracketing each launch of the dominant family.
     dom_keys = {(dom, i) for i in range(len(geoms))}
     _, _, fam_ms, fam_n = time_calls(torch, calls, args.steps, 0, stream, timed_families=dom_keys)
+
+    # Timed region: W warm-up steps, then K steps with events only at its two ends (an
+    # event between two launches serialises them); each layer's weight gradient runs on
+    # a second stream beside its input gradient.
+    stream2 = torch.cuda.Stream(dev)  # default priority
+    ms_step, wall = time_overlapped(torch, layers, args.steps, args.warmup, stream, stream2)
 
     total_flops = sum(9 * unit_flops(L) for L in geoms)
     value = total_flops / (ms_step * 1e-3) / 1e12

@@ -60,7 +60,13 @@ struct FwdArgs {
     int xsq;     // T2: x already holds X o X (squared by a pre-pass), no squaring in the kernel
     EpiArgs epi;
     float *stat_part;  // staged epilogue: per pixel tile ct, partial sums of y' [ct][O] and y'^2 [ct][O]; or NULL
-    FastDiv fd_howo, fd_wo, fd_c, fd_kw;
+    // Position-major pixel order (channel-aligned kernels only): GEMM column m
+    // is output position m / N of image m % N, stored at NHWC row
+    // (m % N) HO WO + m / N.  A pixel tile then spans few positions, and the K
+    // steps of taps that lie in the zero padding for all of them are skipped:
+    // the K range is the tile's in-bounds taps, cps = C / KE steps each.
+    int pm, cps;
+    FastDiv fd_howo, fd_wo, fd_c, fd_kw, fd_n, fd_cps;
 };
 
 // Input gradient: rows = input channels, columns = input pixels,

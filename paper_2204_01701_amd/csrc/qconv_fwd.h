@@ -53,8 +53,30 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     const int split = bid / tiles;
     bid -= split * tiles;
     const int rt = bid % a.row_tiles, ct = bid / a.row_tiles;
+    // Position-major order: the taps in bounds for some position of this
+    // pixel tile (a wave-uniform mask); the tile's K range is those taps only.
+    uint32_t tmask = 0;
+    int kst = a.stages_total;
+    if (CA && a.pm) {
+        const int m_hi = min(ct * BCOL + BCOL, a.M) - 1;
+        for (int pos = (int)fdiv((uint32_t)(ct * BCOL), a.fd_n); pos <= (int)fdiv((uint32_t)m_hi, a.fd_n); ++pos) {
+            const int oh = (int)fdiv((uint32_t)pos, a.fd_wo);
+            const int h0 = oh * a.SH - a.PH, w0 = (pos - oh * a.WO) * a.SW - a.PW;
+            for (int r = 0; r < a.KH; ++r)
+                for (int q = 0; q < a.KW; ++q)
+                    if ((unsigned)(h0 + r) < (unsigned)a.H && (unsigned)(w0 + q) < (unsigned)a.W)
+                        tmask |= 1u << (r * a.KW + q);
+        }
+        kst = __builtin_popcount(tmask) * a.cps;
+    }
     const int s_begin = split * a.stages_per_split;
-    const int nst = min(a.stages_per_split, a.stages_total - s_begin);
+    const int nst = max(0, min(a.stages_per_split, kst - s_begin));
+    // NHWC row of GEMM column m
+    auto prow = [&](int m) -> int {
+        if (!CA || !a.pm) return m;
+        const int pos = (int)fdiv((uint32_t)m, a.fd_n);
+        return (m - pos * a.N) * a.HO * a.WO + pos;
+    };
 
     const T *__restrict__ x = static_cast<const T *>(a.x);
     const T *wp[3] = {static_cast<const T *>(a.w[0]), static_cast<const T *>(a.w[1]),
@@ -114,8 +136,14 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         for (int j = 0; j < NIX; ++j) {
             const int p = RPI * (NIW3 + j) + 16 * wave + (lane >> 2) - 3 * BR;
             const int m = min(ct * BCOL + p, a.M - 1);
-            const int n = (int)fdiv((uint32_t)m, a.fd_howo);
-            const int rem = m - n * a.HO * a.WO;
+            int n, rem;
+            if (a.pm) {
+                rem = (int)fdiv((uint32_t)m, a.fd_n);
+                n = m - rem * a.N;
+            } else {
+                n = (int)fdiv((uint32_t)m, a.fd_howo);
+                rem = m - n * a.HO * a.WO;
+            }
             const int oh = (int)fdiv((uint32_t)rem, a.fd_wo);
             const int ow = rem - oh * a.WO;
             const int h0 = oh * a.SH - a.PH, w0 = ow * a.SW - a.PW;
@@ -133,9 +161,21 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         char *base = smem + slot * STAGE + wave * 1024;
         DmaPart part(lo, hi);
         if constexpr (CA) {
-            const int k0 = min(s, a.stages_total - 1) * KE;
-            const int tap = (int)fdiv((uint32_t)k0, a.fd_c);
-            const int c0 = k0 - tap * a.C;
+            int k0, tap, c0;
+            if (a.pm) {
+                // step s of the tile's K range: tap = the ti-th set bit of tmask
+                const int sc = max(0, min(s, kst - 1));
+                const int ti = (int)fdiv((uint32_t)sc, a.fd_cps);
+                uint32_t mm = tmask;
+                for (int i = 0; i < ti; ++i) mm &= mm - 1;
+                tap = mm ? __builtin_ctz(mm) : 0;
+                c0 = (sc - ti * a.cps) * KE;
+                k0 = tap * a.C + c0;
+            } else {
+                k0 = min(s, a.stages_total - 1) * KE;
+                tap = (int)fdiv((uint32_t)k0, a.fd_c);
+                c0 = k0 - tap * a.C;
+            }
             const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
             const int q = tap - r * a.KW;
             const long long soff = ((long long)r * a.W + q) * a.C + c0;
@@ -245,7 +285,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     // the four shortcut values of a lane's group (channels o .. o + 3 of pixel m), or zeros
     auto xs4 = [&](int m, int o, float *xv) {
         xv[0] = xv[1] = xv[2] = xv[3] = 0.0f;
-        if (shortcut && m < a.M && o < a.O) load4<T>(x + (size_t)m * a.C + o, xv);
+        if (shortcut && m < a.M && o < a.O) load4<T>(x + (size_t)prow(m) * a.C + o, xv);
     };
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
     const bool vec_out = (a.O & 3) == 0;
@@ -318,7 +358,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                                 const int m = ct * BCOL + row, o = rt * BR + cc * (16 / E);
                                 if (m < a.M && o < a.O) {
                                     const v4u val = lds_read16(tile + row * PITCH + cc * 16);
-                                    *reinterpret_cast<v4u *>(outs[j] + (size_t)m * a.O + o) = val;
+                                    *reinterpret_cast<v4u *>(outs[j] + (size_t)prow(m) * a.O + o) = val;
                                     if constexpr (EPI) {
                                         if (j == 0 && stats) {
     #pragma unroll
@@ -382,7 +422,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                             }
                         }
                         if (NTM < 2) tb = nullptr;
-                        const size_t off = (size_t)m * a.O + o;
+                        const size_t off = (size_t)prow(m) * a.O + o;
                         if (vec_out) {
                             if (y) store4<T>(y + off, vy[0], vy[1], vy[2], vy[3]);
                             if (ta) store4<T>(ta + off, va[0], va[1], va[2], va[3]);
@@ -418,7 +458,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                     for (int g = 0; g < 4; ++g) {
                         const int o = orow0 + mr * 32 + 8 * g + 4 * lhi;
                         if (o >= a.O) continue;
-                        const size_t off = (size_t)m * a.O + o;
+                        const size_t off = (size_t)prow(m) * a.O + o;
                         if (vec_out) {
                             store4<float>(ws + off, acc[t][mr][mc][4 * g], acc[t][mr][mc][4 * g + 1],
                                           acc[t][mr][mc][4 * g + 2], acc[t][mr][mc][4 * g + 3]);

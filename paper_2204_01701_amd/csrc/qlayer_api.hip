@@ -149,6 +149,42 @@ void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_s
     splits = cdiv(stages_total, sps);
 }
 
+// Taps (r, q) in bounds for output position pos = (oh, ow): a bit mask.
+uint32_t tap_mask(const Geom &g, int pos) {
+    const int oh = pos / g.WO, ow = pos % g.WO;
+    const int h0 = oh * g.SH - g.PH, w0 = ow * g.SW - g.PW;
+    uint32_t m = 0;
+    for (int r = 0; r < g.KH; ++r)
+        for (int q = 0; q < g.KW; ++q)
+            if (h0 + r >= 0 && h0 + r < g.H && w0 + q >= 0 && w0 + q < g.W) m |= 1u << (r * g.KW + q);
+    return m;
+}
+
+// Position-major pixel order (column m = position m / N of image m % N): the
+// most in-bounds taps of any pixel tile of `bcol` columns (the union over
+// the positions it spans).
+int pm_max_taps(const Geom &g, int bcol, long long M) {
+    int best = 0;
+    for (long long m0 = 0; m0 < M; m0 += bcol) {
+        const long long m1 = std::min(M, m0 + bcol) - 1;
+        uint32_t u = 0;
+        for (long long pos = m0 / g.N; pos <= m1 / g.N; ++pos) u |= tap_mask(g, (int)pos);
+        best = std::max(best, __builtin_popcount(u));
+    }
+    return best;
+}
+
+// Whether to use the position-major order: forced by `env` (0 / 1), else on
+// padded maps of at most 4 positions (2 x 2 maps of a 3 x 3 filter: every
+// position has 4 taps in bounds).  Measured on larger maps (4 x 4, 8 x 8),
+// the order is slower: the interior positions keep every tap, so their tiles
+// bound the kernel's time, and a tile of one position no longer re-reads the
+// X rows its neighbouring pixels share across taps from the caches.
+bool pm_default(const Geom &g, int env) {
+    if (env >= 0) return env != 0;
+    return g.HO * g.WO <= 4 && (g.PH > 0 || g.PW > 0);
+}
+
 // ---------------------------------------------------------------------------
 // Forward planning.
 // ---------------------------------------------------------------------------
@@ -169,6 +205,8 @@ struct FwdPlan {
     int BR, BCOL, KE, slots;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
+    bool ca;  // channel-aligned K steps (C a multiple of KE, at most 32 taps): every step within one tap
+    bool pm;  // position-major pixel order, K steps of padding-only taps skipped (FwdArgs)
     bool pad;                      // X and W_t zero-padded to Cp channels first
     int Cp;
     size_t xpad_bytes, wpad_bytes;  // workspace: [X padded][W_a, W_b, W_c padded][split partials][X o X]
@@ -205,7 +243,14 @@ FwdPlan plan_fwd(const Geom &g) {
     p.row_tiles = cdiv(g.O, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)3 * M * g.O * 4, p.slots, p.splits, p.sps);
+    p.ca = p.veck && p.Cp % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
+    // Position-major order where the maps are small, so that many taps of a
+    // position lie in the padding: the splits are planned for the pixel tile
+    // with the most in-bounds taps.
+    p.pm = p.ca && pm_default(g, env_override("QLAYER_FWD_POSMAJ", -1));
+    int kst = p.stages_total;
+    if (p.pm) kst = pm_max_taps(g, p.BCOL, M) * (p.Cp / p.KE);
+    plan_splits(p.row_tiles * p.col_tiles, kst, 4, (size_t)3 * M * g.O * 4, p.slots, p.splits, p.sps);
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0;
     p.xsq_bytes = g.ne == NEURON_T2 && p.veck ? align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize()) : 0;
     p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes + p.part_bytes + p.xsq_bytes;
@@ -395,6 +440,10 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     a.fd_wo = make_fastdiv(g.WO);
     a.fd_c = make_fastdiv(C);
     a.fd_kw = make_fastdiv(g.KW);
+    a.pm = p.pm ? 1 : 0;
+    a.cps = C / p.KE;
+    a.fd_n = make_fastdiv(g.N);
+    a.fd_cps = make_fastdiv(std::max(1, a.cps));
     a.neuron = g.ne;
     if (p.xsq_bytes) {
         // T2: X o X once, instead of squaring every fragment in the MFMA loop
@@ -410,7 +459,7 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     const int om = g.om();
     if (p.veck && om != OM_QUADRA) {
-        const bool ca = C % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
+        const bool ca = p.ca;
 #define QL_FWD_OM(OM)                                                                                          \
     do {                                                                                                        \
         if (ca)                                                                                                 \
@@ -432,7 +481,7 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
             hipLaunchKernelGGL((qconv_fwd_generic_kernel<T, 64, 128, 2, 2, 64, false, OM_SQIN>), grid, block, 0, st, a);
     } else if (p.veck) {
         // channel-aligned K steps: every step within one tap
-        const bool ca = C % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
+        const bool ca = p.ca;
 #define QL_FWD(BR, BC, WR, WC, NS, NT)                                                                           \
     do {                                                                                                          \
         if (ca)                                                                                                   \
