@@ -160,8 +160,9 @@ class DevEvent:
         return ms.value
 
     def __del__(self):
-        if DevEvent._hip is not None and self.ev:
-            DevEvent._hip.hipEventDestroy(self.ev)
+        hip = getattr(type(self), "_hip", None)   # (None once the interpreter tears the module down)
+        if hip is not None and self.ev:
+            hip.hipEventDestroy(self.ev)
 
 
 def unit_flops(L):

@@ -15,6 +15,7 @@
 #include "qconv_bwd_weight.h"
 #include "qconv_depthwise.h"
 #include "qconv_fwd.h"
+#include "qconv_fwd_smallc.h"
 #include "qconv_generic.h"
 
 namespace ql {
@@ -205,6 +206,7 @@ struct FwdPlan {
     int BR, BCOL, KE, slots;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
+    bool smallc;  // KH KW C + bias columns <= 32, 32 or 64 output channels: qconv_fwd_smallc_kernel, no workspace
     bool ca;  // channel-aligned K steps (C a multiple of KE, at most 32 taps): every step within one tap
     bool pm;  // position-major pixel order, K steps of padding-only taps skipped (FwdArgs)
     bool pad;                      // X and W_t zero-padded to Cp channels first
@@ -217,6 +219,13 @@ struct FwdPlan {
 
 FwdPlan plan_fwd(const Geom &g) {
     FwdPlan p{};
+    const int bias_cols = g.dt == QL_BF16 ? smallc_bias_cols<uint16_t>() : smallc_bias_cols<float>();
+    if (g.ne == NEURON_QUADRA && g.C * g.KH * g.KW + bias_cols <= kSmallcK && (g.O == 32 || g.O == 64) &&
+        env_override("QLAYER_FWD_SMALLC", 1) != 0) {
+        p.smallc = true;
+        p.splits = 1;
+        return p;
+    }
     p.pad = g.pad_small_c();
     p.Cp = p.pad ? g.cpad() : g.C;
     const int M = g.N * g.HO * g.WO, K = g.KH * g.KW * p.Cp;
@@ -402,6 +411,39 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     FwdArgs a{};
     a.epi = epi;
     a.stat_part = stat_part;  // (set by the caller only where the kernel's staged epilogue runs)
+    if (p.smallc) {
+        a.x = x;
+        a.w[0] = wa; a.w[1] = wb; a.w[2] = wc;
+        a.bias[0] = ba; a.bias[1] = bb; a.bias[2] = bc;
+        a.y = y; a.ta = ta; a.tb = tb;
+        a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.O = g.O; a.KH = g.KH; a.KW = g.KW;
+        a.SH = g.SH; a.SW = g.SW; a.PH = g.PH; a.PW = g.PW; a.HO = g.HO; a.WO = g.WO;
+        a.M = g.N * g.HO * g.WO;
+        a.K = g.KH * g.KW * g.C;
+        a.splits = 1;
+        a.fd_howo = make_fastdiv(g.HO * g.WO);
+        a.fd_wo = make_fastdiv(g.WO);
+        a.fd_c = make_fastdiv(g.C);
+        a.fd_kw = make_fastdiv(g.KW);
+        a.neuron = g.ne;
+        const bool ep = epi.scale || epi.shift || epi.relu;
+        // groups of 32 pixels per wave (the next group's loads overlap the current one's stores)
+        const long long groups = cdiv(a.M, 32);
+        const int gpw = std::max(1, env_override("QLAYER_FWD_SMALLC_GPW", 2));
+        const dim3 grid((unsigned)std::max<long long>(
+            1, std::min<long long>(cdiv(groups, (long long)(kThreads / 64) * gpw), 4 * kNumCUs)));
+#define QL_FWD_SMALLC(OB)                                                                              \
+    do {                                                                                               \
+        if (ep)                                                                                        \
+            hipLaunchKernelGGL((qconv_fwd_smallc_kernel<T, OB, true>), grid, dim3(kThreads), 0, st, a);  \
+        else                                                                                           \
+            hipLaunchKernelGGL((qconv_fwd_smallc_kernel<T, OB, false>), grid, dim3(kThreads), 0, st, a); \
+    } while (0)
+        if (g.O == 64) QL_FWD_SMALLC(2);
+        else QL_FWD_SMALLC(1);
+#undef QL_FWD_SMALLC
+        return hip_status();
+    }
     a.x = x;
     a.w[0] = wa; a.w[1] = wb; a.w[2] = wc;
     char *wsb = static_cast<char *>(ws);
@@ -520,7 +562,7 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
 // Whether launch_fwd's kernel writes Y through its staged epilogue, the path
 // that gathers the epilogue statistics itself (qconv_fwd.h).
 bool fwd_stats_fused(const Geom &g, const FwdPlan &p) {
-    if (!p.veck || p.splits != 1 || g.O % (16 / (int)g.esize()) != 0) return false;
+    if (p.smallc || !p.veck || p.splits != 1 || g.O % (16 / (int)g.esize()) != 0) return false;
     const int ns = (g.ne == NEURON_QUADRA && (p.cfg == 4 || p.cfg == 5)) ? 3 : 4;
     return fwd_staged_fits(p.BR, p.BCOL, ns, (int)g.esize());
 }
