@@ -335,17 +335,16 @@ __global__ __launch_bounds__(kThreads) void qconv_pad_channels_kernel(PadSegment
 // workspace, tap-major ([r, q][m][c]), so that the second kernel, which
 // gathers it over the taps in a fixed order, reads consecutive pixels of one
 // tap plane from consecutive lanes.
+// Weight fragments of the per-pixel partial sums in LDS: [t][nb][kc][lane],
+// lane l: column j = 32 nb + l % 32 of W_t[o, (r, q, c)], output channels
+// o = kc KC + VEC (l / 32) .. +VEC (zero past J).
 template <typename T, int NJB>
-__global__ __launch_bounds__(kThreads) void qconv_bwd_data_cols_kernel(
-    const T *__restrict__ gy, const T *__restrict__ gta, const T *__restrict__ gtb, const T *__restrict__ w0,
-    const T *__restrict__ w1, const T *__restrict__ w2, float *__restrict__ P, int M, int O, int C, int J) {
+__device__ __forceinline__ void cols_stage_weights(v4u *wfr, const T *__restrict__ w0, const T *__restrict__ w1,
+                                                   const T *__restrict__ w2, int O, int J) {
     constexpr int VEC = Elem<T>::VEC;
-    constexpr int KC = 2 * VEC;  // K elements (output channels) per MFMA chunk
-    constexpr int KB = 4;        // chunks whose loads are issued together
-    extern __shared__ __attribute__((aligned(16))) v4u wfr[];  // [t][nb][kc][lane]
+    constexpr int KC = 2 * VEC;
     const int nkc = O / KC;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int i = tid; i < 3 * NJB * nkc * 64; i += blockDim.x) {
+    for (int i = threadIdx.x; i < 3 * NJB * nkc * 64; i += blockDim.x) {
         const int l = i & 63, f = i >> 6;
         const int kc = f % nkc, nb = (f / nkc) % NJB, t = f / (nkc * NJB);
         const T *w = t == 0 ? w0 : (t == 1 ? w1 : w2);
@@ -355,6 +354,58 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_cols_kernel(
         for (int e = 0; e < VEC; ++e) v[e] = j < J ? to_f32<T>(w[(size_t)(o0 + e) * J + j]) : 0.0f;
         wfr[i] = vpack<T>(v);
     }
+}
+
+// Partial sums of one wave's 32 output pixels (lane % 32: the pixel whose
+// G / T_a / T_b row it loads, m; ok: m is a pixel): acc[nb] holds column
+// j = 32 nb + lane % 32 of rows (pixels) 8 (v / 4) + 4 (lane / 32) + v % 4.
+template <typename T, int NJB>
+__device__ __forceinline__ void cols_group(const T *__restrict__ gy, const T *__restrict__ gta,
+                                           const T *__restrict__ gtb, const v4u *wfr, long long m, bool ok, int O,
+                                           f32x16_t (&acc)[NJB]) {
+    constexpr int VEC = Elem<T>::VEC;
+    constexpr int KC = 2 * VEC;  // K elements (output channels) per MFMA chunk
+    constexpr int KB = 4;        // chunks whose loads are issued together
+    const int lane = threadIdx.x & 63;
+    const int nkc = O / KC;
+#pragma unroll
+    for (int nb = 0; nb < NJB; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[nb][v] = 0.0f;
+    const size_t rowoff = (size_t)(ok ? m : 0) * O + VEC * (lane >> 5);
+    for (int kb = 0; kb < nkc; kb += KB) {
+        v4u g[KB], ta[KB], tb[KB];
+#pragma unroll
+        for (int u = 0; u < KB; ++u) {
+            const bool in = ok && kb + u < nkc;
+            const size_t off = rowoff + (size_t)(kb + u) * KC;
+            g[u] = ld16(gy + off, in);
+            ta[u] = ld16(gta + off, in);
+            tb[u] = ld16(gtb + off, in);
+        }
+#pragma unroll
+        for (int u = 0; u < KB; ++u) {
+            if (kb + u >= nkc) break;
+            const int kc = kb + u;
+            v4u ga, gb;
+            prologue_frag<T>(g[u], ta[u], tb[u], ga, gb);
+#pragma unroll
+            for (int nb = 0; nb < NJB; ++nb) {
+                mfma_chunk<T>(ga, wfr[((0 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
+                mfma_chunk<T>(gb, wfr[((1 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
+                mfma_chunk<T>(g[u], wfr[((2 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
+            }
+        }
+    }
+}
+
+template <typename T, int NJB>
+__global__ __launch_bounds__(kThreads) void qconv_bwd_data_cols_kernel(
+    const T *__restrict__ gy, const T *__restrict__ gta, const T *__restrict__ gtb, const T *__restrict__ w0,
+    const T *__restrict__ w1, const T *__restrict__ w2, float *__restrict__ P, int M, int O, int C, int J) {
+    extern __shared__ __attribute__((aligned(16))) v4u wfr[];  // [t][nb][kc][lane]
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    cols_stage_weights<T, NJB>(wfr, w0, w1, w2, O, J);
     __syncthreads();
     // This lane's output column j = 32 nb + lane % 32 is (tap, c) = (j / C, j % C).
     int ptap[NJB], pc[NJB];
@@ -368,37 +419,8 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_cols_kernel(
     for (long long mb = (long long)blockIdx.x * (kThreads / 64) + wave; mb < nblk;
          mb += (long long)gridDim.x * (kThreads / 64)) {
         const long long m = mb * 32 + (lane & 31);
-        const bool ok = m < M;
         f32x16_t acc[NJB];
-#pragma unroll
-        for (int nb = 0; nb < NJB; ++nb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[nb][v] = 0.0f;
-        const size_t rowoff = (size_t)(ok ? m : 0) * O + VEC * (lane >> 5);
-        for (int kb = 0; kb < nkc; kb += KB) {
-            v4u g[KB], ta[KB], tb[KB];
-#pragma unroll
-            for (int u = 0; u < KB; ++u) {
-                const bool in = ok && kb + u < nkc;
-                const size_t off = rowoff + (size_t)(kb + u) * KC;
-                g[u] = ld16(gy + off, in);
-                ta[u] = ld16(gta + off, in);
-                tb[u] = ld16(gtb + off, in);
-            }
-#pragma unroll
-            for (int u = 0; u < KB; ++u) {
-                if (kb + u >= nkc) break;
-                const int kc = kb + u;
-                v4u ga, gb;
-                prologue_frag<T>(g[u], ta[u], tb[u], ga, gb);
-#pragma unroll
-                for (int nb = 0; nb < NJB; ++nb) {
-                    mfma_chunk<T>(ga, wfr[((0 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
-                    mfma_chunk<T>(gb, wfr[((1 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
-                    mfma_chunk<T>(g[u], wfr[((2 * NJB + nb) * nkc + kc) * 64 + lane], acc[nb]);
-                }
-            }
-        }
+        cols_group<T, NJB>(gy, gta, gtb, wfr, m, m < M, O, acc);
         // Lane holds column j = 32 nb + lane % 32 of rows 8 (v / 4) + 4 (lane / 32) + v % 4.
 #pragma unroll
         for (int nb = 0; nb < NJB; ++nb) {
@@ -410,6 +432,65 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_cols_kernel(
                 if (row < M) plane[row * C] = acc[nb][v];
             }
         }
+    }
+}
+
+// Floats per output pixel of the fused kernel's LDS partial sums: 32 columns
+// plus one, so that the gather's threads (consecutive pixels) hit distinct banks.
+constexpr int kFusedPitch = 33;
+
+// The two steps above fused for stride 1 (J <= 32): a workgroup takes RB
+// input rows h0 .. h0 + RB - 1 of image n.  Their gradient needs the partial
+// sums of output rows i = h + PH - r, i.e. i_lo .. i_hi (the band plus a halo
+// of KH - 1 rows, recomputed by the neighbouring bands); the waves compute
+// those into LDS (one 32-float row per output pixel, column j = (r, q, c)),
+// and after one barrier each thread gathers dX[n, h, w, c] over the taps in
+// (r, q) order, as the separate gather does.  No partial sums go to HBM.
+template <typename T, int NT>
+__global__ __launch_bounds__(NT) void qconv_bwd_data_cols_fused_kernel(
+    const T *__restrict__ gy, const T *__restrict__ gta, const T *__restrict__ gtb, const T *__restrict__ w0,
+    const T *__restrict__ w1, const T *__restrict__ w2, T *__restrict__ dx, int H, int W, int C, int O, int KH,
+    int KW, int PH, int PW, int HO, int WO, int RB, int wfr_vecs) {
+    extern __shared__ __attribute__((aligned(16))) v4u wfr[];  // weights, then the partial sums
+    float *Pl = reinterpret_cast<float *>(wfr + wfr_vecs);     // [local output pixel][kFusedPitch]
+    const int J = KH * KW * C;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lrow = lane & 31;
+    const int bands = (H + RB - 1) / RB;
+    const int n = blockIdx.x / bands, h0 = (blockIdx.x - n * bands) * RB;
+    const int i_lo = max(0, h0 + PH - (KH - 1)), i_hi = min(HO - 1, h0 + RB - 1 + PH);
+    const int npx = i_hi >= i_lo ? (i_hi - i_lo + 1) * WO : 0;
+    cols_stage_weights<T, 1>(wfr, w0, w1, w2, O, J);
+    __syncthreads();
+    for (int gl = wave; gl * 32 < npx; gl += NT / 64) {
+        const int pl = gl * 32 + lrow;
+        const long long m = ((long long)n * HO + i_lo) * WO + pl;  // local pixels are consecutive output pixels
+        f32x16_t acc[1];
+        cols_group<T, 1>(gy, gta, gtb, wfr, m, pl < npx, O, acc);
+        if (lrow < J) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int row = gl * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                if (row < npx) Pl[row * kFusedPitch + lrow] = acc[0][v];
+            }
+        }
+    }
+    __syncthreads();
+    const int rows = min(RB, H - h0);
+    for (int it = threadIdx.x; it < rows * W * C; it += NT) {
+        const int hl = it / (W * C), rem = it - hl * (W * C);
+        const int w = rem / C, c = rem - w * C;
+        const int h = h0 + hl;
+        float acc = 0.0f;
+        for (int r = 0; r < KH; ++r) {
+            const int i = h + PH - r;
+            if (i < 0 || i >= HO) continue;
+            for (int q = 0; q < KW; ++q) {
+                const int j = w + PW - q;
+                if (j < 0 || j >= WO) continue;
+                acc += Pl[((i - i_lo) * WO + j) * kFusedPitch + (r * KW + q) * C + c];
+            }
+        }
+        dx[(((size_t)n * H + h) * W + w) * C + c] = from_f32<T>(acc);
     }
 }
 

@@ -285,6 +285,8 @@ struct BwdDataPlan {
     bool veck, s1;
     bool natw;    // weights read untransposed through natural LDS tiles (bf16, C % 8 == 0)
     bool smallc;  // C <= 4: per-pixel partial sums by MFMA, then a gather over the taps
+    int fused_rb; // ... stride 1: both steps in one kernel, bands of fused_rb input rows (0: two kernels)
+    size_t fused_smem;
     int njb;      // ... 32-column blocks of (r, q, c)
     size_t smem;  // ... LDS of the weight fragments
     size_t wt_bytes, part_bytes, ws_bytes;
@@ -299,7 +301,20 @@ BwdDataPlan plan_bwd_data(const Geom &g) {
         p.smallc = g.C <= 4 && g.O % (2 * g.vec()) == 0 && p.njb <= 2 && p.smem <= 64 * 1024 &&
                    g.ne == NEURON_QUADRA && env_override("QLAYER_BWD_DATA_SMALLC", 1) != 0;
         if (p.smallc) {
-            p.ws_bytes = align_up((size_t)g.N * g.HO * g.WO * J * sizeof(float));
+            // fused (stride 1): LDS holds the weights and the partial sums of RB + KH - 1
+            // output rows; at most 64 KB, so that two workgroups share a CU
+            int rb = env_override("QLAYER_BWD_DATA_FUSED_RB", 8);  // (0: the two kernels)
+            if (g.SH == 1 && g.SW == 1 && p.njb == 1 && rb > 0) {
+                for (; rb >= 1; --rb) {
+                    const size_t lds = p.smem + (size_t)(rb + g.KH - 1) * g.WO * kFusedPitch * sizeof(float);
+                    if (lds <= 64 * 1024) {
+                        p.fused_rb = rb;
+                        p.fused_smem = lds;
+                        break;
+                    }
+                }
+            }
+            p.ws_bytes = p.fused_rb ? 0 : align_up((size_t)g.N * g.HO * g.WO * J * sizeof(float));
             return p;
         }
     }
@@ -570,6 +585,22 @@ bool fwd_stats_fused(const Geom &g, const FwdPlan &p) {
 template <typename T>
 ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, const void *ta, const void *tb,
                           const void *wa, const void *wb, const void *wc, void *dx, void *ws, hipStream_t st) {
+    if (p.smallc && p.fused_rb) {
+        const int bands = cdiv(g.H, p.fused_rb);
+#define QL_BD_FUSED(NT)                                                                                            \
+    hipLaunchKernelGGL((qconv_bwd_data_cols_fused_kernel<T, NT>), dim3(g.N * bands), dim3(NT), p.fused_smem, st,    \
+                       static_cast<const T *>(gy), static_cast<const T *>(ta), static_cast<const T *>(tb),          \
+                       static_cast<const T *>(wa), static_cast<const T *>(wb), static_cast<const T *>(wc),          \
+                       static_cast<T *>(dx), g.H, g.W, g.C, g.O, g.KH, g.KW, g.PH, g.PW, g.HO, g.WO, p.fused_rb, \
+                       (int)(p.smem / sizeof(v4u)))
+        // 8 waves: each takes one or two 32-pixel groups of the band (measured faster than 4)
+        if (env_override("QLAYER_BWD_DATA_FUSED_NT", 512) == 256)
+            QL_BD_FUSED(256);
+        else
+            QL_BD_FUSED(512);
+#undef QL_BD_FUSED
+        return hip_status();
+    }
     if (p.smallc) {
         const long long Mo = (long long)g.N * g.HO * g.WO;
         const int J = g.KH * g.KW * g.C;
@@ -722,6 +753,34 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     return hip_status();
 }
 
+// The weight-gradient split reduction: dW_t and db_t from the partials
+// [split][3][O KH KW C] and [split][3][O], summed in split order.
+ql_status reduce_bw_partials(const Geom &g, int splits, const BwdWeightArgs &a, float *dwa, float *dwb, float *dwc,
+                             float *dba, float *dbb, float *dbc, hipStream_t st) {
+    const long long ndw = (long long)g.O * g.KH * g.KW * g.C;  // dW_t as stored
+    if (3 * ndw < (1LL << 20) && splits >= 16 && ndw % 4 == 0)
+        hipLaunchKernelGGL(qconv_bwd_weight_reduce2dv_kernel, dim3(grid_1d((3 * ndw / 4 + 3 * g.O) * 16)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db, g.terms());
+    else if (3 * ndw < (1LL << 20) && splits >= 16)
+        hipLaunchKernelGGL((qconv_bwd_weight_reduce2d_kernel<16>), dim3(grid_1d((3 * ndw + 3 * g.O) * 16)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db, g.terms());
+    else if (ndw % 4 == 0)
+        hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<true>), dim3(grid_1d(3 * ndw / 4 + 3 * g.O)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db, g.terms());
+    else
+        hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<false>), dim3(grid_1d(3 * ndw + 3 * g.O)),
+                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
+                           static_cast<const float *>(a.ws_db), splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
+                           a.want_db, g.terms());
+    return hip_status();
+}
+
 template <typename T>
 ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x, const void *gy, const void *ta,
                             const void *tb, float *dwa, float *dwb, float *dwc, float *dba, float *dbb, float *dbc,
@@ -803,28 +862,7 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     }
     ql_status s = hip_status();
     if (s != QL_OK || p.splits == 1) return s;
-    const long long ndw = (long long)g.O * g.KH * g.KW * g.C;  // dW_t as stored
-    if (3 * ndw < (1LL << 20) && p.splits >= 16 && ndw % 4 == 0)
-        hipLaunchKernelGGL(qconv_bwd_weight_reduce2dv_kernel, dim3(grid_1d((3 * ndw / 4 + 3 * g.O) * 16)),
-                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
-                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
-                           a.want_db, g.terms());
-    else if (3 * ndw < (1LL << 20) && p.splits >= 16)
-        hipLaunchKernelGGL((qconv_bwd_weight_reduce2d_kernel<16>), dim3(grid_1d((3 * ndw + 3 * g.O) * 16)),
-                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
-                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
-                           a.want_db, g.terms());
-    else if (ndw % 4 == 0)
-        hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<true>), dim3(grid_1d(3 * ndw / 4 + 3 * g.O)),
-                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
-                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
-                           a.want_db, g.terms());
-    else
-        hipLaunchKernelGGL((qconv_bwd_weight_reduce_kernel<false>), dim3(grid_1d(3 * ndw + 3 * g.O)),
-                           dim3(kThreads), 0, st, static_cast<const float *>(a.ws_dw),
-                           static_cast<const float *>(a.ws_db), p.splits, ndw, g.O, dwa, dwb, dwc, dba, dbb, dbc,
-                           a.want_db, g.terms());
-    return hip_status();
+    return reduce_bw_partials(g, p.splits, a, dwa, dwb, dwc, dba, dbb, dbc, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -115,3 +115,42 @@ def test_smallc_fused_epilogue():
     assert qlh.relerr(ssum.double().cpu().numpy(), yd.sum(axis=(0, 2, 3))) <= 1e-5
     assert qlh.relerr(ssq.double().cpu().numpy(), (yd * yd).sum(axis=(0, 2, 3))) <= 1e-5
     assert qlh.relerr(ssum.double().cpu().numpy(), ref_sum) <= qlh.tol(True, False)
+
+
+# Input gradient of the few-channel layers, stride 1: the per-pixel partial
+# sums and their gather fused in one kernel over bands of input rows (the
+# partial sums of a band's halo rows recomputed), at several band heights.
+FUSED_SHAPES = [
+    (4, 3, 32, 32, 64, 3, 3, 1, 1),     # the RGB stem
+    (2, 1, 9, 9, 64, 5, 5, 1, 2),       # 5 x 5: a halo of 4 rows
+    (3, 2, 11, 7, 32, 3, 3, 1, 0),      # no padding: the output map is smaller
+    (2, 3, 5, 6, 16, 3, 3, 1, 1),       # 16 output channels, bands past the last row
+]
+
+
+@pytest.mark.parametrize("rb", ["1", "3", "8"])
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("shape", FUSED_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_fused_input_gradient_matches_oracle(shape, bf16, rb, monkeypatch):
+    N, C, H, W, O, KH, KW, s, p = shape
+    print(f"fused small-C input gradient rows={rb} shape={shape} bf16={bf16}", flush=True)
+    monkeypatch.setenv("QLAYER_BWD_DATA_FUSED_RB", rb)
+    inp = synth.random_conv_case([803] + list(shape), N, C, H, W, O, KH, KW, s, p, bf16=bf16)
+    got = qlh.conv_to_np(qlh.run_conv(inp, s, p, bf16))
+    ref = _oracle_all(inp, s, p)
+    e = qlh.relerr(got["dx"], ref["dx"])
+    assert e <= qlh.tol(bf16, True), f"dx: normwise relative error {e:.3e}"
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+def test_smallc_dense_layer(bf16):
+    """A fully-connected layer with few inputs (27 -> 64) takes the same kernels (H = W = 1)."""
+    print(f"small-C dense layer bf16={bf16}", flush=True)
+    inp = synth.random_dense_case([806], 300, 27, 64, bf16=bf16)
+    got = {k: v.double().cpu().numpy() for k, v in qlh.run_linear(inp, bf16).items()}
+    y, ta, tb = oracle.linear_fwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"])
+    ref = oracle.linear_bwd(inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"], inp["gy"])
+    ref.update({"y": y, "ta": ta, "tb": tb})
+    for k in KEYS_FWD + KEYS_GRAD:
+        e = qlh.relerr(got[k], ref[k])
+        assert e <= qlh.tol(bf16, k in KEYS_GRAD), f"{k}: normwise relative error {e:.3e}"
