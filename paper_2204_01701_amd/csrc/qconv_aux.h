@@ -311,6 +311,18 @@ __global__ __launch_bounds__(kThreads) void qconv_pad_channels_kernel(PadSegment
     if (blockIdx.y >= NSEG) return;
     const T *__restrict__ src = static_cast<const T *>(sg.src[blockIdx.y]);
     T *__restrict__ dst = static_cast<T *>(sg.dst[blockIdx.y]);
+    if (Cp * (int)sizeof(T) == 16) {
+        // one padded row per 16-byte store (the usual case: 3 channels padded to 8 bf16 or 4 fp32)
+        const long long rows = sg.rows[blockIdx.y];
+        for (long long r = (long long)blockIdx.x * blockDim.x + threadIdx.x; r < rows;
+             r += (long long)gridDim.x * blockDim.x) {
+            float v[16 / sizeof(T)];
+#pragma unroll
+            for (int c = 0; c < (int)(16 / sizeof(T)); ++c) v[c] = c < C ? to_f32<T>(src[r * C + c]) : 0.0f;
+            *reinterpret_cast<v4u *>(dst + r * Cp) = vpack<T>(v);
+        }
+        return;
+    }
     const long long total = sg.rows[blockIdx.y] * Cp;
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (long long)gridDim.x * blockDim.x) {
