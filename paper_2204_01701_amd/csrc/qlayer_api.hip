@@ -474,7 +474,9 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
             sg.dst[i] = wsb + (i == 0 ? 0 : p.xpad_bytes + (size_t)(i - 1) * p.wpad_bytes);
             sg.rows[i] = rows[i];
         }
-        hipLaunchKernelGGL((qconv_pad_channels_kernel<T, 4>), dim3(grid_1d(rows[0] * p.Cp), 4), dim3(kThreads), 0, st,
+        // (one thread per row when a padded row is one 16-byte vector, else per element)
+        const long long pad_items = rows[0] * (p.Cp * (int)sizeof(T) == 16 ? 1 : p.Cp);
+        hipLaunchKernelGGL((qconv_pad_channels_kernel<T, 4>), dim3(grid_1d(pad_items), 4), dim3(kThreads), 0, st,
                            sg, g.C, p.Cp);
         const ql_status s0 = hip_status();
         if (s0 != QL_OK) return s0;
@@ -794,7 +796,8 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
         sg.src[0] = x;
         sg.dst[0] = wsb;
         sg.rows[0] = (long long)g.N * g.H * g.W;
-        hipLaunchKernelGGL((qconv_pad_channels_kernel<T, 1>), dim3(grid_1d(sg.rows[0] * p.Cp), 1), dim3(kThreads), 0, st,
+        const long long pad_items = sg.rows[0] * (p.Cp * (int)sizeof(T) == 16 ? 1 : p.Cp);
+        hipLaunchKernelGGL((qconv_pad_channels_kernel<T, 1>), dim3(grid_1d(pad_items), 1), dim3(kThreads), 0, st,
                            sg, g.C, p.Cp);
         const ql_status s0 = hip_status();
         if (s0 != QL_OK) return s0;
