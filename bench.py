@@ -185,12 +185,13 @@ def time_calls(torch, calls, steps, warmup, stream, timed_families=None):
     t0 = time.perf_counter()
     start = DevEvent()
     stop = DevEvent()
+    ntimed = steps * sum(1 for fam, _ in calls if timed_families is None or fam in timed_families)
+    pool = [(DevEvent(), DevEvent()) for _ in range(ntimed)]  # created before the timed loop
     start.record(stream)
     for _ in range(steps):
         for fam, fn in calls:
             if timed_families is None or fam in timed_families:
-                e0 = DevEvent()
-                e1 = DevEvent()
+                e0, e1 = pool.pop()
                 e0.record(stream)
                 fn(stream)
                 e1.record(stream)
@@ -207,6 +208,24 @@ def time_calls(torch, calls, steps, warmup, stream, timed_families=None):
         fam_ms[fam] = fam_ms.get(fam, 0.0) + e0.elapsed_time(e1)
         fam_n[fam] = fam_n.get(fam, 0) + 1
     return ms_step, wall, fam_ms, fam_n
+
+
+def time_each(torch, calls, reps, stream):
+    """Device time per call of each (key, fn) in `calls`: the call repeated `reps`
+    times back to back (after one untimed call), HIP events at the two ends only,
+    so that the host's launch time between calls stays hidden behind the GPU's
+    work.  Returns {key: ms per call}."""
+    out = {}
+    for key, fn in calls:
+        fn(stream)
+        a, b = DevEvent(), DevEvent()
+        a.record(stream)
+        for _ in range(reps):
+            fn(stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        out[key] = a.elapsed_time(b) / reps
+    return out
 
 
 def time_overlapped(torch, layers, steps, warmup, s1, s2, group=2):
@@ -493,15 +512,19 @@ def main():
         calls.append((("bwd_data", i), ly.bwd_data))
         calls.append((("bwd_weight", i), ly.bwd_weight))
 
-    # Diagnostic pass (not the timed region): every launch bracketed by events, for
-    # the per-layer table and to find the family that takes the most time.
-    _, _, diag_ms, diag_n = time_calls(torch, calls, 2, args.warmup, stream)
+    # Diagnostic pass (not the timed region): each call repeated back to back with
+    # events at the ends, for the per-layer table and to find the family that takes
+    # the most time.
+    for _ in range(args.warmup):  # warm-up steps
+        for _, fn in calls:
+            fn(stream)
+    diag = time_each(torch, calls, 10, stream)
     per_layer = []
     fam_tot = {"fwd": 0.0, "bwd_data": 0.0, "bwd_weight": 0.0}
     for i, L in enumerate(geoms):
         row = {"layer": i + 1, "shape": f"{L.c}->{L.o} {L.h}x{L.w}"}
         for fam in ("fwd", "bwd_data", "bwd_weight"):
-            ms = diag_ms[(fam, i)] / diag_n[(fam, i)]
+            ms = diag[(fam, i)]
             fam_tot[fam] += ms
             row[f"{fam}_us"] = round(ms * 1e3, 1)
             row[f"{fam}_tflops"] = round(3 * unit_flops(L) / (ms * 1e-3) / 1e12, 1)
@@ -665,7 +688,8 @@ def depthwise(ql, torch, dev, stream, reps=10):
     section 4.2 and Table 3), bf16, the proposed neuron: the 13 depthwise /
     pointwise pairs of a CIFAR MobileNet-V1 at batch 128 (summed over the
     layers), and one large depthwise layer (N=64, C=256, 56x56, 3x3) where the
-    direct kernels meet the HBM roofline; each pass timed separately."""
+    direct kernels meet the HBM roofline; each pass timed separately (each call
+    repeated back to back, events at the ends: time_each)."""
     import synth
 
     fams = ("fwd", "bwd_data", "bwd_weight")
@@ -675,12 +699,13 @@ def depthwise(ql, torch, dev, stream, reps=10):
     pws = [Layer(ql, torch, p, 8, i, dev) for i, (_, p) in enumerate(pairs)]
     calls = [((f, "dw", i), getattr(ly, f)) for i, ly in enumerate(dws) for f in fams]
     calls += [((f, "pw", i), getattr(ly, f)) for i, ly in enumerate(pws) for f in fams]
-    ms, _, fam_ms, fam_n = time_calls(torch, calls, reps, 3, stream)
+    ms, _, _, _ = time_calls(torch, calls, reps, 3, stream, timed_families=set())
+    each = time_each(torch, calls, reps, stream)
     r = {"shape": "CIFAR MobileNet-V1, batch 128, 13 pairs of 3x3 depthwise + 1x1 pointwise, bf16",
          "pair_step_us": round(ms * 1e3, 1)}
     for kind, lys in (("dw", dws), ("pw", pws)):
         for f in fams:
-            t = sum(fam_ms[(f, kind, i)] / fam_n[(f, kind, i)] for i in range(len(lys)))
+            t = sum(each[(f, kind, i)] for i in range(len(lys)))
             r[f"{kind}_{f}_us"] = round(t * 1e3, 1)
             if kind == "dw":
                 r[f"{kind}_{f}_gbs"] = round(sum(dw_bytes(ly.L, f) for ly in lys) / (t * 1e-3) / 1e9, 1)
@@ -692,10 +717,11 @@ def depthwise(ql, torch, dev, stream, reps=10):
     L = synth.ConvLayer(n=64, c=256, h=56, w=56, o=256, k=3, stride=1, pad=1)
     ly = Layer(ql, torch, L, 9, 0, dev, depthwise=True)
     calls = [(f, getattr(ly, f)) for f in fams]
-    ms, _, fam_ms, fam_n = time_calls(torch, calls, reps, 3, stream)
+    ly.fwd(stream)
+    each = time_each(torch, calls, reps, stream)
     r = {"shape": "N=64 C=256 56x56, 3x3 depthwise, bf16", "peak_gbs": HBM_PEAK_GBS}
     for f in fams:
-        t = fam_ms[f] / fam_n[f]
+        t = each[f]
         gbs = dw_bytes(L, f) / (t * 1e-3) / 1e9
         r[f"{f}_us"] = round(t * 1e3, 1)
         r[f"{f}_gbs"] = round(gbs, 1)
@@ -743,8 +769,8 @@ def epilogue_cost(ql, torch, dev, stream, reps=10):
                         ("scale_shift_relu", [(i, fwd_ex(i, affs[i][0])) for i in range(len(layers))]),
                         ("plain_then_torch_sums", [c for i in range(len(layers))
                                                    for c in ((i, layers[i].fwd), (("t", i), torch_stats(i)))])):
-        _, _, fam_ms, fam_n = time_calls(torch, calls, reps, 2, stream)
-        res[f"{name}_us"] = round(sum(fam_ms[k] / fam_n[k] for k in fam_ms) * 1e3, 1)
+        each = time_each(torch, calls, reps, stream)
+        res[f"{name}_us"] = round(sum(each.values()) * 1e3, 1)
     del layers
     return res
 
