@@ -257,3 +257,20 @@ def test_epilogue_validation(L):
     dd = ql.conv_desc(8, 32, 32, 32, 32, 3, 3, 1, 1, ql.QL_BF16, 0, groups=32)
     assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(dd), ctypes.byref(relu)) == 0
     assert L.qlayer_conv2d_fwd_ex_workspace_size(ctypes.byref(dd), ctypes.byref(stats)) >= 2 * 32 * 4
+
+
+def test_few_channel_paths_need_no_workspace(L, monkeypatch):
+    """The few-input-channel forward (no zero-padded copies) and the fused input
+    gradient at stride 1 (partial sums in LDS) ask for no workspace; forced off,
+    the padded forward and the two-kernel input gradient ask for their buffers."""
+    for dt in (ql.QL_BF16, ql.QL_F32):
+        stem = ql.conv_desc(128, 3, 32, 32, 64, 3, 3, 1, 1, dt)
+        assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(stem)) == 0
+        assert L.qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(stem)) == 0
+        strided = ql.conv_desc(128, 3, 32, 32, 64, 3, 3, 2, 1, dt)
+        assert L.qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(strided)) >= 128 * 16 * 16 * 27 * 4
+    monkeypatch.setenv("QLAYER_FWD_SMALLC", "0")
+    monkeypatch.setenv("QLAYER_BWD_DATA_FUSED_RB", "0")
+    stem = ql.conv_desc(128, 3, 32, 32, 64, 3, 3, 1, 1, ql.QL_BF16)
+    assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(stem)) >= 128 * 32 * 32 * 8 * 2   # X padded to 8
+    assert L.qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(stem)) >= 128 * 32 * 32 * 27 * 4
