@@ -245,13 +245,14 @@ def linear_dw_row(x, wa, wb, wc, ba, bb, bc, gy, o):
 
 
 # Neuron types (the proposed one and the earlier designs of Table 1 / Table 3).
-NEURON_QUADRA, NEURON_T4, NEURON_T4_IDENTITY, NEURON_T3, NEURON_T2 = 0, 1, 2, 3, 4
-NEURON_TERMS = {0: 3, 1: 2, 2: 2, 3: 1, 4: 1}  # first-order terms (weights) per type
+NEURON_QUADRA, NEURON_T4, NEURON_T4_IDENTITY, NEURON_T3, NEURON_T2, NEURON_T24 = 0, 1, 2, 3, 4, 5
+NEURON_TERMS = {0: 3, 1: 2, 2: 2, 3: 1, 4: 1, 5: 3}  # first-order terms (weights) per type
 
 
 def conv2d_fwd_neuron(neuron, x, wa, wb=None, wc=None, ba=None, bb=None, bc=None, stride=1, pad=0):
     """Forward of neuron type `neuron`: returns (Y, T_a, T_b), N x O x Ho x Wo
-    (T_b is zeros for the one-term types, T_a is W_a*(X o X) + b_a for T2)."""
+    (T_b is zeros for the one-term types, T_a is W_a*(X o X) + b_a for T2;
+    T2&4 = T_a o T_b + W_c*(X o X) + b_c)."""
     lib = _load()
     x, wa, wb, wc, ba, bb, bc = map(_f64, (x, wa, wb, wc, ba, bb, bc))
     g = _conv_geom(x, wa, stride, pad)
@@ -301,6 +302,7 @@ def linear_bwd_neuron(neuron, x, wa, wb, wc, ba, bb, bc, gy):
 
 
 def _dw_geom(neuron, x, w, stride, pad):
+    assert int(neuron) in (0, 1, 2, 3, 4), "the depthwise oracle covers the proposed neuron, T4, T4+identity, T3, T2"
     N, C, H, W = x.shape
     C2, one, KH, KW = w.shape
     assert C2 == C and one == 1, "depthwise weights are C x 1 x KH x KW"

@@ -188,14 +188,18 @@ void oracle_conv2d_bwd(int N, int C, int H, int W, int O, int KH, int KW,
  * The earlier quadratic neuron types the paper compares its design with
  * (Table 1 types and the Table 3 baselines), as convolution layers with the
  * same geometry rules.  neuron: 0 the proposed one (as above), 1 T4, 2 T4 plus
- * identity, 3 T3, 4 T2.  With T_t = W_t * X + b_t:
+ * identity, 3 T3, 4 T2, 5 T2&4.  With T_t = W_t * X + b_t:
  *   T4:            Y = T_a o T_b
  *   T4 + identity: Y = T_a o T_b + X      (C == O, Ho == H, Wo == W: the
  *                                          shortcut adds input channel o)
  *   T3:            Y = T_a o T_a          (the square of one first-order neuron)
  *   T2:            Y = W_a * (X o X) + b_a (a first-order neuron of the squared input)
+ *   T2&4:          Y = T_a o T_b + (W_c * (X o X) + b_c)   (Table 1: the product
+ *                  of two first-order terms plus a first-order neuron of the
+ *                  squared input; the proposed design is this with X in place
+ *                  of X o X in its third term, section 3.1)
  * Unused weights and biases are ignored (may be NULL).  The saved maps:
- * T_a and T_b (T4 types), T_a (T3), none (T2).
+ * T_a and T_b (T4 types, T2&4), T_a (T3), none (T2).
  * ------------------------------------------------------------------------- */
 void oracle_conv2d_fwd_neuron(int neuron, int N, int C, int H, int W, int O, int KH, int KW,
                               int sh, int sw, int ph, int pw,
@@ -211,7 +215,7 @@ void oracle_conv2d_fwd_neuron(int neuron, int N, int C, int H, int W, int O, int
     if (neuron == 2 && (C != O || Ho != H || Wo != W)) return;
     size_t nx = (size_t)N * C * H * W;
     double *x2 = NULL;
-    if (neuron == 4) { /* the squared input, elementwise */
+    if (neuron == 4 || neuron == 5) { /* the squared input, elementwise */
         x2 = (double *)malloc(nx * sizeof(double));
         if (!x2) return;
         for (size_t e = 0; e < nx; ++e) x2[e] = x[e] * x[e];
@@ -233,6 +237,7 @@ void oracle_conv2d_fwd_neuron(int neuron, int N, int C, int H, int W, int O, int
                 Tb = conv_term(C, H, W, KH, KW, sh, sw, ph, pw, x, wb, bb, n, o, i, j);
                 out = Ta * Tb;
                 if (neuron == 2) out += x[IDX4(n, o, i, j, C, H, W)];
+                if (neuron == 5) out += conv_term(C, H, W, KH, KW, sh, sw, ph, pw, x2, wc, bc, n, o, i, j);
             }
         }
         if (y) y[e] = out;
@@ -248,6 +253,9 @@ void oracle_conv2d_fwd_neuron(int neuron, int N, int C, int H, int W, int O, int
  *   T3:                G_a = 2 G o T_a
  *   T2:                G_a = G, the operand being X o X, so dW_a correlates G
  *                      with X o X and dX = 2 X o (transposed convolution of G with W_a)
+ *   T2&4:              G_a = G o T_b, G_b = G o T_a on the operand X, G_c = G on
+ *                      the operand X o X, so dW_c correlates G with X o X and the
+ *                      c term's share of dX is 2 X o (transposed convolution of G with W_c)
  * and each term's weight, bias and input gradients are those of an ordinary
  * convolution (the same loops as oracle_conv2d_bwd, written out again here). */
 void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int KH, int KW,
@@ -270,13 +278,17 @@ void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int
     double *gb = (double *)malloc(P * sizeof(double));
     double *ta = (double *)malloc(P * sizeof(double));
     double *tb = (double *)malloc(P * sizeof(double));
-    double *xo = (double *)malloc(nx * sizeof(double)); /* the operand X (or X o X) */
-    if (!ga || !gb || !ta || !tb || !xo) { free(ga); free(gb); free(ta); free(tb); free(xo); return; }
+    double *xo = (double *)malloc(nx * sizeof(double)); /* the operand X (or X o X) of terms a, b */
+    double *xs = (double *)malloc(nx * sizeof(double)); /* X o X, the operand of T2&4's term c */
+    if (!ga || !gb || !ta || !tb || !xo || !xs) {
+        free(ga); free(gb); free(ta); free(tb); free(xo); free(xs);
+        return;
+    }
     oracle_conv2d_fwd_neuron(neuron, N, C, H, W, O, KH, KW, sh, sw, ph, pw, x, wa, wb, wc, ba, bb, bc,
                              NULL, ta, tb);
-    int nterm = (neuron == 1 || neuron == 2) ? 2 : 1;
+    int nterm = (neuron == 1 || neuron == 2) ? 2 : (neuron == 5 ? 3 : 1);
     for (size_t e = 0; e < P; ++e) {
-        if (nterm == 2) {
+        if (nterm >= 2) {
             ga[e] = gy[e] * tb[e];
             gb[e] = gy[e] * ta[e];
         } else if (neuron == 3) {
@@ -285,17 +297,21 @@ void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int
             ga[e] = gy[e];
         }
     }
-    for (size_t e = 0; e < nx; ++e) xo[e] = neuron == 4 ? x[e] * x[e] : x[e];
-    const double *gt[2] = {ga, gb};
-    double *dwt[2] = {dwa, dwb};
-    double *dbt[2] = {dba, dbb};
-    const double *wt[2] = {wa, wb};
-    (void)wc; (void)bc; (void)dwc; (void)dbc;
+    for (size_t e = 0; e < nx; ++e) {
+        xo[e] = neuron == 4 ? x[e] * x[e] : x[e];
+        xs[e] = x[e] * x[e];
+    }
+    /* per term: its output gradient, operand, weights and outputs */
+    const double *gt[3] = {ga, gb, gy};
+    const double *xt[3] = {xo, xo, xs};
+    double *dwt[3] = {dwa, dwb, dwc};
+    double *dbt[3] = {dba, dbb, dbc};
+    const double *wt[3] = {wa, wb, wc};
 
     long long nw = (long long)O * C * KH * KW;
     for (int t = 0; t < nterm; ++t) {
         if (!dwt[t]) continue;
-        const double *g = gt[t];
+        const double *g = gt[t], *xx = xt[t];
         double *dw = dwt[t];
 #pragma omp parallel for schedule(static)
         for (long long e = 0; e < nw; ++e) {
@@ -309,7 +325,7 @@ void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int
                     for (int j = 0; j < Wo; ++j) {
                         int iw = j * sw - pw + q;
                         if (iw < 0 || iw >= W) continue;
-                        acc += g[IDX4(n, o, i, j, O, Ho, Wo)] * xo[IDX4(n, c, ih, iw, C, H, W)];
+                        acc += g[IDX4(n, o, i, j, O, Ho, Wo)] * xx[IDX4(n, c, ih, iw, C, H, W)];
                     }
                 }
             dw[e] = acc;
@@ -333,7 +349,7 @@ void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int
         for (long long e = 0; e < nxx; ++e) {
             int w_ = (int)(e % W), h = (int)((e / W) % H);
             int c = (int)((e / ((long long)W * H)) % C), n = (int)(e / ((long long)W * H * C));
-            double acc = 0.0;
+            double part[3] = {0.0, 0.0, 0.0}; /* each term's transposed convolution at (n, c, h, w) */
             for (int t = 0; t < nterm; ++t)
                 for (int o = 0; o < O; ++o)
                     for (int r = 0; r < KH; ++r) {
@@ -346,15 +362,18 @@ void oracle_conv2d_bwd_neuron(int neuron, int N, int C, int H, int W, int O, int
                             if (wi < 0 || wi % sw) continue;
                             int j = wi / sw;
                             if (j >= Wo) continue;
-                            acc += gt[t][IDX4(n, o, i, j, O, Ho, Wo)] * wt[t][IDX4(o, c, r, q, C, KH, KW)];
+                            part[t] += gt[t][IDX4(n, o, i, j, O, Ho, Wo)] * wt[t][IDX4(o, c, r, q, C, KH, KW)];
                         }
                     }
-            if (neuron == 4) acc *= 2.0 * x[e];                 /* d(X o X)/dX */
+            double acc;
+            if (neuron == 4) acc = part[0] * (2.0 * x[e]);                  /* d(X o X)/dX */
+            else if (neuron == 5) acc = part[0] + part[1] + part[2] * (2.0 * x[e]);
+            else acc = part[0] + part[1];
             if (neuron == 2) acc += gy[IDX4(n, c, h, w_, O, Ho, Wo)]; /* the identity shortcut */
             dx[e] = acc;
         }
     }
-    free(ga); free(gb); free(ta); free(tb); free(xo);
+    free(ga); free(gb); free(ta); free(tb); free(xo); free(xs);
 }
 
 /* ---------------------------------------------------------------------------

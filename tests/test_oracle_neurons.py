@@ -1,6 +1,7 @@
 """Pins of the oracle's earlier neuron types (arXiv 2204.01701, Table 1 and
 the Table 3 baselines): T4 = T_a o T_b, T4 + identity = T_a o T_b + X,
-T3 = T_a o T_a, T2 = W_a * (X o X) + b_a, with T_t = W_t * X + b_t.
+T3 = T_a o T_a, T2 = W_a * (X o X) + b_a, T2&4 = T_a o T_b + W_c * (X o X) + b_c,
+with T_t = W_t * X + b_t.
 
 Each check ties them to something other than the oracle's own code:
 compositions of library convolutions (torch CPU, fp64) and their autograd,
@@ -15,8 +16,9 @@ import torch.nn.functional as F
 import oracle
 
 T4, T4I, T3, T2 = oracle.NEURON_T4, oracle.NEURON_T4_IDENTITY, oracle.NEURON_T3, oracle.NEURON_T2
-TYPES = [T4, T4I, T3, T2]
-NAMES = {T4: "T4", T4I: "T4+identity", T3: "T3", T2: "T2"}
+T24 = oracle.NEURON_T24
+TYPES = [T4, T4I, T3, T2, T24]
+NAMES = {T4: "T4", T4I: "T4+identity", T3: "T3", T2: "T2", T24: "T2&4"}
 
 
 def _rel(a, b):
@@ -39,6 +41,8 @@ def _torch_neuron(neuron, tx, tw, tb, s, p):
     if neuron == T3:
         return ta * ta
     y = ta * F.conv2d(tx, tw[1], tb[1], stride=s, padding=p)
+    if neuron == T24:
+        return y + F.conv2d(tx * tx, tw[2], tb[2], stride=s, padding=p)
     return y + tx if neuron == T4I else y
 
 
@@ -67,7 +71,7 @@ def test_forward_matches_library_convolutions(neuron, shape):
     ta_ref = F.conv2d(torch.from_numpy(xin), torch.from_numpy(ws[0]), torch.from_numpy(bs[0]), stride=s,
                       padding=p).numpy()
     assert _rel(ta, ta_ref) < 1e-13
-    if neuron in (T4, T4I):
+    if neuron in (T4, T4I, T24):
         tb_ref = F.conv2d(torch.from_numpy(x), torch.from_numpy(ws[1]), torch.from_numpy(bs[1]), stride=s,
                           padding=p).numpy()
         assert _rel(tb, tb_ref) < 1e-13
@@ -87,10 +91,10 @@ def test_gradients_match_autograd_of_composition(neuron, shape):
     d = oracle.conv2d_bwd_neuron(neuron, x, *ws, *bs, gy, stride=s, pad=p)
     assert _rel(d["dx"], tx.grad.numpy()) < 1e-12
     nt = oracle.NEURON_TERMS[neuron]
-    for k, kb, t, tbb in list(zip(("dwa", "dwb"), ("dba", "dbb"), tw, tbias))[:nt]:
+    for k, kb, t, tbb in list(zip(("dwa", "dwb", "dwc"), ("dba", "dbb", "dbc"), tw, tbias))[:nt]:
         assert _rel(d[k], t.grad.numpy()) < 1e-12, k
         assert _rel(d[kb], tbb.grad.numpy()) < 1e-12, kb
-    assert "dwc" not in d and (nt == 2 or "dwb" not in d)
+    assert (nt == 3 or "dwc" not in d) and (nt >= 2 or "dwb" not in d)
 
 
 @pytest.mark.parametrize("neuron", TYPES, ids=[NAMES[n] for n in TYPES])
@@ -102,20 +106,24 @@ def test_gradients_match_finite_differences(neuron):
     x, ws, bs = _case(rng, N, C, H, W, O, K)
     nt = oracle.NEURON_TERMS[neuron]
     params = {"x": x, "wa": ws[0], "ba": bs[0]}
-    if nt == 2:
+    if nt >= 2:
         params.update(wb=ws[1], bb=bs[1])
+    if nt == 3:
+        params.update(wc=ws[2], bc=bs[2])
     y, _, _ = oracle.conv2d_fwd_neuron(neuron, x, *ws, *bs, stride=s, pad=p)
     gy = rng.standard_normal(y.shape)
 
     def loss():
-        yy, _, _ = oracle.conv2d_fwd_neuron(neuron, params["x"], params["wa"], params.get("wb"), None,
-                                            params["ba"], params.get("bb"), None, stride=s, pad=p)
+        yy, _, _ = oracle.conv2d_fwd_neuron(neuron, params["x"], params["wa"], params.get("wb"), params.get("wc"),
+                                            params["ba"], params.get("bb"), params.get("bc"), stride=s, pad=p)
         return float(np.sum(gy * yy))
 
     d = oracle.conv2d_bwd_neuron(neuron, x, *ws, *bs, gy, stride=s, pad=p)
     grads = {"x": d["dx"], "wa": d["dwa"], "ba": d["dba"]}
-    if nt == 2:
+    if nt >= 2:
         grads.update(wb=d["dwb"], bb=d["dbb"])
+    if nt == 3:
+        grads.update(wc=d["dwc"], bc=d["dbc"])
     h = 1e-4
     for name, arr in params.items():
         flat = arr.reshape(-1)
@@ -174,14 +182,33 @@ def test_relations_to_the_proposed_neuron():
     assert _rel(d2["dwa"], dl["dwc"]) < 1e-14 and _rel(d2["dba"], dl["dbc"]) < 1e-14
     # ... with the chain rule through the square
     assert _rel(d2["dx"], 2 * x * dl["dx"]) < 1e-14
+    # T2&4 is the proposed neuron with X o X in place of X in its third term:
+    # T4 (pinned above) plus T2 with (W_c, b_c), outputs and gradients alike
+    y24, ta24, tb24 = oracle.conv2d_fwd_neuron(T24, x, wa, wb, wc, ba, bb, bc, stride=s, pad=p)
+    y2c, _, _ = oracle.conv2d_fwd_neuron(T2, x, wc, None, None, bc, stride=s, pad=p)
+    assert _rel(y24, y4 + y2c) < 1e-15
+    _, ta0, tb0 = oracle.conv2d_fwd(x, wa, wb, z, ba, bb, zb, s, p)
+    assert np.array_equal(ta24, ta0) and np.array_equal(tb24, tb0)
+    d24 = oracle.conv2d_bwd_neuron(T24, x, wa, wb, wc, ba, bb, bc, gy, stride=s, pad=p)
+    for k in ("dwa", "dwb", "dba", "dbb"):
+        assert _rel(d24[k], d4[k]) < 1e-14, k
+    d2c = oracle.conv2d_bwd_neuron(T2, x, wc, None, None, bc, None, None, gy, stride=s, pad=p)
+    assert _rel(d24["dwc"], d2c["dwa"]) < 1e-14 and _rel(d24["dbc"], d2c["dba"]) < 1e-14
+    assert _rel(d24["dx"], d4["dx"] + d2c["dx"]) < 1e-14
+    # ... and with X o X replaced by X it is the proposed neuron itself
+    yq, _, _ = oracle.conv2d_fwd(x, wa, wb, wc, ba, bb, bc, s, p)
+    yq2, _, _ = oracle.conv2d_fwd(x, wa, wb, z, ba, bb, zb, s, p)
+    yqc, _, _ = oracle.conv2d_fwd(x, z, z, wc, zb, zb, bc, s, p)
+    assert _rel(yq, yq2 + yqc) < 1e-14 and _rel(y24 - y2c, yq - yqc) < 1e-14
 
 
 def test_scalar_closed_forms():
     # one pixel, one channel, a 1x1 kernel: every type is a polynomial in x
     x, wa, wb, ba, bb, g = 1.5, -0.75, 2.0, 0.25, -0.5, 0.3
+    wc, bc = 1.25, 0.125
     X = np.full((1, 1, 1, 1), x)
-    Wa, Wb = np.full((1, 1, 1, 1), wa), np.full((1, 1, 1, 1), wb)
-    Ba, Bb = np.array([ba]), np.array([bb])
+    Wa, Wb, Wc = np.full((1, 1, 1, 1), wa), np.full((1, 1, 1, 1), wb), np.full((1, 1, 1, 1), wc)
+    Ba, Bb, Bc = np.array([ba]), np.array([bb]), np.array([bc])
     G = np.full((1, 1, 1, 1), g)
     ta, tb = wa * x + ba, wb * x + bb
     expect = {
@@ -189,11 +216,15 @@ def test_scalar_closed_forms():
         T4I: (ta * tb + x, g * (wa * tb + wb * ta) + g, g * tb * x, g * ta * x),
         T3: (ta * ta, g * 2 * ta * wa, g * 2 * ta * x, None),
         T2: (wa * x * x + ba, g * wa * 2 * x, g * x * x, None),
+        T24: (ta * tb + wc * x * x + bc, g * (wa * tb + wb * ta + 2 * wc * x), g * tb * x, g * ta * x),
     }
     for n, (y, dx, dwa, dwb) in expect.items():
-        yy, _, _ = oracle.conv2d_fwd_neuron(n, X, Wa, Wb, None, Ba, Bb)
+        yy, _, _ = oracle.conv2d_fwd_neuron(n, X, Wa, Wb, Wc, Ba, Bb, Bc)
         assert yy.item() == pytest.approx(y, rel=1e-15), NAMES[n]
-        d = oracle.conv2d_bwd_neuron(n, X, Wa, Wb, None, Ba, Bb, None, G)
+        d = oracle.conv2d_bwd_neuron(n, X, Wa, Wb, Wc, Ba, Bb, Bc, G)
+        if n == T24:
+            assert d["dwc"].item() == pytest.approx(g * x * x, rel=1e-15)
+            assert d["dbc"].item() == pytest.approx(g, rel=1e-15)
         assert d["dx"].item() == pytest.approx(dx, rel=1e-15), NAMES[n]
         assert d["dwa"].item() == pytest.approx(dwa, rel=1e-15), NAMES[n]
         if dwb is not None:
@@ -205,19 +236,23 @@ def test_fc_neurons_match_matrix_closed_forms(neuron):
     rng = np.random.default_rng([24, neuron])
     B, I, O = 5, 6, 6
     x = rng.standard_normal((B, I))
-    wa, wb = rng.standard_normal((O, I)), rng.standard_normal((O, I))
-    ba, bb = rng.standard_normal(O), rng.standard_normal(O)
+    wa, wb, wc = rng.standard_normal((O, I)), rng.standard_normal((O, I)), rng.standard_normal((O, I))
+    ba, bb, bc = rng.standard_normal(O), rng.standard_normal(O), rng.standard_normal(O)
     gy = rng.standard_normal((B, O))
     ta, tb = x @ wa.T + ba, x @ wb.T + bb
+    tc = (x * x) @ wc.T + bc
     if neuron == T2:
         ta = (x * x) @ wa.T + ba
-    y = {T4: ta * tb, T4I: ta * tb + x, T3: ta * ta, T2: ta}[neuron]
-    yy, _, _ = oracle.linear_fwd_neuron(neuron, x, wa, wb, None, ba, bb)
+    y = {T4: ta * tb, T4I: ta * tb + x, T3: ta * ta, T2: ta, T24: ta * tb + tc}[neuron]
+    yy, _, _ = oracle.linear_fwd_neuron(neuron, x, wa, wb, wc, ba, bb, bc)
     assert _rel(yy, y) < 1e-14
-    d = oracle.linear_bwd_neuron(neuron, x, wa, wb, None, ba, bb, None, gy)
-    if neuron in (T4, T4I):
+    d = oracle.linear_bwd_neuron(neuron, x, wa, wb, wc, ba, bb, bc, gy)
+    if neuron in (T4, T4I, T24):
         ga, gb = gy * tb, gy * ta
         dx = ga @ wa + gb @ wb + (gy if neuron == T4I else 0)
+        if neuron == T24:
+            dx = dx + 2 * x * (gy @ wc)
+            assert _rel(d["dwc"], gy.T @ (x * x)) < 1e-14 and _rel(d["dbc"], gy.sum(0)) < 1e-14
         assert _rel(d["dwb"], gb.T @ x) < 1e-14 and _rel(d["dbb"], gb.sum(0)) < 1e-14
         assert _rel(d["dwa"], ga.T @ x) < 1e-14 and _rel(d["dba"], ga.sum(0)) < 1e-14
     elif neuron == T3:

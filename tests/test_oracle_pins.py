@@ -316,15 +316,17 @@ def test_sampled_functions_agree_with_full():
     y, ta, tb = oracle.conv2d_fwd(x, *ws, *bs, s, p)
     gy = rng.standard_normal(y.shape)
     d = oracle.conv2d_bwd(x, *ws, *bs, gy, s, p)
-    idx = np.array([[0, 0, 0, 0], [1, 4, y.shape[2] - 1, y.shape[3] - 1], [1, 2, 1, 2]])
+    # every element of every output (the samplers must agree everywhere, not at a few points)
+    idx = np.array(list(np.ndindex(*y.shape)))
     ys, tas, tbs = oracle.conv2d_fwd_at(x, *ws, *bs, idx, s, p)
-    for k, (n, o, i, j) in enumerate(idx):
-        assert ys[k] == y[n, o, i, j] and tas[k] == ta[n, o, i, j] and tbs[k] == tb[n, o, i, j]
-    xi = np.array([[0, 0, 0, 0], [1, 3, H - 1, W - 1], [0, 2, 3, 1]])
+    n, o, i, j = idx.T
+    assert np.array_equal(ys, y[n, o, i, j]) and np.array_equal(tas, ta[n, o, i, j])
+    assert np.array_equal(tbs, tb[n, o, i, j])
+    xi = np.array(list(np.ndindex(*x.shape)))
     dxs = oracle.conv2d_dx_at(x, *ws, *bs, gy, xi, s, p)
-    ref = np.array([d["dx"][tuple(r)] for r in xi])
-    assert _rel(dxs, ref) < 1e-13
-    for o in (0, 3):
+    ref = d["dx"][tuple(xi.T)]
+    assert np.max(np.abs(dxs - ref)) <= 1e-13 * max(1.0, np.max(np.abs(ref)))
+    for o in range(O):
         dc = oracle.conv2d_dw_channel(x, *ws, *bs, gy, o, s, p)
         for k in ("dwa", "dwb", "dwc"):
             assert _rel(dc[k], d[k][o]) < 1e-13
@@ -335,15 +337,31 @@ def test_sampled_functions_agree_with_full():
     xf = rng.standard_normal((B, I))
     wf = [rng.standard_normal((O2, I)) for _ in range(3)]
     bf = [rng.standard_normal(O2) for _ in range(3)]
-    yf, taf, _ = oracle.linear_fwd(xf, *wf, *bf)
+    yf, taf, tbf = oracle.linear_fwd(xf, *wf, *bf)
     gf = rng.standard_normal(yf.shape)
     df = oracle.linear_bwd(xf, *wf, *bf, gf)
-    ysf, tasf, _ = oracle.linear_fwd_at(xf, *wf, *bf, [[0, 0], [5, 3]])
-    assert ysf[1] == yf[5, 3] and tasf[0] == taf[0, 0]
+    # every output of every sampled element, the whole index space
+    fidx = np.array([[b, o] for b in range(B) for o in range(O2)])
+    ysf, tasf, tbsf = oracle.linear_fwd_at(xf, *wf, *bf, fidx)
+    for k, (b, o) in enumerate(fidx):
+        assert ysf[k] == yf[b, o] and tasf[k] == taf[b, o] and tbsf[k] == tbf[b, o]
     dxr = oracle.linear_dx_rows(xf, *wf, *bf, gf, [2, 4])
     assert _rel(dxr, df["dx"][[2, 4]]) < 1e-13
-    dr = oracle.linear_dw_row(xf, *wf, *bf, gf, 1)
-    assert _rel(dr["dwa"], df["dwa"][1]) < 1e-13 and abs(dr["dbb"][0] - df["dbb"][1]) < 1e-12
+    for o in range(O2):
+        dr = oracle.linear_dw_row(xf, *wf, *bf, gf, o)
+        for k in ("dwa", "dwb", "dwc"):
+            assert _rel(dr[k], df[k][o]) < 1e-13, (k, o)
+        for k in ("dba", "dbb", "dbc"):
+            assert abs(dr[k][0] - df[k][o]) <= 1e-13 * max(1.0, abs(df[k][o])), (k, o)
+    # the full dense backward against numpy closed forms (so that the sampled
+    # functions are pinned through it, not only to it)
+    ga, gb = gf * tbf, gf * taf
+    assert _rel(df["dwa"], ga.T @ xf) < 1e-13 and _rel(df["dwb"], gb.T @ xf) < 1e-13
+    assert _rel(df["dwc"], gf.T @ xf) < 1e-13
+    assert _rel(df["dba"], ga.sum(0)) < 1e-13 and _rel(df["dbb"], gb.sum(0)) < 1e-13
+    assert _rel(df["dbc"], gf.sum(0)) < 1e-13
+    assert _rel(df["dx"], ga @ wf[0] + gb @ wf[1] + gf @ wf[2]) < 1e-13
+    assert _rel(tbf, xf @ wf[1].T + bf[1]) < 1e-13
 
 
 # --- the 3x parameter relation of Table 1 / Table 3 -------------------------
