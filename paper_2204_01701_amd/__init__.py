@@ -74,7 +74,9 @@ class Epilogue(ctypes.Structure):
 
 def epilogue(scale=None, shift=None, relu=False, stat_sum=None, stat_sumsq=None) -> Epilogue:
     """An Epilogue over float32 device tensors of O values (or None); the tensors must outlive the call."""
-    return Epilogue(_ptr(scale), _ptr(shift), int(bool(relu)), _ptr(stat_sum), _ptr(stat_sumsq))
+    e = Epilogue(_ptr(scale), _ptr(shift), int(bool(relu)), _ptr(stat_sum), _ptr(stat_sumsq))
+    e.tensors = [("epi.scale", scale), ("epi.shift", shift), ("epi.sum", stat_sum), ("epi.sumsq", stat_sumsq)]
+    return e
 
 
 def conv_desc(n, c, h, w, o, kh, kw, stride=1, pad=0, dtype=QL_BF16, neuron=QL_NEURON_QUADRA,
@@ -169,8 +171,14 @@ def _stream(stream, device):
     return torch.cuda.current_stream(device).cuda_stream
 
 
-def _workspace(workspace, need, device):
-    """(pointer, bytes) of the workspace; allocates one with torch when none is given."""
+def _workspace(workspace, need, device, stream=None):
+    """(pointer, bytes) of the workspace; allocates one with torch when none is given.
+
+    The allocation is made on the current stream.  When the call runs on
+    another stream, the block is recorded on that stream, so that the caching
+    allocator does not hand it out again while the kernels there still use it;
+    a raw stream handle (an int) cannot be recorded and needs an explicit
+    workspace."""
     if workspace is not None:
         if isinstance(workspace, tuple):
             return workspace
@@ -178,9 +186,70 @@ def _workspace(workspace, need, device):
     if need == 0:
         return None, 0
     import torch
+    if isinstance(stream, int):
+        raise ValueError("a raw stream handle needs an explicit workspace (the allocator cannot track its use)")
     ws = torch.empty(need, dtype=torch.uint8, device=device)
+    if stream is not None and stream != torch.cuda.current_stream(device):
+        ws.record_stream(stream)
     _workspace.keep = ws  # keep alive until the next allocation; the stream orders reuse
     return ws.data_ptr(), need
+
+
+# --- host-side checks of tensor arguments -------------------------------------
+# The C ABI sees bare pointers, so a tensor of the wrong size, dtype or device
+# would make the kernels read or write out of bounds.  Every tensor argument is
+# checked against the descriptor before the call: a CUDA tensor on the
+# device of the others, with the element count and dtype its role requires.
+
+def _act_dtype(code):
+    import torch
+    if code == QL_BF16:
+        return torch.bfloat16
+    if code == QL_F32:
+        return torch.float32
+    return None  # (the library rejects unknown dtypes itself)
+
+
+def _expect(name, t, numel, dtype, device):
+    if t is None or isinstance(t, int):
+        return
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: a CUDA device tensor is required, got one on {t.device}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: on {t.device}, the other tensors on {device}")
+    if t.numel() != numel:
+        raise ValueError(f"{name}: {t.numel()} elements, the descriptor needs {numel}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+
+
+def _conv_sizes(d):
+    """Element counts of X, each W_t, the output-side maps, the biases."""
+    dw = d.groups == d.c and d.c > 1
+    nw = d.o * d.kh * d.kw * (1 if dw else d.c)
+    return d.n * d.h * d.w * d.c, nw, d.n * d.ho * d.wo * d.o, d.o
+
+
+def _linear_sizes(d):
+    return d.batch * d.in_, d.out * d.in_, d.batch * d.out, d.out
+
+
+def _check_args(sizes, dtype_code, device, act=(), weights=(), maps=(), vec32=(), w32=()):
+    """act: (name, tensor) pairs shaped like X; weights like W_t; maps like Y;
+    vec32: float32 vectors of O; w32: float32 tensors shaped like W_t."""
+    nx, nw, ny, no = sizes
+    import torch
+    dt = _act_dtype(dtype_code)
+    for n, t in act:
+        _expect(n, t, nx, dt, device)
+    for n, t in weights:
+        _expect(n, t, nw, dt, device)
+    for n, t in maps:
+        _expect(n, t, ny, dt, device)
+    for n, t in vec32:
+        _expect(n, t, no, torch.float32, device)
+    for n, t in w32:
+        _expect(n, t, nw, torch.float32, device)
 
 
 def _check(func, status):
@@ -197,7 +266,9 @@ def qlayer_conv2d_fwd_workspace_size(desc: ConvDesc) -> int:
 def qlayer_conv2d_fwd(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None, ta=None, tb=None,
                       workspace=None, stream=None):
     dev = _device(x, wa)
-    wp, wn = _workspace(workspace, qlayer_conv2d_fwd_workspace_size(desc), dev)
+    _check_args(_conv_sizes(desc), desc.dtype, dev, act=[("x", x)], weights=[("wa", wa), ("wb", wb), ("wc", wc)],
+                maps=[("y", y), ("ta", ta), ("tb", tb)], vec32=[("ba", ba), ("bb", bb), ("bc", bc)])
+    wp, wn = _workspace(workspace, qlayer_conv2d_fwd_workspace_size(desc), dev, stream)
     _check("qlayer_conv2d_fwd", lib().qlayer_conv2d_fwd(
         ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
         _ptr(y), _ptr(ta), _ptr(tb), wp, wn, _stream(stream, dev)))
@@ -209,7 +280,11 @@ def qlayer_conv2d_bwd_data_workspace_size(desc: ConvDesc) -> int:
 
 def qlayer_conv2d_bwd_data(desc, gy, ta, tb, wa, wb, wc, dx, workspace=None, stream=None):
     dev = _device(gy, wa)
-    wp, wn = _workspace(workspace, qlayer_conv2d_bwd_data_workspace_size(desc), dev)
+    t2 = desc.neuron == QL_NEURON_T2  # (its `ta` carries X)
+    _check_args(_conv_sizes(desc), desc.dtype, dev, act=[("dx", dx)] + ([("ta (X)", ta)] if t2 else []),
+                weights=[("wa", wa), ("wb", wb), ("wc", wc)],
+                maps=[("gy", gy), ("tb", tb)] + ([] if t2 else [("ta", ta)]))
+    wp, wn = _workspace(workspace, qlayer_conv2d_bwd_data_workspace_size(desc), dev, stream)
     _check("qlayer_conv2d_bwd_data", lib().qlayer_conv2d_bwd_data(
         ctypes.byref(desc), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(dx),
         wp, wn, _stream(stream, dev)))
@@ -222,7 +297,9 @@ def qlayer_conv2d_bwd_weight_workspace_size(desc: ConvDesc) -> int:
 def qlayer_conv2d_bwd_weight(desc, x, gy, ta, tb, dwa, dwb, dwc, dba=None, dbb=None, dbc=None,
                              workspace=None, stream=None):
     dev = _device(x, gy)
-    wp, wn = _workspace(workspace, qlayer_conv2d_bwd_weight_workspace_size(desc), dev)
+    _check_args(_conv_sizes(desc), desc.dtype, dev, act=[("x", x)], maps=[("gy", gy), ("ta", ta), ("tb", tb)],
+                w32=[("dwa", dwa), ("dwb", dwb), ("dwc", dwc)], vec32=[("dba", dba), ("dbb", dbb), ("dbc", dbc)])
+    wp, wn = _workspace(workspace, qlayer_conv2d_bwd_weight_workspace_size(desc), dev, stream)
     _check("qlayer_conv2d_bwd_weight", lib().qlayer_conv2d_bwd_weight(
         ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(dwa), _ptr(dwb), _ptr(dwc),
         _ptr(dba), _ptr(dbb), _ptr(dbc), wp, wn, _stream(stream, dev)))
@@ -235,7 +312,9 @@ def qlayer_linear_fwd_workspace_size(desc: LinearDesc) -> int:
 def qlayer_linear_fwd(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None, ta=None, tb=None,
                       workspace=None, stream=None):
     dev = _device(x, wa)
-    wp, wn = _workspace(workspace, qlayer_linear_fwd_workspace_size(desc), dev)
+    _check_args(_linear_sizes(desc), desc.dtype, dev, act=[("x", x)], weights=[("wa", wa), ("wb", wb), ("wc", wc)],
+                maps=[("y", y), ("ta", ta), ("tb", tb)], vec32=[("ba", ba), ("bb", bb), ("bc", bc)])
+    wp, wn = _workspace(workspace, qlayer_linear_fwd_workspace_size(desc), dev, stream)
     _check("qlayer_linear_fwd", lib().qlayer_linear_fwd(
         ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
         _ptr(y), _ptr(ta), _ptr(tb), wp, wn, _stream(stream, dev)))
@@ -253,7 +332,10 @@ def qlayer_conv2d_fwd_ex(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None,
                          workspace=None, stream=None):
     """qlayer_conv2d_fwd with a fused epilogue (an Epilogue, see epilogue())."""
     dev = _device(x, wa)
-    wp, wn = _workspace(workspace, qlayer_conv2d_fwd_ex_workspace_size(desc, epi), dev)
+    _check_args(_conv_sizes(desc), desc.dtype, dev, act=[("x", x)], weights=[("wa", wa), ("wb", wb), ("wc", wc)],
+                maps=[("y", y), ("ta", ta), ("tb", tb)],
+                vec32=[("ba", ba), ("bb", bb), ("bc", bc)] + list(getattr(epi, "tensors", [])))
+    wp, wn = _workspace(workspace, qlayer_conv2d_fwd_ex_workspace_size(desc, epi), dev, stream)
     _check("qlayer_conv2d_fwd_ex", lib().qlayer_conv2d_fwd_ex(
         ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
         _ptr(y), _ptr(ta), _ptr(tb), _epi_ref(epi), wp, wn, _stream(stream, dev)))
@@ -267,7 +349,10 @@ def qlayer_linear_fwd_ex(desc, x, wa, wb, wc, ba=None, bb=None, bc=None, y=None,
                          workspace=None, stream=None):
     """qlayer_linear_fwd with a fused epilogue (an Epilogue, see epilogue())."""
     dev = _device(x, wa)
-    wp, wn = _workspace(workspace, qlayer_linear_fwd_ex_workspace_size(desc, epi), dev)
+    _check_args(_linear_sizes(desc), desc.dtype, dev, act=[("x", x)], weights=[("wa", wa), ("wb", wb), ("wc", wc)],
+                maps=[("y", y), ("ta", ta), ("tb", tb)],
+                vec32=[("ba", ba), ("bb", bb), ("bc", bc)] + list(getattr(epi, "tensors", [])))
+    wp, wn = _workspace(workspace, qlayer_linear_fwd_ex_workspace_size(desc, epi), dev, stream)
     _check("qlayer_linear_fwd_ex", lib().qlayer_linear_fwd_ex(
         ctypes.byref(desc), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(ba), _ptr(bb), _ptr(bc),
         _ptr(y), _ptr(ta), _ptr(tb), _epi_ref(epi), wp, wn, _stream(stream, dev)))
@@ -280,7 +365,10 @@ def qlayer_linear_bwd_workspace_size(desc: LinearDesc) -> int:
 def qlayer_linear_bwd(desc, x, gy, ta, tb, wa, wb, wc, dx=None, dwa=None, dwb=None, dwc=None,
                       dba=None, dbb=None, dbc=None, workspace=None, stream=None):
     dev = _device(x, gy)
-    wp, wn = _workspace(workspace, qlayer_linear_bwd_workspace_size(desc), dev)
+    _check_args(_linear_sizes(desc), desc.dtype, dev, act=[("x", x), ("dx", dx)],
+                weights=[("wa", wa), ("wb", wb), ("wc", wc)], maps=[("gy", gy), ("ta", ta), ("tb", tb)],
+                w32=[("dwa", dwa), ("dwb", dwb), ("dwc", dwc)], vec32=[("dba", dba), ("dbb", dbb), ("dbc", dbc)])
+    wp, wn = _workspace(workspace, qlayer_linear_bwd_workspace_size(desc), dev, stream)
     _check("qlayer_linear_bwd", lib().qlayer_linear_bwd(
         ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc),
         _ptr(dx), _ptr(dwa), _ptr(dwb), _ptr(dwc), _ptr(dba), _ptr(dbb), _ptr(dbc),

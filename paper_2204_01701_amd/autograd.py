@@ -55,13 +55,24 @@ def _nhwc(t: torch.Tensor) -> torch.Tensor:
     return t.contiguous(memory_format=torch.channels_last).permute(0, 2, 3, 1)
 
 
-def _biases(ba, bb, bc, nt=3):
+def _biases(ba, bb, bc, nt, O):
     bs = (ba, bb, bc)[:nt]
     if all(b is None for b in bs):
         return None
     if any(b is None for b in bs):
         raise ValueError("give the biases of every term of the neuron type or none")
+    if any(b.numel() != O for b in bs):
+        raise ValueError(f"each bias must have O = {O} elements")
     return [b.contiguous().float() for b in bs] + [None] * (3 - nt)
+
+
+def _same_device(x, *others):
+    """Every tensor on x's CUDA device (the kernels take raw device pointers)."""
+    if x.device.type != "cuda":
+        raise ValueError(f"the layer runs on a CUDA device; x is on {x.device}")
+    for t in others:
+        if t is not None and t.device != x.device:
+            raise ValueError(f"every tensor must be on {x.device}; one is on {t.device}")
 
 
 def _terms(ws, nt):
@@ -80,10 +91,11 @@ class QuadConv2dFunction(torch.autograd.Function):
         ws = _terms((wa, wb, wc), nt)
         if C2 * groups != C or any(w.shape != wa.shape for w in ws[:nt]):
             raise ValueError("weight shapes must be (O, C / groups, KH, KW) for every term")
+        _same_device(x, *ws, ba, bb, bc)
         d = conv_desc(N, C, H, W, O, KH, KW, stride, pad, _qdtype(x), neuron, groups=groups)
         xn = _nhwc(x)
         wn = [_nhwc(w.to(x.dtype)) if w is not None else None for w in ws]
-        b = _biases(ba, bb, bc, nt)
+        b = _biases(ba, bb, bc, nt, O)
         bl = b if b is not None else [None, None, None]
         y = torch.empty((N, d.ho, d.wo, O), device=x.device, dtype=x.dtype)
         recompute = recompute or neuron == QL_NEURON_T2  # (T2 saves nothing but X)
@@ -93,9 +105,11 @@ class QuadConv2dFunction(torch.autograd.Function):
             qlayer_conv2d_fwd_ex(d, xn, *wn, *bl, y, ta, tb, epi=epilogue(relu=True))
         else:
             qlayer_conv2d_fwd(d, xn, *wn, *bl, y, ta, tb)
-        ctx.maps = None if recompute else (ta, tb)
-        ctx.relu_out = y if relu else None  # the mask y' > 0 of the backward
-        ctx.save_for_backward(xn, *[w for w in wn if w is not None], *[v for v in (b or []) if v is not None])
+        # Everything the backward reads goes through save_for_backward, the
+        # output y' (the ReLU mask) included: an in-place change of any of them
+        # then fails the version check instead of silently changing the
+        # gradients, and no reference cycle through ctx keeps them alive.
+        ctx.save_for_backward(xn, *wn, *bl, ta, tb, y if relu else None)
         ctx.desc, ctx.recompute, ctx.has_bias, ctx.nt, ctx.neuron = d, recompute, b is not None, nt, neuron
         ctx.wdtype = wa.dtype
         return y.permute(0, 3, 1, 2)
@@ -103,22 +117,17 @@ class QuadConv2dFunction(torch.autograd.Function):
     @staticmethod
     def backward(ctx, gy):
         d, nt = ctx.desc, ctx.nt
-        saved = ctx.saved_tensors
-        xn = saved[0]
-        wn = list(saved[1:1 + nt]) + [None] * (3 - nt)
-        bl = (list(saved[1 + nt:1 + 2 * nt]) + [None] * (3 - nt)) if ctx.has_bias else [None, None, None]
-        ta = tb = None
+        xn, wa, wb, wc, ba, bb, bc, ta, tb, relu_y = ctx.saved_tensors
+        wn, bl = [wa, wb, wc], [ba, bb, bc]
         if ctx.neuron == QL_NEURON_T2:
             ta = xn  # its input gradient takes X in place of a saved map
         elif ctx.recompute:
             ta = torch.empty((d.n, d.ho, d.wo, d.o), device=xn.device, dtype=xn.dtype)
             tb = torch.empty_like(ta) if nt >= 2 else None
             qlayer_conv2d_fwd(d, xn, *wn, *bl, None, ta, tb)
-        else:
-            ta, tb = ctx.maps
         gyn = _nhwc(gy.to(xn.dtype))
-        if ctx.relu_out is not None:
-            gyn = gyn * (ctx.relu_out > 0).to(gyn.dtype)
+        if relu_y is not None:
+            gyn = gyn * (relu_y > 0).to(gyn.dtype)
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
         dx = dw = db = None
@@ -142,13 +151,19 @@ class QuadConv2dFunction(torch.autograd.Function):
 class QuadLinearFunction(torch.autograd.Function):
     @staticmethod
     def forward(ctx, x, wa, wb, wc, ba, bb, bc, recompute, neuron=QL_NEURON_QUADRA, relu=False):
+        if x.dim() != 2 or wa.dim() != 2:
+            raise ValueError("x must be (B, I) and the weights (O, I)")
         B, I = x.shape
         O = wa.shape[0]
         nt = NEURON_TERMS[neuron]
+        ws = _terms((wa, wb, wc), nt)
+        if wa.shape[1] != I or any(w.shape != wa.shape for w in ws[:nt]):
+            raise ValueError(f"weight shapes must be (O, {I}) for every term")
+        _same_device(x, *ws, ba, bb, bc)
         d = linear_desc(B, I, O, _qdtype(x), neuron)
         xc = x.contiguous()
-        wl = [w.to(x.dtype).contiguous() if w is not None else None for w in _terms((wa, wb, wc), nt)]
-        b = _biases(ba, bb, bc, nt)
+        wl = [w.to(x.dtype).contiguous() if w is not None else None for w in ws]
+        b = _biases(ba, bb, bc, nt, O)
         bl = b if b is not None else [None, None, None]
         y = torch.empty((B, O), device=x.device, dtype=x.dtype)
         recompute = recompute or neuron == QL_NEURON_T2
@@ -158,9 +173,7 @@ class QuadLinearFunction(torch.autograd.Function):
             qlayer_linear_fwd_ex(d, xc, *wl, *bl, y, ta, tb, epi=epilogue(relu=True))
         else:
             qlayer_linear_fwd(d, xc, *wl, *bl, y, ta, tb)
-        ctx.maps = None if recompute else (ta, tb)
-        ctx.relu_out = y if relu else None
-        ctx.save_for_backward(xc, *[w for w in wl if w is not None], *[v for v in (b or []) if v is not None])
+        ctx.save_for_backward(xc, *wl, *bl, ta, tb, y if relu else None)
         ctx.desc, ctx.recompute, ctx.has_bias, ctx.nt, ctx.neuron = d, recompute, b is not None, nt, neuron
         ctx.wdtype = wa.dtype
         return y
@@ -168,22 +181,17 @@ class QuadLinearFunction(torch.autograd.Function):
     @staticmethod
     def backward(ctx, gy):
         d, nt = ctx.desc, ctx.nt
-        saved = ctx.saved_tensors
-        xc = saved[0]
-        wl = list(saved[1:1 + nt]) + [None] * (3 - nt)
-        bl = (list(saved[1 + nt:1 + 2 * nt]) + [None] * (3 - nt)) if ctx.has_bias else [None, None, None]
-        ta = tb = None
+        xc, wa, wb, wc, ba, bb, bc, ta, tb, relu_y = ctx.saved_tensors
+        wl, bl = [wa, wb, wc], [ba, bb, bc]
         if ctx.neuron == QL_NEURON_T2:
             pass  # the dense backward takes X itself
         elif ctx.recompute:
             ta = torch.empty((d.batch, d.out), device=xc.device, dtype=xc.dtype)
             tb = torch.empty_like(ta) if nt >= 2 else None
             qlayer_linear_fwd(d, xc, *wl, *bl, None, ta, tb)
-        else:
-            ta, tb = ctx.maps
         gyc = gy.to(xc.dtype).contiguous()
-        if ctx.relu_out is not None:
-            gyc = gyc * (ctx.relu_out > 0).to(gyc.dtype)
+        if relu_y is not None:
+            gyc = gyc * (relu_y > 0).to(gyc.dtype)
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
         dx = torch.empty_like(xc) if need_x else None

@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstdlib>
+#include <mutex>
 
 #include "qlayer.h"
 #include "qconv_aux.h"
@@ -24,16 +25,18 @@ __device__ __attribute__((aligned(16))) uint32_t g_zero16[4] = {0u, 0u, 0u, 0u};
 }  // namespace ql
 
 namespace {
-// Device address of g_zero16 on the current device (resolved once per device).
+// Device address of g_zero16 on the current device, resolved once per device
+// (std::call_once: host threads calling concurrently see one resolution).
+constexpr int kMaxDevices = 64;
 const void *zero_page() {
-    static const void *addr[64] = {};
+    static std::once_flag once[kMaxDevices];
+    static const void *addr[kMaxDevices] = {};
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-    if (!addr[dev]) {
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::call_once(once[dev], [dev] {
         void *p = nullptr;
-        if (hipGetSymbolAddress(&p, HIP_SYMBOL(ql::g_zero16)) != hipSuccess) return nullptr;
-        addr[dev] = p;
-    }
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(ql::g_zero16)) == hipSuccess) addr[dev] = p;
+    });
     return addr[dev];
 }
 }  // namespace
