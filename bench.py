@@ -214,17 +214,22 @@ def time_each(torch, calls, reps, stream):
     """Device time per call of each (key, fn) in `calls`: the call repeated `reps`
     times back to back (after one untimed call), HIP events at the two ends only,
     so that the host's launch time between calls stays hidden behind the GPU's
-    work.  Returns {key: ms per call}."""
+    work; the median of three such trials.  Returns {key: ms per call}."""
     out = {}
     for key, fn in calls:
         fn(stream)
-        a, b = DevEvent(), DevEvent()
-        a.record(stream)
-        for _ in range(reps):
-            fn(stream)
-        b.record(stream)
-        torch.cuda.synchronize()
-        out[key] = a.elapsed_time(b) / reps
+        # three trials, the median kept: one host stall (the GPU idling between
+        # two launches) inside a trial does not reach the figure
+        trials = []
+        for _ in range(3):
+            a, b = DevEvent(), DevEvent()
+            a.record(stream)
+            for _ in range(reps):
+                fn(stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            trials.append(a.elapsed_time(b) / reps)
+        out[key] = sorted(trials)[1]
     return out
 
 

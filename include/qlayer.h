@@ -70,18 +70,27 @@ typedef enum { QL_F32 = 0, QL_BF16 = 1 } ql_dtype;
  *                                                         output map the size of the input)
  *   QL_NEURON_T3          Y = T_a o T_a                  (weight a)
  *   QL_NEURON_T2          Y = W_a * (X o X) + b_a        (weight a)
- * Backward, with G = dl/dY: G_a = G o T_b, G_b = G o T_a (T4 types; the
+ *   QL_NEURON_T24         Y = T_a o T_b + W_c * (X o X) + b_c
+ *                         (weights a, b, c; "T2&4", the design section 3.1
+ *                         replaces by putting X in place of X o X in the third term)
+ * Backward, with G = dl/dY: G_a = G o T_b, G_b = G o T_a (T4 types, T2&4; the
  * shortcut adds G to dX), G_a = 2 G o T_a (T3), and for T2 dW_a correlates G
- * with X o X while dX = 2 X o (the transposed convolution of G with W_a).
+ * with X o X while dX = 2 X o (the transposed convolution of G with W_a);
+ * T2&4's third term likewise: dW_c correlates G with X o X and adds
+ * 2 X o (the transposed convolution of G with W_c) to dX.
  * Pointers of terms a type lacks are ignored (may be NULL); the saved maps
- * are T_a, T_b (QUADRA, T4 types), T_a (T3), none (T2; its input gradient
- * takes X itself in the `ta` argument). */
+ * are T_a, T_b (QUADRA, T4 types, T2&4), T_a (T3), none (T2; its input
+ * gradient takes X itself in the `ta` argument, or through
+ * qlayer_conv2d_bwd_data_ex).  The input gradient of T2&4 needs X as well as
+ * T_a and T_b: qlayer_conv2d_bwd_data_ex.  The depthwise layer covers the
+ * types up to QL_NEURON_T2 (T2&4: QL_EUNSUPPORTED). */
 typedef enum {
     QL_NEURON_QUADRA = 0,
     QL_NEURON_T4 = 1,
     QL_NEURON_T4_IDENTITY = 2,
     QL_NEURON_T3 = 3,
-    QL_NEURON_T2 = 4
+    QL_NEURON_T2 = 4,
+    QL_NEURON_T24 = 5
 } ql_neuron;
 
 typedef enum {
@@ -164,6 +173,23 @@ ql_status qlayer_conv2d_bwd_data(const ql_conv_desc *desc, const void *gy,
                                  const void *wa, const void *wb, const void *wc,
                                  void *dx, void *workspace, size_t workspace_bytes,
                                  void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Convolution input gradient with the layer input -- the same operation as
+ * qlayer_conv2d_bwd_data for the neuron types whose terms see X o X (Table 1),
+ * whose chain rule through the square needs X itself:
+ *   x : X (N,H,W,C).  QL_NEURON_T24: required (with ta, tb), its c term adds
+ *       2 X o conv_transpose(G, W_c).  QL_NEURON_T2: used in place of `ta`
+ *       (then `ta` may be NULL).  Other types: ignored (may be NULL).
+ * Other arguments, the workspace (qlayer_conv2d_bwd_data_workspace_size)
+ * and errors as for qlayer_conv2d_bwd_data, which returns QL_EINVAL for
+ * QL_NEURON_T24 (no X).
+ * ------------------------------------------------------------------------- */
+ql_status qlayer_conv2d_bwd_data_ex(const ql_conv_desc *desc, const void *gy,
+                                    const void *ta, const void *tb, const void *x,
+                                    const void *wa, const void *wb, const void *wc,
+                                    void *dx, void *workspace, size_t workspace_bytes,
+                                    void *stream);
 
 /* ---------------------------------------------------------------------------
  * Convolution weight and bias gradients -- section 4.3 eq:SD:

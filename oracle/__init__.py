@@ -35,24 +35,31 @@ _L = ctypes.POINTER(ctypes.c_longlong)
 _I = ctypes.c_int
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (fp64, OpenMP, no FMA contraction)."""
-    if force or not os.path.exists(_LIB_PATH):
-        tmp = _LIB_PATH + ".tmp"
-        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off",
+def build(force: bool = True, out: str | None = None, extra_flags: tuple = ()) -> str:
+    """Compile the oracle with gcc (fp64, OpenMP, no FMA contraction).  `out`
+    and `extra_flags` build another copy (e.g. with sanitizers) elsewhere."""
+    path = out or _LIB_PATH
+    if force or not os.path.exists(path):
+        tmp = path + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off", *extra_flags,
                "-o", tmp, _SRC, "-lm"]
         subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+        os.replace(tmp, path)
+    return path
 
 
 def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
-        build(force=True)
-    lib = ctypes.CDLL(_LIB_PATH)
+    # ORACLE_LIB: a separately built copy of the same source (the sanitizer run of the test-suite)
+    other = os.environ.get("ORACLE_LIB")
+    if other:
+        lib = ctypes.CDLL(other)
+    else:
+        if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB_PATH)
     conv_geom = [_I] * 11
     w6 = [_D] * 6
     lib.oracle_conv2d_fwd.argtypes = conv_geom + [_D] + w6 + [_D, _D, _D]

@@ -21,10 +21,10 @@ import os
 
 __all__ = [
     "QL_F32", "QL_BF16", "QL_NEURON_QUADRA", "QL_NEURON_T4", "QL_NEURON_T4_IDENTITY", "QL_NEURON_T3",
-    "QL_NEURON_T2", "NEURON_TERMS", "QLError", "ConvDesc", "LinearDesc", "conv_desc", "linear_desc", "lib",
+    "QL_NEURON_T2", "QL_NEURON_T24", "NEURON_TERMS", "QLError", "ConvDesc", "LinearDesc", "conv_desc", "linear_desc", "lib",
     "qlayer_version", "qlayer_status_string",
     "qlayer_conv2d_fwd_workspace_size", "qlayer_conv2d_fwd",
-    "qlayer_conv2d_bwd_data_workspace_size", "qlayer_conv2d_bwd_data",
+    "qlayer_conv2d_bwd_data_workspace_size", "qlayer_conv2d_bwd_data", "qlayer_conv2d_bwd_data_ex",
     "qlayer_conv2d_bwd_weight_workspace_size", "qlayer_conv2d_bwd_weight",
     "qlayer_linear_fwd_workspace_size", "qlayer_linear_fwd",
     "qlayer_linear_bwd_workspace_size", "qlayer_linear_bwd",
@@ -34,7 +34,8 @@ QL_F32 = 0
 QL_BF16 = 1
 # neuron types (qlayer.h ql_neuron): the proposed one and the earlier designs of Table 1
 QL_NEURON_QUADRA, QL_NEURON_T4, QL_NEURON_T4_IDENTITY, QL_NEURON_T3, QL_NEURON_T2 = 0, 1, 2, 3, 4
-NEURON_TERMS = {0: 3, 1: 2, 2: 2, 3: 1, 4: 1}  # first-order terms (weights) per type
+QL_NEURON_T24 = 5  # T2&4: T_a o T_b + W_c (X o X) + b_c
+NEURON_TERMS = {0: 3, 1: 2, 2: 2, 3: 1, 4: 1, 5: 3}  # first-order terms (weights) per type
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libqlayer.so")
@@ -115,6 +116,8 @@ def lib():
         f.restype = _sz
     L.qlayer_conv2d_fwd.argtypes = [cd] + [_vp] * 10 + [_vp, _sz, _vp]
     L.qlayer_conv2d_bwd_data.argtypes = [cd] + [_vp] * 7 + [_vp, _sz, _vp]
+    L.qlayer_conv2d_bwd_data_ex.argtypes = [cd] + [_vp] * 8 + [_vp, _sz, _vp]
+    L.qlayer_conv2d_bwd_data_ex.restype = ctypes.c_int
     L.qlayer_conv2d_bwd_weight.argtypes = [cd] + [_vp] * 10 + [_vp, _sz, _vp]
     L.qlayer_linear_fwd.argtypes = [ld] + [_vp] * 10 + [_vp, _sz, _vp]
     L.qlayer_linear_bwd.argtypes = [ld] + [_vp] * 14 + [_vp, _sz, _vp]
@@ -287,6 +290,19 @@ def qlayer_conv2d_bwd_data(desc, gy, ta, tb, wa, wb, wc, dx, workspace=None, str
     wp, wn = _workspace(workspace, qlayer_conv2d_bwd_data_workspace_size(desc), dev, stream)
     _check("qlayer_conv2d_bwd_data", lib().qlayer_conv2d_bwd_data(
         ctypes.byref(desc), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(dx),
+        wp, wn, _stream(stream, dev)))
+
+
+def qlayer_conv2d_bwd_data_ex(desc, gy, ta, tb, x, wa, wb, wc, dx, workspace=None, stream=None):
+    """qlayer_conv2d_bwd_data with the layer input X (T2&4 needs it; T2 may take it in place of `ta`)."""
+    dev = _device(gy, wa)
+    t2 = desc.neuron == QL_NEURON_T2
+    _check_args(_conv_sizes(desc), desc.dtype, dev, act=[("dx", dx), ("x", x)] + ([("ta (X)", ta)] if t2 else []),
+                weights=[("wa", wa), ("wb", wb), ("wc", wc)],
+                maps=[("gy", gy), ("tb", tb)] + ([] if t2 else [("ta", ta)]))
+    wp, wn = _workspace(workspace, qlayer_conv2d_bwd_data_workspace_size(desc), dev, stream)
+    _check("qlayer_conv2d_bwd_data_ex", lib().qlayer_conv2d_bwd_data_ex(
+        ctypes.byref(desc), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(x), _ptr(wa), _ptr(wb), _ptr(wc), _ptr(dx),
         wp, wn, _stream(stream, dev)))
 
 

@@ -14,7 +14,7 @@ section 4.3 (eq:SD).  They offer the two memory modes of section 4.3:
   save mode, since the same kernel produces T_a and T_b in both.
 
 ``neuron`` selects the layer type (``QL_NEURON_*``): the proposed neuron or
-one of the earlier designs of Table 1 (T4, T4 + identity, T3, T2).  Weights
+one of the earlier designs of Table 1 (T4, T4 + identity, T3, T2, T2&4).  Weights
 and biases of the terms a type lacks are passed as None.  T2 saves nothing
 but X in either mode (its backward needs only X).
 
@@ -35,8 +35,9 @@ from __future__ import annotations
 
 import torch
 
-from . import (NEURON_TERMS, QL_BF16, QL_F32, QL_NEURON_QUADRA, QL_NEURON_T2, conv_desc, epilogue, linear_desc,
-               qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_weight, qlayer_conv2d_fwd, qlayer_conv2d_fwd_ex,
+from . import (NEURON_TERMS, QL_BF16, QL_F32, QL_NEURON_QUADRA, QL_NEURON_T2, QL_NEURON_T24, conv_desc, epilogue,
+               linear_desc, qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_data_ex, qlayer_conv2d_bwd_weight,
+               qlayer_conv2d_fwd, qlayer_conv2d_fwd_ex,
                qlayer_linear_bwd, qlayer_linear_fwd, qlayer_linear_fwd_ex)
 
 __all__ = ["quad_conv2d", "quad_linear", "QuadConv2dFunction", "QuadLinearFunction"]
@@ -133,7 +134,10 @@ class QuadConv2dFunction(torch.autograd.Function):
         dx = dw = db = None
         if need_x:
             dxn = torch.empty_like(xn)
-            qlayer_conv2d_bwd_data(d, gyn, ta, tb, *wn, dxn)
+            if ctx.neuron == QL_NEURON_T24:  # (the chain rule through X o X needs X)
+                qlayer_conv2d_bwd_data_ex(d, gyn, ta, tb, xn, *wn, dxn)
+            else:
+                qlayer_conv2d_bwd_data(d, gyn, ta, tb, *wn, dxn)
             dx = dxn.permute(0, 3, 1, 2)
         if need_w or need_b:
             dwn = [torch.empty(wn[0].shape, device=xn.device, dtype=torch.float32) if i < nt else None

@@ -12,18 +12,29 @@ namespace ql {
 //   NEURON_QUADRA  Y = T_a o T_b + T_c      NEURON_T4  Y = T_a o T_b
 //   NEURON_T4I     Y = T_a o T_b + X        NEURON_T3  Y = T_a o T_a
 //   NEURON_T2      Y = W_a (X o X) + b_a
-enum { NEURON_QUADRA = 0, NEURON_T4 = 1, NEURON_T4I = 2, NEURON_T3 = 3, NEURON_T2 = 4 };
+//   NEURON_T24     Y = T_a o T_b + W_c (X o X) + b_c   (T2&4 of Table 1)
+enum { NEURON_QUADRA = 0, NEURON_T4 = 1, NEURON_T4I = 2, NEURON_T3 = 3, NEURON_T2 = 4, NEURON_T24 = 5 };
 // The kernels' compile-time operand mode: which first-order terms exist and
 // what feeds them.  OM_PAIR covers T4 and T4 + identity (they differ only in
-// the epilogue, a run-time switch).
-enum { OM_QUADRA = 0, OM_PAIR = 1, OM_SQUARE = 2, OM_SQIN = 3 };
+// the epilogue, a run-time switch).  OM_QSQ is the three-term layout of
+// OM_QUADRA whose third term sees X o X: the pixel operand of that term's
+// MFMAs is squared in registers (forward: the X tile, weight gradient: the
+// X rows), and its share of the input gradient is accumulated apart and
+// multiplied by 2 X in the epilogue.
+enum { OM_QUADRA = 0, OM_PAIR = 1, OM_SQUARE = 2, OM_SQIN = 3, OM_QSQ = 4 };
 __host__ __device__ constexpr int om_of_neuron(int ne) {
-    return ne == NEURON_QUADRA ? OM_QUADRA : (ne <= NEURON_T4I ? OM_PAIR : (ne == NEURON_T3 ? OM_SQUARE : OM_SQIN));
+    return ne == NEURON_QUADRA ? OM_QUADRA
+                               : (ne == NEURON_T24 ? OM_QSQ
+                                                   : (ne <= NEURON_T4I ? OM_PAIR : (ne == NEURON_T3 ? OM_SQUARE : OM_SQIN)));
 }
 // first-order terms (weights) of a mode
-__host__ __device__ constexpr int om_terms(int om) { return om == OM_QUADRA ? 3 : (om == OM_PAIR ? 2 : 1); }
+__host__ __device__ constexpr int om_terms(int om) {
+    return (om == OM_QUADRA || om == OM_QSQ) ? 3 : (om == OM_PAIR ? 2 : 1);
+}
 // output-side maps the backward stages: G, T_a, T_b / G, T_a / G
 __host__ __device__ constexpr int om_gmaps(int om) { return om == OM_SQIN ? 1 : (om == OM_SQUARE ? 2 : 3); }
+// the modes whose backward operands are G o T_b, G o T_a, G (the proposed neuron's)
+__host__ __device__ constexpr bool om_three(int om) { return om == OM_QUADRA || om == OM_QSQ; }
 
 // Forward epilogue of the layer output (section 4.2, model construction:
 // batch normalization after the quadratic layers, an activation in deeper

@@ -10,7 +10,8 @@
 namespace ql {
 
 // Forward split-K epilogue: T_t = b_t + sum over splits of the partials, then
-// Y = T_a o T_b + T_c (arXiv 2204.01701, eq:2ndneuron3).  ws: [split][3][M*O].
+// Y = T_a o T_b + T_c (arXiv 2204.01701, eq:2ndneuron3; for T2&4 the partials
+// of T_c are already those of W_c (X o X)) or the neuron type's Y.  ws: [split][3][M*O].
 template <typename T, bool V4>
 __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float *__restrict__ ws, int splits,
                                                                      long long MO, int O, const float *b0,
@@ -18,7 +19,8 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float
                                                                      T *tb, int neuron, const T *x, EpiArgs epi) {
     constexpr int E = V4 ? 4 : 1;
     const float *bp[3] = {b0, b1, b2};
-    const int nt = neuron == NEURON_QUADRA ? 3 : (neuron <= NEURON_T4I ? 2 : 1);
+    const bool three = neuron == NEURON_QUADRA || neuron == NEURON_T24;  // (T2&4: T_c already on X o X)
+    const int nt = three ? 3 : (neuron <= NEURON_T4I ? 2 : 1);
     const long long n = MO / E;
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x) {
         const long long idx = i * E;
@@ -46,7 +48,7 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_combine_kernel(const float
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const float fa = t3[0][e], fb = t3[1][e];
-            if (neuron == NEURON_QUADRA) yv[e] = fa * fb + t3[2][e];
+            if (three) yv[e] = fa * fb + t3[2][e];
             else if (neuron == NEURON_T4) yv[e] = fa * fb;
             else if (neuron == NEURON_T4I) yv[e] = fa * fb + to_f32<T>(x[idx + e]);
             else if (neuron == NEURON_T3) yv[e] = fa * fa;
@@ -158,6 +160,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce_kernel(const
 // values, or one bias value after the nterms ndw / 4 vectors); 16 split
 // lanes per item sum every 16th split (unrolled, the loads independent) and
 // the lane sums are added in lane order, the same order as the scalar kernel.
+template <int = 0>  // (a template: defined once across the translation units that include this header)
 __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_reduce2dv_kernel(const float *__restrict__ ws_dw,
                                                                               const float *__restrict__ ws_db,
                                                                               int splits, long long ndw, int O,
@@ -594,6 +597,7 @@ __global__ __launch_bounds__(kThreads) void qconv_channel_stats_kernel(const T *
 // Sum of the per-part statistics [part][2][O] in part order: sum[o] and sumsq[o].
 // A block takes 4 indices j of [2][O]; 64 lanes per index sum every 64th
 // part, and the lane sums are added in lane order.
+template <int = 0>  // (a template: defined once across the translation units that include this header)
 __global__ __launch_bounds__(kThreads) void qconv_stats_reduce_kernel(const float *__restrict__ part, int nparts,
                                                                        int O, float *sum, float *sumsq) {
     __shared__ float red[4][65];

@@ -205,13 +205,22 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         }
     };
 
-    f32x16_t acc[MR][MC];
+    // acc2: T2&4's third term (its operand is X o X), scaled by 2 X in the epilogue
+    f32x16_t acc[MR][MC], acc2[OM == OM_QSQ ? MR : 1][OM == OM_QSQ ? MC : 1];
 #pragma unroll
     for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mr][mc][v] = 0.0f;
+    if constexpr (OM == OM_QSQ) {
+#pragma unroll
+        for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+            for (int mc = 0; mc < MC; ++mc)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc2[mr][mc][v] = 0.0f;
+    }
 
     const int lrow = lane & 31, lhi = lane >> 5;
     const int swz = (lrow >> 2) & 3;
@@ -250,7 +259,15 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
 #pragma unroll
             for (int t = 0; t < NTM; ++t)
 #pragma unroll
-                for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[set][t][mr], bt[t], acc[mr][mc]);
+                for (int mr = 0; mr < MR; ++mr) {
+                    if constexpr (OM == OM_QSQ) {
+                        if (t == 2) {
+                            mfma_chunk<T>(af[set][t][mr], bt[t], acc2[mr][mc]);
+                            continue;
+                        }
+                    }
+                    mfma_chunk<T>(af[set][t][mr], bt[t], acc[mr][mc]);
+                }
         }
     };
     run_ring<NS, NI>(nst, s_begin, issue, read, mma);
@@ -265,6 +282,8 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         if (a.splits == 1 && (OM == OM_SQIN || a.neuron == NEURON_T4I))
             neuron_dx_epilogue<T, OM, MR, MC>(acc, OM == OM_SQIN ? a.xin : a.gy, a.M, a.C, pcol0, crow0, lane);
     }
+    // T2&4: acc += 2 X o acc2, linear, so every split applies it to its own partial
+    if constexpr (OM == OM_QSQ) qsq_dx_epilogue<T, MR, MC>(acc, acc2, a.xin, a.M, a.C, pcol0, crow0, lane);
     const bool vec_out = (a.C & 3) == 0;
     T *__restrict__ dx = static_cast<T *>(a.dx);
 

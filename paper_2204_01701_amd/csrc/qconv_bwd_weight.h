@@ -202,6 +202,11 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
 #pragma unroll
             for (int mr = 0; mr < MR; ++mr) af[set][mr] = square_frag<T>(af[set][mr]);
         }
+        v4u asq[MR];  // T2&4: the third term's X rows squared, once per fragment
+        if constexpr (OM == OM_QSQ) {
+#pragma unroll
+            for (int mr = 0; mr < MR; ++mr) asq[mr] = square_frag<T>(af[set][mr]);
+        }
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
             const v4u &g = gr[set][0][mc];
@@ -210,7 +215,7 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float gv = vget<T>(g, e);
-                if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+                if constexpr (om_three(OM) || OM == OM_PAIR) {
                     op[0][e] = gv * vget<T>(gr[set][NGM >= 3 ? 2 : 0][mc], e);
                     op[1][e] = gv * vget<T>(gr[set][NGM >= 2 ? 1 : 0][mc], e);
                     op[2][e] = gv;
@@ -233,11 +238,12 @@ __device__ __forceinline__ void bwd_weight_body(const BwdWeightArgs &a, char *sm
             }
             v4u bt[NTM];
 #pragma unroll
-            for (int t = 0; t < NTM; ++t) bt[t] = (OM == OM_QUADRA && t == 2) || OM == OM_SQIN ? g : vpack<T>(op[t]);
+            for (int t = 0; t < NTM; ++t) bt[t] = (om_three(OM) && t == 2) || OM == OM_SQIN ? g : vpack<T>(op[t]);
 #pragma unroll
             for (int t = 0; t < NTM; ++t)
 #pragma unroll
-                for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[set][mr], bt[t], acc[t][mr][mc]);
+                for (int mr = 0; mr < MR; ++mr)
+                    mfma_chunk<T>((OM == OM_QSQ && t == 2) ? asq[mr] : af[set][mr], bt[t], acc[t][mr][mc]);
         }
     };
     if constexpr (SETS == 2)

@@ -341,6 +341,7 @@ __global__ __launch_bounds__(kThreads) void qconv_dw_bwd_weight_kernel(const DwA
 // 16 partial indices j, 16 lanes of it sum every 16th split, and the 16 lane
 // sums are added in lane order (a fixed order: the result does not depend on
 // scheduling).  j < nterms C taps are dW values, the next nterms C the db.
+template <int = 0>  // (a template: defined once across the translation units that include this header)
 __global__ __launch_bounds__(kThreads) void qconv_dw_reduce_kernel(const float *__restrict__ ws, int splits, int J,
                                                                    int C, int taps, int nterms, float *dw0,
                                                                    float *dw1, float *dw2, float *db0, float *db1,

@@ -42,7 +42,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     constexpr int MR = BR / WGR / 32, MC = BCOL / WGC / 32;
     static_assert(WGR * WGC == NT / 64, "one wave per wave-tile");
     static_assert((3 * BR) % RPI == 0 && BCOL % RPI == 0 && MR >= 1 && MC >= 1, "tile shape");
-    static_assert(OM == OM_QUADRA || BR % RPI == 0, "each weight DMA instruction within one term block");
+    static_assert(NTM == 3 || BR % RPI == 0, "each weight DMA instruction within one term block");
 
     __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
@@ -252,12 +252,19 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
                 for (int mc = 0; mc < MC; ++mc) bf[set][mc] = square_frag<T>(bf[set][mc]);
             }
         }
+        // T2&4: the third term's pixel operand is X o X, squared here once per fragment
+        v4u bsq[MC];
+        if constexpr (OM == OM_QSQ) {
+#pragma unroll
+            for (int mc = 0; mc < MC; ++mc) bsq[mc] = square_frag<T>(bf[set][mc]);
+        }
 #pragma unroll
         for (int t = 0; t < NTM; ++t)
 #pragma unroll
             for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
-                for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af[set][t][mr], bf[set][mc], acc[t][mr][mc]);
+                for (int mc = 0; mc < MC; ++mc)
+                    mfma_chunk<T>(af[set][t][mr], (OM == OM_QSQ && t == 2) ? bsq[mc] : bf[set][mc], acc[t][mr][mc]);
     };
     if constexpr (SETS == 2)
         run_ring<NS, NI>(nst, s_begin, issue, read, mma);
@@ -270,10 +277,10 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     auto outv = [&](int j, int mr, int mc, int v, float xs) -> float {
         const float fa = acc[0][mr][mc][v];
         if (j == 1) return fa;
-        if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+        if constexpr (om_three(OM) || OM == OM_PAIR) {
             const float fb = acc[1][mr][mc][v];
             if (j == 2) return fb;
-            if constexpr (OM == OM_QUADRA) return fa * fb + acc[2][mr][mc][v];
+            if constexpr (om_three(OM)) return fa * fb + acc[2][mr][mc][v];
             else return fa * fb + xs;
         } else if constexpr (OM == OM_SQUARE) {
             return fa * fa;

@@ -188,13 +188,19 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
 #pragma unroll
             for (int mc = 0; mc < MC; ++mc)
                 bf[mc] = lds_read16(base + (3 * BR + wc * (BCOL / WGC) + mc * 32 + lrow) * PITCH + coff);
+            v4u bsq[MC];  // T2&4: the third term's pixel operand X o X
+            if constexpr (OM == OM_QSQ) {
+#pragma unroll
+                for (int mc = 0; mc < MC; ++mc) bsq[mc] = square_frag<T>(bf[mc]);
+            }
 #pragma unroll
             for (int t = 0; t < NTM; ++t)
 #pragma unroll
                 for (int mr = 0; mr < MR; ++mr) {
                     const v4u af = lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32 + lrow) * PITCH + coff);
 #pragma unroll
-                    for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af, bf[mc], acc[t][mr][mc]);
+                    for (int mc = 0; mc < MC; ++mc)
+                        mfma_chunk<T>(af, (OM == OM_QSQ && t == 2) ? bsq[mc] : bf[mc], acc[t][mr][mc]);
                 }
         }
     };
@@ -217,10 +223,10 @@ __global__ __launch_bounds__(kThreads) void qconv_fwd_generic_kernel(const FwdAr
     auto outv = [&](int j, int mr, int mc, int v, float xs) -> float {
         const float fa = acc[0][mr][mc][v];
         if (j == 1) return fa;
-        if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+        if constexpr (om_three(OM) || OM == OM_PAIR) {
             const float fb = acc[1][mr][mc][v];
             if (j == 2) return fb;
-            if constexpr (OM == OM_QUADRA) return fa * fb + acc[2][mr][mc][v];
+            if constexpr (om_three(OM)) return fa * fb + acc[2][mr][mc][v];
             else return fa * fb + xs;
         } else if constexpr (OM == OM_SQUARE) {
             return fa * fa;
@@ -464,13 +470,22 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
         }
     };
 
-    f32x16_t acc[MR][MC];
+    // acc2: T2&4's third term (its operand is X o X), scaled by 2 X in the epilogue
+    f32x16_t acc[MR][MC], acc2[OM == OM_QSQ ? MR : 1][OM == OM_QSQ ? MC : 1];
 #pragma unroll
     for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mr][mc][v] = 0.0f;
+    if constexpr (OM == OM_QSQ) {
+#pragma unroll
+        for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+            for (int mc = 0; mc < MC; ++mc)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc2[mr][mc][v] = 0.0f;
+    }
 
     const int lrow = lane & 31, lhi = lane >> 5;
     auto compute_stage = [&](int b) {
@@ -490,7 +505,15 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
                     const v4u af =
                         lds_read16(base + (t * BR + wr * (BR / WGR) + mr * 32 + lrow) * PITCH + coff);
 #pragma unroll
-                    for (int mc = 0; mc < MC; ++mc) mfma_chunk<T>(af, bf[mc], acc[mr][mc]);
+                    for (int mc = 0; mc < MC; ++mc) {
+                        if constexpr (OM == OM_QSQ) {
+                            if (t == 2) {
+                                mfma_chunk<T>(af, bf[mc], acc2[mr][mc]);
+                                continue;
+                            }
+                        }
+                        mfma_chunk<T>(af, bf[mc], acc[mr][mc]);
+                    }
                 }
             }
         }
@@ -517,6 +540,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_generic_kernel(const 
         if (a.splits == 1 && (OM == OM_SQIN || a.neuron == NEURON_T4I))
             neuron_dx_epilogue<T, OM, MR, MC>(acc, OM == OM_SQIN ? a.xin : a.gy, a.M, a.C, pcol0, crow0, lane);
     }
+    if constexpr (OM == OM_QSQ) qsq_dx_epilogue<T, MR, MC>(acc, acc2, a.xin, a.M, a.C, pcol0, crow0, lane);
     const bool vec_out = (a.C & 3) == 0;
     T *__restrict__ dx = static_cast<T *>(a.dx);
     float *__restrict__ ws = a.ws + (size_t)split * a.M * a.C;
@@ -711,7 +735,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) {
                     const float g = vget<T>(rg[0][p], e);
-                    if constexpr (OM == OM_QUADRA || OM == OM_PAIR) {
+                    if constexpr (om_three(OM) || OM == OM_PAIR) {
                         gv[0][p][e] = g * vget<T>(rg[2][p], e);
                         gv[1][p][e] = g * vget<T>(rg[1][p], e);
                         gv[2][p][e] = g;
@@ -734,7 +758,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
                         uint32_t d[PXG / 2];
 #pragma unroll
                         for (int i = 0; i < PXG / 2; ++i)
-                            d[i] = ((OM == OM_QUADRA && t == 2) || OM == OM_SQIN)  // the operand is G itself
+                            d[i] = ((om_three(OM) && t == 2) || OM == OM_SQIN)  // the operand is G itself
                                        ? (vraw<T>(rg[0][2 * i], e) | (vraw<T>(rg[0][2 * i + 1], e) << 16))
                                        : pack_bf16x2(gv[t][2 * i][e], gv[t][2 * i + 1][e]);
                         if constexpr (PXG == 4)
@@ -770,10 +794,12 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
 #pragma unroll
         for (int ch = 0; ch < BKB / 32; ++ch) {
             const int coff = ch * 32 + lhi * 16;
-            v4u af[MR];
+            v4u af[MR], asq[MR];  // asq: T2&4's third term sees X o X
 #pragma unroll
-            for (int mr = 0; mr < MR; ++mr)
+            for (int mr = 0; mr < MR; ++mr) {
                 af[mr] = lds_read16(base + (wr * (BKP / WGR) + mr * 32 + lrow) * PITCH + coff);
+                if constexpr (OM == OM_QSQ) asq[mr] = square_frag<T>(af[mr]);
+            }
 #pragma unroll
             for (int t = 0; t < NTM; ++t)
 #pragma unroll
@@ -781,7 +807,8 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_weight_generic_kernel(cons
                     const v4u bf =
                         lds_read16(base + (BKP + t * BO + wc * (BO / WGC) + mc * 32 + lrow) * PITCH + coff);
 #pragma unroll
-                    for (int mr = 0; mr < MR; ++mr) mfma_chunk<T>(af[mr], bf, acc[t][mr][mc]);
+                    for (int mr = 0; mr < MR; ++mr)
+                        mfma_chunk<T>((OM == OM_QSQ && t == 2) ? asq[mr] : af[mr], bf, acc[t][mr][mc]);
                 }
         }
     };

@@ -157,8 +157,8 @@ template <typename T> __device__ __forceinline__ v4u square_frag(const v4u &v) {
 // The output-side MFMA operands of a backward kernel for operand mode OM
 // (qargs.h), formed in fp32 on one 16-byte fragment of G, T_a, T_b and
 // rounded once to T:
-//   OM_QUADRA: G o T_b, G o T_a, G      OM_PAIR: G o T_b, G o T_a
-//   OM_SQUARE: 2 G o T_a                OM_SQIN: G
+//   OM_QUADRA, OM_QSQ: G o T_b, G o T_a, G      OM_PAIR: G o T_b, G o T_a
+//   OM_SQUARE: 2 G o T_a                        OM_SQIN: G
 template <typename T, int OM>
 __device__ __forceinline__ void operands_frag(const v4u &g, const v4u &ta, const v4u &tb, v4u *bt) {
     constexpr int VEC = Elem<T>::VEC;
@@ -171,7 +171,7 @@ __device__ __forceinline__ void operands_frag(const v4u &g, const v4u &ta, const
         bt[0] = vpack<T>(f);
     } else {
         prologue_frag<T>(g, ta, tb, bt[0], bt[1]);
-        if constexpr (OM == OM_QUADRA) bt[2] = g;
+        if constexpr (om_three(OM)) bt[2] = g;
     }
 }
 
@@ -218,6 +218,40 @@ __device__ __forceinline__ void neuron_dx_epilogue(f32x16_t (&acc)[MR][MC], cons
                     const float r = acc[mr][mc][4 * g + i];
                     acc[mr][mc][4 * g + i] = OM == OM_SQIN ? r * (2.0f * v[i]) : r + v[i];
                 }
+            }
+        }
+}
+
+// Input-gradient epilogue of the T2&4 neuron: the terms a, b accumulated in
+// acc, the c term (whose operand is X o X) in acc2; acc += 2 X[m, c] acc2
+// (the chain rule through the square).  X is M x C.  Linear in the
+// accumulators, so each split-K partial may take it before the sum.
+template <typename T, int MR, int MC>
+__device__ __forceinline__ void qsq_dx_epilogue(f32x16_t (&acc)[MR][MC], const f32x16_t (&acc2)[MR][MC],
+                                                const void *xv, int M, int C, int pcol0, int crow0, int lane) {
+    const T *__restrict__ x = static_cast<const T *>(xv);
+    const int lrow = lane & 31, lhi = lane >> 5;
+#pragma unroll
+    for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) {
+            const int m = pcol0 + mc * 32 + lrow;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int c = crow0 + mr * 32 + 8 * g + 4 * lhi;
+                float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                if (m < M) {
+                    if ((C & 3) == 0 && c < C) {
+                        load4<T>(x + (size_t)m * C + c, v);
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (c + i < C) v[i] = to_f32<T>(x[(size_t)m * C + c + i]);
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    acc[mr][mc][4 * g + i] += (2.0f * v[i]) * acc2[mr][mc][4 * g + i];
             }
         }
 }

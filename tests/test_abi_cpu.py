@@ -9,6 +9,7 @@ import ctypes
 import os
 import re
 import subprocess
+import sys
 
 import pytest
 
@@ -169,7 +170,7 @@ int main() {
 
 def test_neuron_type_validation(L):
     # an unknown type, and the identity shortcut without C == O or with a changed map
-    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, 5)) == QL_EINVAL
+    assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, 6)) == QL_EINVAL
     assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, -1)) == QL_EINVAL
     assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 32, 3, 3, 1, 1, ql.QL_F32, ql.QL_NEURON_T4_IDENTITY)) == QL_EINVAL
     assert _fwd(L, ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 2, 1, ql.QL_F32, ql.QL_NEURON_T4_IDENTITY)) == QL_EINVAL
@@ -193,8 +194,17 @@ def test_neuron_type_validation(L):
                                       None, FAKE, ws, None) == QL_EINVAL          # dW_b missing
     assert L.qlayer_conv2d_bwd_weight(ctypes.byref(t4), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, None,
                                       None, FAKE, ws, None) == QL_EINVAL          # biases of some terms only
+    # T2&4: its input gradient needs X (the _ex entry point); the depthwise kernels do not cover it
+    t24 = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, ql.QL_NEURON_T24)
+    assert L.qlayer_conv2d_bwd_data(ctypes.byref(t24), *[FAKE] * 7, FAKE, ws, None) == QL_EINVAL
+    assert L.qlayer_conv2d_bwd_data_ex(ctypes.byref(t24), *[FAKE] * 3, None, *[FAKE] * 4, FAKE, ws,
+                                       None) == QL_EINVAL                          # no X
+    assert L.qlayer_conv2d_bwd_data_ex(ctypes.byref(t24), *[FAKE] * 8, FAKE, 16, None) == QL_EWORKSPACE
+    assert _fwd(L, t24, wc=None) == QL_EINVAL                                      # W_c required
+    dw24 = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32, ql.QL_NEURON_T24, groups=16)
+    assert _fwd(L, dw24) == QL_EUNSUPPORTED
     # the workspace queries accept every type
-    for n in range(5):
+    for n in range(6):
         d = ql.conv_desc(4, 256, 4, 4, 256, 3, 3, 1, 1, ql.QL_BF16, n)
         assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d)) > 0
 
@@ -274,3 +284,45 @@ def test_few_channel_paths_need_no_workspace(L, monkeypatch):
     stem = ql.conv_desc(128, 3, 32, 32, 64, 3, 3, 1, 1, ql.QL_BF16)
     assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(stem)) >= 128 * 32 * 32 * 8 * 2   # X padded to 8
     assert L.qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(stem)) >= 128 * 32 * 32 * 27 * 4
+
+
+def test_valid_call_without_a_device_returns_ehip():
+    """A valid call in a process that sees no GPU reports QL_EHIP (the launch
+    or the device query fails) and returns normally: no abort, no crash.  Run
+    in a child process so that a crash would show as its exit status.  Only
+    where no GPU is present (the fake pointers must never reach a kernel)."""
+    if os.path.exists("/dev/kfd"):
+        pytest.skip("a GPU device node is present")
+    code = (
+        "import ctypes, paper_2204_01701_amd as ql\n"
+        "L = ql.lib()\n"
+        "F = 1 << 20\n"
+        "d = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32)\n"
+        "r1 = L.qlayer_conv2d_fwd(ctypes.byref(d), F, F, F, F, None, None, None, F, None, None, None, 0, None)\n"
+        "dl = ql.linear_desc(64, 32, 48, ql.QL_F32)\n"
+        "r2 = L.qlayer_linear_fwd(ctypes.byref(dl), F, F, F, F, None, None, None, F, None, None, None, 0, None)\n"
+        "print(r1, r2)\n"
+    )
+    env = dict(os.environ, HIP_VISIBLE_DEVICES="", ROCR_VISIBLE_DEVICES="")
+    res = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT, env=env,
+                         timeout=120)
+    assert res.returncode == 0, res.stderr[-2000:]
+    assert res.stdout.split()[-2:] == [str(QL_EHIP), str(QL_EHIP)], res.stdout
+
+
+def test_binding_rejects_host_and_mis_sized_tensors_before_any_call():
+    """The Python binding checks device, element count and dtype of every tensor
+    against the descriptor and raises before the C ABI is reached."""
+    import torch
+    d = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_F32)
+    x = torch.zeros(2, 8, 8, 16)
+    w = [torch.zeros(16, 3, 3, 16) for _ in range(3)]
+    y = torch.zeros(2, 8, 8, 16)
+    with pytest.raises(ValueError, match="CUDA"):
+        ql.qlayer_conv2d_fwd(d, x, *w, None, None, None, y)
+    dl = ql.linear_desc(64, 32, 48, ql.QL_F32)
+    with pytest.raises(ValueError, match="CUDA"):
+        ql.qlayer_linear_fwd(dl, torch.zeros(64, 32), *[torch.zeros(48, 32)] * 3, y=torch.zeros(64, 48))
+    # sizes and dtypes are checked the same way (the device check fires first on the host)
+    with pytest.raises(ValueError):
+        ql._expect("w", torch.zeros(10), 11, None, None)

@@ -109,11 +109,12 @@ def test_recompute_mode_lowers_peak_memory():
 
 import paper_2204_01701_amd as ql  # noqa: E402
 
-NEURONS = [ql.QL_NEURON_T4, ql.QL_NEURON_T4_IDENTITY, ql.QL_NEURON_T3, ql.QL_NEURON_T2]
+NEURONS = [ql.QL_NEURON_T4, ql.QL_NEURON_T4_IDENTITY, ql.QL_NEURON_T3, ql.QL_NEURON_T2, ql.QL_NEURON_T24]
+NEURON_IDS = ["T4", "T4I", "T3", "T2", "T24"]
 
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
-@pytest.mark.parametrize("neuron", NEURONS, ids=["T4", "T4I", "T3", "T2"])
+@pytest.mark.parametrize("neuron", NEURONS, ids=NEURON_IDS)
 def test_conv_autograd_neuron_types(neuron, bf16):
     shape = (2, 16, 8, 8, 16, 3, 3, 1, 1)
     N, C, H, W, O, KH, KW, s, p = shape
@@ -134,7 +135,7 @@ def test_conv_autograd_neuron_types(neuron, bf16):
         out.backward(_t(inp["gy"], dtype, grad=False))
         torch.cuda.synchronize()
         got = {"y": out.detach(), "dx": x.grad}
-        for i, (kw, kb) in enumerate((("dwa", "dba"), ("dwb", "dbb"))[:nt]):
+        for i, (kw, kb) in enumerate((("dwa", "dba"), ("dwb", "dbb"), ("dwc", "dbc"))[:nt]):
             got[kw], got[kb] = w[i].grad, b[i].grad
         for k, v in got.items():
             e = qlh.relerr(v.double().cpu().numpy(), ref[k])
@@ -144,7 +145,7 @@ def test_conv_autograd_neuron_types(neuron, bf16):
         assert torch.equal(grads[False][k], grads[True][k]), k
 
 
-@pytest.mark.parametrize("neuron", NEURONS, ids=["T4", "T4I", "T3", "T2"])
+@pytest.mark.parametrize("neuron", NEURONS, ids=NEURON_IDS)
 def test_linear_autograd_neuron_types(neuron):
     B, I = 64, 48
     O = I if neuron == ql.QL_NEURON_T4_IDENTITY else 40
@@ -162,7 +163,7 @@ def test_linear_autograd_neuron_types(neuron):
     out.backward(_t(inp["gy"], torch.bfloat16, grad=False))
     torch.cuda.synchronize()
     got = {"y": out.detach(), "dx": x.grad}
-    for i, (kw, kb) in enumerate((("dwa", "dba"), ("dwb", "dbb"))[:nt]):
+    for i, (kw, kb) in enumerate((("dwa", "dba"), ("dwb", "dbb"), ("dwc", "dbc"))[:nt]):
         got[kw], got[kb] = w[i].grad, b[i].grad
     for k, v in got.items():
         e = qlh.relerr(v.double().cpu().numpy(), ref[k])

@@ -1,4 +1,4 @@
-"""The earlier neuron types (T4, T4 + identity, T3, T2; arXiv 2204.01701
+"""The earlier neuron types (T4, T4 + identity, T3, T2, T2&4; arXiv 2204.01701
 Table 1 and the Table 3 baselines) through the C ABI against the fp64
 oracle, element by element (normwise relative error), in fp32 and bf16:
 forward Y and saved maps, input gradient, weight and bias gradients, as
@@ -17,7 +17,9 @@ import paper_2204_01701_amd as ql  # noqa: E402
 
 DEV = qlh.DEV
 T4, T4I, T3, T2 = ql.QL_NEURON_T4, ql.QL_NEURON_T4_IDENTITY, ql.QL_NEURON_T3, ql.QL_NEURON_T2
-NAMES = {T4: "T4", T4I: "T4I", T3: "T3", T2: "T2"}
+T24 = ql.QL_NEURON_T24
+TYPES = (T4, T4I, T3, T2, T24)
+NAMES = {T4: "T4", T4I: "T4I", T3: "T3", T2: "T2", T24: "T24"}
 TERMS = ql.NEURON_TERMS
 
 # N, C, H, W, O, K, stride, pad.  The shortcut of T4 + identity needs C == O
@@ -31,7 +33,7 @@ SHAPES = [
     ((2, 128, 6, 6, 128, 1, 1, 0), True),   # 1x1
     ((1, 12, 7, 5, 12, 3, 1, 1), True),     # channels not a multiple of the bf16 vector
 ]
-CASES = [(n, sh) for n in (T4, T4I, T3, T2) for sh, same in SHAPES if n != T4I or same]
+CASES = [(n, sh) for n in TYPES for sh, same in SHAPES if n != T4I or same]
 IDS = [f"{NAMES[n]}-{'x'.join(map(str, sh))}" for n, sh in CASES]
 
 
@@ -50,7 +52,10 @@ def _run_conv_neuron(neuron, inp, s, p, bf16):
     ql.qlayer_conv2d_fwd(d, x, *w, *b, y, ta, tb)
     gy = qlh.nchw_to_dev(inp["gy"], bf16)
     dx = torch.empty_like(x)
-    ql.qlayer_conv2d_bwd_data(d, gy, x if neuron == T2 else ta, tb, *w, dx)
+    if neuron == T24:  # its c term's chain rule through X o X needs X
+        ql.qlayer_conv2d_bwd_data_ex(d, gy, ta, tb, x, *w, dx)
+    else:
+        ql.qlayer_conv2d_bwd_data(d, gy, x if neuron == T2 else ta, tb, *w, dx)
     dw = [torch.empty((O, K, K, C), device=DEV, dtype=torch.float32) if i < nt else None for i in range(3)]
     db = [torch.empty(O, device=DEV, dtype=torch.float32) if i < nt else None for i in range(3)]
     ql.qlayer_conv2d_bwd_weight(d, x, gy, ta, tb, *dw, *db)
@@ -72,8 +77,8 @@ def test_conv_neuron_matches_oracle(neuron, shape, bf16):
     print(f"neuron {NAMES[neuron]} shape {shape} bf16={bf16}", flush=True)
     inp = synth.random_conv_case([500, neuron] + list(shape), N, C, H, W, O, K, K, s, p, bf16=bf16)
     nt = TERMS[neuron]
-    w = [inp["wa"], inp["wb"] if nt >= 2 else None, None]
-    b = [inp["ba"], inp["bb"] if nt >= 2 else None, None]
+    w = [inp["wa"], inp["wb"] if nt >= 2 else None, inp["wc"] if nt >= 3 else None]
+    b = [inp["ba"], inp["bb"] if nt >= 2 else None, inp["bc"] if nt >= 3 else None]
     y, ta, tb = oracle.conv2d_fwd_neuron(neuron, inp["x"], *w, *b, stride=s, pad=p)
     ref = oracle.conv2d_bwd_neuron(neuron, inp["x"], *w, *b, inp["gy"], stride=s, pad=p)
     ref["y"] = y
@@ -89,14 +94,14 @@ def test_conv_neuron_matches_oracle(neuron, shape, bf16):
 
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
-@pytest.mark.parametrize("neuron", [T4, T4I, T3, T2], ids=[NAMES[n] for n in (T4, T4I, T3, T2)])
+@pytest.mark.parametrize("neuron", TYPES, ids=[NAMES[n] for n in TYPES])
 def test_linear_neuron_matches_oracle(neuron, bf16):
     B, I, O = 96, 72, 72 if neuron == T4I else 40
     print(f"neuron {NAMES[neuron]} dense {B}x{I}->{O} bf16={bf16}", flush=True)
     inp = synth.random_dense_case([501, neuron, B, I, O], B, I, O, bf16=bf16)
     nt = TERMS[neuron]
-    w = [inp["wa"], inp["wb"] if nt >= 2 else None, None]
-    b = [inp["ba"], inp["bb"] if nt >= 2 else None, None]
+    w = [inp["wa"], inp["wb"] if nt >= 2 else None, inp["wc"] if nt >= 3 else None]
+    b = [inp["ba"], inp["bb"] if nt >= 2 else None, inp["bc"] if nt >= 3 else None]
     y, ta, tb = oracle.linear_fwd_neuron(neuron, inp["x"], *w, *b)
     ref = oracle.linear_bwd_neuron(neuron, inp["x"], *w, *b, inp["gy"])
     ref["y"] = y
@@ -128,7 +133,7 @@ def test_recompute_mode_regenerates_the_saved_maps_bitwise():
     writes the same T_a (and T_b) as the saving forward."""
     shape = (2, 32, 8, 8, 32, 3, 1, 1)
     N, C, H, W, O, K, s, p = shape
-    for neuron in (T4, T4I, T3):
+    for neuron in (T4, T4I, T3, T24):
         nt = TERMS[neuron]
         inp = synth.random_conv_case([502, neuron], N, C, H, W, O, K, K, s, p, bf16=True)
         d = ql.conv_desc(N, C, H, W, O, K, K, s, p, ql.QL_BF16, neuron)
