@@ -212,6 +212,30 @@ ql_status qlayer_conv2d_bwd_weight(const ql_conv_desc *desc, const void *x, cons
                                    void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * Convolution weight and bias gradients without a workspace -- for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving or training loops, harnesses that forbid hipMalloc.  The same
+ * operation, arguments and errors as qlayer_conv2d_bwd_weight minus the
+ * workspace: the split-K partial sums (and the zero-padded copy of X of
+ * few-channel layers) go to a scratch array the library owns, of
+ * QLAYER_NOALLOC_SCRATCH_BYTES bytes on each GPU it runs on, held until the
+ * process ends.  Where the regular call's workspace query fits that size the
+ * plan, and so every result bit, is the regular call's; otherwise the split
+ * count is lowered to fit (results equal up to summation order); a layer
+ * that does not fit even then returns QL_EWORKSPACE.  No device memory is
+ * allocated by this call; the first call on a device resolves the array's
+ * address there.  Every call on one GPU shares its array, which keeps the
+ * last call's contents (nothing in it needs to start at zero): calls that
+ * overlap on one GPU (several streams or host threads) race, and the caller
+ * must serialize them.
+ * ------------------------------------------------------------------------- */
+#define QLAYER_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+ql_status qlayer_conv2d_bwd_weight_noalloc(const ql_conv_desc *desc, const void *x, const void *gy,
+                                           const void *ta, const void *tb,
+                                           float *dwa, float *dwb, float *dwc,
+                                           float *dba, float *dbb, float *dbc, void *stream);
+
+/* ---------------------------------------------------------------------------
  * Fully-connected forward -- section 3.2 P3: Y = (X W_a^T + b_a) o (X W_b^T + b_b)
  * + X W_c^T + b_c.  Arguments as for qlayer_conv2d_fwd (biases may be NULL,
  * y may be NULL when ta and tb are given).

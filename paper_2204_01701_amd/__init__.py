@@ -25,7 +25,8 @@ __all__ = [
     "qlayer_version", "qlayer_status_string",
     "qlayer_conv2d_fwd_workspace_size", "qlayer_conv2d_fwd",
     "qlayer_conv2d_bwd_data_workspace_size", "qlayer_conv2d_bwd_data", "qlayer_conv2d_bwd_data_ex",
-    "qlayer_conv2d_bwd_weight_workspace_size", "qlayer_conv2d_bwd_weight",
+    "qlayer_conv2d_bwd_weight_workspace_size", "qlayer_conv2d_bwd_weight", "qlayer_conv2d_bwd_weight_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
     "qlayer_linear_fwd_workspace_size", "qlayer_linear_fwd",
     "qlayer_linear_bwd_workspace_size", "qlayer_linear_bwd",
 ]
@@ -119,6 +120,8 @@ def lib():
     L.qlayer_conv2d_bwd_data_ex.argtypes = [cd] + [_vp] * 8 + [_vp, _sz, _vp]
     L.qlayer_conv2d_bwd_data_ex.restype = ctypes.c_int
     L.qlayer_conv2d_bwd_weight.argtypes = [cd] + [_vp] * 10 + [_vp, _sz, _vp]
+    L.qlayer_conv2d_bwd_weight_noalloc.argtypes = [cd] + [_vp] * 10 + [_vp]
+    L.qlayer_conv2d_bwd_weight_noalloc.restype = ctypes.c_int
     L.qlayer_linear_fwd.argtypes = [ld] + [_vp] * 10 + [_vp, _sz, _vp]
     L.qlayer_linear_bwd.argtypes = [ld] + [_vp] * 14 + [_vp, _sz, _vp]
     ep = ctypes.POINTER(Epilogue)
@@ -319,6 +322,21 @@ def qlayer_conv2d_bwd_weight(desc, x, gy, ta, tb, dwa, dwb, dwc, dba=None, dbb=N
     _check("qlayer_conv2d_bwd_weight", lib().qlayer_conv2d_bwd_weight(
         ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(dwa), _ptr(dwb), _ptr(dwc),
         _ptr(dba), _ptr(dbb), _ptr(dbc), wp, wn, _stream(stream, dev)))
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20  # QLAYER_NOALLOC_SCRATCH_BYTES of qlayer.h
+
+
+def qlayer_conv2d_bwd_weight_noalloc(desc, x, gy, ta, tb, dwa, dwb, dwc, dba=None, dbb=None, dbc=None,
+                                     stream=None):
+    """qlayer_conv2d_bwd_weight with the library's own scratch array in place of a
+    workspace: allocates nothing (for graph capture and other callers that cannot)."""
+    dev = _device(x, gy)
+    _check_args(_conv_sizes(desc), desc.dtype, dev, act=[("x", x)], maps=[("gy", gy), ("ta", ta), ("tb", tb)],
+                w32=[("dwa", dwa), ("dwb", dwb), ("dwc", dwc)], vec32=[("dba", dba), ("dbb", dbb), ("dbc", dbc)])
+    _check("qlayer_conv2d_bwd_weight_noalloc", lib().qlayer_conv2d_bwd_weight_noalloc(
+        ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(dwa), _ptr(dwb), _ptr(dwc),
+        _ptr(dba), _ptr(dbb), _ptr(dbc), _stream(stream, dev)))
 
 
 def qlayer_linear_fwd_workspace_size(desc: LinearDesc) -> int:

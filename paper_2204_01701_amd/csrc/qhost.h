@@ -108,8 +108,9 @@ inline ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
 // avoids.  At least min_stages K steps per split, at most kMaxSplitBytes of
 // partial sums (bytes_per_split each).
 inline void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int slots, int &splits,
-                 int &sps) {
-    const int cap_bytes = (int)std::max<size_t>(1, kMaxSplitBytes / std::max<size_t>(bytes_per_split, 1));
+                 int &sps,
+                        size_t max_bytes = kMaxSplitBytes) {
+    const int cap_bytes = (int)std::max<size_t>(1, max_bytes / std::max<size_t>(bytes_per_split, 1));
     const int s_max = std::max(1, std::min(stages_total / std::max(min_stages, 1), cap_bytes));
     double best = 0.0;
     splits = 1;
@@ -356,7 +357,9 @@ struct BwdWeightPlan {
     size_t xpad_bytes, dw_bytes, db_bytes, ws_bytes;  // workspace: [X padded][dW partials][db partials]
 };
 
-inline BwdWeightPlan plan_bwd_weight(const Geom &g) {
+// max_split_bytes: cap on the dW partial sums (the no-allocation entry point
+// plans for its fixed scratch array).
+inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMaxSplitBytes) {
     BwdWeightPlan p{};
     p.pad = g.dt == QL_BF16 && g.pad_small_c() && g.O % g.vec() == 0;
     p.Cp = p.pad ? g.cpad() : g.C;
@@ -380,7 +383,7 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g) {
     p.col_tiles = cdiv(g.O, p.BO);
     p.stages_total = cdiv(M, p.KE);
     plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16),
-                (size_t)3 * g.O * KPO * 4, p.slots, p.splits, p.sps);
+                (size_t)3 * g.O * KPO * 4, p.slots, p.splits, p.sps, max_split_bytes);
     if (p.splits > 1) {
         p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KPO * sizeof(float));
         p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));

@@ -27,6 +27,29 @@ const void *zero_page() {
     return addr[dev];
 }
 }  // namespace host
+
+// Scratch memory of qlayer_conv2d_bwd_weight_noalloc, the entry point for
+// callers that cannot allocate: one array per GPU the library runs on, held
+// until the process ends.  Host code never uses its name as an address (on
+// the host it is a stand-in symbol): the device address comes from
+// hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = QLAYER_NOALLOC_SCRATCH_BYTES;
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kScratchBytes];
+
+namespace host {
+// Device address of `scratch` on the current device (nullptr if it cannot be resolved).
+void *scratch_ptr() {
+    static std::once_flag once[kMaxDevices];
+    static void *addr[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::call_once(once[dev], [dev] {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) addr[dev] = p;
+    });
+    return addr[dev];
+}
+}  // namespace host
 }  // namespace ql
 
 using namespace ql;
@@ -159,9 +182,11 @@ ql_status bwd_data_common(const Geom &g, const void *gy, const void *ta, const v
     return run_bwd_data(g, p, gy, ta, tb, xin, wa, wb, wc, dx, ws, st);
 }
 
+// noalloc: the workspace is the library's scratch array (ws and ws_bytes are
+// ignored); the split-K plan is capped to fit it.
 ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const void *ta, const void *tb,
                             float *dwa, float *dwb, float *dwc, float *dba, float *dbb, float *dbc, void *ws,
-                            size_t ws_bytes, void *stream) {
+                            size_t ws_bytes, void *stream, bool noalloc = false) {
     const int nt = g.terms(), ngm = om_gmaps(g.om());
     // pointers of terms (and maps) the neuron type lacks are ignored
     if (nt < 3) { dwc = nullptr; dbc = nullptr; }
@@ -177,6 +202,12 @@ ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const 
         if (q && !aligned16(q)) return QL_EINVAL;
     if (g.dw) {
         const DwPlan p = plan_dw(g, 2);
+        if (noalloc) {
+            if (p.ws_bytes > kScratchBytes) return QL_EWORKSPACE;
+            ws = scratch_ptr();
+            ws_bytes = kScratchBytes;
+            if (!ws) return QL_EHIP;
+        }
         if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
         if (ws && !aligned16(ws)) return QL_EINVAL;
         float *const dw[3] = {dwa, dwb, dwc};
@@ -184,7 +215,21 @@ ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const 
         hipStream_t st = static_cast<hipStream_t>(stream);
         return run_dw_bwd_weight(g, p, x, gy, ta, tb, dw, db, ws, st);
     }
-    const BwdWeightPlan p = plan_bwd_weight(g);
+    BwdWeightPlan p = plan_bwd_weight(g);
+    if (noalloc) {
+        // the regular plan where it fits (then the results are bitwise those of
+        // the regular entry point), else fewer splits: dW and db partials of
+        // 3 O (KP + 1) floats per split, two 256-byte alignments
+        if (p.ws_bytes > kScratchBytes) {
+            const size_t room = kScratchBytes - std::min(kScratchBytes, p.xpad_bytes + 2 * kAlign);
+            const size_t kpo = (size_t)g.KH * g.KW * g.C;
+            p = plan_bwd_weight(g, room / (kpo + 1) * kpo);
+        }
+        if (p.ws_bytes > kScratchBytes) return QL_EWORKSPACE;
+        ws = scratch_ptr();
+        ws_bytes = kScratchBytes;
+        if (!ws) return QL_EHIP;
+    }
     if (ws_bytes < p.ws_bytes || (p.ws_bytes && !ws)) return QL_EWORKSPACE;
     if (ws && !aligned16(ws)) return QL_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -262,6 +307,15 @@ ql_status qlayer_conv2d_bwd_weight(const ql_conv_desc *desc, const void *x, cons
     const ql_status s = make_geom(desc, g);
     if (s != QL_OK) return s;
     return bwd_weight_common(g, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, workspace, workspace_bytes, stream);
+}
+
+ql_status qlayer_conv2d_bwd_weight_noalloc(const ql_conv_desc *desc, const void *x, const void *gy, const void *ta,
+                                           const void *tb, float *dwa, float *dwb, float *dwc, float *dba,
+                                           float *dbb, float *dbc, void *stream) {
+    Geom g;
+    const ql_status s = make_geom(desc, g);
+    if (s != QL_OK) return s;
+    return bwd_weight_common(g, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, nullptr, 0, stream, true);
 }
 
 size_t qlayer_linear_fwd_workspace_size(const ql_linear_desc *desc) {

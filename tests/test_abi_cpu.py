@@ -326,3 +326,14 @@ def test_binding_rejects_host_and_mis_sized_tensors_before_any_call():
     # sizes and dtypes are checked the same way (the device check fires first on the host)
     with pytest.raises(ValueError):
         ql._expect("w", torch.zeros(10), 11, None, None)
+
+
+def test_noalloc_weight_gradient_rejects_a_layer_beyond_its_scratch(L):
+    """The no-allocation entry point plans for its fixed scratch array: a
+    few-channel bf16 layer whose zero-padded copy of X alone exceeds it is
+    refused with QL_EWORKSPACE before anything is launched."""
+    d = ql.conv_desc(1024, 3, 64, 64, 64, 3, 3, 1, 1, ql.QL_BF16)
+    assert 1024 * 64 * 64 * 8 * 2 > ql.NOALLOC_SCRATCH_BYTES
+    assert L.qlayer_conv2d_bwd_weight_noalloc(ctypes.byref(d), *[FAKE] * 10, None) == QL_EWORKSPACE
+    assert L.qlayer_conv2d_bwd_weight_noalloc(ctypes.byref(d), *[FAKE] * 4, None, *[FAKE] * 5,
+                                              None) == QL_EINVAL                   # dW_a missing
