@@ -126,3 +126,59 @@ def tol(bf16: bool, grad: bool) -> float:
     if bf16:
         return 2e-2
     return 1e-4 if grad else 1e-5
+
+
+# --- elementwise bound -------------------------------------------------------
+# Next to the normwise limit, every element is bounded by the rounding the
+# kernels can do, derived from the arithmetic (the standard model: each
+# rounding to a format with unit u changes a value by at most u relative; a
+# sum of K products accumulated in fp32 errs by at most K 2^-24 times the sum
+# of the magnitudes of its terms).  `mag` is that sum of magnitudes, computed
+# by the oracle itself on |X|, |W_t|, |b_t|, |G| (every product and bias then
+# enters with its absolute value, so the oracle's outputs on them bound the
+# magnitude sums of the true computation).  Per output kind, with
+# g = K 2^-24 for the reduction length K and u = 2^-9 for bf16 (RNE):
+#   forward T_a, T_b (rounded once):        |e| <= u |ref| + 2 g mag
+#   forward Y (three fp32 terms, product):  |e| <= u |ref| + 4 g mag
+#   input gradient (bf16 operands G o T_b): |e| <= u |ref| + (u + 2 g) mag
+#   dW (fp32 out, bf16 operands):           |e| <= 2^-23 |ref| + (u + 2 g) mag
+#   db (fp32 sums of fp32 products):        |e| <= 2^-23 |ref| + 2 g mag
+# fp32 runs use u = 2^-24 throughout.  A factor 2 of slack covers the few
+# fp32 operations outside the accumulations.
+U_BF16 = 2.0 ** -9
+U_F32 = 2.0 ** -24
+
+
+def elem_bound(kind: str, ref, mag, bf16: bool, K: int):
+    u = U_BF16 if bf16 else U_F32
+    g = K * U_F32
+    ref = np.abs(np.asarray(ref, dtype=np.float64))
+    mag = np.asarray(mag, dtype=np.float64)
+    if kind in ("ta", "tb"):
+        b = u * ref + 2 * g * mag
+    elif kind == "y":
+        b = u * ref + 4 * g * mag
+    elif kind == "dx":
+        b = u * ref + (u + 2 * g) * mag
+    elif kind.startswith("dw"):
+        b = 2 * U_F32 * ref + (u + 2 * g) * mag
+    elif kind.startswith("db"):
+        b = 2 * U_F32 * ref + 2 * g * mag
+    else:
+        raise KeyError(kind)
+    return 2.0 * b + 1e-30
+
+
+def check_elementwise(name: str, kind: str, got, ref, mag, bf16: bool, K: int) -> float:
+    """Assert |got - ref| <= elem_bound elementwise; return the largest ratio error / bound."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    bound = elem_bound(kind, ref, mag, bf16, K)
+    err = np.abs(got - ref)
+    ratio = err / bound
+    worst = int(np.argmax(ratio)) if ratio.size else 0
+    r = float(ratio.reshape(-1)[worst]) if ratio.size else 0.0
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    assert r <= 1.0, (f"{name}: element {np.unravel_index(worst, ratio.shape)} off by "
+                      f"{err.reshape(-1)[worst]:.3e} > bound {bound.reshape(-1)[worst]:.3e}")
+    return r

@@ -1,21 +1,23 @@
 """GPU parity at the full workload sizes, in the launch configuration the
 benchmark times (default planner, workspace of the queried size).
 
-The whole outputs are too large for the fp64 oracle, so it recomputes a
-sample of them one by one: forward outputs Y, T_a, T_b at random positions
-plus the corners of the index space, input-gradient entries likewise (border
-pixels included), and the complete weight and bias gradients of a few output
-channels (first, last, one random).  The normwise relative error over each
-sampled set must meet the same limits as the small cases: fp32 forward 1e-5,
-gradients 1e-4; bf16 with fp32 accumulation 2e-2.
+Every output is compared in two ways (qlh):
+* the normwise relative error over the compared set, against the limits
+  fp32 forward 1e-5 / gradients 1e-4, bf16 with fp32 accumulation 2e-2;
+* element by element, against a bound derived from the arithmetic (the
+  rounding of each output and operand plus the fp32 accumulation error of
+  its reduction), with the magnitudes from the oracle on |inputs|.
 
-Workloads: the 13 layers of a CIFAR VGG-16 at batch 128 (bf16), the distinct
-layer shapes of a CIFAR ResNet-20 at batch 256 (fp32 and bf16), one large
-256->256 layer on 64 x 56 x 56 (bf16) and a 8192 x 4096 -> 4096 dense layer
-(bf16).
+Whole tensors where the fp64 oracle can afford them: the 13 layers of a
+CIFAR VGG-16 at batch 128 (bf16), the distinct layer shapes of a CIFAR
+ResNet-20 at batch 256 (fp32 and bf16), the small fp32 layer.  For the
+64 x 256 x 56 x 56 layer and the 8192 x 4096 -> 4096 dense layer, complete
+blocks of every output in the shape of the largest workgroup tile any kernel
+of the pass uses (256 x 256), at the first, the last and one interior tile
+position: forward Y, T_a, T_b; input gradient dX (whole rows of channels for
+the dense layer); whole output channels of dW_t and db_t (all of (r, q, c),
+so every weight-gradient row tile and every split-K part of those channels).
 """
-import itertools
-
 import numpy as np
 import pytest
 import torch
@@ -27,71 +29,40 @@ pytestmark = pytest.mark.gpu
 
 import qlh  # noqa: E402
 
-N_SAMPLES = 96
+TILE = 256  # the largest workgroup tile extent along channels and pixels
 
 
-def _corners(extents):
-    return [list(c) for c in itertools.product(*[(0, e - 1) for e in extents])]
-
-
-def _sample_idx(rng, extents, k=N_SAMPLES):
-    """k index tuples: every corner of the box, the rest uniform."""
-    pts = _corners(extents)
-    rest = k - len(pts)
-    rnd = np.stack([rng.integers(0, e, size=rest) for e in extents], axis=1)
-    return np.concatenate([np.array(pts, dtype=np.int64), rnd.astype(np.int64)], axis=0)
-
-
-def _at(t, *idx):
-    """Gather t[idx] on the device and return it as float64 numpy."""
-    ti = tuple(torch.from_numpy(np.ascontiguousarray(a)).to(t.device) for a in idx)
-    return t[ti].double().cpu().numpy()
-
-
-def _check(name, got, ref, bf16, grad):
+def _check(name, kind, got, ref, mag, bf16, K):
     e = qlh.relerr(got, ref)
-    lim = qlh.tol(bf16, grad)
+    lim = qlh.tol(bf16, kind not in ("y", "ta", "tb"))
     assert e <= lim, f"{name}: normwise relative error {e:.3e} > {lim:.0e}"
+    qlh.check_elementwise(name, kind, got, ref, mag, bf16, K)
     return e
 
 
-def _conv_case(cfg_id, layer_id, L, bf16):
-    print(f"full-size conv cfg={cfg_id} layer={layer_id} N={L.n} C={L.c} {L.h}x{L.w} O={L.o} "
+def _abs_args(f64):
+    return {k: np.abs(v) for k, v in f64.items()}
+
+
+def _conv_whole(cfg_id, layer_id, L, bf16):
+    print(f"full-size conv (whole tensors) cfg={cfg_id} layer={layer_id} N={L.n} C={L.c} {L.h}x{L.w} O={L.o} "
           f"k={L.k} s={L.stride} p={L.pad} bf16={bf16}", flush=True)
     inp = synth.conv_inputs(cfg_id, layer_id, L, bf16=bf16)
-    dev = qlh.run_conv(inp, L.stride, L.pad, bf16)
+    got = qlh.conv_to_np(qlh.run_conv(inp, L.stride, L.pad, bf16))
     f64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in inp.items()}
-    args = (f64["x"], f64["wa"], f64["wb"], f64["wc"], f64["ba"], f64["bb"], f64["bc"])
-    rng = np.random.default_rng([900, cfg_id, layer_id, int(bf16)])
-
-    # forward: (n, o, i, j)
-    idx = _sample_idx(rng, (L.n, L.o, L.ho, L.wo))
-    ry, rta, rtb = oracle.conv2d_fwd_at(*args, idx, L.stride, L.pad)
-    n, o, i, j = idx.T
-    for key, ref in (("y", ry), ("ta", rta), ("tb", rtb)):
-        got = _at(dev[key], n, i, j, o)  # NHWC on the device
-        _check(key, got, ref, bf16, False)
-
-    # input gradient: (n, c, h, w)
-    idx = _sample_idx(rng, (L.n, L.c, L.h, L.w))
-    rdx = oracle.conv2d_dx_at(*args, f64["gy"], idx, L.stride, L.pad)
-    n, c, h, w = idx.T
-    _check("dx", _at(dev["dx"], n, h, w, c), rdx, bf16, True)
-
-    # weight and bias gradients of whole output channels
-    chans = sorted({0, L.o - 1, int(rng.integers(0, L.o))})
-    got = {k: [] for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")}
-    ref = {k: [] for k in got}
-    for oc in chans:
-        r = oracle.conv2d_dw_channel(*args, f64["gy"], oc, L.stride, L.pad)
-        for t in ("a", "b", "c"):
-            # device dW_t is O x KH x KW x C; the oracle's channel slice is C x KH x KW
-            got["dw" + t].append(dev["dw" + t][oc].permute(2, 0, 1).double().cpu().numpy().ravel())
-            ref["dw" + t].append(r["dw" + t].ravel())
-            got["db" + t].append(dev["db" + t][oc:oc + 1].double().cpu().numpy())
-            ref["db" + t].append(r["db" + t])
-    for k in got:
-        _check(k, np.concatenate(got[k]), np.concatenate(ref[k]), bf16, True)
+    keys = ("x", "wa", "wb", "wc", "ba", "bb", "bc")
+    ref = {}
+    ref["y"], ref["ta"], ref["tb"] = oracle.conv2d_fwd(*[f64[k] for k in keys], L.stride, L.pad)
+    ref.update(oracle.conv2d_bwd(*[f64[k] for k in keys], f64["gy"], L.stride, L.pad))
+    a = _abs_args(f64)
+    mag = {}
+    mag["y"], mag["ta"], mag["tb"] = oracle.conv2d_fwd(*[a[k] for k in keys], L.stride, L.pad)
+    mag.update(oracle.conv2d_bwd(*[a[k] for k in keys], a["gy"], L.stride, L.pad))
+    ho, wo = ref["y"].shape[2:]
+    K = {"fwd": L.c * L.k * L.k + 1, "dx": 3 * L.o * L.k * L.k, "dw": L.n * ho * wo}
+    for k in ("y", "ta", "tb", "dx", "dwa", "dwb", "dwc", "dba", "dbb", "dbc"):
+        kk = K["fwd"] if k in ("y", "ta", "tb") else (K["dx"] if k == "dx" else K["dw"])
+        _check(k, k, got[k], ref[k], mag[k], bf16, kk)
 
 
 VGG = synth.vgg16_layers(128)
@@ -99,7 +70,7 @@ VGG = synth.vgg16_layers(128)
 
 @pytest.mark.parametrize("layer_id", range(len(VGG)), ids=lambda i: f"L{i + 1}")
 def test_vgg16_layer_full_size(layer_id):
-    _conv_case(2, layer_id, VGG[layer_id], bf16=True)
+    _conv_whole(2, layer_id, VGG[layer_id], bf16=True)
 
 
 RESNET = synth.resnet20_layers(256)
@@ -118,55 +89,126 @@ def _distinct(layers):
 @pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
 @pytest.mark.parametrize("layer_id", _distinct(RESNET), ids=lambda i: f"conv{i}")
 def test_resnet20_layer_full_size(layer_id, bf16):
-    _conv_case(3, layer_id, RESNET[layer_id], bf16=bf16)
-
-
-def test_large_conv_full_size():
-    _conv_case(4, 0, synth.LARGE_BF16, bf16=True)
-
-
-def test_dense_full_size():
-    D = synth.DENSE_BF16
-    print(f"full-size dense {D.batch}x{D.inp}->{D.out} bf16", flush=True)
-    inp = synth.dense_inputs(5, 0, D, bf16=True)
-    dev = qlh.run_linear(inp, True)
-    f64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in inp.items()}
-    args = (f64["x"], f64["wa"], f64["wb"], f64["wc"], f64["ba"], f64["bb"], f64["bc"])
-    rng = np.random.default_rng([901, 5])
-
-    idx = _sample_idx(rng, (D.batch, D.out))
-    ry, rta, rtb = oracle.linear_fwd_at(*args, idx)
-    b, o = idx.T
-    for key, ref in (("y", ry), ("ta", rta), ("tb", rtb)):
-        _check(key, _at(dev[key], b, o), ref, True, False)
-
-    rows = np.array([0, D.batch - 1, int(rng.integers(0, D.batch))], dtype=np.int64)
-    rdx = oracle.linear_dx_rows(*args, f64["gy"], rows)
-    _check("dx", _at(dev["dx"], rows), rdx, True, True)
-
-    chans = sorted({0, D.out - 1, int(rng.integers(0, D.out))})
-    got = {k: [] for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")}
-    ref = {k: [] for k in got}
-    for oc in chans:
-        r = oracle.linear_dw_row(*args, f64["gy"], oc)
-        for t in ("a", "b", "c"):
-            got["dw" + t].append(dev["dw" + t][oc].double().cpu().numpy())
-            ref["dw" + t].append(r["dw" + t])
-            got["db" + t].append(dev["db" + t][oc:oc + 1].double().cpu().numpy())
-            ref["db" + t].append(r["db" + t])
-    for k in got:
-        # zero biases: db_t is still the column sum of G_t, non-zero
-        _check(k, np.concatenate(got[k]), np.concatenate(ref[k]), True, True)
+    _conv_whole(3, layer_id, RESNET[layer_id], bf16=bf16)
 
 
 def test_small_fp32_whole_tensors():
-    """The small fp32 workload (N=2, 16->16, 8x8) is cheap enough to compare in full."""
-    L = synth.SMALL_FP32
-    inp = synth.conv_inputs(1, 0, L, bf16=False)
-    got = qlh.conv_to_np(qlh.run_conv(inp, L.stride, L.pad, False))
-    args = (inp["x"], inp["wa"], inp["wb"], inp["wc"], inp["ba"], inp["bb"], inp["bc"])
-    y, ta, tb = oracle.conv2d_fwd(*args, L.stride, L.pad)
-    ref = oracle.conv2d_bwd(*args, inp["gy"], L.stride, L.pad)
-    ref.update({"y": y, "ta": ta, "tb": tb})
-    for k in ("y", "ta", "tb", "dx", "dwa", "dwb", "dwc", "dba", "dbb", "dbc"):
-        _check(k, got[k], ref[k], False, k not in ("y", "ta", "tb"))
+    """The small fp32 workload (N=2, 16->16, 8x8), whole tensors."""
+    _conv_whole(1, 0, synth.SMALL_FP32, bf16=False)
+
+
+def _blocks(extent, rng):
+    """Start of the first, the last and one interior TILE-aligned block of an extent."""
+    last = max(0, extent - TILE)
+    mid = int(rng.integers(1, max(2, extent // TILE))) * TILE if extent > 2 * TILE else 0
+    return sorted({0, min(mid, last), last})
+
+
+def _at(t, *idx):
+    ti = tuple(torch.from_numpy(np.ascontiguousarray(a)).to(t.device) for a in idx)
+    return t[ti].double().cpu().numpy()
+
+
+def test_large_conv_full_size_tiles():
+    L = synth.LARGE_BF16
+    print("full-size large conv, complete tile blocks", flush=True)
+    inp = synth.conv_inputs(4, 0, L, bf16=True)
+    dev = qlh.run_conv(inp, L.stride, L.pad, True)
+    f64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in inp.items()}
+    a = _abs_args(f64)
+    keys = ("x", "wa", "wb", "wc", "ba", "bb", "bc")
+    args, aargs = [f64[k] for k in keys], [a[k] for k in keys]
+    rng = np.random.default_rng([900, 4])
+    ho, wo = L.ho, L.wo
+    M = L.n * ho * wo
+
+    # forward: blocks of TILE output channels x TILE output pixels (pixel m = (n ho + i) wo + j)
+    for o0 in _blocks(L.o, rng):
+        for m0 in _blocks(M, rng):
+            o = np.arange(o0, min(L.o, o0 + TILE))
+            m = np.arange(m0, min(M, m0 + TILE))
+            oo, mm = np.meshgrid(o, m, indexing="ij")
+            n, rem = np.divmod(mm.ravel(), ho * wo)
+            i, j = np.divmod(rem, wo)
+            idx = np.stack([n, oo.ravel(), i, j], axis=1)
+            ref = oracle.conv2d_fwd_at(*args, idx, L.stride, L.pad)
+            mag = oracle.conv2d_fwd_at(*aargs, idx, L.stride, L.pad)
+            for key, r, g in zip(("y", "ta", "tb"), ref, mag):
+                _check(f"{key} block o{o0} m{m0}", key, _at(dev[key], n, i, j, idx[:, 1]), r, g, True,
+                       L.c * 9 + 1)
+
+    # input gradient: blocks of TILE input channels x TILE input pixels
+    Mi = L.n * L.h * L.w
+    for c0 in _blocks(L.c, rng):
+        for m0 in _blocks(Mi, rng):
+            c = np.arange(c0, min(L.c, c0 + TILE))
+            m = np.arange(m0, min(Mi, m0 + TILE))
+            cc, mm = np.meshgrid(c, m, indexing="ij")
+            n, rem = np.divmod(mm.ravel(), L.h * L.w)
+            h, w = np.divmod(rem, L.w)
+            idx = np.stack([n, cc.ravel(), h, w], axis=1)
+            ref = oracle.conv2d_dx_at(*args, f64["gy"], idx, L.stride, L.pad)
+            mag = oracle.conv2d_dx_at(*aargs, a["gy"], idx, L.stride, L.pad)
+            _check(f"dx block c{c0} m{m0}", "dx", _at(dev["dx"], n, h, w, idx[:, 1]), ref, mag, True, 3 * L.o * 9)
+
+    # weight and bias gradients: whole output channels, one 64-channel tile at each end
+    chans = list(range(0, 64)) + list(range(L.o - 64, L.o))
+    got = {k: [] for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")}
+    ref = {k: [] for k in got}
+    mag = {k: [] for k in got}
+    for oc in chans:
+        r = oracle.conv2d_dw_channel(*args, f64["gy"], oc, L.stride, L.pad)
+        g = oracle.conv2d_dw_channel(*aargs, a["gy"], oc, L.stride, L.pad)
+        for t in ("a", "b", "c"):
+            got["dw" + t].append(dev["dw" + t][oc].permute(2, 0, 1).double().cpu().numpy().ravel())
+            got["db" + t].append(dev["db" + t][oc:oc + 1].double().cpu().numpy())
+            for dst, src in ((ref, r), (mag, g)):
+                dst["dw" + t].append(src["dw" + t].ravel())
+                dst["db" + t].append(src["db" + t])
+    for k in got:
+        _check(k, k, np.concatenate(got[k]), np.concatenate(ref[k]), np.concatenate(mag[k]), True, M)
+
+
+def test_dense_full_size_tiles():
+    D = synth.DENSE_BF16
+    print(f"full-size dense {D.batch}x{D.inp}->{D.out} bf16, complete tile blocks", flush=True)
+    inp = synth.dense_inputs(5, 0, D, bf16=True)
+    dev = qlh.run_linear(inp, True)
+    f64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in inp.items()}
+    a = _abs_args(f64)
+    keys = ("x", "wa", "wb", "wc", "ba", "bb", "bc")
+    args, aargs = [f64[k] for k in keys], [a[k] for k in keys]
+    rng = np.random.default_rng([901, 5])
+
+    for b0 in _blocks(D.batch, rng):
+        for o0 in _blocks(D.out, rng):
+            bb, oo = np.meshgrid(np.arange(b0, b0 + TILE), np.arange(o0, o0 + TILE), indexing="ij")
+            idx = np.stack([bb.ravel(), oo.ravel()], axis=1)
+            ref = oracle.linear_fwd_at(*args, idx)
+            mag = oracle.linear_fwd_at(*aargs, idx)
+            for key, r, g in zip(("y", "ta", "tb"), ref, mag):
+                _check(f"{key} block b{b0} o{o0}", key, _at(dev[key], idx[:, 0], idx[:, 1]), r, g, True, D.inp + 1)
+
+    # input gradient: whole rows (every input channel), TILE rows at each end
+    for b0 in (0, D.batch - TILE):
+        rows = np.arange(b0, b0 + TILE)
+        ref = oracle.linear_dx_rows(*args, f64["gy"], rows)
+        mag = oracle.linear_dx_rows(*aargs, a["gy"], rows)
+        _check(f"dx rows {b0}", "dx", _at(dev["dx"], rows), ref, mag, True, 3 * D.out)
+
+    # weight and bias gradients: whole rows o, a 64-row tile at each end
+    chans = list(range(0, 64)) + list(range(D.out - 64, D.out))
+    got = {k: [] for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")}
+    ref = {k: [] for k in got}
+    mag = {k: [] for k in got}
+    for oc in chans:
+        r = oracle.linear_dw_row(*args, f64["gy"], oc)
+        g = oracle.linear_dw_row(*aargs, a["gy"], oc)
+        for t in ("a", "b", "c"):
+            got["dw" + t].append(dev["dw" + t][oc].double().cpu().numpy())
+            got["db" + t].append(dev["db" + t][oc:oc + 1].double().cpu().numpy())
+            for dst, src in ((ref, r), (mag, g)):
+                dst["dw" + t].append(src["dw" + t])
+                dst["db" + t].append(src["db" + t])
+    for k in got:
+        _check(k, k, np.concatenate(got[k]), np.concatenate(ref[k]), np.concatenate(mag[k]), True, D.batch)
