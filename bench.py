@@ -52,8 +52,13 @@ def parse():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
                     help="instead of running: HBM bytes per entry call from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
                          "counter tables of the benchmark and of --copy-calibration")
-    ap.add_argument("--leg", choices=("depthwise", "epilogue", "neuron_types"),
-                    help="instead of the benchmark: run one extra leg alone and print its JSON (for profiling)")
+    ap.add_argument("--leg", choices=("depthwise", "epilogue", "neuron_types", "kernels", "resnet20"),
+                    help="instead of the benchmark: run one extra leg alone and print its JSON (for profiling); "
+                         "'kernels' runs every pass of the VGG-16 layers, the large layer and the dense layer "
+                         "KERNEL_REPS times in a fixed order, for counter collection")
+    ap.add_argument("--counter-summary", nargs="+", metavar="COUNTER_CSV",
+                    help="instead of running: per-pass counter table (MFMA busy, VALU per MFMA, LDS) from "
+                         "rocprofv3 --pmc counter_collection tables of the 'kernels' leg")
     return ap.parse_args()
 
 
@@ -484,6 +489,126 @@ def read_traffic(family):
     return int(m.group(1)) if m else None
 
 
+KERNEL_REPS = 3  # calls of each pass in the 'kernels' leg
+
+
+def kernel_leg_sequence():
+    """(workload, layer, pass) of the 'kernels' leg's entry calls in issue order (no GPU needed)."""
+    import synth
+    seq = []
+    for i in range(len(synth.vgg16_layers(128))):
+        for f in ("fwd", "bwd_data", "bwd_weight"):
+            seq += [("vgg16", i + 1, f)] * KERNEL_REPS
+    for f in ("fwd", "bwd_data", "bwd_weight"):
+        seq += [("large", 0, f)] * KERNEL_REPS
+    seq += [("dense", 0, "fwd")] * KERNEL_REPS
+    seq += [("dense", 0, "bwd_data"), ("dense", 0, "bwd_weight")] * KERNEL_REPS  # one call, two main kernels
+    return seq
+
+
+def kernel_leg(ql, torch, dev, stream):
+    """Every pass of the 13 VGG-16 layers, the large layer and the dense layer,
+    KERNEL_REPS calls each, in the order kernel_leg_sequence() gives."""
+    import synth
+    calls = {}
+    for i, L in enumerate(synth.vgg16_layers(128)):
+        ly = Layer(ql, torch, L, 2, i, dev)
+        for f in ("fwd", "bwd_data", "bwd_weight"):
+            for _ in range(KERNEL_REPS):
+                getattr(ly, f)(stream)
+        torch.cuda.synchronize()
+        del ly
+    ly = Layer(ql, torch, synth.LARGE_BF16, 4, 0, dev)
+    for f in ("fwd", "bwd_data", "bwd_weight"):
+        for _ in range(KERNEL_REPS):
+            getattr(ly, f)(stream)
+    torch.cuda.synchronize()
+    del ly
+    D = synth.DENSE_BF16
+    inp = synth.dense_inputs(5, 0, D, bf16=True)
+    dt = torch.bfloat16
+    d = ql.linear_desc(D.batch, D.inp, D.out, ql.QL_BF16)
+    x = torch.from_numpy(inp["x"]).to(dev, dt)
+    w = [torch.from_numpy(inp[k]).to(dev, dt) for k in ("wa", "wb", "wc")]
+    b = [torch.from_numpy(inp[k]).to(dev) for k in ("ba", "bb", "bc")]
+    gy = torch.from_numpy(inp["gy"]).to(dev, dt)
+    y = torch.empty((D.batch, D.out), device=dev, dtype=dt)
+    ta, tb, dx = torch.empty_like(y), torch.empty_like(y), torch.empty_like(x)
+    dw = [torch.empty((D.out, D.inp), device=dev) for _ in range(3)]
+    db = [torch.empty(D.out, device=dev) for _ in range(3)]
+    need = max(ql.qlayer_linear_fwd_workspace_size(d), ql.qlayer_linear_bwd_workspace_size(d))
+    ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    wsp = (ws.data_ptr(), ws.numel())
+    for _ in range(KERNEL_REPS):
+        ql.qlayer_linear_fwd(d, x, *w, *b, y, ta, tb, workspace=wsp, stream=stream)
+    for _ in range(KERNEL_REPS):
+        ql.qlayer_linear_bwd(d, x, gy, ta, tb, *w, dx, *dw, *db, workspace=wsp, stream=stream)
+    torch.cuda.synchronize()
+    calls["calls"] = len(kernel_leg_sequence())
+    return calls
+
+
+def counter_summary(paths):
+    """Markdown table of the 'kernels' leg's counters: per pass (averaged over its
+    calls, main kernel only): the kernel duration and the shader clock it ran at
+    (GRBM_GUI_ACTIVE, which reads the sum over the 8 XCDs, / 8 / duration); MFMA
+    busy = SQ_VALU_MFMA_BUSY_CYCLES (32 per 32x32x16 bf16 MFMA, summed over the
+    SIMDs) / (GRBM_GUI_ACTIVE / 8 x 256 CUs x 4 SIMDs), the fraction of the MFMA
+    peak at the clock the kernel ran at; non-MFMA VALU instructions per MFMA
+    instruction; LDS instructions per MFMA; LDS bank-conflict cycles per LDS
+    instruction."""
+    import csv
+    per = {}  # (file, dispatch id) -> {counter: value}; kernel names and durations
+    names, durs = {}, {}
+    for p in paths:
+        for r in csv.DictReader(open(p)):
+            did = (p, int(r["Dispatch_Id"]))
+            per.setdefault(did, {})
+            per[did][r["Counter_Name"]] = per[did].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            names[did] = r["Kernel_Name"]
+            durs[did] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    # counters of separate runs: dispatches matched by their order among the main kernels
+    seq = kernel_leg_sequence()
+    rows = {}
+    for p in paths:
+        mains = [(p, d) for d in sorted({int(r["Dispatch_Id"]) for r in csv.DictReader(open(p))})
+                 if _family(names[(p, d)])[1]]
+        if len(mains) != len(seq):
+            raise SystemExit(f"{p}: {len(mains)} main-kernel dispatches, the leg makes {len(seq)} calls")
+        for d, key in zip(mains, seq):
+            rows.setdefault(key, {"kernel": names[d], "dur_ns": [], "grbm": []})
+            for c, v in per[d].items():
+                rows[key][c] = rows[key].get(c, 0.0) + v / KERNEL_REPS
+            if "GRBM_GUI_ACTIVE" in per[d]:
+                rows[key]["dur_ns"].append(durs[d])
+                rows[key]["grbm"].append(per[d]["GRBM_GUI_ACTIVE"])
+    lines = ["| workload | layer | pass | main kernel | us (profiled) | clock GHz | MFMA busy % | VALU / MFMA | "
+             "LDS / MFMA | LDS bank conflict cycles / LDS instr |", "|---|---:|---|---|---:|---:|---:|---:|---:|---:|"]
+    nxcd = 8
+    for (wl, layer, f), r in rows.items():
+        g = r.get("GRBM_GUI_ACTIVE")
+        g = g / nxcd if g is not None else None
+        us = sum(r["dur_ns"]) / len(r["dur_ns"]) / 1e3 if r["dur_ns"] else None
+        ghz = sum(gg / nxcd / dd for gg, dd in zip(r["grbm"], r["dur_ns"])) / len(r["dur_ns"]) if r["dur_ns"] else None
+        busy = r.get("SQ_VALU_MFMA_BUSY_CYCLES")
+        mf = r.get("SQ_INSTS_MFMA") or r.get("SQ_INSTS_VALU_MFMA_BF16")
+        va = r.get("SQ_INSTS_VALU")
+        lds = r.get("SQ_INSTS_LDS")
+        bc = r.get("SQ_LDS_BANK_CONFLICT")
+        cell = lambda v: "-" if v is None else v
+        b = f"{100 * busy / (g * 256 * 4):.1f}" if busy is not None and g else "-"
+        vpm = f"{(va - mf) / mf:.1f}" if va is not None and mf else "-"
+        lpm = f"{lds / mf:.2f}" if lds is not None and mf else "-"
+        bpl = f"{bc / lds:.3f}" if bc is not None and lds else "-"
+        k = r["kernel"]
+        k = k[k.find("qconv"):][:60] if "qconv" in k else k[:60]
+        t = f"{us:.1f}" if us is not None else "-"
+        c = f"{ghz:.2f}" if ghz is not None else "-"
+        lines.append(f"| {wl} | {cell(layer)} | {f} | `{k}` | {t} | {c} | {b} | {vpm} | {lpm} | {bpl} |")
+    lines += ["", f"sources: {sources_digest()}"]
+    print("\n".join(lines))
+
+
 def copy_calibration(nbytes):
     import torch
     dev = torch.device("cuda:0")
@@ -507,6 +632,9 @@ def main():
     if args.traffic_summary:
         traffic_summary(*args.traffic_summary, cal_bytes=int(os.environ.get("QL_COPY_BYTES", 1 << 30)))
         return
+    if args.counter_summary:
+        counter_summary(args.counter_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
                           "n_gpus": args.gpus}))
@@ -524,7 +652,8 @@ def main():
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     if args.leg:
-        legs = {"depthwise": depthwise, "epilogue": epilogue_cost, "neuron_types": neuron_types}
+        legs = {"depthwise": depthwise, "epilogue": epilogue_cost, "neuron_types": neuron_types,
+                "kernels": kernel_leg, "resnet20": resnet20_step_leg}
         print(json.dumps({args.leg: legs[args.leg](ql, torch, dev, stream)}), flush=True)
         return
 
@@ -661,7 +790,130 @@ def extra_workloads(ql, torch, dev, stream, reps=10):
     out["neuron_types"] = neuron_types(ql, torch, dev, stream, reps)
     out["depthwise"] = depthwise(ql, torch, dev, stream, reps)
     out["epilogue"] = epilogue_cost(ql, torch, dev, stream, reps)
+    out["resnet20"] = resnet20_step_leg(ql, torch, dev, stream, reps)
     out["hybrid_bp_memory"] = hybrid_bp_memory(torch, dev)
+    return out
+
+
+def resnet20_step_leg(ql, torch, dev, stream, reps=10, drift=True):
+    """The CIFAR ResNet-20 training step (batch 256, 3x32x32; section 4.2 model
+    construction; paper_2204_01701_amd/resnet.py) in fp32 and bf16: forward to
+    the logits and backward to every weight gradient, all in the library's
+    kernels.  Per precision: the step time hot (steps back to back) and cold
+    (a 512 MB buffer written before each step, so that the MALL holds none of
+    the step's tensors; the write is outside the timed interval), the share of
+    the 19 quadratic layers' calls (each call timed on its own, summed), the
+    algorithmic TFLOP/s of the step (the 19 layers' 9U) against the precision's
+    dense MFMA peak, the quadratic layers' algorithmic GB/s, and the end-to-end
+    drift of the logits and weight gradients from the fp64 network oracle."""
+    import numpy as np
+    import synth
+    from paper_2204_01701_amd.resnet import ResNet20Step
+
+    geoms = synth.resnet20_layers(256)
+    flops = sum(9 * unit_flops(L) for L in geoms)
+
+    def qbytes(L, esize):
+        X = L.n * L.h * L.w * L.c
+        P = L.n * L.ho * L.wo * L.o
+        W = L.o * L.c * L.k * L.k
+        return esize * ((X + 3 * W + 3 * P) + (3 * P + 3 * W + X) + (X + 3 * P)) + 4 * (3 * W + 3 * L.o)
+
+    out = {"shape": "CIFAR ResNet-20, batch 256, 3x32x32, 19 quadratic 3x3 convs + BN/ReLU/shortcuts + GAP + "
+                    "quadratic FC 64->10", "gflop_per_step": round(flops / 1e9, 1)}
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    for name, dt, peak in (("fp32", torch.float32, 157.3), ("bf16", torch.bfloat16, BF16_PEAK_TFLOPS)):
+        params, x, g = synth.resnet20_network(256, bf16=dt == torch.bfloat16)
+        net = ResNet20Step(params, x, g, dtype=dt, device=dev)
+        for _ in range(3):
+            net.step(stream)
+        torch.cuda.synchronize()
+        a, b = DevEvent(), DevEvent()
+        a.record(stream)
+        for _ in range(reps):
+            net.step(stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        hot = a.elapsed_time(b) / reps
+        # the step as one HIP graph (about 130 launches; from Python each launch
+        # costs more host time than most of these kernels take on the GPU)
+        net.capture()
+        with torch.cuda.stream(stream):
+            for _ in range(3):
+                net.replay()
+            torch.cuda.synchronize()
+            a, b = DevEvent(), DevEvent()
+            a.record(stream)
+            for _ in range(reps):
+                net.replay()
+            b.record(stream)
+            torch.cuda.synchronize()
+            graph_hot = a.elapsed_time(b) / reps
+            colds = []
+            for _ in range(reps):
+                flush.fill_(1)
+                a, b = DevEvent(), DevEvent()
+                a.record(stream)
+                net.replay()
+                b.record(stream)
+                torch.cuda.synchronize()
+                colds.append(a.elapsed_time(b))
+        cold = sorted(colds)[len(colds) // 2]
+        each = time_each(torch, net.qconv_calls(), reps, stream)
+        qshare = sum(each.values()) / graph_hot
+        esize = 2 if dt == torch.bfloat16 else 4
+        r = {"step_ms_hot": round(graph_hot, 4), "step_ms_cold": round(cold, 4), "step_ms_eager": round(hot, 4),
+             "tflops_hot": round(flops / (graph_hot * 1e-3) / 1e12, 1), "peak_tflops": peak,
+             "pct_of_peak_hot": round(100 * flops / (graph_hot * 1e-3) / 1e12 / peak, 2),
+             "quadratic_layer_share": round(qshare, 3),
+             "quadratic_layers_gbs": round(sum(qbytes(L, esize) for L in geoms) / (sum(each.values()) * 1e-3) / 1e9, 1)}
+        if drift:
+            import oracle
+            from oracle import network as onet
+            f64 = {k: {n: np.asarray(v, np.float64) for n, v in p.items()} for k, p in params.items()}
+            logits, grads, _ = onet.resnet20_step(
+                f64, np.asarray(x, np.float64), np.asarray(g, np.float64), geoms,
+                lambda xx, p, s_, pd: oracle.conv2d_fwd(xx, p["wa"], p["wb"], p["wc"], p["ba"], p["bb"], p["bc"],
+                                                        s_, pd),
+                lambda xx, p, gy, s_, pd: oracle.conv2d_bwd(xx, p["wa"], p["wb"], p["wc"], p["ba"], p["bb"],
+                                                            p["bc"], gy, s_, pd),
+                oracle.linear_fwd, oracle.linear_bwd)
+
+            def rel(a_, b_):
+                return float(np.linalg.norm(a_ - b_) / np.linalg.norm(b_))
+            errs = [rel(net.layers[i]["dw"][t].permute(0, 3, 1, 2).double().cpu().numpy(), grads[i][k])
+                    for i in range(len(geoms)) for t, k in enumerate(("dwa", "dwb", "dwc"))]
+            r["drift_logits"] = round(rel(net.logits.double().cpu().numpy(), logits), 6)
+            r["drift_weight_grad_median"] = round(float(np.median(errs)), 6)
+            r["drift_weight_grad_max"] = round(float(np.max(errs)), 6)
+        out[name] = r
+        del net
+    del flush
+    # the small fp32 layer (N=2, 16 -> 16, 8x8): microseconds per call of each pass,
+    # `reps` calls recorded as one HIP graph and replayed (a call from Python costs
+    # more host time than this layer's kernels take on the GPU)
+    L = synth.SMALL_FP32
+    ly = Layer(ql, torch, L, 1, 0, dev, bf16=False)
+    ly.fwd(stream)
+    torch.cuda.synchronize()
+    res = {}
+    for f in ("fwd", "bwd_data", "bwd_weight"):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            cur = torch.cuda.current_stream(dev)
+            for _ in range(reps):
+                getattr(ly, f)(cur)
+        with torch.cuda.stream(stream):
+            g.replay()
+            torch.cuda.synchronize()
+            a, b = DevEvent(), DevEvent()
+            a.record(stream)
+            for _ in range(5):
+                g.replay()
+            b.record(stream)
+            torch.cuda.synchronize()
+        res[f] = round(a.elapsed_time(b) / (5 * reps) * 1e3, 2)
+    out["small_fp32_layer_us"] = res
     return out
 
 

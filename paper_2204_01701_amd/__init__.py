@@ -67,6 +67,17 @@ class LinearDesc(ctypes.Structure):
                 ("neuron", ctypes.c_int)]
 
 
+class NetShape(ctypes.Structure):
+    """qnet_shape: an NHWC tensor shape."""
+    _fields_ = [(n, ctypes.c_int) for n in ("n", "h", "w", "c")]
+
+
+def net_shape(t_or_dims) -> NetShape:
+    """NetShape of an (N, H, W, C) tensor or tuple."""
+    n, h, w, c = tuple(t_or_dims.shape) if hasattr(t_or_dims, "shape") else tuple(t_or_dims)
+    return NetShape(n, h, w, c)
+
+
 class Epilogue(ctypes.Structure):
     """ql_epilogue: y' = relu(scale * Y + shift) per output channel, and the
     per-channel sum / sum of squares of the stored y' (every member optional)."""
@@ -133,6 +144,18 @@ def lib():
         getattr(L, f"qlayer_{name}").restype = ctypes.c_int
     for name in ("conv2d_fwd", "conv2d_bwd_data", "conv2d_bwd_weight", "linear_fwd", "linear_bwd"):
         getattr(L, f"qlayer_{name}").restype = ctypes.c_int
+    # the network glue (include/qnet.h)
+    sp = ctypes.POINTER(NetShape)
+    L.qnet_bn_act_fwd.argtypes = [sp, ctypes.c_int, _vp, _vp, _vp, ctypes.c_float, _vp, sp, ctypes.c_int, _vp, _vp,
+                                  _vp, _vp]
+    L.qnet_bn_act_bwd_workspace_size.argtypes = [sp]
+    L.qnet_bn_act_bwd_workspace_size.restype = _sz
+    L.qnet_bn_act_bwd.argtypes = [sp, ctypes.c_int, _vp, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    L.qnet_residual_bwd.argtypes = [sp, ctypes.c_int, _vp, _vp, sp, _vp, _vp]
+    L.qnet_gap_fwd.argtypes = [sp, ctypes.c_int, _vp, _vp, _vp]
+    L.qnet_gap_bwd.argtypes = [sp, ctypes.c_int, _vp, _vp, _vp]
+    for name in ("bn_act_fwd", "bn_act_bwd", "residual_bwd", "gap_fwd", "gap_bwd"):
+        getattr(L, f"qnet_{name}").restype = ctypes.c_int
     _lib = L
     return L
 
@@ -407,3 +430,75 @@ def qlayer_linear_bwd(desc, x, gy, ta, tb, wa, wb, wc, dx=None, dwa=None, dwb=No
         ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc),
         _ptr(dx), _ptr(dwa), _ptr(dwb), _ptr(dwc), _ptr(dba), _ptr(dbb), _ptr(dbc),
         wp, wn, _stream(stream, dev)))
+
+
+# --- the network glue (include/qnet.h) ----------------------------------------
+
+def _net_dtype(t):
+    import torch
+    return QL_BF16 if t.dtype == torch.bfloat16 else QL_F32
+
+
+def _net_expect(name, t, shape, dtype, device):
+    _expect(name, t, int(shape[0]) * int(shape[1]) * int(shape[2]) * int(shape[3]) if len(shape) == 4
+            else int(shape[0]) * int(shape[1]), dtype, device)
+
+
+def qnet_bn_act_fwd(y, ssum, ssq, out, mean, rstd, eps=1e-5, res=None, relu=True, stream=None):
+    """out = relu((y - mean) rstd + shortcut(res)); y, out, res NHWC device tensors."""
+    import torch
+    dev = y.device
+    s = net_shape(y)
+    dt = _net_dtype(y)
+    _net_expect("out", out, y.shape, y.dtype, dev)
+    for n, t in (("sum", ssum), ("sumsq", ssq), ("mean", mean), ("rstd", rstd)):
+        _expect(n, t, s.c, torch.float32, dev)
+    rs = net_shape(res) if res is not None else None
+    if res is not None:
+        _expect("res", res, rs.n * rs.h * rs.w * rs.c, y.dtype, dev)
+    _check("qnet_bn_act_fwd", lib().qnet_bn_act_fwd(
+        ctypes.byref(s), dt, _ptr(y), _ptr(ssum), _ptr(ssq), ctypes.c_float(eps), _ptr(res),
+        ctypes.byref(rs) if rs is not None else None, int(bool(relu)), _ptr(out), _ptr(mean), _ptr(rstd),
+        _stream(stream, dev)))
+
+
+def qnet_bn_act_bwd_workspace_size(shape) -> int:
+    return lib().qnet_bn_act_bwd_workspace_size(ctypes.byref(net_shape(shape)))
+
+
+def qnet_bn_act_bwd(dout, out, y, mean, rstd, dy, relu=True, workspace=None, stream=None):
+    """dy = the gradient at y of out = relu(bn(y) [+ r]) given dout."""
+    import torch
+    dev = y.device
+    s = net_shape(y)
+    for n, t in (("dout", dout), ("out", out), ("dy", dy)):
+        _net_expect(n, t, y.shape, y.dtype, dev)
+    for n, t in (("mean", mean), ("rstd", rstd)):
+        _expect(n, t, s.c, torch.float32, dev)
+    wp, wn = _workspace(workspace, qnet_bn_act_bwd_workspace_size(y.shape), dev, stream)
+    _check("qnet_bn_act_bwd", lib().qnet_bn_act_bwd(
+        ctypes.byref(s), _net_dtype(y), _ptr(dout), _ptr(out), int(bool(relu)), _ptr(y), _ptr(mean), _ptr(rstd),
+        _ptr(dy), wp, wn, _stream(stream, dev)))
+
+
+def qnet_residual_bwd(dout, out, dx, stream=None):
+    """dx (the block input's gradient) += the shortcut's share of dout [out > 0]."""
+    dev = dx.device
+    _net_expect("out", out, dout.shape, dout.dtype, dev)
+    _check("qnet_residual_bwd", lib().qnet_residual_bwd(
+        ctypes.byref(net_shape(dout)), _net_dtype(dout), _ptr(dout), _ptr(out), ctypes.byref(net_shape(dx)),
+        _ptr(dx), _stream(stream, dev)))
+
+
+def qnet_gap_fwd(x, y, stream=None):
+    dev = x.device
+    _expect("y", y, x.shape[0] * x.shape[3], x.dtype, dev)
+    _check("qnet_gap_fwd", lib().qnet_gap_fwd(ctypes.byref(net_shape(x)), _net_dtype(x), _ptr(x), _ptr(y),
+                                              _stream(stream, dev)))
+
+
+def qnet_gap_bwd(dy, dx, stream=None):
+    dev = dx.device
+    _expect("dy", dy, dx.shape[0] * dx.shape[3], dx.dtype, dev)
+    _check("qnet_gap_bwd", lib().qnet_gap_bwd(ctypes.byref(net_shape(dx)), _net_dtype(dx), _ptr(dy), _ptr(dx),
+                                              _stream(stream, dev)))

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libqlayer.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 SOURCES = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC)) if f.endswith(".hip")]
-HEADERS = [os.path.join(ROOT, "include", "qlayer.h")] + [
+HEADERS = [os.path.join(ROOT, "include", f) for f in ("qlayer.h", "qnet.h")] + [
     os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC)) if f.endswith(".h")
 ]
 

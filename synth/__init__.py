@@ -164,6 +164,29 @@ def resnet20_layers(batch: int = 256):
     return layers
 
 
+def resnet20_network(batch: int = 256, bf16: bool = False, cfg_id: int = 3, num_classes: int = 10):
+    """Inputs of the whole ResNet-20 training step: per conv layer i the weights
+    and biases conv_inputs(cfg_id, i, ...) draws (He-scaled, biases N(0, 0.01)),
+    the classifier's (64 -> num_classes: W ~ N(0, 1/64), b ~ N(0, 0.01); seeds
+    [cfg_id, 19, *]), the images X ~ N(0, 1) (N, 3, 32, 32) and the gradient of
+    the logits G ~ N(0, 1) (N, num_classes) (seeds [cfg_id, 20, *]).
+    Returns (params, x, g_logits)."""
+    layers = resnet20_layers(batch)
+    params = {}
+    for i, L in enumerate(layers):
+        inp = conv_inputs(cfg_id, i, L, bf16=bf16, with_grad=False)
+        params[i] = {k: inp[k] for k in ("wa", "wb", "wc", "ba", "bb", "bc")}
+    c_last = layers[-1].o
+    head = DenseLayer(batch=batch, inp=c_last, out=num_classes, w_var=1.0 / c_last, b_var=0.01)
+    d = dense_inputs(cfg_id, len(layers), head, bf16=bf16, with_grad=False)
+    params["head"] = {k: d[k] for k in ("wa", "wb", "wc", "ba", "bb", "bc")}
+    x = _normal([cfg_id, len(layers) + 1, X_ID], (batch, 3, 32, 32), 1.0)
+    g = _normal([cfg_id, len(layers) + 1, G_ID], (batch, num_classes), 1.0)
+    if bf16:
+        x, g = round_bf16(x), round_bf16(g)
+    return params, x, g
+
+
 def mobilenet_v1_pairs(batch: int = 128):
     """The 13 depthwise / pointwise pairs of a CIFAR MobileNet-V1 (a 3->32 stem at
     32x32, then blocks of a 3x3 depthwise layer, stride 1 or 2, and a 1x1

@@ -18,6 +18,7 @@ from paper_2204_01701_amd import build as qbuild
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "qlayer.h")
+NET_HEADER = os.path.join(ROOT, "include", "qnet.h")
 
 QL_OK, QL_EINVAL, QL_EUNSUPPORTED, QL_EWORKSPACE, QL_EHIP = range(5)
 
@@ -30,9 +31,9 @@ def L():
 
 
 def _declared_functions():
-    txt = open(HEADER).read()
+    txt = open(HEADER).read() + open(NET_HEADER).read()
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
-    return sorted(set(re.findall(r"\b(qlayer_\w+)\s*\(", txt)))
+    return sorted(set(re.findall(r"\b((?:qlayer|qnet)_\w+)\s*\(", txt)))
 
 
 def test_header_declares_the_five_entry_points():
@@ -45,7 +46,7 @@ def test_header_declares_the_five_entry_points():
 def test_library_exports_every_declared_symbol(L):
     out = subprocess.run(["nm", "-D", "--defined-only", ql.LIB_PATH], capture_output=True, text=True,
                          check=True).stdout
-    exported = set(re.findall(r"\bT (qlayer_\w+)", out))
+    exported = set(re.findall(r"\bT ((?:qlayer|qnet)_\w+)", out))
     missing = [f for f in _declared_functions() if f not in exported]
     assert not missing, missing
     for f in _declared_functions():
