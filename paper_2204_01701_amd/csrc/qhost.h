@@ -35,6 +35,13 @@ constexpr size_t kMaxSplitBytes = 128ull << 20;  // cap on split-K partial sums 
 constexpr double kSharedRound = 1.25;
 constexpr double kBytesPerStep = 3.2e6;
 constexpr double kReduceSteps = 6.0;  // the reduction kernel's launch and ramp
+// A workgroup of two pipelines (one per CU) on the two halves of its K range:
+// the cost of a K step of each pipeline, in the units above.  The two
+// pipelines share the workgroup's barriers, which costs them some of the
+// latency hiding of two independent workgroups (measured on the VGG-16
+// weight gradients: 1.5 reproduces which of the two kernels is faster on
+// every layer).
+constexpr double kPipeRound = 1.5;
 
 // Tuning override: QLAYER_<NAME>=<int> replaces a planner choice (for sweeps).
 inline int env_override(const char *name, int dflt) {
@@ -107,9 +114,8 @@ inline ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
 // workgroup in the last round costs a whole shared round, which the search
 // avoids.  At least min_stages K steps per split, at most kMaxSplitBytes of
 // partial sums (bytes_per_split each).
-inline void plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int slots, int &splits,
-                 int &sps,
-                        size_t max_bytes = kMaxSplitBytes) {
+inline double plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int slots, int &splits,
+                          int &sps, size_t max_bytes = kMaxSplitBytes, int pipes = 1) {
     const int cap_bytes = (int)std::max<size_t>(1, max_bytes / std::max<size_t>(bytes_per_split, 1));
     const int s_max = std::max(1, std::min(stages_total / std::max(min_stages, 1), cap_bytes));
     double best = 0.0;
@@ -124,6 +130,7 @@ inline void plan_splits(int tiles, int stages_total, int min_stages, size_t byte
         double rounds = (double)full * (slots > 1 ? kSharedRound : 1.0);
         if (rest > 0) rounds += rest > kNumCUs ? kSharedRound : 1.0;
         double t = per * rounds;
+        if (pipes > 1) t = (double)cdiv(per, pipes) * (double)(full + (rest > 0)) * kPipeRound;
         if (eff > 1) t += (double)eff * bytes_per_split * 2.0 / kBytesPerStep + kReduceSteps;
         if (s == 1 || t < best) {
             best = t;
@@ -132,6 +139,7 @@ inline void plan_splits(int tiles, int stages_total, int min_stages, size_t byte
     }
     sps = cdiv(stages_total, splits);
     splits = cdiv(stages_total, sps);
+    return best;
 }
 
 // Taps (r, q) in bounds for output position pos = (oh, ow): a bit mask.
@@ -341,10 +349,13 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
 // ---------------------------------------------------------------------------
 // Pipelined (bf16) weight-gradient tile configurations (rows = k', columns =
 // output channels per term):  0: 128 x 64, 1: 128 x 128, 2: 64 x 64.
-constexpr int kBwCfgs = 3;
-constexpr int kBwBKP[kBwCfgs] = {128, 128, 64};
-constexpr int kBwBO[kBwCfgs] = {64, 128, 64};
-constexpr int kBwSlots[kBwCfgs] = {2, 1, 2};  // workgroups one CU holds at once
+// (3: the 128 x 64 tile of the 16 x 16 x 32 kernel, qconv_bwd_weight16.h;
+// 4: the same with two pipelines per 8-wave workgroup)
+constexpr int kBwCfgs = 5;
+constexpr int kBwBKP[kBwCfgs] = {128, 128, 64, 128, 128};
+constexpr int kBwBO[kBwCfgs] = {64, 128, 64, 64, 64};
+constexpr int kBwSlots[kBwCfgs] = {2, 1, 2, 2, 1};  // workgroups one CU holds at once
+constexpr int kBwThreads[kBwCfgs] = {256, 256, 256, 256, 512};
 
 struct BwdWeightPlan {
     int cfg;   // pipelined path only
@@ -367,23 +378,32 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMa
     p.veck = p.Cp % g.vec() == 0 && g.O % g.vec() == 0;
     p.pipe = p.veck && g.dt == QL_BF16;
     if (p.pad) p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
-    if (p.pipe) {
-        p.cfg = env_override("QLAYER_BWD_WEIGHT_CFG", 0);
-        if (p.cfg < 0 || p.cfg >= kBwCfgs || g.ne != NEURON_QUADRA) p.cfg = 0;  // (the other types: tile 0)
-        p.BKP = kBwBKP[p.cfg];
-        p.BO = kBwBO[p.cfg];
-        p.slots = kBwSlots[p.cfg];
-    } else {
-        p.BKP = 128;
-        p.BO = 64;
-        p.slots = 1;
-    }
     p.KE = 64 / (int)g.esize();
-    p.row_tiles = cdiv(KP, p.BKP);
-    p.col_tiles = cdiv(g.O, p.BO);
     p.stages_total = cdiv(M, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16),
-                (size_t)3 * g.O * KPO * 4, p.slots, p.splits, p.sps, max_split_bytes);
+    const int min_stages = env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16);
+    const size_t bytes_per_split = (size_t)3 * g.O * KPO * 4;
+    auto fill = [&](int cfg) {
+        p.cfg = cfg;
+        p.BKP = p.pipe ? kBwBKP[cfg] : 128;
+        p.BO = p.pipe ? kBwBO[cfg] : 64;
+        p.slots = p.pipe ? kBwSlots[cfg] : 1;
+        p.row_tiles = cdiv(KP, p.BKP);
+        p.col_tiles = cdiv(g.O, p.BO);
+        return plan_splits(p.row_tiles * p.col_tiles, p.stages_total, min_stages, bytes_per_split, p.slots, p.splits,
+                           p.sps, max_split_bytes, kBwThreads[cfg] / 256);
+    };
+    if (p.pipe && g.ne == NEURON_QUADRA) {
+        // the 16 x 16 x 32 kernel, one pipeline per workgroup or two, whichever the model finds faster
+        const int forced = env_override("QLAYER_BWD_WEIGHT_CFG", -1);
+        if (forced >= 0 && forced < kBwCfgs) {
+            fill(forced);
+        } else {
+            const double t3 = fill(3), t4 = fill(4);  // (declarators initialise in order)
+            if (!(t4 < t3)) fill(3);
+        }
+    } else {
+        fill(0);  // the other neuron types and fp32: the 128 x 64 tile
+    }
     if (p.splits > 1) {
         p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KPO * sizeof(float));
         p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));

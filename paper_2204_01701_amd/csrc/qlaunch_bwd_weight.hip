@@ -1,6 +1,7 @@
 // qlaunch_bwd_weight.hip -- launches of the weight-gradient kernels (pipelined, generic, split reduction).
 #include "qhost.h"
 #include "qconv_bwd_weight.h"
+#include "qconv_bwd_weight16.h"
 #include "qconv_generic.h"
 
 namespace ql {
@@ -104,6 +105,10 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
             switch (p.cfg) {
                 case 0: hipLaunchKernelGGL((qconv_bwd_weight_kernel<128, 64, 2, 2, 4>), grid, block, 0, st, a); break;
                 case 1: hipLaunchKernelGGL((qconv_bwd_weight_kernel<128, 128, 2, 2, 4>), grid, block, 0, st, a); break;
+                case 3: hipLaunchKernelGGL((qconv_bwd_weight16_kernel<128, 4>), grid, block, 0, st, a); break;
+                case 4:
+                    hipLaunchKernelGGL((qconv_bwd_weight16_kernel<128, 4, 2>), grid, dim3(kBwThreads[4]), 0, st, a);
+                    break;
                 default: hipLaunchKernelGGL((qconv_bwd_weight_kernel<64, 64, 2, 2, 4>), grid, block, 0, st, a); break;
             }
         }
