@@ -350,10 +350,11 @@ _KERNEL_FAMILY = [
     (r"qconv_sum_splits_kernel<", "bwd_data", False),
     (r"qconv_weight_transpose_kernel<", "bwd_data", False),
     (r"qconv_bwd_weight_kernel<", "bwd_weight", True),
+    (r"qconv_bwd_weight16_kernel<", "bwd_weight", True),
     (r"qconv_bwd_weight_generic_kernel<", "bwd_weight", True),
     (r"qconv_bwd_weight_reduce_kernel<", "bwd_weight", False),
     (r"qconv_bwd_weight_reduce2d_kernel<", "bwd_weight", False),
-    (r"qconv_bwd_weight_reduce2dv_kernel\(", "bwd_weight", False),
+    (r"qconv_bwd_weight_reduce2dv_kernel[<(]", "bwd_weight", False),
     (r"qconv_pad_channels_kernel<[^,>]+, 1>", "bwd_weight", False),
 ]
 
@@ -552,11 +553,16 @@ def counter_summary(paths):
     """Markdown table of the 'kernels' leg's counters: per pass (averaged over its
     calls, main kernel only): the kernel duration and the shader clock it ran at
     (GRBM_GUI_ACTIVE, which reads the sum over the 8 XCDs, / 8 / duration); MFMA
-    busy = SQ_VALU_MFMA_BUSY_CYCLES (32 per 32x32x16 bf16 MFMA, summed over the
-    SIMDs) / (GRBM_GUI_ACTIVE / 8 x 256 CUs x 4 SIMDs), the fraction of the MFMA
-    peak at the clock the kernel ran at; non-MFMA VALU instructions per MFMA
-    instruction; LDS instructions per MFMA; LDS bank-conflict cycles per LDS
-    instruction."""
+    busy = SQ_VALU_MFMA_BUSY_CYCLES (32 per 32x32x16 bf16 MFMA, 16 per 16x16x32,
+    summed over the SIMDs) / (GRBM_GUI_ACTIVE / 8 x 256 CUs x 4 SIMDs), the
+    fraction of the MFMA peak at the clock the kernel ran at (GRBM_GUI_ACTIVE also
+    counts the dispatch's own overhead outside the kernel's timestamps, which on
+    kernels of a few tens of microseconds reads as a clock above 2.4 GHz and a
+    busy fraction too low); the same busy cycles over the kernel's duration at
+    the nominal 2.4 GHz, the fraction of the published peak; non-MFMA VALU
+    instructions per MFMA instruction, and per 32 MFMA busy cycles (the work of
+    one 32x32x16 bf16 MFMA, which compares kernels of either MFMA shape); LDS
+    instructions per MFMA; LDS bank-conflict cycles per LDS instruction."""
     import csv
     per = {}  # (file, dispatch id) -> {counter: value}; kernel names and durations
     names, durs = {}, {}
@@ -582,8 +588,9 @@ def counter_summary(paths):
             if "GRBM_GUI_ACTIVE" in per[d]:
                 rows[key]["dur_ns"].append(durs[d])
                 rows[key]["grbm"].append(per[d]["GRBM_GUI_ACTIVE"])
-    lines = ["| workload | layer | pass | main kernel | us (profiled) | clock GHz | MFMA busy % | VALU / MFMA | "
-             "LDS / MFMA | LDS bank conflict cycles / LDS instr |", "|---|---:|---|---|---:|---:|---:|---:|---:|---:|"]
+    lines = ["| workload | layer | pass | main kernel | us (profiled) | clock GHz | MFMA busy % | MFMA busy % at 2.4 GHz "
+             "| VALU / MFMA | VALU / 32 MFMA cycles | LDS / MFMA | LDS bank conflict cycles / LDS instr |",
+             "|---|---:|---|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
     nxcd = 8
     for (wl, layer, f), r in rows.items():
         g = r.get("GRBM_GUI_ACTIVE")
@@ -597,14 +604,16 @@ def counter_summary(paths):
         bc = r.get("SQ_LDS_BANK_CONFLICT")
         cell = lambda v: "-" if v is None else v
         b = f"{100 * busy / (g * 256 * 4):.1f}" if busy is not None and g else "-"
+        b24 = f"{100 * busy / (us * 1e3 * 2.4 * 256 * 4):.1f}" if busy is not None and us else "-"
         vpm = f"{(va - mf) / mf:.1f}" if va is not None and mf else "-"
+        vpc = f"{(va - mf) / (busy / 32):.1f}" if va is not None and mf and busy else "-"
         lpm = f"{lds / mf:.2f}" if lds is not None and mf else "-"
         bpl = f"{bc / lds:.3f}" if bc is not None and lds else "-"
         k = r["kernel"]
         k = k[k.find("qconv"):][:60] if "qconv" in k else k[:60]
         t = f"{us:.1f}" if us is not None else "-"
         c = f"{ghz:.2f}" if ghz is not None else "-"
-        lines.append(f"| {wl} | {cell(layer)} | {f} | `{k}` | {t} | {c} | {b} | {vpm} | {lpm} | {bpl} |")
+        lines.append(f"| {wl} | {cell(layer)} | {f} | `{k}` | {t} | {c} | {b} | {b24} | {vpm} | {vpc} | {lpm} | {bpl} |")
     lines += ["", f"sources: {sources_digest()}"]
     print("\n".join(lines))
 

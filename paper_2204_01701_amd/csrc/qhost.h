@@ -33,6 +33,9 @@ constexpr size_t kMaxSplitBytes = 128ull << 20;  // cap on split-K partial sums 
 // per step each (the second one hides the first one's latency), and one unit
 // of time moves about kBytesPerStep bytes of partial sums through HBM.
 constexpr double kSharedRound = 1.25;
+// ... for the forward kernels, whose second workgroup on a CU adds less (measured on
+// the 4 x 4 VGG-16 layers: two splits of 256 workgroups beat four of 512)
+constexpr double kSharedRoundFwd = 1.6;
 constexpr double kBytesPerStep = 3.2e6;
 constexpr double kReduceSteps = 6.0;  // the reduction kernel's launch and ramp
 // A workgroup of two pipelines (one per CU) on the two halves of its K range:
@@ -115,7 +118,8 @@ inline ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
 // avoids.  At least min_stages K steps per split, at most kMaxSplitBytes of
 // partial sums (bytes_per_split each).
 inline double plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int slots, int &splits,
-                          int &sps, size_t max_bytes = kMaxSplitBytes, int pipes = 1) {
+                          int &sps, size_t max_bytes = kMaxSplitBytes, int pipes = 1,
+                          double shared_round = kSharedRound) {
     const int cap_bytes = (int)std::max<size_t>(1, max_bytes / std::max<size_t>(bytes_per_split, 1));
     const int s_max = std::max(1, std::min(stages_total / std::max(min_stages, 1), cap_bytes));
     double best = 0.0;
@@ -127,8 +131,8 @@ inline double plan_splits(int tiles, int stages_total, int min_stages, size_t by
         const long long wgs = (long long)tiles * eff;
         const long long round = (long long)kNumCUs * std::max(slots, 1);
         const long long full = wgs / round, rest = wgs % round;
-        double rounds = (double)full * (slots > 1 ? kSharedRound : 1.0);
-        if (rest > 0) rounds += rest > kNumCUs ? kSharedRound : 1.0;
+        double rounds = (double)full * (slots > 1 ? shared_round : 1.0);
+        if (rest > 0) rounds += rest > kNumCUs ? shared_round : 1.0;
         double t = per * rounds;
         if (pipes > 1) t = (double)cdiv(per, pipes) * (double)(full + (rest > 0)) * kPipeRound;
         if (eff > 1) t += (double)eff * bytes_per_split * 2.0 / kBytesPerStep + kReduceSteps;
@@ -251,7 +255,8 @@ inline FwdPlan plan_fwd(const Geom &g) {
     p.pm = p.ca && pm_default(g, env_override("QLAYER_FWD_POSMAJ", -1));
     int kst = p.stages_total;
     if (p.pm) kst = pm_max_taps(g, p.BCOL, M) * (p.Cp / p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, kst, 4, (size_t)3 * M * g.O * 4, p.slots, p.splits, p.sps);
+    plan_splits(p.row_tiles * p.col_tiles, kst, env_override("QLAYER_FWD_MINSTAGES", 4), (size_t)3 * M * g.O * 4,
+                p.slots, p.splits, p.sps, kMaxSplitBytes, 1, kSharedRoundFwd);
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0;
     p.xsq_bytes = g.ne == NEURON_T2 && p.veck ? align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize()) : 0;
     p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes + p.part_bytes + p.xsq_bytes;
@@ -319,9 +324,11 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
     if (p.veck) {
         int dflt = 5;
         if (g.C > 64) dflt = M >= 1024 ? 3 : 2;
-        // (measured: faster for 1x1 layers such as the dense layer; for 3x3 layers the
-        // 4-wave tiles win, the wide kernel's 8 waves run their product arithmetic in step)
-        if (wide_ok && g.KH * g.KW == 1 && g.C >= 256 && M >= 1024) dflt = 4;
+        // (measured: faster where its 256 x 256 tiles fill the GPU at least twice, as on
+        // the dense layer and the N=64, 256-channel 56 x 56 layer; on the small maps of
+        // VGG-16 the 4-wave tiles win, the wide kernel's 8 waves run their product
+        // arithmetic in step)
+        if (wide_ok && g.C >= 256 && (long long)cdiv(g.C, 256) * cdiv(M, 256) >= 2 * kNumCUs) dflt = 4;
         p.cfg = env_override("QLAYER_BWD_DATA_CFG", dflt);
         if (p.cfg < 0 || p.cfg >= kBdCfgs || (p.cfg == 4 && !wide_ok)) p.cfg = 0;
         if (g.ne != NEURON_QUADRA) p.cfg = g.C > 64 ? 3 : 5;  // (the other types: tiles 3 and 5 only)
@@ -337,7 +344,8 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
     p.row_tiles = cdiv(g.C, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, 4, (size_t)M * g.C * 4, p.slots, p.splits, p.sps);
+    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_DATA_MINSTAGES", 4),
+                (size_t)M * g.C * 4, p.slots, p.splits, p.sps);
     p.wt_bytes = p.natw ? 0 : align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * M * g.C * sizeof(float)) : 0;
     p.ws_bytes = p.wt_bytes + p.part_bytes;
