@@ -812,7 +812,9 @@ def resnet20_step_leg(ql, torch, dev, stream, reps=10, drift=True):
     (a 512 MB buffer written before each step, so that the MALL holds none of
     the step's tensors; the write is outside the timed interval), the share of
     the 19 quadratic layers' calls (each call timed on its own, summed), the
-    algorithmic TFLOP/s of the step (the 19 layers' 9U) against the precision's
+    algorithmic TFLOP/s of the step (the 19 layers' 9U, less the 3U of the
+    stem's input gradient, which the step does not compute; the dense head's
+    and the glue's few flops are not counted) against the precision's
     dense MFMA peak, the quadratic layers' algorithmic GB/s, and the end-to-end
     drift of the logits and weight gradients from the fp64 network oracle."""
     import numpy as np
@@ -820,7 +822,8 @@ def resnet20_step_leg(ql, torch, dev, stream, reps=10, drift=True):
     from paper_2204_01701_amd.resnet import ResNet20Step
 
     geoms = synth.resnet20_layers(256)
-    flops = sum(9 * unit_flops(L) for L in geoms)
+    # every layer's three passes, except the stem's input gradient, which the step does not compute
+    flops = sum(9 * unit_flops(L) for L in geoms) - 3 * unit_flops(geoms[0])
 
     def qbytes(L, esize):
         X = L.n * L.h * L.w * L.c
