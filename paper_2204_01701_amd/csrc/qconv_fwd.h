@@ -452,6 +452,55 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
         else
             single(std::false_type{});
     } else {
+        // Split-K partials, staged like the outputs: each term's tile goes into
+        // the idle ring as BCOL pixel rows of BR fp32 values and out in 16-byte
+        // chunks, consecutive lanes on consecutive addresses (a wave writes four
+        // whole 256-byte rows of a 64-channel tile per instruction) instead of
+        // 32-byte pieces of 32 rows.
+        constexpr int PITCHF = BR * 4 + 16;
+        constexpr int MAPF = BCOL * PITCHF;
+        constexpr int PERF = 3 * MAPF <= NS * STAGE ? 3 : (2 * MAPF <= NS * STAGE ? 2 : 1);
+        constexpr int CPRF = BR / 4;  // 16-byte chunks per row
+        static_assert(NT % CPRF == 0, "staged partials tile");
+        if constexpr (MAPF <= NS * STAGE) {
+            if (a.O % 4 == 0) {
+#pragma unroll
+                for (int t0 = 0; t0 < NTM; t0 += PERF) {
+                    lds_barrier();  // every wave is done with the ring (or the previous round's copy)
+#pragma unroll
+                    for (int t = t0; t < t0 + PERF && t < NTM; ++t) {
+                        char *tile = smem + (t - t0) * MAPF;
+#pragma unroll
+                        for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+                            for (int mc = 0; mc < MC; ++mc) {
+                                const int pl = wc * (BCOL / WGC) + mc * 32 + lrow;
+#pragma unroll
+                                for (int g = 0; g < 4; ++g) {
+                                    const int ol = wr * (BR / WGR) + mr * 32 + 8 * g + 4 * lhi;
+                                    store4<float>(reinterpret_cast<float *>(tile + pl * PITCHF + ol * 4),
+                                                  acc[t][mr][mc][4 * g], acc[t][mr][mc][4 * g + 1],
+                                                  acc[t][mr][mc][4 * g + 2], acc[t][mr][mc][4 * g + 3]);
+                                }
+                            }
+                    }
+                    lds_barrier();
+#pragma unroll
+                    for (int t = t0; t < t0 + PERF && t < NTM; ++t) {
+                        const char *tile = smem + (t - t0) * MAPF;
+                        float *__restrict__ ws = a.ws + ((size_t)split * 3 + t) * (size_t)a.M * a.O;
+                        for (int c = tid; c < BCOL * CPRF; c += NT) {
+                            const int row = c / CPRF, cc = c % CPRF;
+                            const int m = ct * BCOL + row, o = rt * BR + cc * 4;
+                            if (m < a.M && o < a.O)
+                                *reinterpret_cast<v4u *>(ws + (size_t)prow(m) * a.O + o) =
+                                    lds_read16(tile + row * PITCHF + cc * 16);
+                        }
+                    }
+                }
+                return;
+            }
+        }
 #pragma unroll
         for (int t = 0; t < NTM; ++t) {
             float *__restrict__ ws = a.ws + ((size_t)split * 3 + t) * (size_t)a.M * a.O;
