@@ -311,6 +311,43 @@ ql_status qlayer_linear_fwd_ex(const ql_linear_desc *desc, const void *x,
                                void *y, void *ta, void *tb, const ql_epilogue *epi,
                                void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Backward behind the fused ReLU -- section 4.2, model construction (a ReLU
+ * after each quadratic layer) and section 4.3 eq:SD: the layer's gradients
+ * when its forward ran the epilogue's ReLU, y' = relu(Y) (ql_epilogue.relu,
+ * no scale or shift).  With gy = dl/dy', G = dl/dY = gy o [y' > 0] (zero
+ * where y' <= 0 or is NaN), then dX, dW_t and db_t from G exactly as
+ * qlayer_conv2d_bwd_data / qlayer_conv2d_bwd_weight (qlayer_linear_bwd for
+ * the dense form) compute them, bitwise.  G goes once into the front of the
+ * workspace and feeds both gradients: one pass over gy and y', and no dl/dY
+ * tensor of the caller.
+ *   x       : the layer input (NHWC / (B,I)), required (T2, T2&4 and the
+ *             weight gradient read it).
+ *   gy, y_out : dl/dy' and the stored y', (N,Ho,Wo,O) / (B,O), required.
+ *   ta, tb  : the saved maps of the neuron type (as the regular backward).
+ *   wa, wb, wc : required when dx is requested.
+ *   dx      : or NULL to skip the input gradient.
+ *   dwa.. / dba.. : float32, all of the type's terms or none; db needs dW.
+ *   At least one of dx / dW must be requested.  Every pointer 16-byte
+ *   aligned.  Workspace: at least the query's bytes (which covers both
+ *   gradients); QL_EWORKSPACE if smaller or NULL.  Validation is complete
+ *   before the first launch.
+ * ------------------------------------------------------------------------- */
+size_t qlayer_conv2d_bwd_relu_workspace_size(const ql_conv_desc *desc);
+ql_status qlayer_conv2d_bwd_relu(const ql_conv_desc *desc, const void *x, const void *gy, const void *y_out,
+                                 const void *ta, const void *tb,
+                                 const void *wa, const void *wb, const void *wc, void *dx,
+                                 float *dwa, float *dwb, float *dwc,
+                                 float *dba, float *dbb, float *dbc,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+size_t qlayer_linear_bwd_relu_workspace_size(const ql_linear_desc *desc);
+ql_status qlayer_linear_bwd_relu(const ql_linear_desc *desc, const void *x, const void *gy, const void *y_out,
+                                 const void *ta, const void *tb,
+                                 const void *wa, const void *wb, const void *wc, void *dx,
+                                 float *dwa, float *dwb, float *dwc,
+                                 float *dba, float *dbb, float *dbc,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

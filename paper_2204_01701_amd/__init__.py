@@ -29,6 +29,8 @@ __all__ = [
     "NOALLOC_SCRATCH_BYTES",
     "qlayer_linear_fwd_workspace_size", "qlayer_linear_fwd",
     "qlayer_linear_bwd_workspace_size", "qlayer_linear_bwd",
+    "qlayer_conv2d_bwd_relu_workspace_size", "qlayer_conv2d_bwd_relu",
+    "qlayer_linear_bwd_relu_workspace_size", "qlayer_linear_bwd_relu",
 ]
 
 QL_F32 = 0
@@ -135,6 +137,12 @@ def lib():
     L.qlayer_conv2d_bwd_weight_noalloc.restype = ctypes.c_int
     L.qlayer_linear_fwd.argtypes = [ld] + [_vp] * 10 + [_vp, _sz, _vp]
     L.qlayer_linear_bwd.argtypes = [ld] + [_vp] * 14 + [_vp, _sz, _vp]
+    for name, d in (("conv2d_bwd_relu", cd), ("linear_bwd_relu", ld)):
+        f = getattr(L, f"qlayer_{name}_workspace_size")
+        f.argtypes = [d]
+        f.restype = _sz
+        getattr(L, f"qlayer_{name}").argtypes = [d] + [_vp] * 15 + [_vp, _sz, _vp]
+        getattr(L, f"qlayer_{name}").restype = ctypes.c_int
     ep = ctypes.POINTER(Epilogue)
     for name, d in (("conv2d_fwd_ex", cd), ("linear_fwd_ex", ld)):
         f = getattr(L, f"qlayer_{name}_workspace_size")
@@ -430,6 +438,40 @@ def qlayer_linear_bwd(desc, x, gy, ta, tb, wa, wb, wc, dx=None, dwa=None, dwb=No
         ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc),
         _ptr(dx), _ptr(dwa), _ptr(dwb), _ptr(dwc), _ptr(dba), _ptr(dbb), _ptr(dbc),
         wp, wn, _stream(stream, dev)))
+
+
+def _bwd_relu(name, sizes, wsize, desc, x, gy, y_out, ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc,
+              workspace, stream):
+    dev = _device(x, gy)
+    _check_args(sizes, desc.dtype, dev, act=[("x", x), ("dx", dx)], weights=[("wa", wa), ("wb", wb), ("wc", wc)],
+                maps=[("gy", gy), ("y_out", y_out), ("ta", ta), ("tb", tb)],
+                w32=[("dwa", dwa), ("dwb", dwb), ("dwc", dwc)], vec32=[("dba", dba), ("dbb", dbb), ("dbc", dbc)])
+    wp, wn = _workspace(workspace, wsize(desc), dev, stream)
+    _check(name, getattr(lib(), name)(
+        ctypes.byref(desc), _ptr(x), _ptr(gy), _ptr(y_out), _ptr(ta), _ptr(tb), _ptr(wa), _ptr(wb), _ptr(wc),
+        _ptr(dx), _ptr(dwa), _ptr(dwb), _ptr(dwc), _ptr(dba), _ptr(dbb), _ptr(dbc), wp, wn, _stream(stream, dev)))
+
+
+def qlayer_conv2d_bwd_relu_workspace_size(desc: ConvDesc) -> int:
+    return lib().qlayer_conv2d_bwd_relu_workspace_size(ctypes.byref(desc))
+
+
+def qlayer_conv2d_bwd_relu(desc, x, gy, y_out, ta, tb, wa, wb, wc, dx=None, dwa=None, dwb=None, dwc=None,
+                           dba=None, dbb=None, dbc=None, workspace=None, stream=None):
+    """The layer's backward behind the fused ReLU: G = gy o [y_out > 0], then dX and/or dW_t, db_t from G."""
+    _bwd_relu("qlayer_conv2d_bwd_relu", _conv_sizes(desc), qlayer_conv2d_bwd_relu_workspace_size, desc, x, gy, y_out,
+              ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc, workspace, stream)
+
+
+def qlayer_linear_bwd_relu_workspace_size(desc: LinearDesc) -> int:
+    return lib().qlayer_linear_bwd_relu_workspace_size(ctypes.byref(desc))
+
+
+def qlayer_linear_bwd_relu(desc, x, gy, y_out, ta, tb, wa, wb, wc, dx=None, dwa=None, dwb=None, dwc=None,
+                           dba=None, dbb=None, dbc=None, workspace=None, stream=None):
+    """The dense layer's backward behind the fused ReLU (as qlayer_conv2d_bwd_relu)."""
+    _bwd_relu("qlayer_linear_bwd_relu", _linear_sizes(desc), qlayer_linear_bwd_relu_workspace_size, desc, x, gy,
+              y_out, ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc, workspace, stream)
 
 
 # --- the network glue (include/qnet.h) ----------------------------------------

@@ -20,8 +20,9 @@ but X in either mode (its backward needs only X).
 
 ``relu=True`` applies the activation deeper networks put after each
 quadratic layer (section 4.2, model construction) in the forward kernel's
-epilogue; the backward masks the incoming gradient with y' > 0 before the
-layer's own gradients.  ``groups`` (convolution): 1, or C for the
+epilogue; the backward is one library call that masks the incoming gradient
+with y' > 0 and forms the layer's own gradients from it (no elementwise torch
+operation).  ``groups`` (convolution): 1, or C for the
 depth-wise setting (weights (C, 1, KH, KW)).
 
 Layouts.  Convolution tensors are NCHW-shaped torch tensors; they are used in
@@ -36,9 +37,9 @@ from __future__ import annotations
 import torch
 
 from . import (NEURON_TERMS, QL_BF16, QL_F32, QL_NEURON_QUADRA, QL_NEURON_T2, QL_NEURON_T24, conv_desc, epilogue,
-               linear_desc, qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_data_ex, qlayer_conv2d_bwd_weight,
-               qlayer_conv2d_fwd, qlayer_conv2d_fwd_ex,
-               qlayer_linear_bwd, qlayer_linear_fwd, qlayer_linear_fwd_ex)
+               linear_desc, qlayer_conv2d_bwd_data, qlayer_conv2d_bwd_data_ex, qlayer_conv2d_bwd_relu,
+               qlayer_conv2d_bwd_weight, qlayer_conv2d_fwd, qlayer_conv2d_fwd_ex,
+               qlayer_linear_bwd, qlayer_linear_bwd_relu, qlayer_linear_fwd, qlayer_linear_fwd_ex)
 
 __all__ = ["quad_conv2d", "quad_linear", "QuadConv2dFunction", "QuadLinearFunction"]
 
@@ -127,11 +128,22 @@ class QuadConv2dFunction(torch.autograd.Function):
             tb = torch.empty_like(ta) if nt >= 2 else None
             qlayer_conv2d_fwd(d, xn, *wn, *bl, None, ta, tb)
         gyn = _nhwc(gy.to(xn.dtype))
-        if relu_y is not None:
-            gyn = gyn * (relu_y > 0).to(gyn.dtype)
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
         dx = dw = db = None
+        if relu_y is not None and (need_x or need_w or need_b):
+            # the ReLU's mask and both gradients in one library call (G = gy o [y' > 0] formed once)
+            dxn = torch.empty_like(xn) if need_x else None
+            dwn = [torch.empty(wn[0].shape, device=xn.device, dtype=torch.float32) if i < nt else None
+                   for i in range(3)] if (need_w or need_b) else [None, None, None]
+            db = [torch.empty(d.o, device=xn.device, dtype=torch.float32) if i < nt else None
+                  for i in range(3)] if need_b else None
+            qlayer_conv2d_bwd_relu(d, xn, gyn, relu_y, None if ctx.neuron == QL_NEURON_T2 else ta, tb, *wn, dxn,
+                                   *dwn, *(db or [None, None, None]))
+            dx = dxn.permute(0, 3, 1, 2) if need_x else None
+            dw = [g.permute(0, 3, 1, 2).to(ctx.wdtype) if g is not None else None for g in dwn]
+            db = db or [None, None, None]
+            return (dx, *dw, *db, None, None, None, None, None, None)
         if need_x:
             dxn = torch.empty_like(xn)
             if ctx.neuron == QL_NEURON_T24:  # (the chain rule through X o X needs X)
@@ -194,16 +206,19 @@ class QuadLinearFunction(torch.autograd.Function):
             tb = torch.empty_like(ta) if nt >= 2 else None
             qlayer_linear_fwd(d, xc, *wl, *bl, None, ta, tb)
         gyc = gy.to(xc.dtype).contiguous()
-        if relu_y is not None:
-            gyc = gyc * (relu_y > 0).to(gyc.dtype)
         need_x, need_w = ctx.needs_input_grad[0], any(ctx.needs_input_grad[1:4])
         need_b = ctx.has_bias and any(ctx.needs_input_grad[4:7])
+        if not (need_x or need_w or need_b):
+            return (None,) * 10
         dx = torch.empty_like(xc) if need_x else None
         dw = [torch.empty(wl[0].shape, device=xc.device, dtype=torch.float32) if i < nt else None
               for i in range(3)] if (need_w or need_b) else None
         db = [torch.empty(d.out, device=xc.device, dtype=torch.float32) if i < nt else None
               for i in range(3)] if need_b else None
-        qlayer_linear_bwd(d, xc, gyc, ta, tb, *wl, dx, *(dw or [None] * 3), *(db or [None] * 3))
+        if relu_y is not None:  # the ReLU's mask and both gradients in one library call
+            qlayer_linear_bwd_relu(d, xc, gyc, relu_y, ta, tb, *wl, dx, *(dw or [None] * 3), *(db or [None] * 3))
+        else:
+            qlayer_linear_bwd(d, xc, gyc, ta, tb, *wl, dx, *(dw or [None] * 3), *(db or [None] * 3))
         dw = [g.to(ctx.wdtype) if g is not None else None for g in dw] if dw is not None else [None, None, None]
         db = db or [None, None, None]
         return (dx, *dw, *db, None, None, None)

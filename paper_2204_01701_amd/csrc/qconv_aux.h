@@ -302,6 +302,28 @@ __global__ __launch_bounds__(kThreads) void qconv_square_kernel(const T *__restr
         *reinterpret_cast<v4u *>(dst + i * VEC) = square_frag<T>(*reinterpret_cast<const v4u *>(src + i * VEC));
 }
 
+// The ReLU's backward in front of the layer's: out = g where y > 0, else 0
+// (y the stored activation y' = relu(Y), g = dl/dy'), so out = dl/dY.  16
+// bytes per thread and step, the tail of n past the last whole vector one
+// element per thread.  g, y, out 16-byte aligned.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void qconv_relu_mask_kernel(const T *__restrict__ g, const T *__restrict__ y,
+                                                                   T *__restrict__ out, long long n) {
+    constexpr int VEC = Elem<T>::VEC;
+    const long long nv = n / VEC;
+    const long long stride = (long long)gridDim.x * blockDim.x;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) {
+        const v4u gv = *reinterpret_cast<const v4u *>(g + i * VEC);
+        const v4u yv = *reinterpret_cast<const v4u *>(y + i * VEC);
+        float f[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) f[e] = vget<T>(yv, e) > 0.0f ? vget<T>(gv, e) : 0.0f;
+        *reinterpret_cast<v4u *>(out + i * VEC) = vpack<T>(f);
+    }
+    for (long long i = nv * VEC + (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        out[i] = to_f32(y[i]) > 0.0f ? g[i] : from_f32<T>(0.0f);
+}
+
 struct PadSegments {
     const void *src[4];
     void *dst[4];

@@ -236,6 +236,66 @@ ql_status bwd_weight_common(const Geom &g, const void *x, const void *gy, const 
     return run_bwd_weight(g, p, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, ws, st);
 }
 
+// The layer's backward behind its ReLU (the fused epilogue's activation): G =
+// gy o [y' > 0] into the front of the workspace, then the input gradient (dx
+// non-NULL) and the weight and bias gradients (dwa non-NULL) from it, as the
+// regular entry points compute them, in the rest.  Everything is validated
+// before the first launch.
+size_t bwd_relu_ws_bytes(const Geom &g, bool want_dx, bool want_dw) {
+    const size_t gbytes = align_up((size_t)g.N * g.HO * g.WO * g.O * g.esize());
+    size_t bd = 0, bw = 0;
+    if (want_dx && !g.dw) bd = plan_bwd_data(g).ws_bytes;
+    if (want_dw) bw = g.dw ? plan_dw(g, 2).ws_bytes : plan_bwd_weight(g).ws_bytes;
+    return gbytes + std::max(bd, bw);
+}
+
+ql_status bwd_relu_common(const Geom &g, const void *x, const void *gy, const void *y_out, const void *ta,
+                          const void *tb, const void *wa, const void *wb, const void *wc, void *dx, float *dwa,
+                          float *dwb, float *dwc, float *dba, float *dbb, float *dbc, void *ws, size_t ws_bytes,
+                          void *stream) {
+    const int nt = g.terms(), ngm = om_gmaps(g.om());
+    if (nt < 3) { wc = nullptr; dwc = nullptr; dbc = nullptr; }
+    if (nt < 2) { wb = nullptr; dwb = nullptr; dbb = nullptr; }
+    if (ngm < 3) tb = nullptr;
+    if (ngm < 2) ta = nullptr;  // (T2's input gradient takes X itself)
+    const int nw = (dwa != nullptr) + (dwb != nullptr) + (dwc != nullptr);
+    const int nb = (dba != nullptr) + (dbb != nullptr) + (dbc != nullptr);
+    if ((nw != 0 && nw != nt) || (nb != 0 && nb != nt) || (nb != 0 && nw == 0)) return QL_EINVAL;
+    if (!dx && nw == 0) return QL_EINVAL;
+    if (!x || !gy || !y_out || (ngm >= 2 && !ta) || (ngm >= 3 && !tb)) return QL_EINVAL;
+    if (dx && (!wa || (nt >= 2 && !wb) || (nt >= 3 && !wc))) return QL_EINVAL;
+    const void *ptrs[] = {x, gy, y_out, ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc};
+    for (const void *q : ptrs)
+        if (q && !aligned16(q)) return QL_EINVAL;
+    const size_t need = bwd_relu_ws_bytes(g, dx != nullptr, nw != 0);
+    if (ws_bytes < need || !ws) return QL_EWORKSPACE;
+    if (!aligned16(ws)) return QL_EINVAL;
+    const size_t gbytes = align_up((size_t)g.N * g.HO * g.WO * g.O * g.esize());
+    const long long n = (long long)g.N * g.HO * g.WO * g.O;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int vec = g.vec();
+    const int grid = grid_1d(std::max(1LL, n / vec));
+    if (g.dt == QL_BF16)
+        hipLaunchKernelGGL(qconv_relu_mask_kernel<uint16_t>, dim3(grid), dim3(kThreads), 0, st,
+                           static_cast<const uint16_t *>(gy), static_cast<const uint16_t *>(y_out),
+                           static_cast<uint16_t *>(ws), n);
+    else
+        hipLaunchKernelGGL(qconv_relu_mask_kernel<float>, dim3(grid), dim3(kThreads), 0, st,
+                           static_cast<const float *>(gy), static_cast<const float *>(y_out),
+                           static_cast<float *>(ws), n);
+    ql_status s = hip_status();
+    if (s != QL_OK) return s;
+    const void *gm = ws;
+    char *rest = static_cast<char *>(ws) + gbytes;
+    const size_t rest_bytes = ws_bytes - gbytes;
+    if (dx) {
+        s = bwd_data_common(g, gm, g.ne == NEURON_T2 ? x : ta, tb, x, wa, wb, wc, dx, rest, rest_bytes, stream);
+        if (s != QL_OK) return s;
+    }
+    if (nw) s = bwd_weight_common(g, x, gm, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, rest, rest_bytes, stream);
+    return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -403,6 +463,40 @@ ql_status qlayer_linear_bwd(const ql_linear_desc *desc, const void *x, const voi
     }
     if (nw) s = bwd_weight_common(g, x, gy, ta, tb, dwa, dwb, dwc, dba, dbb, dbc, workspace, workspace_bytes, stream);
     return s;
+}
+
+size_t qlayer_conv2d_bwd_relu_workspace_size(const ql_conv_desc *desc) {
+    Geom g;
+    if (make_geom(desc, g) != QL_OK) return 0;
+    return bwd_relu_ws_bytes(g, true, true);
+}
+
+ql_status qlayer_conv2d_bwd_relu(const ql_conv_desc *desc, const void *x, const void *gy, const void *y_out,
+                                 const void *ta, const void *tb, const void *wa, const void *wb, const void *wc,
+                                 void *dx, float *dwa, float *dwb, float *dwc, float *dba, float *dbb, float *dbc,
+                                 void *workspace, size_t workspace_bytes, void *stream) {
+    Geom g;
+    const ql_status s = make_geom(desc, g);
+    if (s != QL_OK) return s;
+    return bwd_relu_common(g, x, gy, y_out, ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc, workspace,
+                           workspace_bytes, stream);
+}
+
+size_t qlayer_linear_bwd_relu_workspace_size(const ql_linear_desc *desc) {
+    Geom g;
+    if (linear_geom(desc, g) != QL_OK) return 0;
+    return bwd_relu_ws_bytes(g, true, true);
+}
+
+ql_status qlayer_linear_bwd_relu(const ql_linear_desc *desc, const void *x, const void *gy, const void *y_out,
+                                 const void *ta, const void *tb, const void *wa, const void *wb, const void *wc,
+                                 void *dx, float *dwa, float *dwb, float *dwc, float *dba, float *dbb, float *dbc,
+                                 void *workspace, size_t workspace_bytes, void *stream) {
+    Geom g;
+    const ql_status s = linear_geom(desc, g);
+    if (s != QL_OK) return s;
+    return bwd_relu_common(g, x, gy, y_out, ta, tb, wa, wb, wc, dx, dwa, dwb, dwc, dba, dbb, dbc, workspace,
+                           workspace_bytes, stream);
 }
 
 }  // extern "C"

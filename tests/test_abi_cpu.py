@@ -338,3 +338,30 @@ def test_noalloc_weight_gradient_rejects_a_layer_beyond_its_scratch(L):
     assert L.qlayer_conv2d_bwd_weight_noalloc(ctypes.byref(d), *[FAKE] * 10, None) == QL_EWORKSPACE
     assert L.qlayer_conv2d_bwd_weight_noalloc(ctypes.byref(d), *[FAKE] * 4, None, *[FAKE] * 5,
                                               None) == QL_EINVAL                   # dW_a missing
+
+
+def test_relu_backward_validation(L):
+    """The backward behind the fused ReLU: y' required, at least one gradient,
+    a workspace of at least the query's size (which holds G before the larger
+    of the two passes' workspaces)."""
+    d = ql.conv_desc(2, 16, 8, 8, 16, 3, 3, 1, 1, ql.QL_BF16)
+    need = L.qlayer_conv2d_bwd_relu_workspace_size(ctypes.byref(d))
+    g_bytes = 2 * 8 * 8 * 16 * 2
+    assert need >= g_bytes and need % 256 == 0
+    assert need >= (g_bytes + 255) // 256 * 256 + max(L.qlayer_conv2d_bwd_data_workspace_size(ctypes.byref(d)),
+                                                      L.qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(d)))
+    full = [FAKE] * 9 + [FAKE] * 6   # x gy y' ta tb wa wb wc dx | dw x3, db x3
+    fn = L.qlayer_conv2d_bwd_relu
+    assert fn(ctypes.byref(d), *full, FAKE, need - 1, None) == QL_EWORKSPACE
+    assert fn(ctypes.byref(d), *full, None, need, None) == QL_EWORKSPACE
+    no_y = list(full)
+    no_y[2] = None
+    assert fn(ctypes.byref(d), *no_y, FAKE, need, None) == QL_EINVAL
+    none_wanted = full[:8] + [None] * 7
+    assert fn(ctypes.byref(d), *none_wanted, FAKE, need, None) == QL_EINVAL
+    db_without_dw = full[:9] + [None] * 3 + [FAKE] * 3
+    assert fn(ctypes.byref(d), *db_without_dw, FAKE, need, None) == QL_EINVAL
+    dl = ql.linear_desc(64, 32, 48, ql.QL_F32)
+    needl = L.qlayer_linear_bwd_relu_workspace_size(ctypes.byref(dl))
+    assert needl >= 64 * 48 * 4
+    assert L.qlayer_linear_bwd_relu(ctypes.byref(dl), *no_y, FAKE, needl, None) == QL_EINVAL
