@@ -22,6 +22,10 @@
 // the step's k' fragments 0-3 (set 0, with the G-side fragments) and 4-7
 // (set 1); the products are formed once per step, in the first half.
 //
+// BO = 128 puts eight waves side by side (one workgroup per CU, 160 KB of
+// LDS): each K step copies 32 KB for twice the MFMAs of a 64-channel tile's
+// 20 KB, so the same LDS holds more MFMA work in flight.
+//
 // KG = 2 runs two such 4-wave pipelines in one 8-wave workgroup (one per CU,
 // each pipeline with its own LDS ring), on the two halves of the
 // workgroup's K range, and adds their accumulators in LDS before the
@@ -88,11 +92,11 @@ __device__ __forceinline__ v4u w16_frag_bf16(const char *tile, int k0, int m0, i
     return out;
 }
 
-template <int BKP, int NS, int KG, bool SUM, bool LIN>
+template <int BKP, int NS, int KG, int BO, bool SUM, bool LIN>
 __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *smem_all) {
     using T = uint16_t;
-    constexpr int BO = 64;              // output channels per term (four waves of 16)
-    constexpr int NT = 256;             // threads of one pipeline
+    // BO: output channels per term of the tile, 16 per wave (four or eight waves)
+    constexpr int NT = BO * 4;          // threads of one pipeline
     constexpr int NTW = NT * KG;        // threads of the workgroup
     constexpr int KE = 32;              // output pixels per K step (one 16x16x32 k-chunk)
     constexpr int SX = BKP / 8;
@@ -110,9 +114,10 @@ __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *
     constexpr int MH = MR / 2;          // ... per half step (register set)
     static_assert(XB % (NT * 16) == 0 && GB % (NT * 16) == 0 && MR % 2 == 0, "tile shape");
     static_assert(KG == 1 || KG == 2, "one or two pipelines");
+    static_assert(BO == 64 || (BO == 128 && KG == 1), "four waves per pipeline, or eight in a single one");
 
     const int tid = threadIdx.x, lane = tid & 63;
-    const int grp = wave_id() >> 2, wave = wave_id() & 3;  // pipeline, wave within it
+    const int grp = KG == 1 ? 0 : wave_id() / NW, wave = KG == 1 ? wave_id() : wave_id() % NW;  // pipeline, wave in it
     char *const smem = smem_all + grp * (NS * STAGE);
     int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int tiles = a.row_tiles * a.col_tiles;
@@ -391,20 +396,20 @@ __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *
     }
 }
 
-template <int BKP, int NS, int KG = 1>
-__global__ __launch_bounds__(256 * KG) void qconv_bwd_weight16_kernel(const BwdWeightArgs a) {
-    constexpr int STAGE = 32 * BKP * 2 + 3 * 32 * 64 * 2;
+template <int BKP, int NS, int KG = 1, int BO = 64>
+__global__ __launch_bounds__(BO * 4 * KG) void qconv_bwd_weight16_kernel(const BwdWeightArgs a) {
+    constexpr int STAGE = 32 * BKP * 2 + 3 * 32 * BO * 2;
     __shared__ __attribute__((aligned(1024))) char smem[KG * NS * STAGE];
     int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int tiles = a.row_tiles * a.col_tiles;
     bid -= (bid / tiles) * tiles;
     const bool sum = a.want_db && bid % a.row_tiles == 0;
     if (a.lin) {
-        if (sum) bwd_weight16_body<BKP, NS, KG, true, true>(a, smem);
-        else bwd_weight16_body<BKP, NS, KG, false, true>(a, smem);
+        if (sum) bwd_weight16_body<BKP, NS, KG, BO, true, true>(a, smem);
+        else bwd_weight16_body<BKP, NS, KG, BO, false, true>(a, smem);
     } else {
-        if (sum) bwd_weight16_body<BKP, NS, KG, true, false>(a, smem);
-        else bwd_weight16_body<BKP, NS, KG, false, false>(a, smem);
+        if (sum) bwd_weight16_body<BKP, NS, KG, BO, true, false>(a, smem);
+        else bwd_weight16_body<BKP, NS, KG, BO, false, false>(a, smem);
     }
 }
 

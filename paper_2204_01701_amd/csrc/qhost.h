@@ -45,6 +45,10 @@ constexpr double kReduceSteps = 6.0;  // the reduction kernel's launch and ramp
 // weight gradients: 1.5 reproduces which of the two kernels is faster on
 // every layer).
 constexpr double kPipeRound = 1.5;
+// A K step of the 8-wave workgroup with the 128-channel tile (one per CU, twice
+// the MFMAs of a 64-channel step), in the same units (measured on the same
+// layers: 1.2 reproduces where it is the fastest of the three kernels).
+constexpr double kFatStep = 1.2;
 
 // Tuning override: QLAYER_<NAME>=<int> replaces a planner choice (for sweeps).
 inline int env_override(const char *name, int dflt) {
@@ -119,7 +123,7 @@ inline ql_status linear_geom(const ql_linear_desc *d, Geom &g) {
 // partial sums (bytes_per_split each).
 inline double plan_splits(int tiles, int stages_total, int min_stages, size_t bytes_per_split, int slots, int &splits,
                           int &sps, size_t max_bytes = kMaxSplitBytes, int pipes = 1,
-                          double shared_round = kSharedRound) {
+                          double shared_round = kSharedRound, double step_cost = 1.0) {
     const int cap_bytes = (int)std::max<size_t>(1, max_bytes / std::max<size_t>(bytes_per_split, 1));
     const int s_max = std::max(1, std::min(stages_total / std::max(min_stages, 1), cap_bytes));
     double best = 0.0;
@@ -133,7 +137,7 @@ inline double plan_splits(int tiles, int stages_total, int min_stages, size_t by
         const long long full = wgs / round, rest = wgs % round;
         double rounds = (double)full * (slots > 1 ? shared_round : 1.0);
         if (rest > 0) rounds += rest > kNumCUs ? shared_round : 1.0;
-        double t = per * rounds;
+        double t = per * rounds * step_cost;
         if (pipes > 1) t = (double)cdiv(per, pipes) * (double)(full + (rest > 0)) * kPipeRound;
         if (eff > 1) t += (double)eff * bytes_per_split * 2.0 / kBytesPerStep + kReduceSteps;
         if (s == 1 || t < best) {
@@ -358,12 +362,14 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
 // Pipelined (bf16) weight-gradient tile configurations (rows = k', columns =
 // output channels per term):  0: 128 x 64, 1: 128 x 128, 2: 64 x 64.
 // (3: the 128 x 64 tile of the 16 x 16 x 32 kernel, qconv_bwd_weight16.h;
-// 4: the same with two pipelines per 8-wave workgroup)
-constexpr int kBwCfgs = 5;
-constexpr int kBwBKP[kBwCfgs] = {128, 128, 64, 128, 128};
-constexpr int kBwBO[kBwCfgs] = {64, 128, 64, 64, 64};
-constexpr int kBwSlots[kBwCfgs] = {2, 1, 2, 2, 1};  // workgroups one CU holds at once
-constexpr int kBwThreads[kBwCfgs] = {256, 256, 256, 256, 512};
+// 4: the same with two pipelines per 8-wave workgroup; 5: its 128 x 128 tile,
+// eight waves side by side in one pipeline)
+constexpr int kBwCfgs = 6;
+constexpr int kBwBKP[kBwCfgs] = {128, 128, 64, 128, 128, 128};
+constexpr int kBwBO[kBwCfgs] = {64, 128, 64, 64, 64, 128};
+constexpr int kBwSlots[kBwCfgs] = {2, 1, 2, 2, 1, 1};  // workgroups one CU holds at once
+constexpr int kBwThreads[kBwCfgs] = {256, 256, 256, 256, 512, 512};
+constexpr int kBwPipes[kBwCfgs] = {1, 1, 1, 1, 2, 1};  // pipelines per workgroup (K halves)
 
 struct BwdWeightPlan {
     int cfg;   // pipelined path only
@@ -398,16 +404,20 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMa
         p.row_tiles = cdiv(KP, p.BKP);
         p.col_tiles = cdiv(g.O, p.BO);
         return plan_splits(p.row_tiles * p.col_tiles, p.stages_total, min_stages, bytes_per_split, p.slots, p.splits,
-                           p.sps, max_split_bytes, kBwThreads[cfg] / 256);
+                           p.sps, max_split_bytes, kBwPipes[cfg], kSharedRound, cfg == 5 ? kFatStep : 1.0);
     };
     if (p.pipe && g.ne == NEURON_QUADRA) {
-        // the 16 x 16 x 32 kernel, one pipeline per workgroup or two, whichever the model finds faster
+        // the 16 x 16 x 32 kernel: four waves on a 64-channel tile, two such pipelines per
+        // workgroup, or eight waves on a 128-channel tile, whichever the model finds fastest
         const int forced = env_override("QLAYER_BWD_WEIGHT_CFG", -1);
         if (forced >= 0 && forced < kBwCfgs) {
             fill(forced);
         } else {
+            // the 128-channel tile only where it has no empty columns
             const double t3 = fill(3), t4 = fill(4);  // (declarators initialise in order)
-            if (!(t4 < t3)) fill(3);
+            const double t5 = g.O % 128 == 0 ? fill(5) : 1e30;
+            const int best = t5 < t3 && t5 < t4 ? 5 : (t4 < t3 ? 4 : 3);
+            if (best != 5) fill(best);
         }
     } else {
         fill(0);  // the other neuron types and fp32: the 128 x 64 tile

@@ -109,6 +109,10 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
                 case 4:
                     hipLaunchKernelGGL((qconv_bwd_weight16_kernel<128, 4, 2>), grid, dim3(kBwThreads[4]), 0, st, a);
                     break;
+                case 5:
+                    hipLaunchKernelGGL((qconv_bwd_weight16_kernel<128, 5, 1, 128>), grid, dim3(kBwThreads[5]), 0, st,
+                                       a);
+                    break;
                 default: hipLaunchKernelGGL((qconv_bwd_weight_kernel<64, 64, 2, 2, 4>), grid, block, 0, st, a); break;
             }
         }
