@@ -92,17 +92,41 @@ __device__ __forceinline__ v4u w16_frag_bf16(const char *tile, int k0, int m0, i
     return out;
 }
 
-template <int BKP, int NS, int KG, int BO, bool SUM, bool LIN>
+// fp32 tiles (16-byte slots of 4 values; the swizzle XORs the slot with row
+// bits 0-1, by 4, 8, 12): the operand of v_mfma_f32_16x16x4f32, lane l
+// gets GEMM row m0 + l % 16 at reduction row k0 + l / 16 (one ds_read_b32;
+// the 16 lanes of a group read 64 contiguous bytes of one row, the four
+// groups four rows in distinct banks).
+template <int S16>
+__device__ __forceinline__ float f32_frag(const char *tile, int k0, int m0, int lane) {
+    const int row = k0 + (lane >> 4), col = m0 + (lane & 15);
+    return *reinterpret_cast<const float *>(tile + row * (S16 * 16) + (((col >> 2) ^ ((row & 3) << 2)) << 4) +
+                                            (col & 3) * 4);
+}
+
+// The slot swizzle of a tile row: bf16 tiles the one of w16_off, fp32 tiles
+// the one of f32_frag.
+template <typename T, int S16>
+__device__ __forceinline__ int tile_swz(int row) {
+    if constexpr (sizeof(T) == 2) return w16_swz<S16>(row);
+    else return (row & 3) << 2;
+}
+
+// T: uint16_t (bf16, 16x16x32 MFMAs, K steps of 32 pixels) or float (fp32,
+// 16x16x4 fp32 MFMAs, K steps of 16 pixels); the tiles are the same bytes.
+template <typename T, int BKP, int NS, int KG, int BO, bool SUM, bool LIN>
 __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *smem_all) {
-    using T = uint16_t;
     // BO: output channels per term of the tile, 16 per wave (four or eight waves)
+    constexpr bool BF = sizeof(T) == 2;
+    constexpr int ES = (int)sizeof(T);
+    constexpr int EPS = 16 / ES;        // elements per 16-byte slot
     constexpr int NT = BO * 4;          // threads of one pipeline
     constexpr int NTW = NT * KG;        // threads of the workgroup
-    constexpr int KE = 32;              // output pixels per K step (one 16x16x32 k-chunk)
-    constexpr int SX = BKP / 8;
-    constexpr int SG = BO / 8;
-    constexpr int XB = KE * BKP * 2;
-    constexpr int GB = KE * BO * 2;
+    constexpr int KE = 64 / ES;         // output pixels per K step (one bf16 k-chunk, four fp32 ones)
+    constexpr int SX = BKP / EPS;
+    constexpr int SG = BO / EPS;
+    constexpr int XB = KE * BKP * ES;
+    constexpr int GB = KE * BO * ES;
     constexpr int STAGE = XB + 3 * GB;
     constexpr int NW = NT / 64;
     constexpr int NIX = XB / (NT * 16);
@@ -137,10 +161,12 @@ __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *
                                      static_cast<const T *>(a.tb)};
 
     // DMA fill geometry (as in qconv_bwd_weight.h; the swizzle needs the tile
-    // row mod 16, which instruction 0's row gives for every instruction)
-    static_assert((RX * NW) % 16 == 0 && (RG * NW) % 16 == 0, "swizzle phase");
-    const int xslot = (lane % SX) ^ w16_swz<SX>(RX * wave + lane / SX);
-    const int kp = rt * BKP + 8 * xslot;
+    // row mod 16 (bf16) or 4 (fp32), which instruction 0's row gives for every
+    // instruction)
+    constexpr int PHASE = BF ? 16 : 4;  // the rows the swizzle tells apart
+    static_assert((RX * NW) % PHASE == 0 && (RG * NW) % PHASE == 0, "swizzle phase");
+    const int xslot = (lane % SX) ^ tile_swz<T, SX>(RX * wave + lane / SX);
+    const int kp = rt * BKP + EPS * xslot;
     const bool kp_ok = kp < a.KP;
     int xr, xq, xc;
     {
@@ -149,8 +175,8 @@ __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *
         xr = (int)fdiv((uint32_t)tap, a.fd_kw);
         xq = tap - xr * a.KW;
     }
-    const int gslot = (lane % SG) ^ w16_swz<SG>(RG * wave + lane / SG);
-    const int og = ct * BO + 8 * gslot;
+    const int gslot = (lane % SG) ^ tile_swz<T, SG>(RG * wave + lane / SG);
+    const int og = ct * BO + EPS * gslot;
     const bool og_ok = og < a.O;
 
     const int dh = xr - a.PH, dw = xq - a.PW;
@@ -236,44 +262,74 @@ __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *
         for (int mr = 0; mr < MR; ++mr) acc[t][mr] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
     float dsum[3] = {0.0f, 0.0f, 0.0f};
 
-    // set 0: k' fragments 0 .. MH-1 and the G-side fragments; set 1: fragments MH .. MR-1
-    v4u af[2][MH], gr[3], bt[3];
     const int ocol = wave * 16;  // this wave's 16 output channels within the tile
+    // bf16 -- set 0: k' fragments 0 .. MH-1 and the G-side fragments; set 1: fragments MH .. MR-1.
+    // fp32 -- set s: k-chunks 2 s, 2 s + 1 of the step, every k' fragment and the G-side values.
+    v4u af[2][MH], gr[3], bt[3];
+    float fa[2][2][MR], fg[2][2][3];
     auto read = [&](int slot, int ch, int set) {
         const char *xt = smem + slot * STAGE;
+        if constexpr (BF) {
 #pragma unroll
-        for (int h = 0; h < MH; ++h) af[set][h] = w16_frag_bf16<SX>(xt, 0, (ch * MH + h) * 16, lane);
-        if (ch == 0) {
+            for (int h = 0; h < MH; ++h) af[set][h] = w16_frag_bf16<SX>(xt, 0, (ch * MH + h) * 16, lane);
+            if (ch == 0) {
 #pragma unroll
-            for (int u = 0; u < 3; ++u) gr[u] = w16_frag_bf16<SG>(xt + XB + u * GB, 0, ocol, lane);
+                for (int u = 0; u < 3; ++u) gr[u] = w16_frag_bf16<SG>(xt + XB + u * GB, 0, ocol, lane);
+            }
+        } else {
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const int k0 = 4 * (2 * ch + kc);
+#pragma unroll
+                for (int mr = 0; mr < MR; ++mr) fa[set][kc][mr] = f32_frag<SX>(xt, k0, mr * 16, lane);
+#pragma unroll
+                for (int u = 0; u < 3; ++u) fg[set][kc][u] = f32_frag<SG>(xt + XB + u * GB, k0, ocol, lane);
+            }
         }
     };
     auto mma = [&](int set) {
-        if (set == 0) {
-            // the step's products, in fp32 (the bias sums use them before rounding), formed once
-            float op[2][8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float gv = vget<T>(gr[0], e);
-                op[0][e] = gv * vget<T>(gr[2], e);
-                op[1][e] = gv * vget<T>(gr[1], e);
-            }
-            if constexpr (SUM) {
+        if constexpr (BF) {
+            if (set == 0) {
+                // the step's products, in fp32 (the bias sums use them before rounding), formed once
+                float op[2][8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    dsum[0] += op[0][e];
-                    dsum[1] += op[1][e];
-                    dsum[2] += vget<T>(gr[0], e);
+                    const float gv = vget<T>(gr[0], e);
+                    op[0][e] = gv * vget<T>(gr[2], e);
+                    op[1][e] = gv * vget<T>(gr[1], e);
                 }
+                if constexpr (SUM) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        dsum[0] += op[0][e];
+                        dsum[1] += op[1][e];
+                        dsum[2] += vget<T>(gr[0], e);
+                    }
+                }
+                bt[0] = vpack<T>(op[0]);
+                bt[1] = vpack<T>(op[1]);
+                bt[2] = gr[0];
             }
-            bt[0] = vpack<T>(op[0]);
-            bt[1] = vpack<T>(op[1]);
-            bt[2] = gr[0];
+#pragma unroll
+            for (int h = 0; h < MH; ++h)
+#pragma unroll
+                for (int t = 0; t < 3; ++t) mfma16(af[set][h], bt[t], acc[t][set * MH + h]);
+        } else {
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const float gv = fg[set][kc][0];
+                const float op[3] = {gv * fg[set][kc][2], gv * fg[set][kc][1], gv};
+                if constexpr (SUM) {
+#pragma unroll
+                    for (int t = 0; t < 3; ++t) dsum[t] += op[t];
+                }
+#pragma unroll
+                for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+                    for (int t = 0; t < 3; ++t)
+                        acc[t][mr] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[set][kc][mr], op[t], acc[t][mr], 0, 0, 0);
+            }
         }
-#pragma unroll
-        for (int h = 0; h < MH; ++h)
-#pragma unroll
-            for (int t = 0; t < 3; ++t) mfma16(af[set][h], bt[t], acc[t][set * MH + h]);
     };
     run_ring<NS, NI>(nst, s_begin, issue, read, mma);
 
@@ -396,20 +452,20 @@ __device__ __forceinline__ void bwd_weight16_body(const BwdWeightArgs &a, char *
     }
 }
 
-template <int BKP, int NS, int KG = 1, int BO = 64>
+template <int BKP, int NS, int KG = 1, int BO = 64, typename T = uint16_t>
 __global__ __launch_bounds__(BO * 4 * KG) void qconv_bwd_weight16_kernel(const BwdWeightArgs a) {
-    constexpr int STAGE = 32 * BKP * 2 + 3 * 32 * BO * 2;
+    constexpr int STAGE = 64 * BKP + 3 * 64 * BO;  // a K step: 64 bytes of every X and G-side tile row
     __shared__ __attribute__((aligned(1024))) char smem[KG * NS * STAGE];
     int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int tiles = a.row_tiles * a.col_tiles;
     bid -= (bid / tiles) * tiles;
     const bool sum = a.want_db && bid % a.row_tiles == 0;
     if (a.lin) {
-        if (sum) bwd_weight16_body<BKP, NS, KG, BO, true, true>(a, smem);
-        else bwd_weight16_body<BKP, NS, KG, BO, false, true>(a, smem);
+        if (sum) bwd_weight16_body<T, BKP, NS, KG, BO, true, true>(a, smem);
+        else bwd_weight16_body<T, BKP, NS, KG, BO, false, true>(a, smem);
     } else {
-        if (sum) bwd_weight16_body<BKP, NS, KG, BO, true, false>(a, smem);
-        else bwd_weight16_body<BKP, NS, KG, BO, false, false>(a, smem);
+        if (sum) bwd_weight16_body<T, BKP, NS, KG, BO, true, false>(a, smem);
+        else bwd_weight16_body<T, BKP, NS, KG, BO, false, false>(a, smem);
     }
 }
 

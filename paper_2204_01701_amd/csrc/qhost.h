@@ -390,7 +390,9 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMa
     p.Cp = p.pad ? g.cpad() : g.C;
     const int M = g.N * g.HO * g.WO, KP = g.KH * g.KW * p.Cp, KPO = g.KH * g.KW * g.C;
     p.veck = p.Cp % g.vec() == 0 && g.O % g.vec() == 0;
-    p.pipe = p.veck && g.dt == QL_BF16;
+    // pipelined kernels: bf16 every neuron type; fp32 the proposed neuron (the 16 x 16 kernel's fp32 form)
+    p.pipe = p.veck && (g.dt == QL_BF16 ||
+                        (g.ne == NEURON_QUADRA && env_override("QLAYER_BWD_WEIGHT_F32_PIPE", 1) != 0));
     if (p.pad) p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
     p.KE = 64 / (int)g.esize();
     p.stages_total = cdiv(M, p.KE);
@@ -410,7 +412,7 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMa
         // the 16 x 16 x 32 kernel: four waves on a 64-channel tile, two such pipelines per
         // workgroup, or eight waves on a 128-channel tile, whichever the model finds fastest
         const int forced = env_override("QLAYER_BWD_WEIGHT_CFG", -1);
-        if (forced >= 0 && forced < kBwCfgs) {
+        if (forced >= (g.dt == QL_BF16 ? 0 : 3) && forced < kBwCfgs) {  // (fp32: configurations 3-5 only)
             fill(forced);
         } else {
             // the 128-channel tile only where it has no empty columns

@@ -117,6 +117,23 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
             }
         }
     }
+    if constexpr (sizeof(T) == 4) {
+        if (p.pipe && om == OM_QUADRA) {
+            switch (p.cfg) {
+                case 4:
+                    hipLaunchKernelGGL((qconv_bwd_weight16_kernel<128, 4, 2, 64, float>), grid, dim3(kBwThreads[4]), 0,
+                                       st, a);
+                    break;
+                case 5:
+                    hipLaunchKernelGGL((qconv_bwd_weight16_kernel<128, 5, 1, 128, float>), grid, dim3(kBwThreads[5]),
+                                       0, st, a);
+                    break;
+                default:
+                    hipLaunchKernelGGL((qconv_bwd_weight16_kernel<128, 4, 1, 64, float>), grid, block, 0, st, a);
+                    break;
+            }
+        }
+    }
     if (!p.pipe && om == OM_QUADRA) {
         if (p.veck)
             hipLaunchKernelGGL((qconv_bwd_weight_generic_kernel<T, 128, 64, 2, 2, 64, 4, true>), grid, block, 0, st, a);
