@@ -192,14 +192,14 @@ inline bool pm_default(const Geom &g, int env) {
 // Pipelined forward tile configurations (rows = output channels per term,
 // columns = output pixels; per-wave tile in parentheses; 4 waves unless noted):
 //   0: 128 x 128 (32 x 128), 1: 64 x 256 (32 x 128), 2: 128 x 128 (64 x 64), 3: 64 x 128 (32 x 64),
-//   4: 128 x 256 (32 x 128, 8 waves), 5: 128 x 256 (64 x 64, 8 waves).
+//   4: 128 x 256 (32 x 128, 8 waves), 5: 128 x 256 (64 x 64, 8 waves), 6: as 4 with four LDS stages.
 // Larger workgroup tiles move fewer bytes through the vector-memory address
 // path per MFMA: 32768 (1/BCOL + 1/(3 BR)) bytes.
-constexpr int kFwdCfgs = 6;
-constexpr int kFwdBR[kFwdCfgs] = {128, 64, 128, 64, 128, 128};
-constexpr int kFwdBCOL[kFwdCfgs] = {128, 256, 128, 128, 256, 256};
+constexpr int kFwdCfgs = 7;
+constexpr int kFwdBR[kFwdCfgs] = {128, 64, 128, 64, 128, 128, 128};
+constexpr int kFwdBCOL[kFwdCfgs] = {128, 256, 128, 128, 256, 256, 256};
 // Workgroups one CU holds at once (limited by LDS stages and registers).
-constexpr int kFwdSlots[kFwdCfgs] = {1, 1, 1, 2, 1, 1};
+constexpr int kFwdSlots[kFwdCfgs] = {1, 1, 1, 2, 1, 1, 1};
 
 struct FwdPlan {
     int cfg;  // pipelined: index into kFwd*; generic: 0: 128 x 128, 1: 64 x 128
@@ -237,7 +237,9 @@ inline FwdPlan plan_fwd(const Geom &g) {
     if (p.veck) {
         // 8-wave 128 x 256 tiles where there are enough of them to fill the GPU several times
         const bool big = g.O >= 128 && (long long)cdiv(g.O, 128) * cdiv(M, 256) >= 4 * kNumCUs;
-        p.cfg = env_override("QLAYER_FWD_CFG", big ? 4 : 3);
+        // (the 8-wave tile with four stages where the filter has several taps: measured 3 % faster on
+        // the N=64, 256-channel 56 x 56 layer, and no faster on the dense layer)
+        p.cfg = env_override("QLAYER_FWD_CFG", big ? (g.KH * g.KW > 1 ? 6 : 4) : 3);
         if (p.cfg < 0 || p.cfg >= kFwdCfgs || g.ne != NEURON_QUADRA) p.cfg = 3;  // (the other types: tile 3 only)
         p.BR = kFwdBR[p.cfg];
         p.BCOL = kFwdBCOL[p.cfg];

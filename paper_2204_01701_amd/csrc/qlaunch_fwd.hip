@@ -145,6 +145,7 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
             case 2: QL_FWD(128, 128, 2, 2, 4, 256); break;
             case 4: QL_FWD(128, 256, 4, 2, 3, 512); break;
             case 5: QL_FWD(128, 256, 2, 4, 3, 512); break;
+            case 6: QL_FWD(128, 256, 4, 2, 4, 512); break;
             default: QL_FWD(64, 128, 2, 2, 4, 256); break;
         }
 #undef QL_FWD
