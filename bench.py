@@ -52,7 +52,7 @@ def parse():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
                     help="instead of running: HBM bytes per entry call from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
                          "counter tables of the benchmark and of --copy-calibration")
-    ap.add_argument("--leg", choices=("depthwise", "epilogue", "neuron_types", "kernels", "resnet20"),
+    ap.add_argument("--leg", choices=("depthwise", "epilogue", "neuron_types", "kernels", "resnet20", "cold"),
                     help="instead of the benchmark: run one extra leg alone and print its JSON (for profiling); "
                          "'kernels' runs every pass of the VGG-16 layers, the large layer and the dense layer "
                          "KERNEL_REPS times in a fixed order, for counter collection")
@@ -661,7 +661,7 @@ def main():
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     if args.leg:
-        legs = {"depthwise": depthwise, "epilogue": epilogue_cost, "neuron_types": neuron_types,
+        legs = {"depthwise": depthwise, "epilogue": epilogue_cost, "neuron_types": neuron_types, "cold": cold_cache,
                 "kernels": kernel_leg, "resnet20": resnet20_step_leg}
         print(json.dumps({args.leg: legs[args.leg](ql, torch, dev, stream)}), flush=True)
         return
@@ -750,6 +750,76 @@ def main():
     print(json.dumps(result), flush=True)
 
 
+def conv_bytes(L, fam, esize=2):
+    """Algorithmic HBM bytes of one pass of a dense quadratic conv layer (every
+    input and output tensor once): fwd (X + 3 W + 3 P) eb, bwd_data
+    (3 P + 3 W + X) eb, bwd_weight (X + 3 P) eb + 4 (3 W + 3 O)."""
+    X = L.n * L.h * L.w * L.c
+    P = L.n * L.ho * L.wo * L.o
+    W = L.o * L.c * L.k * L.k
+    if fam == "fwd":
+        return esize * (X + 3 * W + 3 * P)
+    if fam == "bwd_data":
+        return esize * (3 * P + 3 * W + X)
+    return esize * (X + 3 * P) + 4 * (3 * W + 3 * L.o)
+
+
+def cold_cache(ql, torch, dev, stream, reps=20):
+    """The layers below the MFMA ridge, each pass hot and cold: the VGG-16 stem
+    (3 -> 64, 32 x 32) and the 2 x 2 layers 11-13 (512 -> 512, one shape), and
+    the large depthwise layer (N=64, C=256, 56 x 56).  Hot: `reps` calls back to
+    back between two device-scope events, per call (the GPU runs ahead of the
+    host, so host launch time stays hidden); cold: the median of single calls,
+    each after a 512 MB scratch write, so that the MALL holds none of the
+    layer's tensors (the write is outside the timed interval and keeps the GPU
+    busy while the call is submitted).  GB/s: algorithmic bytes over the time,
+    and the fraction of the 8 TB/s HBM spec."""
+    import synth
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    geoms = synth.vgg16_layers(128)
+    cases = [("vgg16_L1", Layer(ql, torch, geoms[0], 2, 0, dev), conv_bytes),
+             ("vgg16_L11_13", Layer(ql, torch, geoms[10], 2, 10, dev), conv_bytes),
+             ("large_dw", Layer(ql, torch, synth.ConvLayer(n=64, c=256, h=56, w=56, o=256, k=3, stride=1, pad=1),
+                                9, 0, dev, depthwise=True), dw_bytes)]
+    out = {}
+    for name, ly, nbytes in cases:
+        ly.fwd(stream)
+        r = {"shape": f"N={ly.L.n} {ly.L.c}->{ly.L.o} {ly.L.h}x{ly.L.w}" + (" depthwise" if name == "large_dw" else "")}
+        for f in ("fwd", "bwd_data", "bwd_weight"):
+            fn = getattr(ly, f)
+            for _ in range(3):
+                fn(stream)
+            torch.cuda.synchronize()
+            a, b = DevEvent(), DevEvent()
+            a.record(stream)
+            for _ in range(reps):
+                fn(stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            th = a.elapsed_time(b) / reps
+            cold = []
+            for _ in range(reps):
+                with torch.cuda.stream(stream):
+                    flush.fill_(1)
+                a, b = DevEvent(), DevEvent()
+                a.record(stream)
+                fn(stream)
+                b.record(stream)
+                torch.cuda.synchronize()
+                cold.append(a.elapsed_time(b))
+            tc = sorted(cold)[reps // 2]
+            nb = nbytes(ly.L, f)
+            r[f"{f}_us_hot"] = round(th * 1e3, 1)
+            r[f"{f}_us_cold"] = round(tc * 1e3, 1)
+            r[f"{f}_gbs_hot"] = round(nb / (th * 1e-3) / 1e9, 1)
+            r[f"{f}_gbs_cold"] = round(nb / (tc * 1e-3) / 1e9, 1)
+            r[f"{f}_hbm_frac_cold"] = round(nb / (tc * 1e-3) / 1e9 / 8000.0, 3)
+        out[name] = r
+        del ly
+    del flush
+    return out
+
+
 def extra_workloads(ql, torch, dev, stream, reps=10):
     """The large single layer (N=64, 256->256, 56x56) and the dense layer (8192 x 4096 -> 4096),
     each pass timed separately (reported beside the main metric)."""
@@ -800,6 +870,7 @@ def extra_workloads(ql, torch, dev, stream, reps=10):
     out["depthwise"] = depthwise(ql, torch, dev, stream, reps)
     out["epilogue"] = epilogue_cost(ql, torch, dev, stream, reps)
     out["resnet20"] = resnet20_step_leg(ql, torch, dev, stream, reps)
+    out["cold_cache"] = cold_cache(ql, torch, dev, stream)
     out["hybrid_bp_memory"] = hybrid_bp_memory(torch, dev)
     return out
 
