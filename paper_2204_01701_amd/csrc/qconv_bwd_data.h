@@ -103,9 +103,11 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
     // Channel-aligned K steps (CA: O a multiple of KE, stride 1): a K step lies
     // within one tap, so tap and output-channel offset are wave-uniform and
     // each DMA address is a per-lane base plus a scalar offset.  Weight
-    // columns past C and pixels past M re-read valid data (their results are
-    // never stored); taps whose output pixel lies outside the map are a
-    // per-lane bit mask.
+    // columns past C load the zero page (a fixed per-lane predicate: on layers
+    // with few input channels most of the tile, which re-reading valid columns
+    // would turn into real traffic); pixels past M re-read valid data (their
+    // results are never stored); taps whose output pixel lies outside the map
+    // are a per-lane bit mask.
     const T *wrow[NATW ? NIW : 1];
     long long go[NIP];
     uint32_t gmask[NIP];
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
             const long long sw = ((long long)o0 * khkw + tap) * a.C;
 #pragma unroll
             for (int i = 0; i < NIW; ++i)
-                if (part.take()) dma16(wrow[i] + sw, base + i * 4096);
+                if (part.take()) dma16(dma_src(wc_ok, wrow[i] + sw, a.zero), base + i * 4096);
             const long long sg = o0 - ((long long)r * a.WO + q) * a.O;
 #pragma unroll
             for (int j = 0; j < NIP; ++j) {

@@ -119,18 +119,23 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
     // Channel-aligned K steps (CA: C a multiple of KE, KH*KW <= 32): a K step
     // lies within one tap, so tap and channel offset are wave-uniform and each
     // DMA address is a per-lane base plus a scalar offset.  Weight rows past O
-    // and pixels past M re-read a valid row instead of zeros: their results are
-    // never stored.  Taps that land in the zero padding are a per-lane bit mask.
+    // load the zero page (a fixed per-lane predicate: on layers with few
+    // output channels most of the tile's rows, which re-reading a valid row
+    // would turn into real traffic); pixels past M re-read a valid row (their
+    // results are never stored).  Taps that land in the zero padding are a
+    // per-lane bit mask.
     const T *wrow[NIW];
     long long xo[NIX];
     uint32_t xmask[NIX];
+    bool wok[NIW];
     if constexpr (CA) {
 #pragma unroll
         for (int i = 0; i < NIW; ++i) {
             const int row = RPI * i + 16 * wave + (lane >> 2);
             const int t = row / BR;
-            const int o = min(rt * BR + (row - t * BR), a.O - 1);
-            wrow[i] = wp[t] + (size_t)o * a.K + kcol * VEC;
+            const int o = rt * BR + (row - t * BR);
+            wok[i] = o < a.O;
+            wrow[i] = wp[t] + (size_t)min(o, a.O - 1) * a.K + kcol * VEC;
         }
 #pragma unroll
         for (int j = 0; j < NIX; ++j) {
@@ -181,7 +186,7 @@ __global__ __launch_bounds__(NT) void qconv_fwd_kernel(const FwdArgs a) {
             const long long soff = ((long long)r * a.W + q) * a.C + c0;
 #pragma unroll
             for (int i = 0; i < NIW; ++i)
-                if (part.take()) dma16(wrow[i] + k0, base + i * (NT * 16));
+                if (part.take()) dma16(dma_src(wok[i], wrow[i] + k0, a.zero), base + i * (NT * 16));
 #pragma unroll
             for (int j = 0; j < NIX; ++j) {
                 const bool ok = live && ((xmask[j] >> tap) & 1u);

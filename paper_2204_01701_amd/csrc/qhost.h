@@ -254,11 +254,18 @@ inline FwdPlan plan_fwd(const Geom &g) {
     p.row_tiles = cdiv(g.O, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    p.ca = p.veck && p.Cp % p.KE == 0 && g.KH * g.KW <= 32 && env_override("QLAYER_FWD_CA", 1) != 0;
     // Position-major order where the maps are small, so that many taps of a
     // position lie in the padding: the splits are planned for the pixel tile
-    // with the most in-bounds taps.
-    p.pm = p.ca && pm_default(g, env_override("QLAYER_FWD_POSMAJ", -1));
+    // with the most in-bounds taps.  It needs channel-aligned K steps.  Without
+    // it they are on by default in fp32 only: in bf16 they measured slower than
+    // the per-lane (r, q, c) addresses (the VGG-16 and CIFAR ResNet layers with
+    // 32 to 512 channels and the 256-channel 56 x 56 layer, 2 to 20 %), in fp32
+    // 2 to 3 % faster (the ResNet layers with 32 and 64 channels).
+    const int ca_env = env_override("QLAYER_FWD_CA", -1);
+    const bool pm_want = pm_default(g, env_override("QLAYER_FWD_POSMAJ", -1));
+    p.ca = p.veck && p.Cp % p.KE == 0 && g.KH * g.KW <= 32 &&
+           (ca_env >= 0 ? ca_env != 0 : (pm_want || g.dt == QL_F32));
+    p.pm = p.ca && pm_want;
     int kst = p.stages_total;
     if (p.pm) kst = pm_max_taps(g, p.BCOL, M) * (p.Cp / p.KE);
     plan_splits(p.row_tiles * p.col_tiles, kst, env_override("QLAYER_FWD_MINSTAGES", 4), (size_t)3 * M * g.O * 4,

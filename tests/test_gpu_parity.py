@@ -103,7 +103,9 @@ def test_no_bias_and_zero_product_weight(bf16):
 # only some of them for the small shapes above).
 TILE_CONFIGS = ([("QLAYER_FWD_CFG", c) for c in range(7)] +
                 [("QLAYER_BWD_DATA_CFG", c) for c in range(6)] +
-                [("QLAYER_BWD_WEIGHT_CFG", c) for c in range(6)])
+                [("QLAYER_BWD_WEIGHT_CFG", c) for c in range(6)] +
+                # channel-aligned forward K steps in image-major order (by default fp32 and position-major only)
+                [("QLAYER_FWD_CA", 1)])
 TILE_SHAPES = [(2, 24, 10, 9, 48, 3, 3, 1, 1), (1, 264, 5, 7, 144, 3, 3, 1, 1), (2, 32, 9, 9, 16, 3, 3, 2, 1)]
 
 

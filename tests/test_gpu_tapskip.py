@@ -46,6 +46,8 @@ def test_tap_skipping_matches_oracle(shape, bf16, order, monkeypatch):
     N, C, H, W, O, KH, KW, s, p = shape
     print(f"tap skipping order={order} shape={shape} bf16={bf16}", flush=True)
     monkeypatch.setenv("QLAYER_FWD_POSMAJ", order)
+    if order == "0":  # the channel-aligned K steps without the position-major order
+        monkeypatch.setenv("QLAYER_FWD_CA", "1")
     inp = synth.random_conv_case([700] + list(shape), N, C, H, W, O, KH, KW, s, p, bf16=bf16)
     got = qlh.conv_to_np(qlh.run_conv(inp, s, p, bf16))
     ref = _oracle_all(inp, s, p)
