@@ -616,27 +616,27 @@ __global__ __launch_bounds__(kThreads) void qconv_channel_stats_kernel(const T *
     }
 }
 
-// Sum of the per-part statistics [part][2][O] in part order: sum[o] and sumsq[o].
-// A block takes 4 indices j of [2][O]; 64 lanes per index sum every 64th
-// part, and the lane sums are added in lane order.
+// Sum of the per-part statistics [part][2][O] in a fixed order: sum[o] and
+// sumsq[o].  One workgroup per index j of [2][O] (launch 2 O workgroups).
 template <int = 0>  // (a template: defined once across the translation units that include this header)
 __global__ __launch_bounds__(kThreads) void qconv_stats_reduce_kernel(const float *__restrict__ part, int nparts,
                                                                        int O, float *sum, float *sumsq) {
-    __shared__ float red[4][65];
-    const int jl = threadIdx.x >> 6, sl = threadIdx.x & 63;
-    const int j = blockIdx.x * 4 + jl;
+    // one sum j per workgroup: thread i adds parts i, i + 256, ... in order, then a fixed tree
+    __shared__ float red[kThreads];
+    const int j = blockIdx.x, tid = threadIdx.x;
     float s = 0.0f;
-    if (j < 2 * O) {
 #pragma unroll 4
-        for (int p = sl; p < nparts; p += 64) s += part[(size_t)p * 2 * O + j];
-    }
-    red[jl][sl] = s;
+    for (int p = tid; p < nparts; p += kThreads) s += part[(size_t)p * 2 * O + j];
+    red[tid] = s;
     __syncthreads();
-    if (sl == 0 && j < 2 * O) {
-        float t = 0.0f;
-        for (int l = 0; l < 64; ++l) t += red[jl][l];
-        if (j < O) sum[j] = t;
-        else sumsq[j - O] = t;
+#pragma unroll
+    for (int w = kThreads / 2; w > 0; w >>= 1) {
+        if (tid < w) red[tid] += red[tid + w];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        if (j < O) sum[j] = red[0];
+        else sumsq[j - O] = red[0];
     }
 }
 

@@ -16,6 +16,7 @@
 #include "qconv_aux.h"
 #include "qconv_depthwise.h"
 #include "qconv_fwd_smallc.h"
+#include "qconv_fwd_narrow.h"
 
 namespace ql {
 namespace host {
@@ -201,12 +202,22 @@ constexpr int kFwdBCOL[kFwdCfgs] = {128, 256, 128, 128, 256, 256, 256};
 // Workgroups one CU holds at once (limited by LDS stages and registers).
 constexpr int kFwdSlots[kFwdCfgs] = {1, 1, 1, 2, 1, 1, 1};
 
+// Waves of the narrow kernels (a multiple of the four per workgroup): one per
+// 16-pixel block up to three per SIMD, then more blocks per wave.
+inline int narrow_waves(long long pixels) {
+    const long long waves = std::min<long long>(std::max<long long>(1, cdiv(pixels, 16)), 3LL * 4 * kNumCUs);
+    return (int)(cdiv(waves, 4) * 4);
+}
+
 struct FwdPlan {
     int cfg;  // pipelined: index into kFwd*; generic: 0: 128 x 128, 1: 64 x 128
     int BR, BCOL, KE, slots;
     int row_tiles, col_tiles, splits, sps, stages_total;
     bool veck;
     bool smallc;  // KH KW C + bias columns <= 32, 32 or 64 output channels: qconv_fwd_smallc_kernel, no workspace
+    bool narrow;  // at most 32 output channels, short J: qconv_fwd_narrow_kernel (OB row blocks, NCH chunks)
+    int ob, nch;
+    int stat_parts;  // partial sums of the epilogue statistics the kernel writes (fused path)
     bool ca;  // channel-aligned K steps (C a multiple of KE, at most 32 taps): every step within one tap
     bool pm;  // position-major pixel order, K steps of padding-only taps skipped (FwdArgs)
     bool pad;                      // X and W_t zero-padded to Cp channels first
@@ -234,6 +245,21 @@ inline FwdPlan plan_fwd(const Geom &g) {
         p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
         p.wpad_bytes = align_up((size_t)g.O * g.KH * g.KW * p.Cp * g.esize());
     }
+    // Narrow layers: the weight fragments of all three terms (3 OB NCH runs of
+    // 16 bytes per lane) stay in registers for the whole kernel.
+    p.ob = cdiv(g.O, 16);
+    p.nch = cdiv(K, 4 * g.vec());
+    // (one 16-channel row block: two measured slower than the tiled kernel on the
+    // 16 -> 32-channel stride-2 layer of a CIFAR ResNet)
+    if (p.veck && g.ne == NEURON_QUADRA && g.O % 4 == 0 && p.ob == 1 && p.nch <= 9 &&
+        env_override("QLAYER_FWD_NARROW", 1) != 0) {
+        p.narrow = true;
+        p.splits = 1;
+        p.KE = 64 / (int)g.esize();
+        p.stat_parts = narrow_waves(M);
+        p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes;
+        return p;
+    }
     if (p.veck) {
         // 8-wave 128 x 256 tiles where there are enough of them to fill the GPU several times
         const bool big = g.O >= 128 && (long long)cdiv(g.O, 128) * cdiv(M, 256) >= 4 * kNumCUs;
@@ -253,6 +279,7 @@ inline FwdPlan plan_fwd(const Geom &g) {
     p.KE = 64 / (int)g.esize();
     p.row_tiles = cdiv(g.O, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
+    p.stat_parts = p.col_tiles;
     p.stages_total = cdiv(K, p.KE);
     // Position-major order where the maps are small, so that many taps of a
     // position lie in the padding: the splits are planned for the pixel tile
@@ -295,6 +322,8 @@ struct BwdDataPlan {
     bool veck, s1;
     bool natw;    // weights read untransposed through natural LDS tiles (bf16, C % 8 == 0)
     bool smallc;  // C <= 4: per-pixel partial sums by MFMA, then a gather over the taps
+    bool narrow;  // at most 32 input channels, short K: qconv_bwd_data_narrow_kernel (CB row blocks, NCH chunks)
+    int cb, nch;
     int fused_rb; // ... stride 1: both steps in one kernel, bands of fused_rb input rows (0: two kernels)
     size_t fused_smem;
     int njb;      // ... 32-column blocks of (r, q, c)
@@ -330,8 +359,19 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
     }
     const int M = g.N * g.H * g.W, K = g.KH * g.KW * g.O;
     p.veck = g.O % g.vec() == 0;
-    p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
     p.s1 = g.SH == 1 && g.SW == 1;
+    // Narrow layers: the transposed weight runs of all three terms stay in registers.
+    p.cb = cdiv(g.C, 16);
+    p.nch = cdiv(K, 4 * g.vec());
+    if (p.veck && g.ne == NEURON_QUADRA && g.C % 4 == 0 && p.cb == 1 && p.nch <= 9 &&
+        env_override("QLAYER_BWD_DATA_NARROW", 1) != 0) {
+        p.narrow = true;
+        p.splits = 1;
+        p.wt_bytes = align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
+        p.ws_bytes = p.wt_bytes;
+        return p;
+    }
+    p.natw = p.veck && g.dt == QL_BF16 && g.C % 8 == 0;
     // the wide kernel: bf16, natural weight tiles, stride 1, 16-channel K steps within one tap
     const bool wide_ok = p.natw && p.s1 && g.O % 16 == 0 && g.KH * g.KW <= 32;
     if (p.veck) {
@@ -457,6 +497,7 @@ inline int grid_1d(long long total) {
 // Whether launch_fwd's kernel writes Y through its staged epilogue, the path
 // that gathers the epilogue statistics itself (qconv_fwd.h).
 inline bool fwd_stats_fused(const Geom &g, const FwdPlan &p) {
+    if (p.narrow) return true;
     if (p.smallc || !p.veck || p.splits != 1 || g.O % (16 / (int)g.esize()) != 0) return false;
     const int ns = (g.ne == NEURON_QUADRA && (p.cfg == 4 || p.cfg == 5)) ? 3 : 4;
     return fwd_staged_fits(p.BR, p.BCOL, ns, (int)g.esize());

@@ -2,6 +2,7 @@
 #include "qhost.h"
 #include "qconv_bwd_data.h"
 #include "qconv_bwd_data_wide.h"
+#include "qconv_bwd_data_narrow.h"
 #include "qconv_generic.h"
 
 namespace ql {
@@ -85,6 +86,30 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.fd_sw = make_fastdiv(g.SW);
     a.neuron = g.ne;
     a.xin = xin;
+    if (p.narrow) {
+        const dim3 grid((unsigned)(narrow_waves(a.M) / (kThreads / 64)));
+#define QL_BD_NARROW(CB, NCH)                                                                                        \
+    do {                                                                                                             \
+        if (p.s1)                                                                                                    \
+            hipLaunchKernelGGL((qconv_bwd_data_narrow_kernel<T, CB, NCH, true>), grid, dim3(kThreads), 0, st, a);  \
+        else                                                                                                         \
+            hipLaunchKernelGGL((qconv_bwd_data_narrow_kernel<T, CB, NCH, false>), grid, dim3(kThreads), 0, st, a); \
+    } while (0)
+        switch (p.nch) {
+            case 1: QL_BD_NARROW(1, 1); break;
+            case 2: QL_BD_NARROW(1, 2); break;
+            case 3: QL_BD_NARROW(1, 3); break;
+            case 4: QL_BD_NARROW(1, 4); break;
+            case 5: QL_BD_NARROW(1, 5); break;
+            case 6: QL_BD_NARROW(1, 6); break;
+            case 7: QL_BD_NARROW(1, 7); break;
+            case 8: QL_BD_NARROW(1, 8); break;
+            case 9: QL_BD_NARROW(1, 9); break;
+            default: return QL_EINVAL;  // (the planner takes no other shape)
+        }
+#undef QL_BD_NARROW
+        return hip_status();
+    }
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     // channel-aligned K steps (each within one tap): stride 1, natural weight tiles, O a multiple of KE
     const bool bd_ca = p.s1 && p.natw && g.O % p.KE == 0 && g.KH * g.KW <= 32 &&

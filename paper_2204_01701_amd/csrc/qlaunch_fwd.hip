@@ -92,6 +92,31 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
     a.fd_n = make_fastdiv(g.N);
     a.fd_cps = make_fastdiv(std::max(1, a.cps));
     a.neuron = g.ne;
+    if (p.narrow) {
+        const dim3 grid((unsigned)(narrow_waves(a.M) / (kThreads / 64)));
+        const bool ep = epi.scale || epi.shift || epi.relu || stat_part != nullptr;
+#define QL_FWD_NARROW(OB, NCH)                                                                                  \
+    do {                                                                                                        \
+        if (ep)                                                                                                 \
+            hipLaunchKernelGGL((qconv_fwd_narrow_kernel<T, OB, NCH, true>), grid, dim3(kThreads), 0, st, a);  \
+        else                                                                                                    \
+            hipLaunchKernelGGL((qconv_fwd_narrow_kernel<T, OB, NCH, false>), grid, dim3(kThreads), 0, st, a); \
+    } while (0)
+        switch (p.nch) {
+            case 1: QL_FWD_NARROW(1, 1); break;
+            case 2: QL_FWD_NARROW(1, 2); break;
+            case 3: QL_FWD_NARROW(1, 3); break;
+            case 4: QL_FWD_NARROW(1, 4); break;
+            case 5: QL_FWD_NARROW(1, 5); break;
+            case 6: QL_FWD_NARROW(1, 6); break;
+            case 7: QL_FWD_NARROW(1, 7); break;
+            case 8: QL_FWD_NARROW(1, 8); break;
+            case 9: QL_FWD_NARROW(1, 9); break;
+            default: return QL_EINVAL;  // (the planner takes no other shape)
+        }
+#undef QL_FWD_NARROW
+        return hip_status();
+    }
     if (p.xsq_bytes) {
         // T2: X o X once, instead of squaring every fragment in the MFMA loop
         T *xsq = reinterpret_cast<T *>(wsb + p.xpad_bytes + 3 * p.wpad_bytes + p.part_bytes);

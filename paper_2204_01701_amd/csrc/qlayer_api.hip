@@ -75,7 +75,7 @@ StatPlan plan_stats(const Geom &g, const ql_epilogue *e) {
     if (!g.dw) p = plan_fwd(g);
     s.fused = !g.dw && fwd_stats_fused(g, p);
     if (s.fused) {
-        s.nparts = p.col_tiles;
+        s.nparts = p.stat_parts;
     } else {
         s.rpp = std::max(64, cdiv(M, 1024));
         s.nparts = cdiv(M, s.rpp);
@@ -144,7 +144,7 @@ ql_status fwd_common(const Geom &g, const void *x, const void *wa, const void *w
         s = hip_status();
         if (s != QL_OK) return s;
     }
-    hipLaunchKernelGGL(qconv_stats_reduce_kernel<>, dim3(cdiv(2 * g.O, 4)), dim3(kThreads), 0, st, stat_part,
+    hipLaunchKernelGGL(qconv_stats_reduce_kernel<>, dim3(2 * g.O), dim3(kThreads), 0, st, stat_part,
                        sp.nparts, g.O, e->sum, e->sumsq);
     return hip_status();
 }

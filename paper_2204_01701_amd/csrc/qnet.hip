@@ -88,7 +88,7 @@ ql_status qnet_bn_act_bwd(const qnet_shape *s, ql_dtype dtype, const void *dout,
         hipLaunchKernelGGL(qnet_bn_act_bwd_reduce_kernel<T>, rgrid, dim3(kThreads), 0, st, ns(s),
                            static_cast<const T *>(dout), static_cast<const T *>(out), relu, static_cast<const T *>(y),
                            mean, rstd, rpp, part);
-        hipLaunchKernelGGL(qconv_stats_reduce_kernel<>, dim3(cdiv(2 * s->c, 4)), dim3(kThreads), 0, st, part, parts,
+        hipLaunchKernelGGL(qconv_stats_reduce_kernel<>, dim3(2 * s->c), dim3(kThreads), 0, st, part, parts,
                            s->c, sums, sums + s->c);
         hipLaunchKernelGGL(qnet_bn_act_bwd_apply_kernel<T>, agrid, dim3(kThreads), 0, st, ns(s),
                            static_cast<const T *>(dout), static_cast<const T *>(out), relu, static_cast<const T *>(y),
@@ -98,7 +98,7 @@ ql_status qnet_bn_act_bwd(const qnet_shape *s, ql_dtype dtype, const void *dout,
         hipLaunchKernelGGL(qnet_bn_act_bwd_reduce_kernel<T>, rgrid, dim3(kThreads), 0, st, ns(s),
                            static_cast<const T *>(dout), static_cast<const T *>(out), relu, static_cast<const T *>(y),
                            mean, rstd, rpp, part);
-        hipLaunchKernelGGL(qconv_stats_reduce_kernel<>, dim3(cdiv(2 * s->c, 4)), dim3(kThreads), 0, st, part, parts,
+        hipLaunchKernelGGL(qconv_stats_reduce_kernel<>, dim3(2 * s->c), dim3(kThreads), 0, st, part, parts,
                            s->c, sums, sums + s->c);
         hipLaunchKernelGGL(qnet_bn_act_bwd_apply_kernel<T>, agrid, dim3(kThreads), 0, st, ns(s),
                            static_cast<const T *>(dout), static_cast<const T *>(out), relu, static_cast<const T *>(y),
