@@ -32,13 +32,6 @@ constexpr int kSmallcK = 32;  // reduction columns of the kernel: J + bias colum
 // Bias columns after the J weight columns: three bf16 parts, or one fp32 value.
 template <typename T> constexpr int smallc_bias_cols() { return sizeof(T) == 2 ? 3 : 1; }
 
-// Wave-local ordering of LDS writes before reads of other lanes of the wave.
-__device__ __forceinline__ void wave_lds_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 // Part p of the fp32 bias value b in the element type: bf16 parts are the
 // successive round-to-nearest residues (b = p0 + p1 + p2 exactly).
 template <typename T> __device__ __forceinline__ float bias_part(float b, int p);

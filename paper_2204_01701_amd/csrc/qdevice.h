@@ -82,6 +82,13 @@ template <typename T> __device__ __forceinline__ uint32_t vraw(const v4u &v, int
     }
 }
 
+// Wave-local ordering of LDS writes before reads of other lanes of the wave.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // The forward epilogue of output channel o (EpiArgs): scale, shift, ReLU.
 __device__ __forceinline__ float epi_apply(const EpiArgs &e, int o, float v) {
     if (e.scale) v *= e.scale[o];

@@ -421,6 +421,8 @@ constexpr int kBwThreads[kBwCfgs] = {256, 256, 256, 256, 512, 512};
 constexpr int kBwPipes[kBwCfgs] = {1, 1, 1, 1, 2, 1};  // pipelines per workgroup (K halves)
 
 struct BwdWeightPlan {
+    bool narrow;  // at most 16 output channels, KH KW C <= 144: qconv_bwd_weight_narrow_kernel (NF fragments)
+    int nf;
     int cfg;   // pipelined path only
     bool pipe; // bf16 and vectorizable: pipelined kernel; otherwise the generic one
     int BKP, BO, KE, slots;
@@ -435,7 +437,13 @@ struct BwdWeightPlan {
 // plans for its fixed scratch array).
 inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMaxSplitBytes) {
     BwdWeightPlan p{};
-    p.pad = g.dt == QL_BF16 && g.pad_small_c() && g.O % g.vec() == 0;
+    // the narrow kernel: at most 16 output channels, rows k' of at most 144 (after the channel padding)
+    const int cp_small = g.pad_small_c() ? g.cpad() : g.C;
+    const bool narrow_shape = g.ne == NEURON_QUADRA && g.O <= 16 && g.O % g.vec() == 0 && cp_small % g.vec() == 0 &&
+                              cdiv(g.KH * g.KW * cp_small, 16) <= 9 &&
+                              env_override("QLAYER_BWD_WEIGHT_NARROW", 1) != 0;
+    // (fp32 pads only for the narrow kernel)
+    p.pad = g.pad_small_c() && g.O % g.vec() == 0 && (g.dt == QL_BF16 || narrow_shape);
     p.Cp = p.pad ? g.cpad() : g.C;
     const int M = g.N * g.HO * g.WO, KP = g.KH * g.KW * p.Cp, KPO = g.KH * g.KW * g.C;
     p.veck = p.Cp % g.vec() == 0 && g.O % g.vec() == 0;
@@ -447,6 +455,24 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMa
     p.stages_total = cdiv(M, p.KE);
     const int min_stages = env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16);
     const size_t bytes_per_split = (size_t)3 * g.O * KPO * 4;
+    // Narrow layers: the whole gradient is one tile; about two workgroups per CU,
+    // at least four K steps per wave, the partial sums within max_split_bytes.
+    p.nf = cdiv(KP, 16);
+    if (narrow_shape && p.Cp == cp_small) {
+        p.narrow = true;
+        p.stages_total = cdiv(M, g.dt == QL_BF16 ? 32 : 16);
+        int splits = std::min(2 * kNumCUs, std::max(1, cdiv(p.stages_total, 16)));
+        splits = env_override("QLAYER_BWD_WEIGHT_NARROW_SPLITS", splits);
+        splits = std::max(1, std::min(splits, (int)std::max<size_t>(1, max_split_bytes / bytes_per_split)));
+        p.sps = cdiv(p.stages_total, splits);
+        p.splits = cdiv(p.stages_total, p.sps);
+        if (p.splits > 1) {
+            p.dw_bytes = align_up((size_t)p.splits * 3 * g.O * KPO * sizeof(float));
+            p.db_bytes = align_up((size_t)p.splits * 3 * g.O * sizeof(float));
+        }
+        p.ws_bytes = p.xpad_bytes + p.dw_bytes + p.db_bytes;
+        return p;
+    }
     auto fill = [&](int cfg) {
         p.cfg = cfg;
         p.BKP = p.pipe ? kBwBKP[cfg] : 128;

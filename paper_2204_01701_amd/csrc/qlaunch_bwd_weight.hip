@@ -2,6 +2,7 @@
 #include "qhost.h"
 #include "qconv_bwd_weight.h"
 #include "qconv_bwd_weight16.h"
+#include "qconv_bwd_weight_narrow.h"
 #include "qconv_generic.h"
 
 namespace ql {
@@ -78,6 +79,26 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     a.lin_dq = (p.KE / g.WO) % g.HO;
     a.lin_dr = p.KE % g.WO;
     a.neuron = g.ne;
+    if (p.narrow) {
+#define QL_BW_NARROW(NF) \
+    hipLaunchKernelGGL((qconv_bwd_weight_narrow_kernel<T, NF>), dim3(p.splits), dim3(kThreads), 0, st, a)
+        switch (p.nf) {
+            case 1: QL_BW_NARROW(1); break;
+            case 2: QL_BW_NARROW(2); break;
+            case 3: QL_BW_NARROW(3); break;
+            case 4: QL_BW_NARROW(4); break;
+            case 5: QL_BW_NARROW(5); break;
+            case 6: QL_BW_NARROW(6); break;
+            case 7: QL_BW_NARROW(7); break;
+            case 8: QL_BW_NARROW(8); break;
+            case 9: QL_BW_NARROW(9); break;
+            default: return QL_EINVAL;  // (the planner takes no other shape)
+        }
+#undef QL_BW_NARROW
+        const ql_status s = hip_status();
+        if (s != QL_OK || p.splits == 1) return s;
+        return reduce_bw_partials(g, p.splits, a, dwa, dwb, dwc, dba, dbb, dbc, st);
+    }
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     const int om = g.om();
     if (om != OM_QUADRA) {
