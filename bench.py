@@ -339,6 +339,7 @@ _KERNEL_FAMILY = [
     (r"qconv_fwd_kernel<", "fwd", True),
     (r"qconv_fwd_generic_kernel<", "fwd", True),
     (r"qconv_fwd_smallc_kernel<", "fwd", True),
+    (r"qconv_fwd_narrow_kernel<", "fwd", True),
     (r"qconv_fwd_combine_kernel<", "fwd", False),
     (r"qconv_pad_channels_kernel<[^,>]+, 4>", "fwd", False),
     (r"qconv_bwd_data_kernel<", "bwd_data", True),
@@ -346,12 +347,14 @@ _KERNEL_FAMILY = [
     (r"qconv_bwd_data_wide_kernel<", "bwd_data", True),
     (r"qconv_bwd_data_cols_kernel<", "bwd_data", True),
     (r"qconv_bwd_data_cols_fused_kernel<", "bwd_data", True),
+    (r"qconv_bwd_data_narrow_kernel<", "bwd_data", True),
     (r"qconv_bwd_data_col2im_kernel<", "bwd_data", False),
     (r"qconv_sum_splits_kernel<", "bwd_data", False),
     (r"qconv_weight_transpose_kernel<", "bwd_data", False),
     (r"qconv_bwd_weight_kernel<", "bwd_weight", True),
     (r"qconv_bwd_weight16_kernel<", "bwd_weight", True),
     (r"qconv_bwd_weight_generic_kernel<", "bwd_weight", True),
+    (r"qconv_bwd_weight_narrow_kernel<", "bwd_weight", True),
     (r"qconv_bwd_weight_reduce_kernel<", "bwd_weight", False),
     (r"qconv_bwd_weight_reduce2d_kernel<", "bwd_weight", False),
     (r"qconv_bwd_weight_reduce2dv_kernel[<(]", "bwd_weight", False),
