@@ -32,6 +32,8 @@ CONV_CASES = [
     ("split-k", 4, 256, 4, 4, 256, 3, 1, 1, 1, {}),
     ("generic", 2, 12, 7, 5, 20, 3, 1, 1, 1, {}),
     ("odd-out-channels", 2, 16, 8, 8, 12, 3, 2, 1, 1, {}),
+    ("narrow", 4, 16, 12, 12, 16, 3, 1, 1, 1, {}),          # the narrow forward (sums per wave)
+    ("narrow-stem", 3, 3, 10, 10, 16, 3, 1, 1, 1, {}),       # ... on the zero-padded 3-channel stem
     ("depthwise", 2, 32, 9, 7, 32, 3, 1, 1, 32, {}),
     ("depthwise-5x5", 2, 24, 8, 8, 24, 5, 1, 2, 24, {}),
 ]

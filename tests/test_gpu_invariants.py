@@ -18,7 +18,8 @@ import qlh  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 SHAPES = [(2, 16, 8, 8, 32, 3, 3, 1, 1), (2, 64, 4, 4, 64, 3, 3, 1, 1), (1, 5, 6, 6, 7, 3, 3, 2, 1),
-          (4, 16, 16, 16, 32, 3, 3, 1, 1)]
+          (4, 16, 16, 16, 32, 3, 3, 1, 1),
+          (4, 16, 12, 12, 16, 3, 3, 1, 1)]  # (the narrow kernels of all three passes)
 
 
 def _eq(a, b):
