@@ -37,8 +37,14 @@ def _obj(src: str) -> str:
     return os.path.join(BUILD_DIR, os.path.basename(src)[:-4] + ".o")
 
 
+# Per-file flags: the small-output forward keeps its MFMA accumulators in VGPRs
+# (in the AGPR form, at one workgroup per CU, the compiler moved them between
+# registers on every K step).
+FILE_FLAGS = {"qlaunch_fwd_ksplit.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def compile_command(src: str, obj: str) -> list[str]:
-    return [HIPCC, *FLAGS, "-c", "-o", obj, src]
+    return [HIPCC, *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", "-o", obj, src]
 
 
 def link_command(objs: list[str], out: str = LIB) -> list[str]:

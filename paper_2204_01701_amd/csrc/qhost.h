@@ -217,6 +217,8 @@ struct FwdPlan {
     bool smallc;  // KH KW C + bias columns <= 32, 32 or 64 output channels: qconv_fwd_smallc_kernel, no workspace
     bool narrow;  // at most 32 output channels, short J: qconv_fwd_narrow_kernel (OB row blocks, NCH chunks)
     int ob, nch;
+    bool ksplit;  // small outputs: qconv_fwd_ksplit_kernel (tiles of 3 x 16 krb rows by 16 kcb pixels, K split by waves)
+    int krb, kcb;
     int stat_parts;  // partial sums of the epilogue statistics the kernel writes (fused path)
     bool ca;  // channel-aligned K steps (C a multiple of KE, at most 32 taps): every step within one tap
     bool pm;  // position-major pixel order, K steps of padding-only taps skipped (FwdArgs)
@@ -297,6 +299,37 @@ inline FwdPlan plan_fwd(const Geom &g) {
     if (p.pm) kst = pm_max_taps(g, p.BCOL, M) * (p.Cp / p.KE);
     plan_splits(p.row_tiles * p.col_tiles, kst, env_override("QLAYER_FWD_MINSTAGES", 4), (size_t)3 * M * g.O * 4,
                 p.slots, p.splits, p.sps, kMaxSplitBytes, 1, kSharedRoundFwd);
+    // Where these tiles would split K over workgroups (small outputs: the 4 x 4
+    // and 2 x 2 maps of a CIFAR VGG-16), the in-workgroup K split of
+    // qconv_fwd_ksplit.h instead: tiles small enough to fill the GPU, no
+    // partial sums in HBM.  (32-bit element offsets into X and the weights.)
+    // By default only where each wave's K range is at most 768 in bf16, 512 in
+    // fp32 (on longer K the tiled kernel's split-K measured faster: the
+    // 512-channel 4 x 4 layers, 1152 per wave, 51 against 46 us per call in
+    // bf16; the 256-channel one, 576 per wave, 139 against 127 us in fp32).
+    const int ks_env = env_override("QLAYER_FWD_KSPLIT", -1);
+    const int ks_k = (pm_want ? pm_max_taps(g, 64, M) : g.KH * g.KW) * p.Cp;
+    const int ks_kmax = g.dt == QL_BF16 ? 768 : 512;
+    if (p.veck && g.ne == NEURON_QUADRA && g.O % 4 == 0 && p.Cp % p.KE == 0 && g.KH * g.KW <= 32 &&
+        (long long)g.N * g.H * g.W * p.Cp < (1LL << 31) && (long long)g.O * K < (1LL << 31) &&
+        (ks_env >= 0 ? ks_env != 0 : p.splits > 1 && ks_k <= 4 * ks_kmax)) {
+        // the larger tile where its count fills the GPU, else the smaller one (or as forced)
+        constexpr int kKsRB[3] = {2, 1, 2}, kKsCB[3] = {4, 4, 2};
+        int t = cdiv(g.O, 32) * cdiv(M, 64) >= kNumCUs ? 0 : 1;
+        t = env_override("QLAYER_FWD_KSPLIT_TILE", t);
+        if (t < 0 || t > 2) t = 1;
+        p.ksplit = true;
+        p.krb = kKsRB[t];
+        p.kcb = kKsCB[t];
+        p.pm = pm_want;
+        p.row_tiles = cdiv(g.O, 16 * p.krb);
+        p.col_tiles = cdiv(M, 16 * p.kcb);
+        p.splits = 1;
+        p.sps = p.stages_total;
+        p.stat_parts = p.col_tiles * p.kcb;
+        p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes;
+        return p;
+    }
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * 3 * M * g.O * sizeof(float)) : 0;
     p.xsq_bytes = g.ne == NEURON_T2 && p.veck ? align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize()) : 0;
     p.ws_bytes = p.xpad_bytes + 3 * p.wpad_bytes + p.part_bytes + p.xsq_bytes;
@@ -523,7 +556,7 @@ inline int grid_1d(long long total) {
 // Whether launch_fwd's kernel writes Y through its staged epilogue, the path
 // that gathers the epilogue statistics itself (qconv_fwd.h).
 inline bool fwd_stats_fused(const Geom &g, const FwdPlan &p) {
-    if (p.narrow) return true;
+    if (p.narrow || p.ksplit) return true;
     if (p.smallc || !p.veck || p.splits != 1 || g.O % (16 / (int)g.esize()) != 0) return false;
     const int ns = (g.ne == NEURON_QUADRA && (p.cfg == 4 || p.cfg == 5)) ? 3 : 4;
     return fwd_staged_fits(p.BR, p.BCOL, ns, (int)g.esize());
@@ -630,6 +663,10 @@ inline DwArgs dw_args(const Geom &g, const DwPlan &p) {
 ql_status run_fwd(const Geom &g, const FwdPlan &p, const void *x, const void *wa, const void *wb, const void *wc,
                   const float *ba, const float *bb, const float *bc, void *y, void *ta, void *tb, void *ws,
                   const EpiArgs &epi, float *stat_part, hipStream_t st);
+// The small-output forward (qlaunch_fwd_ksplit.hip, its own translation unit:
+// compiled with the MFMA accumulators in VGPRs) with the arguments run_fwd set up.
+template <typename T>
+ql_status launch_fwd_ksplit(const FwdPlan &p, const FwdArgs &a, bool ep, hipStream_t st);
 ql_status run_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, const void *ta, const void *tb,
                        const void *xin, const void *wa, const void *wb, const void *wc, void *dx, void *ws,
                        hipStream_t st);

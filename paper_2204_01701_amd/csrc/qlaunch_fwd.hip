@@ -117,6 +117,7 @@ ql_status launch_fwd(const Geom &g, const FwdPlan &p, const void *x, const void 
 #undef QL_FWD_NARROW
         return hip_status();
     }
+    if (p.ksplit) return launch_fwd_ksplit<T>(p, a, epi.scale || epi.shift || epi.relu || stat_part != nullptr, st);
     if (p.xsq_bytes) {
         // T2: X o X once, instead of squaring every fragment in the MFMA loop
         T *xsq = reinterpret_cast<T *>(wsb + p.xpad_bytes + 3 * p.wpad_bytes + p.part_bytes);

@@ -119,11 +119,15 @@ def test_backward_validation(L):
 
 
 def test_workspace_queries_are_consistent(L):
-    # split-K only where the output tiles cannot fill the GPU
+    # split-K partials only where the output tiles cannot fill the GPU and each
+    # wave's K range is long (the 512-channel 4 x 4 layer); the 2 x 2 layer's
+    # waves split K within the workgroup and need no workspace
     big = ql.conv_desc(64, 256, 56, 56, 256, 3, 3, 1, 1, ql.QL_BF16)
-    small = ql.conv_desc(128, 512, 2, 2, 512, 3, 3, 1, 1, ql.QL_BF16)
+    small = ql.conv_desc(128, 512, 4, 4, 512, 3, 3, 1, 1, ql.QL_BF16)
+    tiny = ql.conv_desc(128, 512, 2, 2, 512, 3, 3, 1, 1, ql.QL_BF16)
     assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(big)) == 0
     assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(small)) > 0
+    assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(tiny)) == 0
     assert L.qlayer_conv2d_bwd_weight_workspace_size(ctypes.byref(big)) > 0
     # bf16 reads the weights untransposed; fp32 stages a transposed copy in the workspace
     dl = ql.linear_desc(8192, 4096, 4096, ql.QL_BF16)
@@ -206,7 +210,7 @@ def test_neuron_type_validation(L):
     assert _fwd(L, dw24) == QL_EUNSUPPORTED
     # the workspace queries accept every type
     for n in range(6):
-        d = ql.conv_desc(4, 256, 4, 4, 256, 3, 3, 1, 1, ql.QL_BF16, n)
+        d = ql.conv_desc(4, 512, 4, 4, 512, 3, 3, 1, 1, ql.QL_BF16, n)
         assert L.qlayer_conv2d_fwd_workspace_size(ctypes.byref(d)) > 0
 
 

@@ -29,7 +29,9 @@ CONV_CASES = [
     ("staged", 2, 64, 16, 16, 64, 3, 1, 1, 1, {}),
     ("staged-ragged", 3, 32, 9, 7, 48, 3, 1, 1, 1, {}),
     ("eight-wave-tile", 2, 64, 16, 16, 128, 3, 1, 1, 1, {"QLAYER_FWD_CFG": "4"}),
-    ("split-k", 4, 256, 4, 4, 256, 3, 1, 1, 1, {}),
+    ("split-k", 4, 256, 4, 4, 256, 3, 1, 1, 1, {"QLAYER_FWD_KSPLIT": "0"}),  # the tiled kernel's combine
+    ("ksplit", 4, 256, 4, 4, 256, 3, 1, 1, 1, {}),            # the small-output forward (sums per block)
+    ("ksplit-2x2", 16, 64, 2, 2, 68, 3, 1, 1, 1, {}),         # ... position-major, ragged rows
     ("generic", 2, 12, 7, 5, 20, 3, 1, 1, 1, {}),
     ("odd-out-channels", 2, 16, 8, 8, 12, 3, 2, 1, 1, {}),
     ("narrow", 4, 16, 12, 12, 16, 3, 1, 1, 1, {}),          # the narrow forward (sums per wave)
@@ -205,7 +207,8 @@ def test_epilogue_full_size_layer_and_repeatability():
     assert qlh.relerr(got, ref) <= qlh.tol(True, False)
 
 
-@pytest.mark.parametrize("case", [CONV_CASES[0], CONV_CASES[3], CONV_CASES[6]], ids=["staged", "split-k", "depthwise"])
+@pytest.mark.parametrize("case", [CONV_CASES[0], CONV_CASES[3], CONV_CASES[4], CONV_CASES[8]],
+                         ids=["staged", "split-k", "ksplit", "depthwise"])
 def test_epilogue_invariants(case, env):
     """fwd_ex with no epilogue (or an empty one) writes the plain forward's bits; the sums
     taken with the epilogue equal those of the plain output stored by it; scale = 1, shift = 0

@@ -4,7 +4,8 @@ forward and backward, against the fp64 oracle with the order forced on and
 off, on shapes where tiles hold one position, several positions, ragged
 tails, stride 2, 5 x 5 filters and positions with no tap in bounds at all
 (their outputs are the bias terms alone; eq:2ndneuron3 with every product
-term zero)."""
+term zero).  Each shape runs in the tiled kernel and in the small-output
+kernel whose waves split K (qconv_fwd_ksplit.h)."""
 import pytest
 import torch
 
@@ -39,13 +40,15 @@ def _oracle_all(inp, s, p):
     return d
 
 
+@pytest.mark.parametrize("kernel", ["0", "1"], ids=["tiled", "ksplit"])
 @pytest.mark.parametrize("order", ["1", "0"], ids=["posmajor", "imagemajor"])
 @pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
-def test_tap_skipping_matches_oracle(shape, bf16, order, monkeypatch):
+def test_tap_skipping_matches_oracle(shape, bf16, order, kernel, monkeypatch):
     N, C, H, W, O, KH, KW, s, p = shape
-    print(f"tap skipping order={order} shape={shape} bf16={bf16}", flush=True)
+    print(f"tap skipping order={order} ksplit={kernel} shape={shape} bf16={bf16}", flush=True)
     monkeypatch.setenv("QLAYER_FWD_POSMAJ", order)
+    monkeypatch.setenv("QLAYER_FWD_KSPLIT", kernel)  # the tiled kernel, or the small-output one
     if order == "0":  # the channel-aligned K steps without the position-major order
         monkeypatch.setenv("QLAYER_FWD_CA", "1")
     inp = synth.random_conv_case([700] + list(shape), N, C, H, W, O, KH, KW, s, p, bf16=bf16)
