@@ -56,7 +56,8 @@ __device__ __forceinline__ uint32_t fwd_column_taps(const FwdArgs &a, int m) {
 // C is a multiple of the chunk (narrow_chunk), so a chunk lies within one
 // tap; O a multiple of 4.
 template <typename T, int RB, int CB, int NS, bool EPI>
-__global__ __launch_bounds__(kThreads, 2) void qconv_fwd_ksplit_kernel(const FwdArgs a) {
+__global__ __launch_bounds__(kThreads, 4 * NS * (3 * RB + CB) * 1024 > 80 * 1024 ? 1 : 2) void qconv_fwd_ksplit_kernel(
+    const FwdArgs a) {
     constexpr int CK = narrow_chunk<T>();
     constexpr int VEC = Elem<T>::VEC;
     constexpr int NWV = kThreads / 64;
@@ -75,9 +76,13 @@ __global__ __launch_bounds__(kThreads, 2) void qconv_fwd_ksplit_kernel(const Fwd
     const int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int rt = bid / a.col_tiles, ct = bid - rt * a.col_tiles;
     const int o0 = rt * 16 * RB, m0 = ct * BCOL;
-    const T *__restrict__ x = static_cast<const T *>(a.x);
-    const T *wp[3] = {static_cast<const T *>(a.w[0]), static_cast<const T *>(a.w[1]),
-                      static_cast<const T *>(a.w[2])};
+    constexpr int ES = (int)sizeof(T);
+    // Buffer resources of X and the weights (byte offsets of 32 bits: the
+    // planner keeps both below 2^31 bytes); an offset past the end reads zeros.
+    const __amdgpu_buffer_rsrc_t xrs = raw_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ES);
+    const uint32_t wbytes = (uint32_t)a.O * a.K * ES;
+    const __amdgpu_buffer_rsrc_t wrs[3] = {raw_rsrc(a.w[0], wbytes), raw_rsrc(a.w[1], wbytes),
+                                           raw_rsrc(a.w[2], wbytes)};
     char *const ring = smem + wave * (NS * STAGE);
 
     // The tile's taps: lane l < BCOL takes column m0 + l, the wave ORs them.
@@ -93,27 +98,25 @@ __global__ __launch_bounds__(kThreads, 2) void qconv_fwd_ksplit_kernel(const Fwd
     // DMA geometry: one instruction fills a fragment's 64 LDS slots, lane l
     // the slot of row l / 4 and logical 16-byte column dcol (the KM layout of
     // qpipe.h, whose swizzle puts the fragment reads of 16 consecutive rows in
-    // distinct bank groups).  A: weight row o = o0 + 16 rb + l / 4 (rows past O
-    // load zeros).
+    // distinct bank groups).  A: weight row o = o0 + 16 rb + l / 4, its byte
+    // offset fixed per lane (rows past O re-read row O - 1: their results are
+    // never stored), the chunk's offset a scalar.
     const int drow = lane >> 2, dcol = km_fill_col(lane);
-    int woff[RB];
-    bool wok[RB];
+    uint32_t woff[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int o = o0 + 16 * rb + drow;
-        wok[rb] = o < a.O;
-        woff[rb] = min(o, a.O - 1) * a.K + VEC * dcol;
+        woff[rb] = (uint32_t)((min(o, a.O - 1) * a.K + VEC * dcol) * ES);
     }
     // B: column m = m0 + 16 cb + l / 4: the window origin (ih0, iw0) of its
-    // pixel and the element offset of that origin's run dcol (columns past M
-    // load zeros).
+    // pixel and the element offset of that origin's run dcol; columns past M
+    // and taps in the padding read zeros (an out-of-range offset).
     int xoff[CB], xh[CB], xw[CB];
-    bool mok[CB];
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
         const int m = m0 + 16 * cb + drow;
-        mok[cb] = m < a.M;
-        const int mm = mok[cb] ? m : a.M - 1;
+        const bool mok = m < a.M;
+        const int mm = mok ? m : a.M - 1;
         int n, pos;
         if (a.pm) {
             pos = (int)fdiv((uint32_t)mm, a.fd_n);
@@ -123,9 +126,9 @@ __global__ __launch_bounds__(kThreads, 2) void qconv_fwd_ksplit_kernel(const Fwd
             pos = mm - n * a.HO * a.WO;
         }
         const int oh = (int)fdiv((uint32_t)pos, a.fd_wo);
-        xh[cb] = oh * a.SH - a.PH;
+        xh[cb] = mok ? oh * a.SH - a.PH : -(1 << 20);  // (no tap brings it in bounds)
         xw[cb] = (pos - oh * a.WO) * a.SW - a.PW;
-        xoff[cb] = ((n * a.H + xh[cb]) * a.W + xw[cb]) * a.C + VEC * dcol;
+        xoff[cb] = ((n * a.H + oh * a.SH - a.PH) * a.W + xw[cb]) * a.C + VEC * dcol;
     }
 
     // Chunk state (wave-uniform): channel chunk cc of tap `tap` = (tr, tq); `rest`
@@ -137,22 +140,21 @@ __global__ __launch_bounds__(kThreads, 2) void qconv_fwd_ksplit_kernel(const Fwd
     int tap = rest ? __builtin_ctz(rest) : 0;
     int tr = (int)fdiv((uint32_t)tap, a.fd_kw), tq = tap - tr * a.KW;
 
-    // Copy the current chunk into ring slot `slot` (zeros when !live), then step
-    // to the next chunk.
-    auto issue = [&](int slot, bool live) {
+    // Copy the current chunk into ring slot `slot`, then step to the next chunk.
+    // (Chunks past the wave's range, copied to keep the ring's count of copies
+    // fixed, are never read into an MFMA.)
+    auto issue = [&](int slot) {
         char *base = ring + slot * STAGE;
-        const int kw = tap * a.C + cc * CK;
+        const int kw = (tap * a.C + cc * CK) * ES;
 #pragma unroll
         for (int t = 0; t < 3; ++t)
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-                dma16(dma_src(live && wok[rb], wp[t] + (woff[rb] + kw), a.zero), base + (t * RB + rb) * 1024);
+            for (int rb = 0; rb < RB; ++rb) dma16_buf(wrs[t], woff[rb], kw, base + (t * RB + rb) * 1024);
         const int kx = (tr * a.W + tq) * a.C + cc * CK;
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb) {
-            const bool ok = live && mok[cb] && (unsigned)(xh[cb] + tr) < (unsigned)a.H &&
-                            (unsigned)(xw[cb] + tq) < (unsigned)a.W;
-            dma16(dma_src(ok, x + (xoff[cb] + kx), a.zero), base + (3 * RB + cb) * 1024);
+            const bool ok = (unsigned)(xh[cb] + tr) < (unsigned)a.H && (unsigned)(xw[cb] + tq) < (unsigned)a.W;
+            dma16_buf(xrs, ok ? (uint32_t)((xoff[cb] + kx) * ES) : 0x80000000u, 0, base + (3 * RB + cb) * 1024);
         }
         if (++cc == a.cps) {
             cc = 0;
@@ -203,7 +205,7 @@ __global__ __launch_bounds__(kThreads, 2) void qconv_fwd_ksplit_kernel(const Fwd
     constexpr int VMC = (NS - 1) * NF;
     constexpr int VM_IMM = (VMC & 15) | ((VMC >> 4) << 14) | (7 << 4) | (15 << 8);
 #pragma unroll
-    for (int j = 0; j < NS; ++j) issue(j, k0 + j < k1);
+    for (int j = 0; j < NS; ++j) issue(j);
     v4u fa[3][RB], fb[CB];
     constexpr int VM0 = (NS - 1) * NF;
     __builtin_amdgcn_s_waitcnt((VM0 & 15) | ((VM0 >> 4) << 14) | (7 << 4) | (15 << 8));  // chunk k0 landed
@@ -214,7 +216,7 @@ __global__ __launch_bounds__(kThreads, 2) void qconv_fwd_ksplit_kernel(const Fwd
         mma(fa, fb);
         const int s1 = slot + 1 == NS ? 0 : slot + 1;
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // chunk k's fragments read
-        issue(slot, k + NS < k1);
+        issue(slot);
         __builtin_amdgcn_s_waitcnt(VM_IMM);  // chunk k + 1 landed
         asm volatile("" ::: "memory");
         read(s1, fa, fb);

@@ -302,16 +302,17 @@ inline FwdPlan plan_fwd(const Geom &g) {
     // Where these tiles would split K over workgroups (small outputs: the 4 x 4
     // and 2 x 2 maps of a CIFAR VGG-16), the in-workgroup K split of
     // qconv_fwd_ksplit.h instead: tiles small enough to fill the GPU, no
-    // partial sums in HBM.  (32-bit element offsets into X and the weights.)
-    // By default only where each wave's K range is at most 768 in bf16, 512 in
-    // fp32 (on longer K the tiled kernel's split-K measured faster: the
-    // 512-channel 4 x 4 layers, 1152 per wave, 51 against 46 us per call in
-    // bf16; the 256-channel one, 576 per wave, 139 against 127 us in fp32).
+    // partial sums in HBM.  (32-bit byte offsets into X and the weights.)
+    // By default only where each wave's K range is at most 768 in bf16 (on
+    // longer K the tiled kernel's split-K measured faster: the 512-channel
+    // 4 x 4 layers, 1152 per wave, 52 against 47 us per call), 1152 in fp32
+    // (the longest measured: the same layers, 215 against 228 us).
     const int ks_env = env_override("QLAYER_FWD_KSPLIT", -1);
     const int ks_k = (pm_want ? pm_max_taps(g, 64, M) : g.KH * g.KW) * p.Cp;
-    const int ks_kmax = g.dt == QL_BF16 ? 768 : 512;
+    const int ks_kmax = g.dt == QL_BF16 ? 768 : 1152;
     if (p.veck && g.ne == NEURON_QUADRA && g.O % 4 == 0 && p.Cp % p.KE == 0 && g.KH * g.KW <= 32 &&
-        (long long)g.N * g.H * g.W * p.Cp < (1LL << 31) && (long long)g.O * K < (1LL << 31) &&
+        (long long)g.N * g.H * g.W * p.Cp * (long long)g.esize() < (1LL << 31) &&
+        (long long)g.O * K * (long long)g.esize() < (1LL << 31) &&
         (ks_env >= 0 ? ks_env != 0 : p.splits > 1 && ks_k <= 4 * ks_kmax)) {
         // the larger tile where its count fills the GPU, else the smaller one (or as forced)
         constexpr int kKsRB[3] = {2, 1, 2}, kKsCB[3] = {4, 4, 2};

@@ -48,6 +48,20 @@ __device__ __forceinline__ void dma16(const void *gptr, char *wave_base) {
     asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gptr), "{m0}"(lds));
 }
 
+// The same copy through a buffer resource: 16 bytes per lane from byte offset
+// voff + soff of the buffer (zeros where voff is at or past its size, so a lane
+// with nothing to load passes an out-of-range offset) into LDS at
+// wave_base + 16 * lane.  Asm for the same reason as dma16.
+__device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t rs, uint32_t voff, int soff, char *wave_base) {
+    const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_void_t *)wave_base);
+    asm volatile("buffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rs), "s"(soff), "{m0}"(lds));
+}
+
+// Buffer resource of `bytes` bytes at p (raw: no stride, bounds-checked offsets).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
 // The DMA instructions of a K step are numbered 0 .. NI - 1 in issue order;
 // a ring may issue them in two parts, issue(step, slot, live, lo, hi) copying
 // those numbered lo .. hi - 1.  take() is called once per instruction in
