@@ -93,7 +93,12 @@ struct BwdDataArgs {
     int row_tiles, col_tiles, splits, stages_per_split, stages_total;
     int neuron;       // NEURON_*: the epilogue adds G (T4 + identity) or multiplies by 2 X (T2)
     const void *xin;  // X (N x H x W x C) for T2, else unused
-    FastDiv fd_hw, fd_w, fd_o, fd_kw, fd_sh, fd_sw;
+    // Position-major pixel order (channel-aligned kernels, the proposed neuron
+    // only): GEMM column m is input position m / N of image m % N, at NHWC row
+    // (m % N) H W + m / N; a tile's K range is the taps whose output pixel lies
+    // in the map for some position of the tile, ops = O / KE steps each.
+    int pm, ops;
+    FastDiv fd_hw, fd_w, fd_o, fd_kw, fd_sh, fd_sw, fd_n, fd_ops;
 };
 
 // Weight/bias gradients: rows = k' = (r, q, c), columns = (t, o), K = output pixels.

@@ -57,8 +57,31 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
     const int split = bid / tiles;
     bid -= split * tiles;
     const int rt = bid % a.row_tiles, ct = bid / a.row_tiles;
+    // Position-major order (CA): the taps whose output pixel lies in the map
+    // for some position of this pixel tile (a wave-uniform mask); the tile's K
+    // range is those taps only.
+    uint32_t tmask = 0;
+    int kst = a.stages_total;
+    if (CA && a.pm) {
+        const int m_hi = min(ct * BCOL + BCOL, a.M) - 1;
+        for (int pos = (int)fdiv((uint32_t)(ct * BCOL), a.fd_n); pos <= (int)fdiv((uint32_t)m_hi, a.fd_n); ++pos) {
+            const int h = (int)fdiv((uint32_t)pos, a.fd_w);
+            const int i0 = h + a.PH, j0 = pos - h * a.W + a.PW;  // output pixel of tap (0, 0)
+            for (int r = 0; r < a.KH; ++r)
+                for (int q = 0; q < a.KW; ++q)
+                    if ((unsigned)(i0 - r) < (unsigned)a.HO && (unsigned)(j0 - q) < (unsigned)a.WO)
+                        tmask |= 1u << (r * a.KW + q);
+        }
+        kst = __builtin_popcount(tmask) * a.ops;
+    }
     const int s_begin = split * a.stages_per_split;
-    const int nst = min(a.stages_per_split, a.stages_total - s_begin);
+    const int nst = max(0, min(a.stages_per_split, kst - s_begin));
+    // NHWC row of GEMM column m
+    auto prow = [&](int m) -> int {
+        if (!CA || !a.pm) return m;
+        const int pos = (int)fdiv((uint32_t)m, a.fd_n);
+        return (m - pos * a.N) * a.H * a.W + pos;
+    };
 
     const T *__restrict__ gsrc[3] = {static_cast<const T *>(a.gy), static_cast<const T *>(a.ta),
                                      static_cast<const T *>(a.tb)};
@@ -122,8 +145,14 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
 #pragma unroll
         for (int j = 0; j < NIP; ++j) {
             const int m = min(ct * BCOL + 16 * (4 * j + wave) + (lane >> 2), a.M - 1);
-            const int n = (int)fdiv((uint32_t)m, a.fd_hw);
-            const int rem = m - n * a.H * a.W;
+            int n, rem;
+            if (a.pm) {
+                rem = (int)fdiv((uint32_t)m, a.fd_n);
+                n = m - rem * a.N;
+            } else {
+                n = (int)fdiv((uint32_t)m, a.fd_hw);
+                rem = m - n * a.H * a.W;
+            }
             const int h = (int)fdiv((uint32_t)rem, a.fd_w);
             const int w = rem - h * a.W;
             const int i0 = h + a.PH, j0 = w + a.PW;  // output pixel of tap (0, 0)
@@ -141,9 +170,20 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
         char *base = smem + slot * STAGE + wave * 1024;
         DmaPart part(lo, hi);
         if constexpr (CA) {
-            const int k0 = min(s, a.stages_total - 1) * KE;
-            const int tap = (int)fdiv((uint32_t)k0, a.fd_o);
-            const int o0 = k0 - tap * a.O;
+            int tap, o0;
+            if (a.pm) {
+                // step s: output channels ((s mod ops) KE ..) of the tile's (s / ops)-th tap
+                const int sc = max(0, min(s, kst - 1));  // (dead steps past the range re-read a valid one)
+                const int ti = (int)fdiv((uint32_t)sc, a.fd_ops);
+                o0 = (sc - ti * a.ops) * KE;
+                uint32_t rest = tmask;
+                for (int i = 0; i < ti; ++i) rest &= rest - 1;
+                tap = rest ? __builtin_ctz(rest) : 0;
+            } else {
+                const int k0 = min(s, a.stages_total - 1) * KE;
+                tap = (int)fdiv((uint32_t)k0, a.fd_o);
+                o0 = k0 - tap * a.O;
+            }
             const int r = (int)fdiv((uint32_t)tap, a.fd_kw);
             const int q = tap - r * a.KW;
             const long long sw = ((long long)o0 * khkw + tap) * a.C;
@@ -279,7 +319,9 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
     const int pcol0 = ct * BCOL + wc * (BCOL / WGC);
     // The neuron type's last step (whole K range only; split partials get it
     // in the reduction): the shortcut of T4 + identity adds G at the same pixel
-    // and channel (C == O, unchanged map), T2's square contributes 2 X.
+    // and channel (C == O, unchanged map), T2's square contributes 2 X.  (These
+    // types run in image-major order: the planner sets pm for the proposed
+    // neuron only.)
     if constexpr (OM == OM_PAIR || OM == OM_SQIN) {
         if (a.splits == 1 && (OM == OM_SQIN || a.neuron == NEURON_T4I))
             neuron_dx_epilogue<T, OM, MR, MC>(acc, OM == OM_SQIN ? a.xin : a.gy, a.M, a.C, pcol0, crow0, lane);
@@ -318,7 +360,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
             const int row = c / CPR, cc = c % CPR;
             const int m = ct * BCOL + row, ch = rt * BR + cc * (16 / E);
             if (m < a.M && ch < a.C)
-                *reinterpret_cast<v4u *>(out + (size_t)m * a.C + ch) = lds_read16(smem + row * PITCH + cc * 16);
+                *reinterpret_cast<v4u *>(out + (size_t)prow(m) * a.C + ch) = lds_read16(smem + row * PITCH + cc * 16);
         }
         return true;
     };
@@ -333,7 +375,7 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
             for (int g = 0; g < 4; ++g) {
                 const int c = crow0 + mr * 32 + 8 * g + 4 * lhi;
                 if (c >= a.C) continue;
-                const size_t off = (size_t)m * a.C + c;
+                const size_t off = (size_t)prow(m) * a.C + c;
                 const float v0 = acc[mr][mc][4 * g], v1 = acc[mr][mc][4 * g + 1];
                 const float v2 = acc[mr][mc][4 * g + 2], v3 = acc[mr][mc][4 * g + 3];
                 if (a.splits == 1) {

@@ -187,6 +187,30 @@ inline bool pm_default(const Geom &g, int env) {
     return g.HO * g.WO <= 4 && (g.PH > 0 || g.PW > 0);
 }
 
+// Input gradient at stride 1: the taps (r, q) whose output pixel
+// (h + PH - r, w + PW - q) lies in the map, for input position pos = h W + w.
+inline uint32_t bd_tap_mask(const Geom &g, int pos) {
+    const int h = pos / g.W, w = pos % g.W;
+    uint32_t u = 0;
+    for (int r = 0; r < g.KH; ++r)
+        for (int q = 0; q < g.KW; ++q)
+            if (h + g.PH - r >= 0 && h + g.PH - r < g.HO && w + g.PW - q >= 0 && w + g.PW - q < g.WO)
+                u |= 1u << (r * g.KW + q);
+    return u;
+}
+
+// The most taps any pixel tile of bcol position-major columns keeps.
+inline int bd_pm_max_taps(const Geom &g, int bcol, long long M) {
+    int best = 0;
+    for (long long m0 = 0; m0 < M; m0 += bcol) {
+        const long long m1 = std::min(M, m0 + bcol) - 1;
+        uint32_t u = 0;
+        for (long long pos = m0 / g.N; pos <= m1 / g.N; ++pos) u |= bd_tap_mask(g, (int)pos);
+        best = std::max(best, __builtin_popcount(u));
+    }
+    return best;
+}
+
 // ---------------------------------------------------------------------------
 // Forward planning.
 // ---------------------------------------------------------------------------
@@ -358,6 +382,7 @@ struct BwdDataPlan {
     bool smallc;  // C <= 4: per-pixel partial sums by MFMA, then a gather over the taps
     bool narrow;  // at most 32 input channels, short K: qconv_bwd_data_narrow_kernel (CB row blocks, NCH chunks)
     int cb, nch;
+    bool ca, pm;  // channel-aligned K steps; position-major order with taps skipped (BwdDataArgs)
     int fused_rb; // ... stride 1: both steps in one kernel, bands of fused_rb input rows (0: two kernels)
     size_t fused_smem;
     int njb;      // ... 32-column blocks of (r, q, c)
@@ -431,7 +456,16 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
     p.row_tiles = cdiv(g.C, p.BR);
     p.col_tiles = cdiv(M, p.BCOL);
     p.stages_total = cdiv(K, p.KE);
-    plan_splits(p.row_tiles * p.col_tiles, p.stages_total, env_override("QLAYER_BWD_DATA_MINSTAGES", 4),
+    // Channel-aligned K steps (each within one tap) in the 4-wave kernels, and
+    // with them, on small padded maps, the position-major order that skips
+    // the taps whose output pixel lies outside the map for every position of
+    // a pixel tile (the proposed neuron: 5 of 9 taps on a 2 x 2 map).
+    p.ca = p.s1 && p.natw && p.cfg != 4 && g.O % p.KE == 0 && g.KH * g.KW <= 32 &&
+           env_override("QLAYER_BWD_DATA_CA", 1) != 0;
+    p.pm = p.ca && g.ne == NEURON_QUADRA && pm_default(g, env_override("QLAYER_BWD_DATA_POSMAJ", -1));
+    int kst = p.stages_total;
+    if (p.pm) kst = bd_pm_max_taps(g, p.BCOL, M) * (g.O / p.KE);
+    plan_splits(p.row_tiles * p.col_tiles, kst, env_override("QLAYER_BWD_DATA_MINSTAGES", 4),
                 (size_t)M * g.C * 4, p.slots, p.splits, p.sps);
     p.wt_bytes = p.natw ? 0 : align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * M * g.C * sizeof(float)) : 0;

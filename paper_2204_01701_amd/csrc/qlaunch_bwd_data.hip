@@ -86,6 +86,10 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.fd_sw = make_fastdiv(g.SW);
     a.neuron = g.ne;
     a.xin = xin;
+    a.pm = p.pm ? 1 : 0;
+    a.ops = std::max(1, g.O / p.KE);
+    a.fd_n = make_fastdiv(g.N);
+    a.fd_ops = make_fastdiv(a.ops);
     if (p.narrow) {
         const dim3 grid((unsigned)(narrow_waves(a.M) / (kThreads / 64)));
 #define QL_BD_NARROW(CB, NCH)                                                                                        \
@@ -112,8 +116,7 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     }
     const dim3 grid(p.row_tiles * p.col_tiles * p.splits), block(kThreads);
     // channel-aligned K steps (each within one tap): stride 1, natural weight tiles, O a multiple of KE
-    const bool bd_ca = p.s1 && p.natw && g.O % p.KE == 0 && g.KH * g.KW <= 32 &&
-                       env_override("QLAYER_BWD_DATA_CA", 1) != 0;
+    const bool bd_ca = p.ca;
     const int om = g.om();
 #define QL_BD_PIPE_N(BR, BCOL, WR, WC, NS, NW, OM)                                                                     \
     do {                                                                                                               \

@@ -5,7 +5,9 @@ off, on shapes where tiles hold one position, several positions, ragged
 tails, stride 2, 5 x 5 filters and positions with no tap in bounds at all
 (their outputs are the bias terms alone; eq:2ndneuron3 with every product
 term zero).  Each shape runs in the tiled kernel and in the small-output
-kernel whose waves split K (qconv_fwd_ksplit.h)."""
+kernel whose waves split K (qconv_fwd_ksplit.h); in bf16 at stride 1 the
+input gradient's channel-aligned kernel takes the same order (its taps whose
+output pixel lies outside the map skipped)."""
 import pytest
 import torch
 
@@ -48,6 +50,7 @@ def test_tap_skipping_matches_oracle(shape, bf16, order, kernel, monkeypatch):
     N, C, H, W, O, KH, KW, s, p = shape
     print(f"tap skipping order={order} ksplit={kernel} shape={shape} bf16={bf16}", flush=True)
     monkeypatch.setenv("QLAYER_FWD_POSMAJ", order)
+    monkeypatch.setenv("QLAYER_BWD_DATA_POSMAJ", order)  # (bf16, stride 1: the input gradient's order too)
     monkeypatch.setenv("QLAYER_FWD_KSPLIT", kernel)  # the tiled kernel, or the small-output one
     if order == "0":  # the channel-aligned K steps without the position-major order
         monkeypatch.setenv("QLAYER_FWD_CA", "1")
