@@ -10,7 +10,9 @@
 //   G_a = G o T_b,  G_b = G o T_a,  G_c = G
 //
 // The tile is the whole gradient: all k' rows (NF fragments of 16) by the 16
-// output channels of all three terms, so every MFMA is useful work.  Each
+// output channels of all three terms, so every MFMA is useful work (wider
+// layers, up to 64 channels such as the 3-channel stem of a CIFAR VGG-16,
+// take one 16-channel slice per workgroup row of the grid).  Each
 // wave runs its own contiguous range of K steps (KE output pixels) with a
 // private LDS area and no barriers:
 //   - its lanes load the step's im2col rows of X (one 16-byte run of k' per
@@ -86,8 +88,11 @@ __device__ __forceinline__ void bwd_weight_narrow_body(const BwdWeightArgs &a, c
         xr[i] = (int)fdiv((uint32_t)tap, a.fd_kw);
         xq[i] = tap - xr[i] * a.KW;
     }
-    const int o0 = VEC * rg;  // this lane's G-side run: channels o0 .. o0 + VEC
-    const bool ook = o0 < a.O;
+    // this workgroup's 16 output channels ob0 .. ob0 + 16 (blockIdx.y), and
+    // this lane's G-side run of them: channels ob0 + o0 .. + VEC
+    const int ob0 = blockIdx.y * 16;
+    const int o0 = VEC * rg;
+    const bool ook = ob0 + o0 < a.O;
 
     // this wave's K steps: a contiguous quarter of the workgroup's
     const int split = blockIdx.x;
@@ -113,7 +118,7 @@ __device__ __forceinline__ void bwd_weight_narrow_body(const BwdWeightArgs &a, c
             xv[i] = ok ? *reinterpret_cast<const v4u *>(x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + xc[i]) : zero;
         }
         const bool gok = mok && ook;
-        const size_t off = (size_t)mm * a.O + o0;
+        const size_t off = (size_t)mm * a.O + ob0 + o0;
 #pragma unroll
         for (int u = 0; u < 3; ++u) gv[u] = gok ? *reinterpret_cast<const v4u *>(gsrc[u] + off) : zero;
     };
@@ -235,7 +240,7 @@ __device__ __forceinline__ void bwd_weight_narrow_body(const BwdWeightArgs &a, c
         __syncthreads();
     }
     if (wave != 0) return;
-    const int o = lane & 15, lg = lane >> 4;
+    const int ol = lane & 15, o = ob0 + ol, lg = lane >> 4;
     // dW_t rows as stored: KH KW C_out (X zero-padded to C channels: the padded columns are dropped)
     const bool padded = a.C_out != a.C;
     const int KPO = a.KH * a.KW * a.C_out;
@@ -262,8 +267,8 @@ __device__ __forceinline__ void bwd_weight_narrow_body(const BwdWeightArgs &a, c
         }
         if constexpr (SUM) {
             if (lg == 0 && o < a.O) {
-                const float tot = dred[(0 * 3 + t) * 16 + o] + dred[(1 * 3 + t) * 16 + o] +
-                                  dred[(2 * 3 + t) * 16 + o] + dred[(3 * 3 + t) * 16 + o];
+                const float tot = dred[(0 * 3 + t) * 16 + ol] + dred[(1 * 3 + t) * 16 + ol] +
+                                  dred[(2 * 3 + t) * 16 + ol] + dred[(3 * 3 + t) * 16 + ol];
                 if (a.splits == 1) a.db[t][o] = tot;
                 else a.ws_db[((size_t)split * 3 + t) * a.O + o] = tot;
             }

@@ -489,8 +489,8 @@ constexpr int kBwThreads[kBwCfgs] = {256, 256, 256, 256, 512, 512};
 constexpr int kBwPipes[kBwCfgs] = {1, 1, 1, 1, 2, 1};  // pipelines per workgroup (K halves)
 
 struct BwdWeightPlan {
-    bool narrow;  // at most 16 output channels, KH KW C <= 144: qconv_bwd_weight_narrow_kernel (NF fragments)
-    int nf;
+    bool narrow;  // KH KW C <= 144: qconv_bwd_weight_narrow_kernel (NF fragments, NOB 16-channel slices)
+    int nf, nob;
     int cfg;   // pipelined path only
     bool pipe; // bf16 and vectorizable: pipelined kernel; otherwise the generic one
     int BKP, BO, KE, slots;
@@ -505,9 +505,14 @@ struct BwdWeightPlan {
 // plans for its fixed scratch array).
 inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMaxSplitBytes) {
     BwdWeightPlan p{};
-    // the narrow kernel: at most 16 output channels, rows k' of at most 144 (after the channel padding)
+    // the narrow kernel: rows k' of at most 144 (after the channel padding)
     const int cp_small = g.pad_small_c() ? g.cpad() : g.C;
-    const bool narrow_shape = g.ne == NEURON_QUADRA && g.O <= 16 && g.O % g.vec() == 0 && cp_small % g.vec() == 0 &&
+    // (wider layers, up to 64 channels, in 16-channel slices, one per workgroup row of the
+    // grid: by default in fp32, where the 16 -> 32-channel stride-2 CIFAR ResNet layer
+    // measured 37 against 66 us per call; in bf16 it and the VGG-16 stem were no faster)
+    const int narrow_max_o = env_override("QLAYER_BWD_WEIGHT_NARROW_MAXO", g.dt == QL_F32 ? 64 : 16);
+    const bool narrow_shape = g.ne == NEURON_QUADRA && (g.O <= 16 || (g.O % 16 == 0 && g.O <= narrow_max_o)) &&
+                              g.O % g.vec() == 0 && cp_small % g.vec() == 0 &&
                               cdiv(g.KH * g.KW * cp_small, 16) <= 9 &&
                               env_override("QLAYER_BWD_WEIGHT_NARROW", 1) != 0;
     // (fp32 pads only for the narrow kernel)
@@ -523,13 +528,15 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMa
     p.stages_total = cdiv(M, p.KE);
     const int min_stages = env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16);
     const size_t bytes_per_split = (size_t)3 * g.O * KPO * 4;
-    // Narrow layers: the whole gradient is one tile; about two workgroups per CU,
-    // at least four K steps per wave, the partial sums within max_split_bytes.
+    // Narrow layers: the whole gradient of a 16-channel slice is one tile; about
+    // two workgroups per CU in all, at least four K steps per wave, the partial
+    // sums within max_split_bytes.
     p.nf = cdiv(KP, 16);
     if (narrow_shape && p.Cp == cp_small) {
         p.narrow = true;
+        p.nob = cdiv(g.O, 16);
         p.stages_total = cdiv(M, g.dt == QL_BF16 ? 32 : 16);
-        int splits = std::min(2 * kNumCUs, std::max(1, cdiv(p.stages_total, 16)));
+        int splits = std::min(std::max(1, 2 * kNumCUs / p.nob), std::max(1, cdiv(p.stages_total, 16)));
         splits = env_override("QLAYER_BWD_WEIGHT_NARROW_SPLITS", splits);
         splits = std::max(1, std::min(splits, (int)std::max<size_t>(1, max_split_bytes / bytes_per_split)));
         p.sps = cdiv(p.stages_total, splits);

@@ -87,7 +87,7 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.neuron = g.ne;
     a.xin = xin;
     a.pm = p.pm ? 1 : 0;
-    a.ops = std::max(1, g.O / p.KE);
+    a.ops = p.KE > 0 ? std::max(1, g.O / p.KE) : 1;  // (the narrow and few-channel plans set no K step)
     a.fd_n = make_fastdiv(g.N);
     a.fd_ops = make_fastdiv(a.ops);
     if (p.narrow) {

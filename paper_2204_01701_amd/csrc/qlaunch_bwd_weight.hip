@@ -81,7 +81,7 @@ ql_status launch_bwd_weight(const Geom &g, const BwdWeightPlan &p, const void *x
     a.neuron = g.ne;
     if (p.narrow) {
 #define QL_BW_NARROW(NF) \
-    hipLaunchKernelGGL((qconv_bwd_weight_narrow_kernel<T, NF>), dim3(p.splits), dim3(kThreads), 0, st, a)
+    hipLaunchKernelGGL((qconv_bwd_weight_narrow_kernel<T, NF>), dim3(p.splits, p.nob), dim3(kThreads), 0, st, a)
         switch (p.nf) {
             case 1: QL_BW_NARROW(1); break;
             case 2: QL_BW_NARROW(2); break;
