@@ -340,6 +340,7 @@ _KERNEL_FAMILY = [
     (r"qconv_fwd_generic_kernel<", "fwd", True),
     (r"qconv_fwd_smallc_kernel<", "fwd", True),
     (r"qconv_fwd_narrow_kernel<", "fwd", True),
+    (r"qconv_fwd_ksplit_kernel<", "fwd", True),
     (r"qconv_fwd_combine_kernel<", "fwd", False),
     (r"qconv_pad_channels_kernel<[^,>]+, 4>", "fwd", False),
     (r"qconv_bwd_data_kernel<", "bwd_data", True),

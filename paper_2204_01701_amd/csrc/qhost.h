@@ -526,7 +526,9 @@ inline BwdWeightPlan plan_bwd_weight(const Geom &g, size_t max_split_bytes = kMa
     if (p.pad) p.xpad_bytes = align_up((size_t)g.N * g.H * g.W * p.Cp * g.esize());
     p.KE = 64 / (int)g.esize();
     p.stages_total = cdiv(M, p.KE);
-    const int min_stages = env_override("QLAYER_BWD_WEIGHT_MINSTAGES", 16);
+    // (the generic kernel's K steps are latency-bound: splits down to one step
+    // each, e.g. the 64 -> 10 head of a CIFAR ResNet at batch 256, 53 -> 17 us)
+    const int min_stages = env_override("QLAYER_BWD_WEIGHT_MINSTAGES", p.pipe ? 16 : 1);
     const size_t bytes_per_split = (size_t)3 * g.O * KPO * 4;
     // Narrow layers: the whole gradient of a 16-channel slice is one tile; about
     // two workgroups per CU in all, at least four K steps per wave, the partial
