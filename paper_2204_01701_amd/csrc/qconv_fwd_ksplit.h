@@ -9,15 +9,16 @@
 // go through HBM to a combine kernel.  Here a workgroup's tile is small
 // (3 x 16 RB weight rows by 16 CB pixels), so that the tiles alone fill the
 // GPU, and the four waves of the workgroup split the tile's K range:
-//   - each wave loads its MFMA operands straight from global memory into
-//     registers in fragment layout, as in qconv_fwd_narrow.h: the 16 x 16
-//     operand of a lane is one 16-byte run of the reduction index within one
-//     tap, contiguous in an OHWI weight row and in a pixel's NHWC channels;
-//     the runs of the next few chunks are in flight during the current
-//     chunk's MFMAs, and the loop has no LDS traffic and no barrier;
+//   - each wave copies its chunks (32 bf16 or 16 fp32 reduction values
+//     within one tap: 64 contiguous bytes of each OHWI weight row and of each
+//     pixel's NHWC channels) into a private LDS ring with buffer loads, one
+//     coalesced instruction per 16-row fragment (the swizzled 64-byte-row
+//     layout of qpipe.h), and reads each MFMA operand back as one 16-byte
+//     run per lane; its waits are its own (vmcnt, lgkmcnt), with no barrier
+//     in the loop;
 //   - the waves' fp32 accumulators are then added through LDS in wave order
 //     (a fixed order, so results are bitwise repeatable), and each wave
-//     finishes a quarter of the tile's 16 x 16 blocks: the biases,
+//     finishes its share of the tile's 16 x 16 blocks: the biases,
 //     Y = T_a o T_b + T_c, the fused scale / shift / ReLU and statistics, the
 //     stores of Y, T_a and T_b.  No term map leaves the chip unfinished.
 // The K range of a tile is its in-bounds taps only (the union over its
@@ -199,9 +200,7 @@ __global__ __launch_bounds__(kThreads, 4 * NS * (3 * RB + CB) * 1024 > 80 * 1024
     // (vmcnt, lgkmcnt) and there is no barrier; the copies are asm the
     // compiler cannot order against LDS reads, hence the explicit waits with
     // memory clobbers.  (One register set: the reads of chunk k + 1 overlap the
-    // MFMAs of chunk k in the matrix pipeline, and the accumulators stay in
-    // place, where two alternating sets made the compiler rotate them through
-    // copies.)
+    // MFMAs of chunk k in the matrix pipeline.)
     constexpr int VMC = (NS - 1) * NF;
     constexpr int VM_IMM = (VMC & 15) | ((VMC >> 4) << 14) | (7 << 4) | (15 << 8);
 #pragma unroll
