@@ -19,7 +19,8 @@ pytestmark = pytest.mark.gpu
 
 SHAPES = [(2, 16, 8, 8, 32, 3, 3, 1, 1), (2, 64, 4, 4, 64, 3, 3, 1, 1), (1, 5, 6, 6, 7, 3, 3, 2, 1),
           (4, 16, 16, 16, 32, 3, 3, 1, 1),
-          (4, 16, 12, 12, 16, 3, 3, 1, 1)]  # (the narrow kernels of all three passes)
+          (4, 16, 12, 12, 16, 3, 3, 1, 1),  # (the narrow kernels of all three passes)
+          (16, 64, 2, 2, 64, 3, 3, 1, 1)]   # (position-major small-output forward and input gradient)
 
 
 def _eq(a, b):
