@@ -98,6 +98,7 @@ struct BwdDataArgs {
     // (m % N) H W + m / N; a tile's K range is the taps whose output pixel lies
     // in the map for some position of the tile, ops = O / KE steps each.
     int pm, ops;
+    int order;  // block order of the split-K grid (tile_coord)
     FastDiv fd_hw, fd_w, fd_o, fd_kw, fd_sh, fd_sw, fd_n, fd_ops;
 };
 

@@ -52,11 +52,8 @@ __global__ __launch_bounds__(kThreads) void qconv_bwd_data_kernel(const BwdDataA
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
     const int wr = wave / WGC, wc = wave % WGC;
-    int bid = xcd_remap(blockIdx.x, gridDim.x);
-    const int tiles = a.row_tiles * a.col_tiles;
-    const int split = bid / tiles;
-    bid -= split * tiles;
-    const int rt = bid % a.row_tiles, ct = bid / a.row_tiles;
+    const TileCoord tc = tile_coord(xcd_remap(blockIdx.x, gridDim.x), a.order, a.row_tiles, a.col_tiles, a.splits);
+    const int split = tc.split, rt = tc.rt, ct = tc.ct;
     // Position-major order (CA): the taps whose output pixel lies in the map
     // for some position of this pixel tile (a wave-uniform mask); the tile's K
     // range is those taps only.

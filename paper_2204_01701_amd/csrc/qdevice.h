@@ -282,4 +282,36 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblk) {
     return (bid & 7) * (full >> 3) + (bid >> 3);
 }
 
+// Logical block -> (split, row tile, column tile) of a split-K grid, in one of
+// three orders; with xcd_remap, the order decides what the blocks of one XCD
+// share, and so which operand each XCD reads whole from beyond its L2:
+//   0 split-major   (split, column tile, row tile): a K range;
+//   1 tile-major    (column tile, row tile, split): output tiles, all K;
+//   2 row-major     (row tile, split, column tile): the K rows of a row tile.
+struct TileCoord {
+    int split, rt, ct;
+};
+__device__ __forceinline__ TileCoord tile_coord(int bid, int order, int row_tiles, int col_tiles, int splits) {
+    TileCoord c;
+    if (order == 1) {
+        c.split = bid % splits;
+        bid /= splits;
+        c.rt = bid % row_tiles;
+        c.ct = bid / row_tiles;
+    } else if (order == 2) {
+        const int per = splits * col_tiles;
+        c.rt = bid / per;
+        bid -= c.rt * per;
+        c.split = bid / col_tiles;
+        c.ct = bid - c.split * col_tiles;
+    } else {
+        const int tiles = row_tiles * col_tiles;
+        c.split = bid / tiles;
+        bid -= c.split * tiles;
+        c.rt = bid % row_tiles;
+        c.ct = bid / row_tiles;
+    }
+    return c;
+}
+
 }  // namespace ql

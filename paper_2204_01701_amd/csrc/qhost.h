@@ -383,6 +383,7 @@ struct BwdDataPlan {
     bool narrow;  // at most 32 input channels, short K: qconv_bwd_data_narrow_kernel (CB row blocks, NCH chunks)
     int cb, nch;
     bool ca, pm;  // channel-aligned K steps; position-major order with taps skipped (BwdDataArgs)
+    int order;  // block order of the split-K grid (tile_coord)
     int fused_rb; // ... stride 1: both steps in one kernel, bands of fused_rb input rows (0: two kernels)
     size_t fused_smem;
     int njb;      // ... 32-column blocks of (r, q, c)
@@ -467,6 +468,18 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
     if (p.pm) kst = bd_pm_max_taps(g, p.BCOL, M) * (g.O / p.KE);
     plan_splits(p.row_tiles * p.col_tiles, kst, env_override("QLAYER_BWD_DATA_MINSTAGES", 4),
                 (size_t)M * g.C * 4, p.slots, p.splits, p.sps);
+    // Block order of the split grid: tile-major (each XCD's blocks share pixel
+    // tiles and read all of the weights) unless the weights outweigh G, T_a, T_b
+    // by more than 4x (the 2 x 2 maps of a CIFAR VGG-16: split-major, each XCD
+    // reading its K range of the weights).  Measured on the VGG-16 layers at
+    // batch 128 (bitwise the same results in every order): tile-major 0.3-1.4
+    // us per call faster on layers 5-10 (34.0 -> 33.1 us on layer 5), 1 us
+    // slower on the 2 x 2 layers 11-13.
+    {
+        const int dflt = 4LL * M >= (long long)g.C * g.KH * g.KW ? 1 : 0;
+        p.order = p.splits > 1 ? env_override("QLAYER_BWD_DATA_ORDER", dflt) : 0;
+        if (p.order < 0 || p.order > 2) p.order = 0;
+    }
     p.wt_bytes = p.natw ? 0 : align_up(3 * (size_t)g.O * g.KH * g.KW * g.C * g.esize());
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * M * g.C * sizeof(float)) : 0;
     p.ws_bytes = p.wt_bytes + p.part_bytes;

@@ -90,6 +90,7 @@ ql_status launch_bwd_data(const Geom &g, const BwdDataPlan &p, const void *gy, c
     a.ops = p.KE > 0 ? std::max(1, g.O / p.KE) : 1;  // (the narrow and few-channel plans set no K step)
     a.fd_n = make_fastdiv(g.N);
     a.fd_ops = make_fastdiv(a.ops);
+    a.order = p.order;
     if (p.narrow) {
         const dim3 grid((unsigned)(narrow_waves(a.M) / (kThreads / 64)));
 #define QL_BD_NARROW(CB, NCH)                                                                                        \

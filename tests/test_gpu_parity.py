@@ -122,3 +122,29 @@ def test_conv_tile_configs(env, cfg, shape, bf16, monkeypatch):
     for k in KEYS_FWD + KEYS_GRAD:
         e = qlh.relerr(got[k], ref[k])
         assert e <= qlh.tol(bf16, k in KEYS_GRAD), f"{k}: normwise relative error {e:.3e}"
+
+
+# Block orders of the input gradient's split-K grid (split-major, tile-major,
+# row-major), forced through the planner's override on layers whose input
+# gradient splits K: the same split partials in every order, so the same bits,
+# and within the oracle's limit.
+ORDER_SHAPES = [(16, 256, 4, 4, 256, 3, 3, 1, 1), (8, 128, 8, 8, 256, 3, 3, 1, 1), (3, 72, 5, 6, 96, 3, 3, 1, 1),
+                (32, 512, 2, 2, 512, 3, 3, 1, 1)]
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("shape", ORDER_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_bwd_data_block_orders(shape, bf16, monkeypatch):
+    N, C, H, W, O, KH, KW, s, p = shape
+    print(f"bwd_data block orders shape={shape} bf16={bf16}", flush=True)
+    inp = synth.random_conv_case([301] + list(shape), N, C, H, W, O, KH, KW, s, p, bf16=bf16)
+    ref = _oracle_all(inp, s, p)
+    dx = []
+    for order in (0, 1, 2):
+        monkeypatch.setenv("QLAYER_BWD_DATA_ORDER", str(order))
+        got = qlh.conv_to_np(qlh.run_conv(inp, s, p, bf16))
+        e = qlh.relerr(got["dx"], ref["dx"])
+        assert e <= qlh.tol(bf16, True), f"order {order}: normwise relative error {e:.3e}"
+        dx.append(got["dx"])
+    for order in (1, 2):
+        assert np.array_equal(dx[0], dx[order]), f"order {order} differs from order 0"
