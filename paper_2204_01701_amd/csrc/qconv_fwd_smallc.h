@@ -17,8 +17,14 @@
 //   - the epilogue forms Y = T_a o T_b + T_c, applies the fused epilogue
 //     y' = relu(scale y + shift) when asked, and writes Y, T_a, T_b through a
 //     per-wave LDS tile: the 32 pixels are 32 consecutive NHWC rows, so each
-//     map's block is one contiguous run of 32 O elements, copied out in
-//     16-byte chunks.
+//     map's tile is one contiguous run of 32 O elements, copied out in
+//     16-byte chunks.  In bf16 the tile holds whole rows (all O channels) of
+//     one map, so the chunks cover whole 128-byte cache lines (a 32-channel
+//     block alone is half a line); the MFMAs of a map's terms are then redone
+//     per map (Y: all three, T_a and T_b: one), a few more cycles of an
+//     otherwise idle unit, so that one 32-channel block of accumulators is
+//     live.  In fp32 a 32-channel block is a whole line: the tile holds one
+//     block of each map in turn, and the three terms' MFMAs run once.
 // The layer is bound by the stores of Y, T_a and T_b.
 #pragma once
 
@@ -57,8 +63,10 @@ __global__ __launch_bounds__(kThreads, 4) void qconv_fwd_smallc_kernel(const Fwd
     constexpr int NB = smallc_bias_cols<T>();
     constexpr int E = (int)sizeof(T);
     constexpr int O = 32 * OB;
-    constexpr int PITCH = 32 * E + 16;            // LDS bytes per staged pixel row (one 32-channel block)
-    constexpr int CPR = 32 * E / 16;              // 16-byte chunks per staged row
+    constexpr bool ROWS = E == 2;                 // bf16: whole rows of one map per tile
+    constexpr int SB = ROWS ? O : 32;             // channels of a staged pixel row
+    constexpr int PITCH = SB * E + 16;            // LDS bytes per staged pixel row
+    constexpr int CPR = SB * E / 16;              // 16-byte chunks per staged row
     constexpr int NWAVE = kThreads / 64;
     constexpr int NWF = 3 * OB * NKC;             // weight fragments
     __shared__ __attribute__((aligned(16))) v4u wfr[NWF][64];
@@ -147,45 +155,70 @@ __global__ __launch_bounds__(kThreads, 4) void qconv_fwd_smallc_kernel(const Fwd
         }
         const long long m0 = gi * 32;
         if (gi + stride < ngroups) gather(gi + stride);
-#pragma unroll
-        for (int ob = 0; ob < OB; ++ob) {
-            f32x16_t acc[3];
+        // Map jm = 0: Y (through the fused epilogue), 1: T_a, 2: T_b.
+        // terms(): the accumulators of 32-channel block ob (only term jm - 1
+        // for map jm > 0 when `need` is set); emit(): block ob of map jm into
+        // channels 32 slot .. +32 of the staged rows; flush(): the staged
+        // rows of map jm to channels c0 .. c0 + SB of its 32 NHWC rows.
+        f32x16_t acc[3];
+        auto terms = [&](int ob, int jm, bool need) {
 #pragma unroll
             for (int t = 0; t < 3; ++t) {
+                if (need && jm != 0 && t != jm - 1) continue;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[t][v] = 0.0f;
 #pragma unroll
                 for (int kc = 0; kc < NKC; ++kc) mfma_chunk<T>(wfr[(t * OB + ob) * NKC + kc][lane], pf[kc], acc[t]);
             }
-            // Epilogue of channels 32 ob .. +32: map 0 = Y (through the fused
-            // epilogue), 1 = T_a, 2 = T_b.
+        };
+        auto emit = [&](int jm, int ob, int slot) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int ol = 8 * g + 4 * lhi;
+                float v[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int k = 4 * g + i;
+                    v[i] = jm == 1 ? acc[0][k] : (jm == 2 ? acc[1][k] : acc[0][k] * acc[1][k] + acc[2][k]);
+                    if constexpr (EPI) {
+                        if (jm == 0) v[i] = epi_apply(a.epi, 32 * ob + ol + i, v[i]);
+                    }
+                }
+                store4<T>(reinterpret_cast<T *>(buf + lrow * PITCH + (32 * slot + ol) * E), v[0], v[1], v[2], v[3]);
+            }
+        };
+        auto flush = [&](int jm, int c0) {
+            wave_lds_sync();
+            T *__restrict__ dst = outs[jm] + m0 * O + c0;
+#pragma unroll
+            for (int c = lane; c < 32 * CPR; c += 64) {
+                const int row = c / CPR, cc = c - (c / CPR) * CPR;
+                if (m0 + row < a.M)
+                    *reinterpret_cast<v4u *>(dst + (size_t)row * O + cc * (16 / E)) = lds_read16(buf + row * PITCH + cc * 16);
+            }
+            wave_lds_sync();  // the tile is read before the next map overwrites it
+        };
+        if constexpr (ROWS) {
 #pragma unroll
             for (int jm = 0; jm < 3; ++jm) {
                 if (!outs[jm]) continue;
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int ol = 8 * g + 4 * lhi;
-                    float v[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int k = 4 * g + i;
-                        v[i] = jm == 1 ? acc[0][k] : (jm == 2 ? acc[1][k] : acc[0][k] * acc[1][k] + acc[2][k]);
-                        if constexpr (EPI) {
-                            if (jm == 0) v[i] = epi_apply(a.epi, 32 * ob + ol + i, v[i]);
-                        }
-                    }
-                    store4<T>(reinterpret_cast<T *>(buf + lrow * PITCH + ol * E), v[0], v[1], v[2], v[3]);
+                for (int ob = 0; ob < OB; ++ob) {
+                    terms(ob, jm, true);
+                    emit(jm, ob, ob);
                 }
-                wave_lds_sync();
-                T *__restrict__ dst = outs[jm] + m0 * O + 32 * ob;
+                flush(jm, 0);
+            }
+        } else {
 #pragma unroll
-                for (int c = lane; c < 32 * CPR; c += 64) {
-                    const int row = c / CPR, cc = c - (c / CPR) * CPR;
-                    if (m0 + row < a.M)
-                        *reinterpret_cast<v4u *>(dst + (size_t)row * O + cc * (16 / E)) =
-                            lds_read16(buf + row * PITCH + cc * 16);
+            for (int ob = 0; ob < OB; ++ob) {
+                terms(ob, 0, false);
+#pragma unroll
+                for (int jm = 0; jm < 3; ++jm) {
+                    if (!outs[jm]) continue;
+                    emit(jm, ob, 0);
+                    flush(jm, 32 * ob);
                 }
-                wave_lds_sync();  // the tile is read before the next map overwrites it
             }
         }
     }
