@@ -66,6 +66,7 @@ def _load():
     lib.oracle_conv2d_bwd.argtypes = conv_geom + [_D] + w6 + [_D] + [_D] * 7
     lib.oracle_conv2d_fwd_at.argtypes = conv_geom + [_D] + w6 + [ctypes.c_longlong, _L, _D, _D, _D]
     lib.oracle_conv2d_dx_at.argtypes = conv_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
+    lib.oracle_conv2d_dx_pixels.argtypes = conv_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
     lib.oracle_conv2d_dw_channel.argtypes = conv_geom + [_D] + w6 + [_D, _I] + [_D] * 6
     lib.oracle_conv2d_fwd_neuron.argtypes = [_I] + conv_geom + [_D] + w6 + [_D, _D, _D]
     lib.oracle_conv2d_bwd_neuron.argtypes = [_I] + conv_geom + [_D] + w6 + [_D] + [_D] * 7
@@ -81,7 +82,7 @@ def _load():
     lib.oracle_linear_fwd_at.argtypes = fc_geom + [_D] + w6 + [ctypes.c_longlong, _L, _D, _D, _D]
     lib.oracle_linear_dx_rows.argtypes = fc_geom + [_D] + w6 + [_D, ctypes.c_longlong, _L, _D]
     lib.oracle_linear_dw_row.argtypes = fc_geom + [_D] + w6 + [_D, _I] + [_D] * 6
-    for f in ("oracle_dwconv2d_fwd", "oracle_dwconv2d_bwd", "oracle_conv2d_fwd_neuron", "oracle_conv2d_bwd_neuron", "oracle_conv2d_fwd", "oracle_conv2d_bwd", "oracle_conv2d_fwd_at", "oracle_conv2d_dx_at",
+    for f in ("oracle_dwconv2d_fwd", "oracle_dwconv2d_bwd", "oracle_conv2d_fwd_neuron", "oracle_conv2d_bwd_neuron", "oracle_conv2d_fwd", "oracle_conv2d_bwd", "oracle_conv2d_fwd_at", "oracle_conv2d_dx_at", "oracle_conv2d_dx_pixels",
               "oracle_conv2d_dw_channel", "oracle_linear_fwd", "oracle_linear_bwd",
               "oracle_linear_fwd_at", "oracle_linear_dx_rows", "oracle_linear_dw_row"):
         getattr(lib, f).restype = None
@@ -174,6 +175,19 @@ def conv2d_dx_at(x, wa, wb, wc, ba, bb, bc, gy, idx, stride=1, pad=0):
     dx = np.empty(k)
     lib.oracle_conv2d_dx_at(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy), k,
                             _pl(idx), _p(dx))
+    return dx
+
+
+def conv2d_dx_pixels(x, wa, wb, wc, ba, bb, bc, gy, pix, stride=1, pad=0):
+    """dX at every input channel of the input pixels pix (k x 3 array of (n, h, w)): k x C."""
+    lib = _load()
+    x, wa, wb, wc, ba, bb, bc, gy = map(_f64, (x, wa, wb, wc, ba, bb, bc, gy))
+    g = _conv_geom(x, wa, stride, pad)
+    pix = np.ascontiguousarray(np.asarray(pix, dtype=np.int64).reshape(-1, 3))
+    k = pix.shape[0]
+    dx = np.empty((k, x.shape[1]))
+    lib.oracle_conv2d_dx_pixels(*g, _p(x), _p(wa), _p(wb), _p(wc), _p(ba), _p(bb), _p(bc), _p(gy), k,
+                                _pl(pix), _p(dx))
     return dx
 
 

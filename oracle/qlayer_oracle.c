@@ -582,6 +582,45 @@ void oracle_conv2d_dx_at(int N, int C, int H, int W, int O, int KH, int KW,
     }
 }
 
+/* dX at every input channel of count input pixels pix[3*k..] = (n, h, w),
+ * into dx[k*C + c]: the gather form of oracle_conv2d_dx_at, with T_a and T_b
+ * of each output pixel a tap reaches regenerated once and used for all C
+ * channels (the same terms added in the same order per element). */
+void oracle_conv2d_dx_pixels(int N, int C, int H, int W, int O, int KH, int KW,
+                             int sh, int sw, int ph, int pw,
+                             const double *x, const double *wa, const double *wb, const double *wc,
+                             const double *ba, const double *bb, const double *bc,
+                             const double *gy, long long count, const long long *pix, double *dx) {
+    (void)N; (void)bc;
+    int Ho = out_size(H, KH, sh, ph), Wo = out_size(W, KW, sw, pw);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (long long k = 0; k < count; ++k) {
+        int n = (int)pix[3 * k], h = (int)pix[3 * k + 1], w_ = (int)pix[3 * k + 2];
+        double *acc = dx + (size_t)k * C;
+        for (int c = 0; c < C; ++c) acc[c] = 0.0;
+        for (int o = 0; o < O; ++o)
+            for (int r = 0; r < KH; ++r) {
+                int hi = h + ph - r;
+                if (hi < 0 || hi % sh) continue;
+                int i = hi / sh;
+                if (i >= Ho) continue;
+                for (int q = 0; q < KW; ++q) {
+                    int wi = w_ + pw - q;
+                    if (wi < 0 || wi % sw) continue;
+                    int j = wi / sw;
+                    if (j >= Wo) continue;
+                    double g = gy[IDX4(n, o, i, j, O, Ho, Wo)];
+                    double Ta = conv_term(C, H, W, KH, KW, sh, sw, ph, pw, x, wa, ba, n, o, i, j);
+                    double Tb = conv_term(C, H, W, KH, KW, sh, sw, ph, pw, x, wb, bb, n, o, i, j);
+                    for (int c = 0; c < C; ++c)
+                        acc[c] += g * Tb * wa[IDX4(o, c, r, q, C, KH, KW)]
+                                + g * Ta * wb[IDX4(o, c, r, q, C, KH, KW)]
+                                + g * wc[IDX4(o, c, r, q, C, KH, KW)];
+                }
+            }
+    }
+}
+
 /* Weight and bias gradients of one output channel o: dW_t[o,:,:,:] (C*KH*KW
  * values each) and db_t[o].  Any output pointer may be NULL. */
 void oracle_conv2d_dw_channel(int N, int C, int H, int W, int O, int KH, int KW,

@@ -16,7 +16,8 @@ blocks of every output in the shape of the largest workgroup tile any kernel
 of the pass uses (256 x 256), at the first, the last and one interior tile
 position: forward Y, T_a, T_b; input gradient dX (whole rows of channels for
 the dense layer); whole output channels of dW_t and db_t (all of (r, q, c),
-so every weight-gradient row tile and every split-K part of those channels).
+so every weight-gradient row tile and every split-K part of those channels:
+the first 64-channel tile and the last 16 channels for the 56 x 56 layer).
 """
 import numpy as np
 import pytest
@@ -137,22 +138,39 @@ def test_large_conv_full_size_tiles():
                 _check(f"{key} block o{o0} m{m0}", key, _at(dev[key], n, i, j, idx[:, 1]), r, g, True,
                        L.c * 9 + 1)
 
-    # input gradient: blocks of TILE input channels x TILE input pixels
+    # input gradient: blocks of TILE input channels x TILE input pixels (the
+    # oracle's dX at every channel of each block's pixels)
     Mi = L.n * L.h * L.w
-    for c0 in _blocks(L.c, rng):
-        for m0 in _blocks(Mi, rng):
+    for m0 in _blocks(Mi, rng):
+        m = np.arange(m0, min(Mi, m0 + TILE))
+        n, rem = np.divmod(m, L.h * L.w)
+        h, w = np.divmod(rem, L.w)
+        pix = np.stack([n, h, w], axis=1)
+        ref_all = oracle.conv2d_dx_pixels(*args, f64["gy"], pix, L.stride, L.pad)
+        mag_all = oracle.conv2d_dx_pixels(*aargs, a["gy"], pix, L.stride, L.pad)
+        for c0 in _blocks(L.c, rng):
             c = np.arange(c0, min(L.c, c0 + TILE))
-            m = np.arange(m0, min(Mi, m0 + TILE))
-            cc, mm = np.meshgrid(c, m, indexing="ij")
-            n, rem = np.divmod(mm.ravel(), L.h * L.w)
-            h, w = np.divmod(rem, L.w)
-            idx = np.stack([n, cc.ravel(), h, w], axis=1)
-            ref = oracle.conv2d_dx_at(*args, f64["gy"], idx, L.stride, L.pad)
-            mag = oracle.conv2d_dx_at(*aargs, a["gy"], idx, L.stride, L.pad)
-            _check(f"dx block c{c0} m{m0}", "dx", _at(dev["dx"], n, h, w, idx[:, 1]), ref, mag, True, 3 * L.o * 9)
+            mm, cc = np.meshgrid(np.arange(len(m)), c, indexing="ij")
+            got = _at(dev["dx"], n[mm.ravel()], h[mm.ravel()], w[mm.ravel()], cc.ravel())
+            _check(f"dx block c{c0} m{m0}", "dx", got, ref_all[mm.ravel(), cc.ravel()], mag_all[mm.ravel(), cc.ravel()],
+                   True, 3 * L.o * 9)
 
-    # weight and bias gradients: whole output channels, one 64-channel tile at each end
-    chans = list(range(0, 64)) + list(range(L.o - 64, L.o))
+
+def test_large_conv_full_size_weight_channels():
+    """Whole output channels of dW_t and db_t of the large layer: the first
+    64-channel tile complete and the last 16 channels (one wave's slice of the
+    last tile)."""
+    L = synth.LARGE_BF16
+    print("full-size large conv, weight-gradient channels", flush=True)
+    inp = synth.conv_inputs(4, 0, L, bf16=True)
+    dev = qlh.run_conv(inp, L.stride, L.pad, True)
+    f64 = {k: np.ascontiguousarray(v, dtype=np.float64) for k, v in inp.items()}
+    a = _abs_args(f64)
+    keys = ("x", "wa", "wb", "wc", "ba", "bb", "bc")
+    args, aargs = [f64[k] for k in keys], [a[k] for k in keys]
+    M = L.n * L.ho * L.wo
+
+    chans = list(range(0, 64)) + list(range(L.o - 16, L.o))
     got = {k: [] for k in ("dwa", "dwb", "dwc", "dba", "dbb", "dbc")}
     ref = {k: [] for k in got}
     mag = {k: [] for k in got}

@@ -326,6 +326,16 @@ def test_sampled_functions_agree_with_full():
     dxs = oracle.conv2d_dx_at(x, *ws, *bs, gy, xi, s, p)
     ref = d["dx"][tuple(xi.T)]
     assert np.max(np.abs(dxs - ref)) <= 1e-13 * max(1.0, np.max(np.abs(ref)))
+    # every channel at every input pixel: the same terms in the same order as the
+    # per-element sampler, so the same bits, and the full oracle's dX
+    pix = np.array(list(np.ndindex(N, H, W)))
+    dxp = oracle.conv2d_dx_pixels(x, *ws, *bs, gy, pix, s, p)
+    pn, ph_, pw_ = pix.T
+    assert dxp.shape == (len(pix), C)
+    assert np.max(np.abs(dxp - d["dx"][pn, :, ph_, pw_])) <= 1e-13 * max(1.0, np.max(np.abs(ref)))
+    per_elem = oracle.conv2d_dx_at(x, *ws, *bs, gy,
+                                   np.array([[n_, c_, h_, w_] for (n_, h_, w_) in pix for c_ in range(C)]), s, p)
+    assert np.array_equal(dxp.ravel(), per_elem)
     for o in range(O):
         dc = oracle.conv2d_dw_channel(x, *ws, *bs, gy, o, s, p)
         for k in ("dwa", "dwb", "dwc"):
