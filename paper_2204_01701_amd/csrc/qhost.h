@@ -469,14 +469,16 @@ inline BwdDataPlan plan_bwd_data(const Geom &g) {
     plan_splits(p.row_tiles * p.col_tiles, kst, env_override("QLAYER_BWD_DATA_MINSTAGES", 4),
                 (size_t)M * g.C * 4, p.slots, p.splits, p.sps);
     // Block order of the split grid: tile-major (each XCD's blocks share pixel
-    // tiles and read all of the weights) unless the weights outweigh G, T_a, T_b
-    // by more than 4x (the 2 x 2 maps of a CIFAR VGG-16: split-major, each XCD
-    // reading its K range of the weights).  Measured on the VGG-16 layers at
-    // batch 128 (bitwise the same results in every order): tile-major 0.3-1.4
-    // us per call faster on layers 5-10 (34.0 -> 33.1 us on layer 5), 1 us
-    // slower on the 2 x 2 layers 11-13.
+    // tiles: their rows of G, T_a, T_b once, all of the weights) where G, T_a,
+    // T_b are at least the weight bytes (M >= C KH KW), split-major otherwise
+    // (each XCD reads its K range of the weights and all of G, T_a, T_b).
+    // Measured on the VGG-16 layers at batch 128 (bitwise the same results in
+    // every order): the 128 -> 256 8 x 8 layer reads 44 instead of 115 MB per
+    // call from beyond the L2s and runs 34.0 -> 33.1 us; on the 4 x 4 layers
+    // tile-major read twice the bytes (142 against 72 MB per call on 512 ->
+    // 512) for at most 1 us, and on the 2 x 2 layers it was 1 us slower.
     {
-        const int dflt = 4LL * M >= (long long)g.C * g.KH * g.KW ? 1 : 0;
+        const int dflt = (long long)M >= (long long)g.C * g.KH * g.KW ? 1 : 0;
         p.order = p.splits > 1 ? env_override("QLAYER_BWD_DATA_ORDER", dflt) : 0;
         if (p.order < 0 || p.order > 2) p.order = 0;
     }
